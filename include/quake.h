@@ -1,0 +1,148 @@
+/*
+ * quake.h — C ABI of libquake, the MI355X (gfx950) implementation of QuAKE:
+ * the IEEE-754 bit-construction approximation of exp with the affine input
+ * transform folded into its two constants, the second-order (QuAKE2) mantissa
+ * refinement, and the Softmax, GELU and Logistic operators built on it.
+ *
+ * Paper: S. K. Narayanaswami, G. Srinivasan, B. Ravindran, "QuAKE: Speeding up
+ * Model Inference Using Quick and Approximate Kernels for Exponential
+ * Non-Linearities", arXiv:2412.00408.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Pointers x and y are DEVICE pointers (memory the caller allocated on the
+ *   current HIP device, e.g. by torch). The library never allocates, frees or
+ *   retains them. x and y have the same element type (quake_dtype); all
+ *   arithmetic is binary32. In-place (x == y) is allowed; partial overlap is
+ *   undefined. Any alignment is accepted; 16-byte-aligned buffers (and, for
+ *   softmax, row strides that are a multiple of 16 bytes) take the vectorised
+ *   path.
+ * - `stream` is a hipStream_t passed as an opaque pointer (NULL = the legacy
+ *   default stream). Every call is asynchronous and stream-ordered: the status
+ *   covers argument validation and the launch itself (hipGetLastError right
+ *   after the launch); a fault inside a kernel surfaces at the caller's next
+ *   synchronisation.
+ * - A size of zero returns QUAKE_OK and launches nothing. Negative sizes, a
+ *   NULL pointer with a nonzero size, or a row stride smaller than the row
+ *   length return QUAKE_EINVAL before any HIP call. Unknown enum values return
+ *   QUAKE_EDTYPE / QUAKE_EMODE. No C++ exception crosses this interface.
+ * - Sizes above 2^31 elements are split into several launches by the library.
+ * - NaN inputs give unspecified (but finite-time, fault-free) outputs.
+ *
+ * The three modes (quake_mode):
+ *   QUAKE_EXACT  the same fused binary32 argument, exponentiated with the GPU's
+ *                hardware base-2 exponential instead of the bit construction.
+ *                This is the comparison ("vanilla") kernel.
+ *   QUAKE_1      first-order QuAKE, Sec. III-A: l = c0*x + c1 (Eq. 5, one fused
+ *                multiply-add), z = convert_to_int(l), result = bits of z read
+ *                as a float (Eq. 2, Eq. 3).
+ *   QUAKE_2      QuAKE2, Sec. III-B and Algorithm 1: the mantissa of z is
+ *                refined with y_m = (a_m^2 + 2)/3 (Eq. 6 with a0 = 1/3, a1 = 0,
+ *                a2 = 2/3), evaluated as fmaf(a_m, a_m, 2) * fl(1/3), and joined
+ *                to the exponent field of z.
+ *   Before convert_to_int, l is clamped to [0, 255 * 2^23] (our reading of the
+ *   v_min clamp of Algorithm 2, applied to every operator): inputs whose result
+ *   underflows give 0 (or a denormal ramp), +inf or overflowing inputs give
+ *   +inf, and the float-to-int conversion can never overflow.
+ */
+#ifndef QUAKE_H
+#define QUAKE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define QUAKE_ABI_VERSION 1
+
+typedef enum {
+  QUAKE_F32 = 0,  /* IEEE binary32 */
+  QUAKE_F16 = 1,  /* IEEE binary16 */
+  QUAKE_BF16 = 2  /* bfloat16 (upper half of binary32) */
+} quake_dtype;
+
+typedef enum {
+  QUAKE_EXACT = 0,
+  QUAKE_1 = 1,
+  QUAKE_2 = 2
+} quake_mode;
+
+typedef enum {
+  QUAKE_OK = 0,
+  QUAKE_EINVAL = 1,  /* bad pointer / size / stride / scalar argument */
+  QUAKE_EDTYPE = 2,  /* unknown quake_dtype */
+  QUAKE_EMODE = 3,   /* unknown quake_mode */
+  QUAKE_EHIP = 4     /* a HIP runtime call or kernel launch failed */
+} quake_status;
+
+/*
+ * quake_exp — y[i] = e^(a*x[i] + b), elementwise over n contiguous elements.
+ * Sec. III-A, Eq. 5: the affine map is folded into the constants,
+ *   c0 = fl32(2^23 * a / ln2),  c1 = fl32(2^23 * (127 - beta + b / ln2)),
+ * each evaluated in double and rounded once. beta is the Schraudolph bias
+ * 0.0436 in QUAKE_1 (Sec. III-A) and 0 in QUAKE_2 (QuAKE2 is exact at integer
+ * powers of two, Sec. III-B). QUAKE_EXACT computes exp2(fmaf(x, fl32(a/ln2),
+ * fl32(b/ln2))) with the hardware exp2.
+ *   x, y : device buffers of n elements of `dtype`, contiguous.
+ *   a, b : finite; otherwise QUAKE_EINVAL.
+ * QUAKE_1 and QUAKE_2 outputs are bit-exact functions of the input.
+ */
+quake_status quake_exp(const void* x, void* y, int64_t n, quake_dtype dtype,
+                       quake_mode mode, float a, float b, void* stream);
+
+/*
+ * quake_softmax — row-wise softmax(t * x) of a row-major matrix,
+ * Sec. III-C, Algorithm 2: m = max_j x[r, j]; c0 = fl32(2^23 * t / ln2);
+ * c1 = fmaf(-c0, m, 127 * 2^23); y[r, j] = QuAKEx(x[r, j]) / sum_j QuAKEx(x[r, j]).
+ * Every exponent of a row is taken against the row's final maximum (QuAKE is
+ * not multiplicative, so online rescaling of partial sums would change the
+ * result); sums are accumulated in fp32 per vector and in double across lanes,
+ * waves and workgroups.
+ *   x    : device, rows x cols elements, row r at x + r*ldx (elements).
+ *   y    : device, row r at y + r*ldy (elements).
+ *   ldx, ldy >= cols. cols >= 1 when rows >= 1.
+ *   t    : temperature, finite and > 0; otherwise QUAKE_EINVAL.
+ * Rows may hold -inf (masking); those entries give exactly 0, and a row that
+ * is entirely -inf gives a row of zeros. +inf inputs are unspecified.
+ * Rows longer than one workgroup's registers are split over several
+ * workgroups that exchange (max, sum) through a small per-stream device
+ * workspace the library allocates on first use and keeps until exit.
+ */
+quake_status quake_softmax(const void* x, void* y, int64_t rows, int64_t cols,
+                           int64_t ldx, int64_t ldy, quake_dtype dtype,
+                           quake_mode mode, float t, void* stream);
+
+/*
+ * quake_gelu — tanh-form GELU (Sec. II-C, Eq. 4) rewritten as
+ * x * sigma(2*0.044715*sqrt(2/pi) * x * (1/0.044715 + x^2)) (Sec. III-D, Eq. 7):
+ *   u = fmaf(x, x, fl32(1/0.044715)); w = x*u;
+ *   e = QuAKEx(w) with c0 = fl32(-2^23 * 2*0.044715*sqrt(2/pi) / ln2),
+ *       c1 = 127*2^23 (QUAKE_2) or (127 - 0.0436)*2^23 (QUAKE_1);
+ *   y = x / (1 + e).
+ * x, y: device buffers of n contiguous elements. GELU(+-inf) is unspecified.
+ */
+quake_status quake_gelu(const void* x, void* y, int64_t n, quake_dtype dtype,
+                        quake_mode mode, void* stream);
+
+/*
+ * quake_sigmoid — Logistic sigma(x) = 1 / (1 + e^-x) (Sec. III-D), or, when
+ * silu != 0, SiLU x * sigma(x) = x / (1 + e^-x). e^-x is QuAKEx with
+ * c0 = fl32(-2^23 / ln2) (Eq. 5 with p = -1) and the c1 of quake_exp.
+ * x, y: device buffers of n contiguous elements. +-inf inputs are allowed
+ * (sigma(-inf) = 0, sigma(+inf) = 1).
+ */
+quake_status quake_sigmoid(const void* x, void* y, int64_t n, quake_dtype dtype,
+                           quake_mode mode, int silu, void* stream);
+
+/* Static, human-readable name of a status code (never NULL). */
+const char* quake_status_str(quake_status s);
+
+/* Returns QUAKE_ABI_VERSION of the built library. */
+int quake_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QUAKE_H */

@@ -1,0 +1,207 @@
+"""CPU oracle for QuAKE (arXiv:2412.00408) — TEST INFRASTRUCTURE.
+
+This package wraps ``quake_oracle.c`` (plain scalar C, built with gcc,
+fp-contraction off) with ctypes. Only the test suite, the smoke check and
+the CPU baseline of the benchmark may import it; the HIP library and its
+Python binding never do, and the two share no code.
+
+Arrays are numpy arrays holding elements of the I/O format:
+``float32`` arrays for ``"f32"``, and ``uint16`` (or ``float16``) arrays of
+raw bits for ``"f16"`` and ``"bf16"``. Every function returns a new array of
+the same numpy dtype as its input.
+
+Parity notes: every function here is pinned by the ``-m "not gpu"`` tests
+(closed forms of Eq. 2-3, Algorithm 1's continuity conditions, the error
+bounds of Sec. III-A/III-B against exact exp over every binary32 input,
+monotonicity, Algorithm 2's invariants, Eq. 4 = Eq. 7, and the rounding and
+decoding routines against numpy/torch). No function is "parity unpinned".
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "quake_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+# A test may point the wrapper at a deliberately mutated build of the oracle
+# (see tests/test_oracle_mutants.py) to show that the pins catch the mistake.
+_OVERRIDE = os.environ.get("QUAKE_ORACLE_LIB")
+
+EXACT, Q1, Q2, Q2_DIV = 0, 1, 2, 3
+DTYPES = {"f32": 0, "f16": 1, "bf16": 2}
+
+CFLAGS = ["-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared"]
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc into oracle/liboracle.so."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if _OVERRIDE:
+            L = ctypes.CDLL(_OVERRIDE)
+        else:
+            if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+                build(force=True)
+            L = ctypes.CDLL(_LIB)
+        vp, i64, ci, cf = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float
+        L.qo_constants.argtypes = [vp]
+        L.qo_softmax_c0.argtypes = [cf, ci]
+        L.qo_softmax_c0.restype = cf
+        L.qo_quake.argtypes = [vp, vp, i64, cf, cf, ci]
+        L.qo_exp.argtypes = [vp, vp, i64, ci, ci, cf, cf]
+        L.qo_sigmoid.argtypes = [vp, vp, i64, ci, ci, ci]
+        L.qo_gelu.argtypes = [vp, vp, i64, ci, ci]
+        L.qo_softmax.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp]
+        L.qo_round.argtypes = [vp, vp, i64, ci]
+        L.qo_decode.argtypes = [vp, vp, i64, ci]
+        for f in (L.qo_quake, L.qo_exp, L.qo_sigmoid, L.qo_gelu, L.qo_softmax,
+                  L.qo_round, L.qo_decode):
+            f.restype = ci
+        _lib = L
+    return _lib
+
+
+def _ptr(a: np.ndarray) -> int:
+    return a.ctypes.data
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise ValueError("oracle call failed with code %d" % rc)
+
+
+def _prep(x: np.ndarray, dt: str) -> np.ndarray:
+    if dt not in DTYPES:
+        raise ValueError(dt)
+    want = np.float32 if dt == "f32" else (np.uint16, np.float16)
+    if dt == "f32" and x.dtype != np.float32:
+        raise TypeError("f32 oracle input must be float32")
+    if dt != "f32" and x.dtype not in want:
+        raise TypeError("16-bit oracle input must be uint16 or float16 bits")
+    return np.ascontiguousarray(x)
+
+
+def _split(n: int, threads: int):
+    threads = max(1, min(threads, n))
+    step = -(-n // threads)
+    return [(s, min(n, s + step)) for s in range(0, n, step)]
+
+
+def constants() -> dict:
+    out = np.zeros(10, np.float32)
+    lib().qo_constants(_ptr(out))
+    names = ["C0_EXP", "K127", "C1_Q1", "L_HI", "A_GELU", "C0_GELU", "THIRD",
+             "C0_NEG", "LOG2E", "C0E_GELU"]
+    return dict(zip(names, out.tolist()))
+
+
+def softmax_c0(t: float, mode: int) -> float:
+    return float(lib().qo_softmax_c0(t, mode))
+
+
+def quake(x: np.ndarray, c0: float, c1: float, order: int) -> np.ndarray:
+    """Raw QuAKE (order Q1) / QuAKE2 (Q2, Q2_DIV) of binary32 inputs."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    y = np.empty_like(x)
+    _check(lib().qo_quake(_ptr(x), _ptr(y), x.size, c0, c1, order))
+    return y
+
+
+def _elementwise(fn, x, dt, extra, threads):
+    x = _prep(x, dt)
+    y = np.empty_like(x)
+    n = x.size
+    isz = x.itemsize
+    xb, yb = _ptr(x), _ptr(y)
+
+    def run(rng):
+        s, e = rng
+        _check(fn(xb + s * isz, yb + s * isz, e - s, DTYPES[dt], *extra))
+
+    if threads <= 1 or n < 4096:
+        if n:
+            run((0, n))
+    else:
+        with ThreadPoolExecutor(threads) as ex:
+            list(ex.map(run, _split(n, threads)))
+    return y
+
+
+def exp(x, dt="f32", mode=Q2, a=1.0, b=0.0, threads=1):
+    """y = e^(a x + b) (Sec. III-A)."""
+    return _elementwise(lib().qo_exp, x, dt, (mode, ctypes.c_float(a), ctypes.c_float(b)), threads)
+
+
+def sigmoid(x, dt="f32", mode=Q2, silu=False, threads=1):
+    """Logistic (silu=False) or SiLU (silu=True)."""
+    return _elementwise(lib().qo_sigmoid, x, dt, (mode, int(bool(silu))), threads)
+
+
+def gelu(x, dt="f32", mode=Q2, threads=1):
+    """GELU through Eq. 7."""
+    return _elementwise(lib().qo_gelu, x, dt, (mode,), threads)
+
+
+def softmax(x, dt="f32", mode=Q2, t=1.0, cols=None, ldx=None, ldy=None, threads=1):
+    """Row softmax of t*x (Algorithm 2). x: 2-D array (rows, ldx) of elements.
+
+    If cols < ldx only the first cols elements of each row are used; the
+    output has shape (rows, ldy) with untouched padding set to zero.
+    """
+    x = _prep(x, dt)
+    if x.ndim != 2:
+        raise ValueError("softmax oracle wants a 2-D array")
+    rows, width = x.shape
+    cols = width if cols is None else cols
+    ldx = width if ldx is None else ldx
+    ldy = cols if ldy is None else ldy
+    y = np.zeros((rows, ldy), dtype=x.dtype)
+    isz = x.itemsize
+    xb, yb = _ptr(x), _ptr(y)
+
+    def run(rng):
+        s, e = rng
+        tmp = np.empty(max(cols, 1), np.float64)
+        _check(lib().qo_softmax(xb + s * ldx * isz, yb + s * ldy * isz, e - s, cols, ldx,
+                                ldy, DTYPES[dt], mode, ctypes.c_float(t), _ptr(tmp)))
+
+    if rows == 0:
+        return y
+    if threads <= 1 or rows < 2:
+        run((0, rows))
+    else:
+        with ThreadPoolExecutor(threads) as ex:
+            list(ex.map(run, _split(rows, threads)))
+    return y
+
+
+def round_to(v: np.ndarray, dt: str) -> np.ndarray:
+    """Round float64 values once to the format dt (RNE)."""
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    out = np.empty(v.shape, np.float32 if dt == "f32" else np.uint16)
+    _check(lib().qo_round(_ptr(v), _ptr(out), v.size, DTYPES[dt]))
+    return out
+
+
+def decode(x: np.ndarray, dt: str) -> np.ndarray:
+    """Decode elements of format dt to float32 values."""
+    x = _prep(x, dt)
+    out = np.empty(x.shape, np.float32)
+    _check(lib().qo_decode(_ptr(x), _ptr(out), x.size, DTYPES[dt]))
+    return out

@@ -1,0 +1,324 @@
+/*
+ * quake_oracle.c — plain, slow, obviously-correct CPU oracle for QuAKE
+ * (arXiv:2412.00408).
+ *
+ * TEST INFRASTRUCTURE. Only the test suite, the smoke check and the CPU
+ * baseline of the benchmark load this library. The HIP product path never
+ * includes, links or calls anything here, and nothing here is shared with it.
+ *
+ * Build (fp contraction OFF, no fast-math, so every fused multiply-add the
+ * method prescribes is an explicit fmaf() and nothing else is fused):
+ *   gcc -O2 -std=c11 -ffp-contract=off -fno-fast-math -fPIC -shared \
+ *       -o liboracle.so quake_oracle.c -lm
+ *
+ * What each function follows:
+ *   qo_quake      Sec. II-B Eq. 2-3, Sec. III-A Eq. 5 (QuAKE), Sec. III-B Eq. 6
+ *                 and Algorithm 1 (QuAKE2), with explicit constants c0, c1.
+ *   qo_exp        Sec. III-A: e^(a x + b) with the affine map folded into c0, c1.
+ *   qo_softmax    Sec. III-C, Algorithm 2 (SoftMax-QuAKEx).
+ *   qo_gelu       Sec. II-C Eq. 4 rewritten as Sec. III-D Eq. 7.
+ *   qo_sigmoid    Sec. III-D logistic function (and SiLU = x * logistic).
+ *   qo_round      IEEE-754 round-to-nearest-even from double to binary32,
+ *                 binary16 and bfloat16 (the output formats).
+ *
+ * Readings taken where the paper is silent (each also listed in the design
+ * notes): convert_to_int truncates toward zero; x*c0 + c1 is one binary32 fma;
+ * (a_m^2 + 2)/3 is fmaf(a_m, a_m, 2) * fl32(1/3) (QO_Q2_DIV keeps the literal
+ * division for comparison); l is clamped to [0, 255*2^23] before the
+ * conversion (the v_min clamp of Algorithm 2, which as printed mixes units);
+ * the Schraudolph bias 0.0436 applies to first-order QuAKE outside softmax
+ * only; an all -inf softmax row gives zeros; constants are evaluated in double
+ * from their definitions and rounded once to binary32; sums are accumulated in
+ * double and the final division is done in double and rounded once.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+/* ---- mode / dtype codes (same numeric values as the public ABI enums) ---- */
+enum { QO_EXACT = 0, QO_Q1 = 1, QO_Q2 = 2, QO_Q2_DIV = 3 };
+enum { QO_F32 = 0, QO_F16 = 1, QO_BF16 = 2 };
+
+/* ---- IEEE binary32 layout, Sec. II-A Eq. 1: l_e = 8, l_m = 23, B = 127 ---- */
+#define LM 23
+#define BIAS 127
+/* Masks of Algorithm 1: keep mantissa / keep sign+exponent / exponent := B. */
+#define MASK_MANT 0x007FFFFFu
+#define MASK_SIGN_EXP 0xFF800000u
+#define EXP_B 0x3F800000u
+
+static const double LN2 = 0.693147180559945309417232121458176568; /* ln 2 */
+static const double TWO_LM = 8388608.0;                            /* 2^23 */
+
+static uint32_t f2u(float f) { uint32_t u; memcpy(&u, &f, 4); return u; }
+static float u2f(uint32_t u) { float f; memcpy(&f, &u, 4); return f; }
+
+/* ------------------------------------------------------------------------ */
+/* Constants, each from its real-number definition in double, rounded once. */
+/* ------------------------------------------------------------------------ */
+
+/* 127 * 2^23: c1 of the plain natural exponential (Sec. III-A). */
+static float k127(void) { return (float)(BIAS * TWO_LM); }
+
+/* Upper clamp of l: biased exponent 255, mantissa 0 = bits of +inf. */
+static float l_hi(void) { return (float)(255.0 * TWO_LM); }
+
+/* Eq. 5 with p = a/ln2 (natural exp folded into base 2): c0 = 2^23 * p. */
+static float c0_of(double a) { return (float)((a / LN2) * TWO_LM); }
+
+/* Eq. 5 with q = b/ln2, plus the Schraudolph bias for first order:
+ * c1 = 2^23 * (B - beta + q), beta = 0.0436 (Sec. III-A). */
+static float c1_of(double b, int mode) {
+  double beta = (mode == QO_Q1) ? 0.0436 : 0.0;
+  return (float)(((BIAS - beta) + b / LN2) * TWO_LM);
+}
+
+/* fl32(1/3): a0 = 1/3 of the continuity-constrained coefficients, Sec. III-B. */
+static float third(void) { return (float)(1.0 / 3.0); }
+
+/* 1/0.044715 of Eq. 7. */
+static float a_gelu(void) { return (float)(1.0 / 0.044715); }
+
+/* Scale of the logistic argument in Eq. 7: 2 * 0.044715 * sqrt(2/pi). */
+static double k_gelu(void) { return 2.0 * 0.044715 * sqrt(2.0 / 3.14159265358979323846264338327950288); }
+
+/* ------------------------------------------------------------------------ */
+/* The approximation itself.                                                */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * QuAKE / QuAKE2 of one binary32 input with explicit c0, c1.
+ *   order QO_Q1     : Eq. 2-3 — z = int(l), result = z's bits as a float.
+ *   order QO_Q2     : Algorithm 1 — a_m = 1 + {.} from z's mantissa with the
+ *                     exponent field set to B; y_m = (a_m^2 + 2)/3 (Eq. 6,
+ *                     a0 = 1/3, a1 = 0, a2 = 2/3) as fmaf(a_m, a_m, 2) * fl(1/3);
+ *                     result = z's sign+exponent field joined with y_m's mantissa.
+ *   order QO_Q2_DIV : as QO_Q2 with the literal float expression (a*a + 2) / 3.
+ */
+static float quake_one(float x, float c0, float c1, int order) {
+  float l = fmaf(x, c0, c1);             /* Eq. 5, one rounding */
+  if (!(l > 0.0f)) l = 0.0f;             /* clamp below (also -inf, NaN) */
+  if (l > l_hi()) l = l_hi();            /* clamp above (+inf, overflow) */
+  int32_t z = (int32_t)l;                /* convert_to_int, toward zero */
+  if (order == QO_Q1) return u2f((uint32_t)z);   /* int_bits_as_float */
+
+  float am = u2f(((uint32_t)z & MASK_MANT) | EXP_B);
+  float ym;
+  if (order == QO_Q2_DIV) {
+    ym = (am * am + 2.0f) / 3.0f;
+  } else {
+    ym = fmaf(am, am, 2.0f) * third();
+  }
+  uint32_t yi = ((uint32_t)z & MASK_SIGN_EXP) + f2u(ym) - EXP_B;
+  return u2f(yi);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Format conversion (I/O only; the method computes in binary32).           */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Round a double to a binary format with p significand bits (implicit bit
+ * included) and normal exponents [emin, emax], round-to-nearest-even, with
+ * gradual underflow and overflow to infinity. Returns the rounded value as a
+ * double (exactly representable in the target format).
+ */
+static double round_format(double v, int p, int emin, int emax) {
+  if (isnan(v) || isinf(v) || v == 0.0) return v;
+  double a = fabs(v);
+  int e2;
+  frexp(a, &e2);                 /* a = f * 2^e2, f in [0.5, 1) */
+  int E = e2 - 1;                /* floor(log2 a) */
+  if (E < emin) E = emin;        /* subnormal range: fixed quantum */
+  double quantum = ldexp(1.0, E - (p - 1));
+  double r = nearbyint(a / quantum) * quantum;   /* ties to even */
+  double maxfin = ldexp(2.0 - ldexp(1.0, 1 - p), emax);
+  if (r > maxfin) r = INFINITY;
+  return copysign(r, v);
+}
+
+static uint16_t enc_bf16(double v) {
+  if (isnan(v)) return (uint16_t)(signbit(v) ? 0xFFC0u : 0x7FC0u);
+  double r = round_format(v, 8, -126, 127);     /* exact in binary32 */
+  return (uint16_t)(f2u((float)r) >> 16);
+}
+
+static uint16_t enc_f16(double v) {
+  uint16_t s = signbit(v) ? 0x8000u : 0u;
+  if (isnan(v)) return (uint16_t)(s | 0x7E00u);
+  double r = fabs(round_format(v, 11, -14, 15));
+  if (isinf(r)) return (uint16_t)(s | 0x7C00u);
+  if (r == 0.0) return s;
+  int e2;
+  frexp(r, &e2);
+  int E = e2 - 1;
+  if (E < -14) return (uint16_t)(s | (uint16_t)ldexp(r, 24));   /* subnormal */
+  uint16_t mant = (uint16_t)(ldexp(r, -E) * 1024.0 - 1024.0);
+  return (uint16_t)(s | (uint16_t)((E + 15) << 10) | mant);
+}
+
+static float dec_bf16(uint16_t h) { return u2f((uint32_t)h << 16); }
+
+static float dec_f16(uint16_t h) {
+  int s = (h >> 15) & 1, e = (h >> 10) & 31, m = h & 1023;
+  float v;
+  if (e == 0) v = ldexpf((float)m, -24);
+  else if (e == 31) v = m ? NAN : INFINITY;
+  else v = ldexpf((float)(1024 + m), e - 25);
+  return s ? -v : v;
+}
+
+static float load_el(const void* p, int64_t i, int dt) {
+  if (dt == QO_F32) return ((const float*)p)[i];
+  if (dt == QO_F16) return dec_f16(((const uint16_t*)p)[i]);
+  return dec_bf16(((const uint16_t*)p)[i]);
+}
+
+/* Store a value, rounding once from double to the output format. */
+static void store_el(void* p, int64_t i, int dt, double v) {
+  if (dt == QO_F32) ((float*)p)[i] = (float)v;
+  else if (dt == QO_F16) ((uint16_t*)p)[i] = enc_f16(v);
+  else ((uint16_t*)p)[i] = enc_bf16(v);
+}
+
+static int bad_args(int dt, int mode) {
+  if (dt < QO_F32 || dt > QO_BF16) return 2;
+  if (mode < QO_EXACT || mode > QO_Q2_DIV) return 3;
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Exported functions.                                                      */
+/* ------------------------------------------------------------------------ */
+
+/* Fixed constants, for tests: fills out[0..9]. */
+void qo_constants(float* out) {
+  out[0] = c0_of(1.0);             /* C0_EXP  = 2^23 log2 e          */
+  out[1] = k127();                 /* K127    = 127 * 2^23           */
+  out[2] = c1_of(0.0, QO_Q1);      /* C1_Q1   = (127 - 0.0436) 2^23  */
+  out[3] = l_hi();                 /* L_HI    = 255 * 2^23           */
+  out[4] = a_gelu();               /* A_GELU  = 1/0.044715           */
+  out[5] = (float)(-(k_gelu() / LN2) * TWO_LM);   /* C0_GELU         */
+  out[6] = third();                /* THIRD                          */
+  out[7] = c0_of(-1.0);            /* C0_NEG  = -2^23 log2 e         */
+  out[8] = (float)(1.0 / LN2);     /* log2 e (EXACT-mode scale)      */
+  out[9] = (float)(-k_gelu() / LN2);   /* EXACT-mode GELU scale      */
+}
+
+/* c0 of the softmax for temperature t (Algorithm 2): 2^23 t / ln2. */
+float qo_softmax_c0(float t, int mode) {
+  if (mode == QO_EXACT) return (float)((double)t / LN2);
+  return (float)(((double)t / LN2) * TWO_LM);
+}
+
+/* Raw QuAKE with explicit constants, binary32 in and out. */
+int qo_quake(const float* x, float* y, int64_t n, float c0, float c1, int order) {
+  if (order != QO_Q1 && order != QO_Q2 && order != QO_Q2_DIV) return 3;
+  for (int64_t i = 0; i < n; ++i) y[i] = quake_one(x[i], c0, c1, order);
+  return 0;
+}
+
+/* e^(a x + b), Sec. III-A. */
+int qo_exp(const void* x, void* y, int64_t n, int dt, int mode, float a, float b) {
+  int err = bad_args(dt, mode);
+  if (err) return err;
+  if (mode == QO_EXACT) {
+    float c0e = (float)((double)a / LN2), c1e = (float)((double)b / LN2);
+    for (int64_t i = 0; i < n; ++i) {
+      float s = fmaf(load_el(x, i, dt), c0e, c1e);
+      store_el(y, i, dt, exp2((double)s));
+    }
+  } else {
+    float c0 = c0_of(a), c1 = c1_of(b, mode);
+    for (int64_t i = 0; i < n; ++i)
+      store_el(y, i, dt, (double)quake_one(load_el(x, i, dt), c0, c1, mode));
+  }
+  return 0;
+}
+
+/* Logistic function (silu = 0) or SiLU x * logistic(x) (silu != 0). */
+int qo_sigmoid(const void* x, void* y, int64_t n, int dt, int mode, int silu) {
+  int err = bad_args(dt, mode);
+  if (err) return err;
+  float c0 = c0_of(-1.0), c1 = c1_of(0.0, mode);
+  float c0e = (float)(-1.0 / LN2);
+  for (int64_t i = 0; i < n; ++i) {
+    float xv = load_el(x, i, dt);
+    double e = (mode == QO_EXACT) ? exp2((double)fmaf(xv, c0e, 0.0f))
+                                  : (double)quake_one(xv, c0, c1, mode);
+    double num = silu ? (double)xv : 1.0;
+    store_el(y, i, dt, num / (1.0 + e));
+  }
+  return 0;
+}
+
+/* GELU via Eq. 7: x * sigma(k * x * (1/0.044715 + x^2)), k = 2*0.044715*sqrt(2/pi). */
+int qo_gelu(const void* x, void* y, int64_t n, int dt, int mode) {
+  int err = bad_args(dt, mode);
+  if (err) return err;
+  float A = a_gelu();
+  float c0 = (float)(-(k_gelu() / LN2) * TWO_LM), c1 = c1_of(0.0, mode);
+  float c0e = (float)(-k_gelu() / LN2);
+  for (int64_t i = 0; i < n; ++i) {
+    float xv = load_el(x, i, dt);
+    float u = fmaf(xv, xv, A);      /* 1/0.044715 + x^2, one FMA */
+    float w = xv * u;
+    double e = (mode == QO_EXACT) ? exp2((double)fmaf(w, c0e, 0.0f))
+                                  : (double)quake_one(w, c0, c1, mode);
+    store_el(y, i, dt, (double)xv / (1.0 + e));
+  }
+  return 0;
+}
+
+/*
+ * Row softmax of t*x, Algorithm 2. `tmp` is caller scratch of cols doubles.
+ * Row r of x starts at element r*ldx, row r of y at r*ldy.
+ */
+int qo_softmax(const void* x, void* y, int64_t rows, int64_t cols, int64_t ldx,
+               int64_t ldy, int dt, int mode, float t, double* tmp) {
+  int err = bad_args(dt, mode);
+  if (err) return err;
+  float c0 = qo_softmax_c0(t, mode);
+  for (int64_t r = 0; r < rows; ++r) {
+    const int64_t bx = r * ldx, by = r * ldy;
+    float m = -INFINITY;
+    for (int64_t j = 0; j < cols; ++j) {
+      float v = load_el(x, bx + j, dt);
+      if (v > m) m = v;
+    }
+    if (m == -INFINITY) {                       /* fully masked row */
+      for (int64_t j = 0; j < cols; ++j) store_el(y, by + j, dt, 0.0);
+      continue;
+    }
+    double sum = 0.0;
+    if (mode == QO_EXACT) {
+      float c1e = fmaf(-c0, m, 0.0f);
+      for (int64_t j = 0; j < cols; ++j) {
+        tmp[j] = exp2((double)fmaf(load_el(x, bx + j, dt), c0, c1e));
+        sum += tmp[j];
+      }
+    } else {
+      float c1 = fmaf(-c0, m, k127());          /* 127*2^23 - c0*m */
+      for (int64_t j = 0; j < cols; ++j) {
+        tmp[j] = (double)quake_one(load_el(x, bx + j, dt), c0, c1, mode);
+        sum += tmp[j];
+      }
+    }
+    for (int64_t j = 0; j < cols; ++j) store_el(y, by + j, dt, tmp[j] / sum);
+  }
+  return 0;
+}
+
+/* Rounding of doubles to an output format, exposed for tests. */
+int qo_round(const double* v, void* out, int64_t n, int dt) {
+  if (dt < QO_F32 || dt > QO_BF16) return 2;
+  for (int64_t i = 0; i < n; ++i) store_el(out, i, dt, v[i]);
+  return 0;
+}
+
+/* Decoding of an input format to binary32, exposed for tests. */
+int qo_decode(const void* in, float* out, int64_t n, int dt) {
+  if (dt < QO_F32 || dt > QO_BF16) return 2;
+  for (int64_t i = 0; i < n; ++i) out[i] = load_el(in, i, dt);
+  return 0;
+}

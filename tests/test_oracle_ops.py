@@ -1,0 +1,213 @@
+"""Pins of the oracle's operators: Softmax (Algorithm 2), GELU (Eq. 4 / Eq. 7),
+Logistic and SiLU, and e^(a x + b) with the affine map folded (Eq. 5).
+
+Reference values come from numpy / scipy in double precision, and the bounds
+from the exhaustive error range of the scalar approximation: QuAKE2's relative
+error lies in [-0.18748 %, +0.34185 %], first order's in [-2.9777 %, +2.9881 %].
+"""
+import math
+
+import numpy as np
+import pytest
+from scipy.special import expit, softmax as sp_softmax
+
+LN2 = math.log(2.0)
+EPS = {1: 0.0298805 + 2e-5, 2: 0.0034185 + 2e-5}         # max |rel err| of e, + l spacing
+RATIO = {1: (1 + 0.0298805) / (1 - 0.0297765) - 1 + 4e-5,
+         2: (1 + 0.0034185) / (1 - 0.0018748) - 1 + 4e-5}
+
+
+def _rows(seed, rows, cols, scale):
+    return (np.random.default_rng(seed).standard_normal((rows, cols)) * scale).astype(np.float32)
+
+
+# ------------------------------ softmax ------------------------------------
+
+@pytest.mark.parametrize("mode", [0, 1, 2])
+@pytest.mark.parametrize("cols,t", [(1, 1.0), (7, 1.0), (128, 0.125), (1000, 3.0), (4099, 1.0)])
+def test_softmax_rows_sum_to_one(oracle, mode, cols, t):
+    x = _rows(cols, 6, cols, 4.0)
+    y = oracle.softmax(x, "f32", mode, t=t)
+    s = y.astype(np.float64).sum(axis=1)
+    assert np.all(np.abs(s - 1) <= cols * 2.0 ** -24 + 1e-12)
+
+
+@pytest.mark.parametrize("mode", [0, 1, 2])
+def test_softmax_single_and_constant_rows(oracle, mode):
+    assert oracle.softmax(np.array([[3.5]], np.float32), "f32", mode)[0, 0] == 1.0
+    for n in (2, 3, 10, 512, 1000):
+        y = oracle.softmax(np.full((1, n), -2.25, np.float32), "f32", mode, t=0.7)
+        assert np.all(y == y[0, 0])
+        assert abs(float(y[0, 0]) * n - 1) <= 2.0 ** -23
+
+
+@pytest.mark.parametrize("mode", [0, 1, 2])
+@pytest.mark.parametrize("t", [1.0, 0.125, 2.5])
+def test_softmax_against_exact(oracle, mode, t):
+    x = _rows(3, 32, 300, 3.0)
+    y = oracle.softmax(x, "f32", mode, t=t).astype(np.float64)
+    ref = sp_softmax(t * x.astype(np.float64), axis=1)
+    rel = np.abs(y / ref - 1)
+    big = ref > 1e-30
+    if mode == 0:
+        # binary32 rounding of c0, c1 and of s grows with |s| = t |x - m| / ln 2
+        arg = t * (x.max(axis=1, keepdims=True) - x).astype(np.float64)
+        bound = (4 * 2.0 ** -24 * (1 + arg) + 2e-7)[big]
+    else:
+        bound = RATIO[mode]
+    assert np.all(rel[big] <= bound)
+    if mode == 2:
+        assert rel[big].max() > 0.002        # the approximation is really used
+
+
+@pytest.mark.parametrize("mode", [1, 2])
+def test_softmax_shift_invariance(oracle, mode):
+    # Algorithm 2 folds the max into c1, so adding a constant to a row changes
+    # only the binary32 rounding of l.
+    x = (np.round(_rows(4, 16, 200, 2.0) * 256) / 256).astype(np.float32)
+    y0 = oracle.softmax(x, "f32", mode).astype(np.float64)
+    for c in (0.5, -7.0, 40.0):
+        y1 = oracle.softmax((x + np.float32(c)).astype(np.float32), "f32", mode).astype(np.float64)
+        assert np.max(np.abs(y1 / y0 - 1)) < 1e-4
+
+
+@pytest.mark.parametrize("mode", [0, 1, 2])
+def test_softmax_masking(oracle, mode):
+    x = _rows(5, 8, 64, 2.0)
+    keep = np.random.default_rng(6).random((8, 64)) < 0.6
+    keep[:, 0] = True
+    xm = np.where(keep, x, -np.inf).astype(np.float32)
+    y = oracle.softmax(xm, "f32", mode)
+    assert np.all(y[~keep] == 0.0)
+    for r in range(8):
+        sub = oracle.softmax(x[r, keep[r]][None, :].copy(), "f32", mode)
+        assert np.array_equal(y[r, keep[r]], sub[0])
+    z = oracle.softmax(np.full((2, 16), -np.inf, np.float32), "f32", mode)
+    assert np.all(z == 0.0)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16", "f16"])
+def test_softmax_row_strides(oracle, dt):
+    x = _rows(7, 5, 40, 1.5)
+    xs = oracle.round_to(x.astype(np.float64), dt)
+    padded = np.zeros((5, 48), xs.dtype)
+    padded[:, :40] = xs
+    a = oracle.softmax(padded, dt, 2, cols=40, ldx=48, ldy=44)
+    b = oracle.softmax(xs, dt, 2)
+    assert np.array_equal(a[:, :40], b)
+    assert np.all(a[:, 40:] == 0)
+
+
+# ------------------------------ GELU ----------------------------------------
+
+def _gelu_tanh(x):
+    """Eq. 4 in double. 0.5 (1 + tanh a) is evaluated as expit(2 a), the same
+    function without the cancellation of 1 + tanh a for very negative a."""
+    x = x.astype(np.float64)
+    a = math.sqrt(2 / math.pi) * (x + 0.044715 * x ** 3)
+    return x * expit(2 * a)
+
+
+def _gelu_tanh_literal(x):
+    x = x.astype(np.float64)
+    return 0.5 * x * (1 + np.tanh(math.sqrt(2 / math.pi) * (x + 0.044715 * x ** 3)))
+
+
+def test_gelu_exact_mode_is_eq4(oracle):
+    # Eq. 7 is an exact rewrite of Eq. 4: with exact exp the two agree up to
+    # the binary32 rounding of u, w and the scaled argument.
+    x = np.concatenate([np.linspace(-10, 10, 200001), [0.0, -0.0, 1e-30, -1e-30]]).astype(np.float32)
+    y = oracle.gelu(x, "f32", 0).astype(np.float64)
+    ref = _gelu_tanh(x)
+    err = np.abs(y - ref)
+    assert np.all(err <= 2e-5 * np.abs(ref) + 1e-44)
+    mid = np.abs(x) <= 4
+    lit = _gelu_tanh_literal(x[mid])
+    assert np.all(np.abs(y[mid] - lit) <= 2e-5 * np.abs(lit) + 1e-15)
+
+
+@pytest.mark.parametrize("mode", [1, 2])
+def test_gelu_quake_bound(oracle, mode):
+    x = np.linspace(-12, 12, 400001).astype(np.float32)
+    y = oracle.gelu(x, "f32", mode).astype(np.float64)
+    ref = _gelu_tanh(x)
+    eps = EPS[mode]
+    bound = np.abs(x.astype(np.float64)) * (eps / (4 * (1 - eps)) + 2.0 ** -23) + 1e-37
+    assert np.all(np.abs(y - ref) <= bound)
+    assert np.max(np.abs(y - ref) / np.maximum(np.abs(x), 1e-30)) > eps / 40
+
+
+@pytest.mark.parametrize("mode", [1, 2])
+def test_gelu_special_values(oracle, mode):
+    y = oracle.gelu(np.array([0.0, 5.5, 8.0, 100.0, 3e4], np.float32), "f32", mode)
+    assert y[0] == 0.0
+    assert np.array_equal(y[1:], np.array([5.5, 8.0, 100.0, 3e4], np.float32))
+    # very negative inputs: e overflows to +inf after the clamp, output is -0
+    yn = oracle.gelu(np.array([-11.0, -50.0], np.float32), "f32", mode)
+    assert np.all(yn == 0.0)
+
+
+# ------------------------------ logistic / SiLU -----------------------------
+
+@pytest.mark.parametrize("mode", [0, 1, 2])
+def test_sigmoid_bound(oracle, mode):
+    x = np.concatenate([np.linspace(-30, 30, 300001), [-80, 80, -88, 88, -100, 100]]).astype(np.float32)
+    y = oracle.sigmoid(x, "f32", mode).astype(np.float64)
+    ref = expit(x.astype(np.float64))
+    if mode == 0:
+        # rounding of the binary32 argument s = x * fl(-1/ln2) grows with |x|
+        rel = 4 * 2.0 ** -24 * (1 + np.abs(x.astype(np.float64)))
+        assert np.all(np.abs(y - ref) <= rel * ref + 2.0 ** -126)
+    else:
+        eps = EPS[mode]
+        assert np.all(np.abs(y - ref) <= eps / (4 * (1 - eps)) + 2.0 ** -24)
+
+
+@pytest.mark.parametrize("mode", [0, 1, 2])
+def test_silu_bound(oracle, mode):
+    x = np.linspace(-40, 40, 300001).astype(np.float32)
+    y = oracle.sigmoid(x, "f32", mode, silu=True).astype(np.float64)
+    xd = x.astype(np.float64)
+    ref = xd * expit(xd)
+    eps = 4 * 2.0 ** -24 * (1 + np.abs(xd)) if mode == 0 else EPS[mode] / (4 * (1 - EPS[mode]))
+    assert np.all(np.abs(y - ref) <= np.abs(xd) * (eps + 2.0 ** -24) + 2.0 ** -126)
+
+
+def test_sigmoid_special_values(oracle):
+    x = np.array([0.0, -np.inf, np.inf, 80.0, -80.0], np.float32)
+    for mode in (0, 1, 2):
+        y = oracle.sigmoid(x, "f32", mode)
+        assert y[1] == 0.0 and y[2] == 1.0 and y[3] == 1.0
+        assert 0.0 < y[4] < 1e-33
+    assert oracle.sigmoid(x, "f32", 2)[0] == 0.5           # QuAKE2 is exact at 0
+    s = oracle.sigmoid(x[:1], "f32", 2, silu=True)
+    assert s[0] == 0.0
+
+
+# ------------------------------ e^(a x + b) ---------------------------------
+
+@pytest.mark.parametrize("a,b", [(1.0, 0.0), (-1.0, 0.0), (0.37, 2.0), (-3.0, -1.5), (10.0, 5.0)])
+@pytest.mark.parametrize("mode", [0, 1, 2])
+def test_affine_exp_against_exact(oracle, a, b, mode):
+    x = np.random.default_rng(12).uniform(-8, 8, 200000).astype(np.float32)
+    y = oracle.exp(x, "f32", mode, a=a, b=b).astype(np.float64)
+    ref = np.exp(np.float64(a) * x + np.float64(b))
+    ok = (ref > 2.0 ** -125) & (ref < 3e38)
+    rel = np.abs(y[ok] / ref[ok] - 1)
+    if mode == 0:
+        # binary32 rounding of the folded constants and of s, then exact exp2
+        s = np.abs(np.float64(a) * x[ok] + b) / LN2
+        assert np.all(rel <= 4 * 2.0 ** -24 * (1 + s * LN2) + 1e-12)
+    else:
+        # folded constants are rounded once; the argument keeps ~2^-17 relative spacing
+        assert rel.max() <= EPS[mode] + 2e-5 * max(1.0, abs(a) * 8 + abs(b)) / 8
+
+
+def test_folded_exp_equals_raw_quake(oracle):
+    c = oracle.constants()
+    x = np.random.default_rng(13).uniform(-87, 88, 100000).astype(np.float32)
+    assert np.array_equal(oracle.exp(x, "f32", 2), oracle.quake(x, c["C0_EXP"], c["K127"], 2))
+    assert np.array_equal(oracle.exp(x, "f32", 1), oracle.quake(x, c["C0_EXP"], c["C1_Q1"], 1))
+    assert np.array_equal(oracle.sigmoid(x, "f32", 2),
+                          (1.0 / (1.0 + oracle.quake(x, c["C0_NEG"], c["K127"], 2).astype(np.float64)))
+                          .astype(np.float32))

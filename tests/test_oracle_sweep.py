@@ -1,0 +1,128 @@
+"""Exhaustive pins of the oracle's natural exp over every finite binary32 input.
+
+Against exact exp (numpy, double):
+  * QuAKE2's relative error range equals the extremes of the continuous error
+    function of Eq. 6 with a0 = 1/3, a2 = 2/3 (found here by a dense grid and a
+    bounded scalar minimiser), widened only by the binary32 spacing of l; its
+    maximum is the paper's 0.34 % (Sec. III-B).
+  * First-order QuAKE with bias 0.0436 stays inside the 4.3 % the paper quotes
+    (Sec. III-B), with extremes 2^-0.0436 - 1 and the maximum of (1+f) 2^(-f-beta).
+  * Both are monotone non-decreasing over all finite inputs.
+"""
+import os
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+import pytest
+from scipy.optimize import minimize_scalar
+
+BETA = 0.0436
+CHUNK = 1 << 24
+THREADS = max(1, min(8, os.cpu_count() or 1))
+TINY = 2.0 ** -125
+
+
+def _ranges():
+    """All finite binary32 bit patterns in increasing order of value."""
+    out = []
+    # negatives: 0xFF7FFFFF (-max) ... 0x80000000 (-0) = descending bits
+    hi = 0xFF7FFFFF
+    while hi >= 0x80000000:
+        lo = max(0x80000000, hi - CHUNK + 1)
+        out.append(("neg", lo, hi))
+        hi = lo - 1
+    lo = 0
+    while lo <= 0x7F7FFFFF:
+        hi = min(0x7F7FFFFF, lo + CHUNK - 1)
+        out.append(("pos", lo, hi))
+        lo = hi + 1
+    return out
+
+
+def _sweep(oracle, mode):
+    def work(rng):
+        kind, lo, hi = rng
+        b = np.arange(lo, hi + 1, dtype=np.uint32)
+        if kind == "neg":
+            b = b[::-1].copy()
+        x = b.view(np.float32)
+        y = oracle.exp(x, "f32", mode)
+        viol = int(np.count_nonzero(np.diff(y) < 0))
+        ref = np.exp(x.astype(np.float64))
+        ok = np.isfinite(y) & (ref >= TINY) & np.isfinite(ref)
+        if ok.any():
+            rel = y[ok].astype(np.float64) / ref[ok] - 1.0
+            emin, emax, cnt = float(rel.min()), float(rel.max()), int(ok.sum())
+        else:
+            emin, emax, cnt = np.inf, -np.inf, 0
+        return float(y[0]), float(y[-1]), viol, emin, emax, cnt
+
+    with ThreadPoolExecutor(THREADS) as ex:
+        res = list(ex.map(work, _ranges()))
+    viol = sum(r[2] for r in res)
+    # order across chunk boundaries
+    for a, b in zip(res[:-1], res[1:]):
+        if b[0] < a[1]:
+            viol += 1
+    return dict(viol=viol, emin=min(r[3] for r in res), emax=max(r[4] for r in res),
+                count=sum(r[5] for r in res))
+
+
+def _extremes(fn):
+    f = np.linspace(0.0, 1.0, 2_000_001)
+    g = fn(f)
+    i, j = int(np.argmin(g)), int(np.argmax(g))
+    lo = minimize_scalar(fn, bounds=(max(0, f[i] - 1e-5), min(1, f[i] + 1e-5)), method="bounded",
+                         options={"xatol": 1e-12}).fun
+    hi = -minimize_scalar(lambda t: -fn(t), bounds=(max(0, f[j] - 1e-5), min(1, f[j] + 1e-5)),
+                          method="bounded", options={"xatol": 1e-12}).fun
+    return min(lo, g.min()), max(hi, g.max())
+
+
+# relative error of Eq. 6 (a0=1/3, a1=0, a2=2/3) against 2^f
+def _q2_err(f):
+    return ((1 + f) ** 2 + 2) / 3 / np.exp2(f) - 1
+
+
+# first order with the Schraudolph bias: (1+f) 2^(-f-beta)
+def _q1_err(f):
+    return (1 + f) * np.exp2(-f - BETA) - 1
+
+
+# binary32 spacing of l near 2^30 is 128 units of 2^-23 in the base-2 exponent
+L_SLACK = 128 * 2.0 ** -23 * np.log(2) * 1.1
+
+
+@pytest.fixture(scope="module")
+def sweep_q2(oracle):
+    return _sweep(oracle, oracle.Q2)
+
+
+@pytest.fixture(scope="module")
+def sweep_q1(oracle):
+    return _sweep(oracle, oracle.Q1)
+
+
+@pytest.mark.slow
+def test_quake2_error_matches_eq6_extremes(sweep_q2):
+    lo, hi = _extremes(_q2_err)
+    assert abs(sweep_q2["emax"] - hi) <= L_SLACK
+    assert abs(sweep_q2["emin"] - lo) <= L_SLACK
+    # the paper's stated maximum deviation, 0.34 % (Sec. III-B)
+    assert round(100 * max(abs(sweep_q2["emin"]), sweep_q2["emax"]), 2) == 0.34
+    assert sweep_q2["count"] > 2_200_000_000
+
+
+@pytest.mark.slow
+def test_quake1_error_within_quoted_bound(sweep_q1):
+    lo, hi = _extremes(_q1_err)
+    assert abs(lo - (2 ** -BETA - 1)) < 1e-9
+    assert abs(sweep_q1["emax"] - hi) <= L_SLACK
+    assert abs(sweep_q1["emin"] - lo) <= L_SLACK
+    assert max(abs(sweep_q1["emin"]), sweep_q1["emax"]) <= 0.043   # "about 4.3 %"
+
+
+@pytest.mark.slow
+def test_monotone_over_all_finite_inputs(sweep_q1, sweep_q2):
+    assert sweep_q1["viol"] == 0
+    assert sweep_q2["viol"] == 0
