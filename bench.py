@@ -1,0 +1,309 @@
+#!/usr/bin/env python3
+"""Benchmark of the QuAKE hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--mode quake2]
+
+A step is one launch of the operator over the whole workload (every step of
+the fused path: load + widen, (row max), affine map, clamp, convert, QuAKE2
+refinement, consumer, narrow + store). The default workload is the GELU of a
+BERT-base MLP activation, bf16 [4096, 3072]. Inputs are seeded synthetic data
+resident in HBM before the timed region; the timed launches rotate over
+enough input/output buffer pairs (>= 1 GiB) that the 256 MB Infinity Cache
+cannot serve them. Launch sequences are captured in a HIP graph (eager
+launches if capture is not possible) and timed with HIP events on the
+launching stream. The same kernel with the hardware exp2 (EXACT) and with
+first-order QuAKE is timed in the same process for the speedup.
+
+Prints ONE JSON line. The oracle (CPU, plain C) is timed on the host cores on
+the same workload as `cpu_baseline`.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0       # MI355X HBM3E, AMD published peak
+MODE_IDS = {"exact": 0, "quake1": 1, "quake2": 2}
+KERNEL_SOURCES = ["paper_2412_00408_amd/csrc/elementwise.hip",
+                  "paper_2412_00408_amd/csrc/softmax.hip",
+                  "paper_2412_00408_amd/csrc/quake_device.hpp"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--workload", default="gelu_bf16_4096x3072")
+    ap.add_argument("--mode", default="quake2", choices=sorted(MODE_IDS))
+    ap.add_argument("--launch", default="graph", choices=["graph", "eager"])
+    ap.add_argument("--only", action="store_true",
+                    help="time only --workload in --mode (for profiler passes)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="also run torch copies of MIB MiB (reference kernel for counters)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="CPU work (thread-seconds) spent timing the oracle")
+    return ap.parse_args()
+
+
+# ---------------------------------------------------------------------------
+# GPU side
+# ---------------------------------------------------------------------------
+
+def make_launcher(q, w, mode, xs, ys):
+    """Returns f(i) that launches the operator on buffer pair i (raw C ABI)."""
+    import torch
+    L = q.lib
+    dt = q.DTYPES[xs[0].dtype]
+    n = xs[0].numel()
+    stream = lambda: int(torch.cuda.current_stream().cuda_stream)  # noqa: E731
+    xp = [x.data_ptr() for x in xs]
+    yp = [y.data_ptr() for y in ys]
+    if w.op == "gelu":
+        def f(i):
+            return L.quake_gelu(xp[i], yp[i], n, dt, mode, stream())
+    elif w.op in ("sigmoid", "silu"):
+        silu = int(w.op == "silu")
+
+        def f(i):
+            return L.quake_sigmoid(xp[i], yp[i], n, dt, mode, silu, stream())
+    elif w.op == "softmax":
+        rows, cols = w.rows, w.cols
+
+        def f(i):
+            return L.quake_softmax(xp[i], yp[i], rows, cols, cols, cols, dt, mode, w.t, stream())
+    else:
+        raise KeyError(w.op)
+    return f
+
+
+def time_workload(q, w, mode, x_host, steps, warmup, launch_kind):
+    import torch
+    nbuf = min(64, max(2, math.ceil((1 << 30) / w.algo_bytes)))
+    xs, ys = [], []
+    x0 = x_host.to("cuda:0")
+    for _ in range(nbuf):
+        xs.append(x0.clone())
+        ys.append(torch.empty_like(x0))
+    del x0
+    f = make_launcher(q, w, mode, xs, ys)
+    for i in range(max(warmup, nbuf)):
+        rc = f(i % nbuf)
+        if rc != 0:
+            raise RuntimeError("launch failed: %s" % q.status_str(rc))
+    torch.cuda.synchronize()
+
+    kind = launch_kind
+    graph = None
+    if kind == "graph":
+        try:
+            s = torch.cuda.Stream()
+            s.wait_stream(torch.cuda.current_stream())
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.stream(s):
+                with torch.cuda.graph(graph, stream=s):
+                    for i in range(nbuf):
+                        rc = f(i)
+                        if rc != 0:
+                            raise RuntimeError(q.status_str(rc))
+            torch.cuda.synchronize()
+            graph.replay()
+            torch.cuda.synchronize()
+        except Exception as e:  # cooperative launches may not be capturable
+            graph = None
+            kind = "eager (graph capture failed: %s)" % str(e).splitlines()[0][:80]
+            torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    if graph is not None:
+        reps = max(1, steps // nbuf)
+        launches = reps * nbuf
+        graph.replay()
+        torch.cuda.synchronize()
+        start.record(stream)
+        for _ in range(reps):
+            graph.replay()
+        end.record(stream)
+    else:
+        launches = steps
+        start.record(stream)
+        for i in range(steps):
+            f(i % nbuf)
+        end.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / launches
+    out = ys[(launches - 1) % nbuf]
+    del xs
+    return ms, launches, nbuf, kind, out
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the oracle as it stands, on the host cores
+# ---------------------------------------------------------------------------
+
+def cpu_baseline(w, x_host, cpu_seconds):
+    import oracle
+    from paper_2412_00408_amd import synth
+    try:
+        threads = len(os.sched_getaffinity(0))
+    except AttributeError:
+        threads = os.cpu_count() or 1
+    threads = max(1, min(threads, 16))
+    xb = synth.bits(x_host)
+    mode = oracle.Q2
+
+    def run(th, sample):
+        xs = xb[:sample] if w.op != "softmax" else xb[:sample]
+        if w.op == "gelu":
+            oracle.gelu(xs, w.dt, mode, threads=th)
+        elif w.op in ("sigmoid", "silu"):
+            oracle.sigmoid(xs, w.dt, mode, silu=(w.op == "silu"), threads=th)
+        else:
+            oracle.softmax(xs.reshape(-1, w.cols), w.dt, mode, t=w.t, threads=th)
+
+    # size the sample so one pass is ~0.5 s of CPU work on one thread
+    unit = w.cols if w.op == "softmax" else 1
+    total_units = w.numel // unit
+    probe = max(1, min(total_units, (1 << 20) // unit))
+    t0 = time.perf_counter()
+    run(1, probe * unit if w.op != "softmax" else probe)
+    per_unit = (time.perf_counter() - t0) / probe
+    sample_units = int(min(total_units, max(1, 0.5 * threads / max(per_unit, 1e-12))))
+    sample = sample_units * unit if w.op != "softmax" else sample_units
+    elems = sample_units * unit
+    reps, wall = 0, 0.0
+    while wall * threads < cpu_seconds and reps < 1000:
+        t0 = time.perf_counter()
+        run(threads, sample)
+        wall += time.perf_counter() - t0
+        reps += 1
+    gbps = (2 * synth.ELEM_BYTES[w.dt] * elems * reps) / wall / 1e9
+    # single thread, as the paper's protocol (one pass)
+    t0 = time.perf_counter()
+    run(1, sample)
+    one = (2 * synth.ELEM_BYTES[w.dt] * elems) / (time.perf_counter() - t0) / 1e9
+    return {
+        "value": round(gbps, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
+        "sample": "%d of %d elements of %s, quake2, %d passes over %.1f s wall" % (
+            elems, w.numel, w.name, reps, wall),
+        "single_thread_value": round(one, 3),
+    }
+
+
+def traffic_for(name, hash_now):
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None, None
+    e = t.get(name)
+    if not e or e.get("source_hash") != hash_now:
+        return None, e
+    return e.get("bytes_per_launch"), e
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print("bench.py measures one GPU only: this build's hot path runs on a single MI355X and "
+              "has no multi-GPU mode (asked for --gpus %d)" % a.gpus, file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2412_00408_amd import quake as q, synth
+
+    assert torch.cuda.is_available(), "bench.py needs cuda:0"
+    w = synth.WORKLOADS[a.workload]
+    x_host = w.make()
+    if a.calibrate_copy:
+        nb = a.calibrate_copy << 20
+        src = torch.empty(nb // 4, dtype=torch.float32, device="cuda:0").fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+
+    modes = [a.mode] if a.only else ["exact", "quake1", "quake2"]
+    res = {}
+    for m in modes:
+        ms, launches, nbuf, kind, _ = time_workload(q, w, MODE_IDS[m], x_host, a.steps, a.warmup,
+                                                    a.launch)
+        res[m] = dict(ms=ms, gbps=w.algo_bytes / (ms * 1e-3) / 1e9, launches=launches, nbuf=nbuf,
+                      launch=kind)
+    head = res[a.mode]
+    hnow = source_hash()
+    tb, tentry = traffic_for(w.name + ":" + a.mode, hnow)
+    line = {
+        "metric": "GB/s of algorithmic HBM traffic (input read once + output written once) and "
+                  "fraction of MI355X peak HBM bandwidth; speedup vs the exact-exp kernel",
+        "value": round(head["gbps"], 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": head["launches"],
+        "warmup": a.warmup,
+        "ms_per_step": head["ms"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded, %s)" % w.name,
+        "config": {"workload": w.name, "op": w.op, "io_dtype": w.dt, "shape": list(w.shape),
+                   "mode": a.mode, "elements": w.numel, "algo_bytes": w.algo_bytes,
+                   "launch": head["launch"], "rotating_buffer_pairs": head["nbuf"]},
+        "roofline": {"bound": "hbm", "achieved": round(head["gbps"], 2), "peak": PEAK_HBM_GBPS,
+                     "unit": "GB/s", "frac": round(head["gbps"] / PEAK_HBM_GBPS, 4),
+                     "traffic": tb},
+        "modes": {m: {"ms_per_launch": r["ms"], "gbps": round(r["gbps"], 2),
+                      "elements_per_s": w.numel / (r["ms"] * 1e-3)} for m, r in res.items()},
+    }
+    if "exact" in res:
+        line["speedup_vs_exact"] = {m: round(res["exact"]["ms"] / r["ms"], 4)
+                                    for m, r in res.items() if m != "exact"}
+    if not a.no_cpu_baseline and not a.only:
+        line["cpu_baseline"] = cpu_baseline(w, x_host, a.cpu_seconds)
+    if not a.no_secondary and not a.only:
+        sec = {}
+        for name, w2 in synth.WORKLOADS.items():
+            if name == w.name:
+                continue
+            xh = w2.make()
+            r2 = {}
+            for m in ("exact", "quake1", "quake2"):
+                ms, launches, nbuf, kind, _ = time_workload(q, w2, MODE_IDS[m], xh,
+                                                            min(a.steps, 1000), a.warmup, a.launch)
+                r2[m] = (ms, kind)
+            ms2 = r2["quake2"][0]
+            gb = w2.algo_bytes / (ms2 * 1e-3) / 1e9
+            sec[name] = {"quake2_ms": ms2, "quake2_gbps": round(gb, 2),
+                         "frac_of_peak": round(gb / PEAK_HBM_GBPS, 4),
+                         "speedup_vs_exact": round(r2["exact"][0] / ms2, 4),
+                         "quake1_speedup_vs_exact": round(r2["exact"][0] / r2["quake1"][0], 4),
+                         "launch": r2["quake2"][1]}
+            del xh
+        line["secondary"] = sec
+    line["kernel_source_hash"] = hnow
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,203 @@
+// quake_device.hpp — device-side building blocks of libquake (gfx950 / CDNA4).
+//
+// The per-element arithmetic of QuAKE (arXiv:2412.00408):
+//   Sec. III-A, Eq. 5   l = c0*x + c1, one v_fma_f32
+//   (clamp)             l = med3(l, 0, 255*2^23), one v_med3_f32
+//   Eq. 3               z = convert_to_int(l), one v_cvt_i32_f32 (truncating)
+//   Eq. 2 (QuAKE)       result = bits of z
+//   Alg. 1 (QuAKE2)     a_m = (z & 0x007FFFFF) | 0x3F800000   (v_and_or_b32)
+//                       y_m = fma(a_m, a_m, 2) * fl(1/3)      (Eq. 6, a0=1/3, a2=2/3)
+//                       result = (z & 0xFF800000) + bits(y_m) - 0x3F800000 (v_and + v_add3)
+// plus 16-byte vector I/O for binary32 / binary16 / bfloat16 and the 64-lane
+// DPP reductions used by the softmax kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace qk {
+
+enum Mode : int { EXACT = 0, Q1 = 1, Q2 = 2 };
+enum Dt : int { F32 = 0, F16 = 1, BF16 = 2 };
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Clamp bound of l: biased exponent 255, mantissa 0 (the bits of +inf).
+constexpr float kLHi = 2139095040.0f;                 // 255 * 2^23, exact
+constexpr float kK127 = 1065353216.0f;                // 127 * 2^23, exact
+constexpr float kThird = (float)(1.0 / 3.0);          // fl32(1/3)
+constexpr uint32_t kMantMask = 0x007FFFFFu;           // Alg. 1: keep mantissa
+constexpr uint32_t kSignExpMask = 0xFF800000u;        // Alg. 1: keep sign + exponent
+constexpr uint32_t kExpB = 0x3F800000u;               // Alg. 1: exponent field := B
+
+__device__ __forceinline__ uint32_t umin32(uint32_t a, uint32_t b) { return a < b ? a : b; }
+
+__device__ __forceinline__ float as_f(uint32_t u) { return __builtin_bit_cast(float, u); }
+__device__ __forceinline__ uint32_t as_u(float f) { return __builtin_bit_cast(uint32_t, f); }
+
+// QuAKE / QuAKE2 of an already affine-mapped argument l (Eq. 5 applied).
+template <int MODE>
+__device__ __forceinline__ float quake_of_l(float l) {
+  l = __builtin_amdgcn_fmed3f(l, 0.0f, kLHi);
+  const uint32_t z = (uint32_t)(int32_t)l;
+  if constexpr (MODE == Q1) {
+    return as_f(z);
+  } else {
+    const float am = as_f((z & kMantMask) | kExpB);
+    const float ym = __builtin_fmaf(am, am, 2.0f) * kThird;
+    return as_f((z & kSignExpMask) + as_u(ym) - kExpB);
+  }
+}
+
+// e^(p x + q) with c0, c1 folded on the host (Eq. 5). EXACT: the same fused
+// binary32 argument in base 2, exponentiated by the hardware v_exp_f32.
+template <int MODE>
+__device__ __forceinline__ float qexp(float x, float c0, float c1) {
+  const float l = __builtin_fmaf(x, c0, c1);
+  if constexpr (MODE == EXACT) {
+    return __builtin_amdgcn_exp2f(l);
+  } else {
+    return quake_of_l<MODE>(l);
+  }
+}
+
+// num / (1 + e) with one v_rcp_f32. Both operands are scaled by 1/4 (exact
+// in binary32) so that the reciprocal of 1 + e stays a normal number for every
+// finite e (v_rcp_f32 flushes subnormal results): (num/4) * rcp((1 + e)/4),
+// where (1 + e)/4 = fma(e, 1/4, 1/4) is exactly the rounded 1 + e scaled.
+__device__ __forceinline__ float div_one_plus(float num, float e) {
+  return (num * 0.25f) * __builtin_amdgcn_rcpf(__builtin_fmaf(e, 0.25f, 0.25f));
+}
+
+// ---------------------------------------------------------------------------
+// Element formats. A 16-byte vector holds kV<DT> elements.
+// ---------------------------------------------------------------------------
+template <int DT>
+constexpr int kV = (DT == F32) ? 4 : 8;
+template <int DT>
+constexpr int kEsz = (DT == F32) ? 4 : 2;
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return as_f(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return as_f(w & 0xFFFF0000u); }
+__device__ __forceinline__ float f16_lo(uint32_t w) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)(w & 0xFFFFu));
+}
+__device__ __forceinline__ float f16_hi(uint32_t w) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)(w >> 16));
+}
+
+// Round-to-nearest-even narrowing (v_cvt_pk_bf16_f32 / v_cvt_f16_f32).
+__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
+  const uint32_t lo = __builtin_bit_cast(uint16_t, (__bf16)a);
+  const uint32_t hi = __builtin_bit_cast(uint16_t, (__bf16)b);
+  return lo | (hi << 16);
+}
+__device__ __forceinline__ uint32_t pack_f16(float a, float b) {
+  const uint32_t lo = __builtin_bit_cast(uint16_t, (_Float16)a);
+  const uint32_t hi = __builtin_bit_cast(uint16_t, (_Float16)b);
+  return lo | (hi << 16);
+}
+
+template <int DT>
+__device__ __forceinline__ void unpack(const u32x4 v, float* f) {
+  if constexpr (DT == F32) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) f[k] = as_f(v[k]);
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      f[2 * k] = (DT == BF16) ? bf16_lo(v[k]) : f16_lo(v[k]);
+      f[2 * k + 1] = (DT == BF16) ? bf16_hi(v[k]) : f16_hi(v[k]);
+    }
+  }
+}
+
+template <int DT>
+__device__ __forceinline__ u32x4 pack(const float* f) {
+  u32x4 v;
+  if constexpr (DT == F32) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = as_u(f[k]);
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      v[k] = (DT == BF16) ? pack_bf16(f[2 * k], f[2 * k + 1]) : pack_f16(f[2 * k], f[2 * k + 1]);
+  }
+  return v;
+}
+
+template <int DT>
+__device__ __forceinline__ float load1(const void* p, int64_t i) {
+  if constexpr (DT == F32) {
+    return static_cast<const float*>(p)[i];
+  } else {
+    const uint16_t h = static_cast<const uint16_t*>(p)[i];
+    return (DT == BF16) ? as_f((uint32_t)h << 16) : (float)__builtin_bit_cast(_Float16, h);
+  }
+}
+
+template <int DT>
+__device__ __forceinline__ void store1(void* p, int64_t i, float v) {
+  if constexpr (DT == F32) {
+    static_cast<float*>(p)[i] = v;
+  } else if constexpr (DT == BF16) {
+    static_cast<uint16_t*>(p)[i] = __builtin_bit_cast(uint16_t, (__bf16)v);
+  } else {
+    static_cast<uint16_t*>(p)[i] = __builtin_bit_cast(uint16_t, (_Float16)v);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 64-lane reductions. Four DPP steps make every lane of a 16-lane row hold the
+// row's result (xor 1, xor 2 via quad_perm; xor 4 via row_half_mirror; xor 8
+// via row_mirror), then the four rows are combined from lanes 0, 16, 32, 48
+// with v_readlane. Every lane returns the same value; the combination order is
+// fixed, so the result is deterministic. All 64 lanes must be active.
+// ---------------------------------------------------------------------------
+constexpr int kDppXor1 = 0xB1;          // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;          // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;   // row_half_mirror
+constexpr int kDppMirror = 0x140;       // row_mirror
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return as_f((uint32_t)__builtin_amdgcn_update_dpp(0, (int)as_u(v), CTRL, 0xF, 0xF, false));
+}
+
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, CTRL, 0xF, 0xF, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), CTRL, 0xF, 0xF, false);
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+__device__ __forceinline__ float readlane_f32(float v, int lane) {
+  return as_f((uint32_t)__builtin_amdgcn_readlane((int)as_u(v), lane));
+}
+
+__device__ __forceinline__ double readlane_f64(double v, int lane) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), lane);
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+  v = fmaxf(v, dpp_f32<kDppXor1>(v));
+  v = fmaxf(v, dpp_f32<kDppXor2>(v));
+  v = fmaxf(v, dpp_f32<kDppHalfMirror>(v));
+  v = fmaxf(v, dpp_f32<kDppMirror>(v));
+  return fmaxf(fmaxf(readlane_f32(v, 0), readlane_f32(v, 16)),
+               fmaxf(readlane_f32(v, 32), readlane_f32(v, 48)));
+}
+
+__device__ __forceinline__ double wave_sum(double v) {
+  v += dpp_f64<kDppXor1>(v);
+  v += dpp_f64<kDppXor2>(v);
+  v += dpp_f64<kDppHalfMirror>(v);
+  v += dpp_f64<kDppMirror>(v);
+  return (readlane_f64(v, 0) + readlane_f64(v, 16)) + (readlane_f64(v, 32) + readlane_f64(v, 48));
+}
+
+}  // namespace qk

@@ -1,0 +1,138 @@
+"""ctypes binding of libquake (include/quake.h) — argument marshalling only.
+
+Every function takes CUDA (HIP) torch tensors, passes their device pointers,
+sizes and torch's current stream to the C ABI of the same name, and raises
+`QuakeError` on a non-OK status. No arithmetic happens here, and there is no
+fallback: importing this module without a built libquake.so raises.
+
+Build the library with ``python -m paper_2412_00408_amd.build``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libquake.so")
+
+EXACT, QUAKE_1, QUAKE_2 = 0, 1, 2
+MODES = {"exact": EXACT, "quake1": QUAKE_1, "quake2": QUAKE_2, EXACT: EXACT, QUAKE_1: QUAKE_1,
+         QUAKE_2: QUAKE_2}
+DTYPES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
+OK, EINVAL, EDTYPE, EMODE, EHIP = 0, 1, 2, 3, 4
+
+
+class QuakeError(RuntimeError):
+    def __init__(self, fn: str, code: int):
+        super().__init__("%s failed: %s" % (fn, status_str(code)))
+        self.code = code
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError("libquake.so is not built (%s); run python -m paper_2412_00408_amd.build"
+                          % _LIB_PATH)
+    L = ctypes.CDLL(_LIB_PATH)
+    vp, i64, ci, cf = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float
+    L.quake_exp.argtypes = [vp, vp, i64, ci, ci, cf, cf, vp]
+    L.quake_softmax.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp]
+    L.quake_gelu.argtypes = [vp, vp, i64, ci, ci, vp]
+    L.quake_sigmoid.argtypes = [vp, vp, i64, ci, ci, ci, vp]
+    for f in (L.quake_exp, L.quake_softmax, L.quake_gelu, L.quake_sigmoid):
+        f.restype = ci
+    L.quake_status_str.argtypes = [ci]
+    L.quake_status_str.restype = ctypes.c_char_p
+    L.quake_abi_version.argtypes = []
+    L.quake_abi_version.restype = ci
+    return L
+
+
+lib = _load()
+
+
+def status_str(code: int) -> str:
+    return lib.quake_status_str(code).decode()
+
+
+def abi_version() -> int:
+    return lib.quake_abi_version()
+
+
+def _stream(t: torch.Tensor, stream) -> int:
+    if stream is not None:
+        return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+    return int(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _check_io(x: torch.Tensor, y: torch.Tensor | None, contiguous=True) -> torch.Tensor:
+    if not x.is_cuda:
+        raise ValueError("libquake takes device tensors")
+    if x.dtype not in DTYPES:
+        raise TypeError("libquake takes float32, float16 or bfloat16 tensors, got %s" % x.dtype)
+    if contiguous and not x.is_contiguous():
+        raise ValueError("input must be contiguous")
+    if y is None:
+        y = torch.empty_like(x, memory_format=torch.contiguous_format)
+    if y.dtype != x.dtype or y.device != x.device or y.shape != x.shape:
+        raise ValueError("output must match the input's dtype, device and shape")
+    if contiguous and not y.is_contiguous():
+        raise ValueError("output must be contiguous")
+    return y
+
+
+def _raise(fn, rc):
+    if rc != OK:
+        raise QuakeError(fn, rc)
+
+
+def quake_exp(x, y=None, mode=QUAKE_2, a=1.0, b=0.0, stream=None):
+    """y = e^(a x + b) elementwise."""
+    y = _check_io(x, y)
+    _raise("quake_exp", lib.quake_exp(x.data_ptr(), y.data_ptr(), x.numel(), DTYPES[x.dtype],
+                                      MODES[mode], a, b, _stream(x, stream)))
+    return y
+
+
+def quake_gelu(x, y=None, mode=QUAKE_2, stream=None):
+    """tanh-form GELU through Eq. 7."""
+    y = _check_io(x, y)
+    _raise("quake_gelu", lib.quake_gelu(x.data_ptr(), y.data_ptr(), x.numel(), DTYPES[x.dtype],
+                                        MODES[mode], _stream(x, stream)))
+    return y
+
+
+def quake_sigmoid(x, y=None, mode=QUAKE_2, silu=False, stream=None):
+    """Logistic sigma(x), or SiLU x*sigma(x) with silu=True."""
+    y = _check_io(x, y)
+    _raise("quake_sigmoid", lib.quake_sigmoid(x.data_ptr(), y.data_ptr(), x.numel(),
+                                              DTYPES[x.dtype], MODES[mode], int(bool(silu)),
+                                              _stream(x, stream)))
+    return y
+
+
+def _rows_view(t: torch.Tensor, what: str):
+    """(rows, cols, row stride) of a contiguous tensor, or of a 2-D tensor with a
+    contiguous last dimension (a slice of a wider matrix)."""
+    cols = t.shape[-1]
+    if t.is_contiguous():
+        return t.numel() // max(cols, 1) if cols else 0, cols, cols
+    if t.dim() == 2 and (t.stride(1) == 1 or cols == 1):
+        return t.shape[0], cols, t.stride(0)
+    raise ValueError("%s must be contiguous, or 2-D with a contiguous last dimension" % what)
+
+
+def quake_softmax(x, y=None, mode=QUAKE_2, t=1.0, stream=None):
+    """Softmax of t*x over the last dimension (Algorithm 2)."""
+    if x.dim() == 0:
+        raise ValueError("softmax needs at least one dimension")
+    _check_io(x, None, contiguous=False)
+    if y is None:
+        y = torch.empty_like(x, memory_format=torch.contiguous_format)
+    if y.dtype != x.dtype or y.device != x.device or y.shape != x.shape:
+        raise ValueError("output must match the input's dtype, device and shape")
+    rows, cols, ldx = _rows_view(x, "input")
+    _, _, ldy = _rows_view(y, "output")
+    _raise("quake_softmax", lib.quake_softmax(x.data_ptr(), y.data_ptr(), rows, cols, ldx, ldy,
+                                              DTYPES[x.dtype], MODES[mode], t, _stream(x, stream)))
+    return y

@@ -1,0 +1,107 @@
+"""Host-side checks of the C ABI (no GPU): the library loads, exports every
+function include/quake.h declares, and rejects bad arguments with the
+documented status before any HIP call is made."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "quake.h")
+LIB = os.path.join(ROOT, "paper_2412_00408_amd", "libquake.so")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^[A-Za-z_][\w\s\*]*?\b(quake_\w+)\s*\(", src, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def q():
+    if not os.path.exists(LIB):
+        pytest.fail("libquake.so is not built; run python -m paper_2412_00408_amd.build")
+    from paper_2412_00408_amd import quake
+    return quake
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for f in ["quake_exp", "quake_softmax", "quake_gelu", "quake_sigmoid", "quake_status_str",
+              "quake_abi_version"]:
+        assert f in names
+
+
+def test_library_exports_every_declared_symbol(q):
+    lib = ctypes.CDLL(LIB)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_version_and_status_strings(q):
+    src = open(HEADER).read()
+    ver = int(re.search(r"#define QUAKE_ABI_VERSION (\d+)", src).group(1))
+    assert q.abi_version() == ver
+    for code, tag in [(0, "QUAKE_OK"), (1, "QUAKE_EINVAL"), (2, "QUAKE_EDTYPE"), (3, "QUAKE_EMODE"),
+                      (4, "QUAKE_EHIP")]:
+        assert q.status_str(code).startswith(tag)
+    assert q.status_str(99).startswith("QUAKE_?")
+
+
+FAKE = 0x1000  # never dereferenced: every call below returns before touching memory
+
+
+def test_elementwise_validation(q):
+    L = q.lib
+    for fn, extra in [(L.quake_exp, (1.0, 0.0)), (L.quake_gelu, ()), (L.quake_sigmoid, (0,))]:
+        def call(x, y, n, dt, mode, ex=extra):
+            return fn(x, y, n, dt, mode, *ex, None)
+        assert call(FAKE, FAKE, 0, 0, 2) == q.OK            # empty: no launch
+        assert call(None, None, 0, 0, 2) == q.OK
+        assert call(FAKE, FAKE, -1, 0, 2) == q.EINVAL
+        assert call(None, FAKE, 10, 0, 2) == q.EINVAL
+        assert call(FAKE, None, 10, 0, 2) == q.EINVAL
+        assert call(FAKE, FAKE, 10, 3, 2) == q.EDTYPE
+        assert call(FAKE, FAKE, 10, -1, 2) == q.EDTYPE
+        assert call(FAKE, FAKE, 10, 0, 3) == q.EMODE
+        assert call(FAKE, FAKE, 0, 7, 2) == q.EDTYPE        # enums are checked first
+    nan, inf = float("nan"), float("inf")
+    assert L.quake_exp(FAKE, FAKE, 10, 0, 2, nan, 0.0, None) == q.EINVAL
+    assert L.quake_exp(FAKE, FAKE, 10, 0, 2, 1.0, inf, None) == q.EINVAL
+    assert L.quake_exp(FAKE, FAKE, 10, 0, 2, 3e38, 0.0, None) == q.EINVAL   # c0 overflows
+
+
+def test_softmax_validation(q):
+    f = q.lib.quake_softmax
+    ok = dict(x=FAKE, y=FAKE, rows=4, cols=8, ldx=8, ldy=8, dt=0, mode=2, t=1.0)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(a["x"], a["y"], a["rows"], a["cols"], a["ldx"], a["ldy"], a["dt"], a["mode"],
+                 a["t"], None)
+
+    assert call(rows=0) == q.OK
+    assert call(rows=0, x=None, y=None) == q.OK
+    assert call(rows=-1) == q.EINVAL
+    assert call(cols=-1) == q.EINVAL
+    assert call(cols=0) == q.EINVAL
+    assert call(ldx=7) == q.EINVAL
+    assert call(ldy=7) == q.EINVAL
+    assert call(x=None) == q.EINVAL
+    assert call(y=None) == q.EINVAL
+    assert call(t=0.0) == q.EINVAL
+    assert call(t=-1.0) == q.EINVAL
+    assert call(t=float("inf")) == q.EINVAL
+    assert call(t=float("nan")) == q.EINVAL
+    assert call(t=1e38) == q.EINVAL            # c0 = 2^23 t / ln2 overflows
+    assert call(dt=5) == q.EDTYPE
+    assert call(mode=9) == q.EMODE
+
+
+def test_binding_rejects_host_tensors(q):
+    import torch
+    with pytest.raises(ValueError):
+        q.quake_gelu(torch.zeros(4))
+    with pytest.raises(ValueError):
+        q.quake_softmax(torch.zeros(2, 4))

@@ -1,0 +1,193 @@
+"""GPU parity of quake_softmax (Algorithm 2) against the oracle, through the C
+ABI, on cuda:0: every kernel family (wave per row, workgroup per row, split
+rows, generic), ragged lengths, strides, masking, temperatures, modes and the
+three workload shapes."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from compare import check_bits
+from gpu_util import THREADS, assert_parity, host_bits, say
+from paper_2412_00408_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+MODES = [0, 1, 2]
+
+
+@pytest.fixture(scope="module")
+def q():
+    assert torch.cuda.is_available(), "GPU tests need cuda:0"
+    from paper_2412_00408_amd import quake
+    return quake
+
+
+def _run(q, x_cpu, mode, t, ld_pad=0, offset=0):
+    """Softmax of a [rows, cols] CPU tensor on the GPU and in the oracle.
+
+    ld_pad > 0 stores rows with stride cols + ld_pad (input and output);
+    offset > 0 shifts both base pointers by that many elements."""
+    dt = {torch.float32: "f32", torch.float16: "f16", torch.bfloat16: "bf16"}[x_cpu.dtype]
+    rows, cols = x_cpu.shape
+    ld = cols + ld_pad
+    xb = host_bits(x_cpu)
+    if ld_pad or offset:
+        big = torch.zeros(rows * ld + offset + 8, dtype=x_cpu.dtype)
+        view = big[offset:offset + rows * ld].view(rows, ld)[:, :cols]
+        view.copy_(x_cpu)
+        gx = big.to("cuda:0")
+        xg = gx[offset:offset + rows * ld].view(rows, ld)[:, :cols]
+        gy = torch.full_like(gx, 7.0)
+        yg = gy[offset:offset + rows * ld].view(rows, ld)[:, :cols]
+        q.quake_softmax(xg, yg, mode=mode, t=t)
+        torch.cuda.synchronize()
+        out = gy.cpu()
+        # padding around the rows must be untouched
+        pad = torch.ones_like(out, dtype=torch.bool)
+        pad[offset:offset + rows * ld].view(rows, ld)[:, :cols] = False
+        assert torch.all(out[pad] == 7.0)
+        g = host_bits(out[offset:offset + rows * ld].view(rows, ld)[:, :cols].contiguous())
+    else:
+        xg = x_cpu.to("cuda:0")
+        yg = q.quake_softmax(xg, mode=mode, t=t)
+        torch.cuda.synchronize()
+        g = host_bits(yg)
+    ref = oracle.softmax(xb.reshape(rows, cols), dt, mode, t=t, threads=THREADS)
+    return g, ref, dt
+
+
+COLS_F32 = [1, 2, 3, 4, 100, 128, 252, 256, 260, 512, 1000, 1024, 2048, 4096, 8188, 8192, 8196,
+            10000, 65536, 128256, 200000]
+COLS_16 = [1, 8, 24, 512, 1000, 1024, 2048, 4096, 8192, 16384, 16392, 32768, 128256]
+
+
+@pytest.mark.parametrize("cols", COLS_F32)
+@pytest.mark.parametrize("mode", MODES)
+def test_lengths_f32(q, cols, mode):
+    rows = 5 if cols >= 65536 else 37
+    x = synth.normal((rows, cols), 3.0, "f32", 200 + cols % 97)
+    say("softmax f32", rows, cols, mode)
+    g, r, dt = _run(q, x, mode, 1.0)
+    assert_parity(g, r, dt, "op", "softmax f32 %dx%d mode %d" % (rows, cols, mode))
+
+
+@pytest.mark.parametrize("cols", COLS_16)
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+@pytest.mark.parametrize("mode", MODES)
+def test_lengths_16bit(q, cols, dt, mode):
+    rows = 5 if cols >= 32768 else 29
+    x = synth.normal((rows, cols), 2.0, dt, 300 + cols % 89)
+    say("softmax", dt, rows, cols, mode)
+    g, r, d = _run(q, x, mode, 0.7)
+    assert_parity(g, r, d, "op", "softmax %s %dx%d mode %d" % (dt, rows, cols, mode))
+
+
+@pytest.mark.parametrize("cols", [128, 512, 3000, 8192, 50000])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_strides_and_misalignment(q, cols, dt):
+    x = synth.normal((9, cols), 2.0, dt, 400)
+    for pad, off in [(8, 0), (3, 0), (0, 1), (5, 3)]:
+        say("softmax strided", dt, cols, pad, off)
+        g, r, d = _run(q, x, 2, 1.0, ld_pad=pad, offset=off)
+        assert_parity(g, r, d, "op", "softmax %s cols %d pad %d off %d" % (dt, cols, pad, off))
+
+
+@pytest.mark.parametrize("cols", [64, 512, 4096, 128256])
+@pytest.mark.parametrize("mode", MODES)
+def test_masked_rows(q, cols, mode):
+    r = np.random.default_rng(7)
+    v = r.standard_normal((12, cols)).astype(np.float32) * 3
+    v[r.random((12, cols)) < 0.7] = -np.inf
+    v[3] = -np.inf                       # fully masked row -> zeros
+    v[5, :] = -np.inf
+    v[5, cols - 1] = 1.5                 # only the last entry is live -> one-hot
+    for dt in ("f32", "bf16"):
+        x = synth.to_format(v, dt)
+        say("softmax masked", dt, cols, mode)
+        g, ref, d = _run(q, x, mode, 1.0)
+        assert_parity(g, ref, d, "op", "masked %s cols %d mode %d" % (dt, cols, mode))
+        gv = oracle.decode(g.reshape(-1), d).reshape(12, cols)
+        assert np.all(gv[3] == 0.0)
+        assert abs(float(gv[5, cols - 1]) - 1.0) <= 2.0 ** -23 and np.all(gv[5, :-1] == 0.0)
+
+
+@pytest.mark.parametrize("t", [0.125, 0.5, 1.0, 3.0, 20.0])
+@pytest.mark.parametrize("cols", [512, 128256])
+def test_temperatures(q, t, cols):
+    x = synth.normal((6, cols), 2.0, "f32", 500)
+    for mode in MODES:
+        say("softmax t", t, cols, mode)
+        g, r, d = _run(q, x, mode, t)
+        assert_parity(g, r, d, "op", "t %g cols %d mode %d" % (t, cols, mode))
+
+
+def test_many_rows_split_path_multiple_launches(q):
+    # 600 rows of 100000 fp32: more row chunks than fit co-resident at once
+    x = synth.normal((600, 100000), 3.0, "f32", 600)
+    say("softmax split 600x100000")
+    g, r, d = _run(q, x, 2, 1.0)
+    assert_parity(g, r, d, "op", "split 600x100000")
+
+
+def test_inplace_and_determinism(q):
+    for cols in (512, 4096, 128256, 1001):
+        x = synth.normal((7, cols), 3.0, "bf16", 700).to("cuda:0")
+        a = q.quake_softmax(x, mode=2)
+        b = q.quake_softmax(x, mode=2)
+        z = x.clone()
+        q.quake_softmax(z, z, mode=2)
+        torch.cuda.synchronize()
+        say("softmax inplace/determinism", cols)
+        assert check_bits(host_bits(a), host_bits(b)) is None
+        assert check_bits(host_bits(a), host_bits(z)) is None
+
+
+def test_split_path_on_two_streams(q):
+    x = synth.normal((64, 128256), 3.0, "f32", 800).to("cuda:0")
+    ref = q.quake_softmax(x, mode=2)
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    s1.wait_stream(torch.cuda.current_stream())
+    s2.wait_stream(torch.cuda.current_stream())
+    outs = []
+    for s in (s1, s2, s1, s2):
+        with torch.cuda.stream(s):
+            outs.append(q.quake_softmax(x, mode=2))
+    torch.cuda.synchronize()
+    for o in outs:
+        assert check_bits(host_bits(o), host_bits(ref)) is None
+
+
+# ---------------------------------------------------------------- workloads
+
+@pytest.mark.parametrize("mode", MODES)
+def test_workload_softmax_f32_64x128(q, mode):
+    w = synth.WORKLOADS["softmax_f32_64x128"]
+    say(w.name, mode)
+    g, r, d = _run(q, w.make(), mode, w.t)
+    assert_parity(g, r, d, "op", "%s mode %d" % (w.name, mode))
+    s = oracle.decode(g, "f32").reshape(w.rows, w.cols).astype(np.float64).sum(axis=1)
+    assert np.all(np.abs(s - 1) < 1e-5)
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_workload_attn_softmax_bf16_causal(q, mode):
+    w = synth.WORKLOADS["attn_softmax_bf16_causal"]
+    say(w.name, mode)
+    x = w.make()
+    g, r, d = _run(q, x, mode, w.t)
+    assert_parity(g, r, d, "op", "%s mode %d" % (w.name, mode))
+    # masked region is exactly zero
+    gv = g.reshape(w.rows, w.cols)
+    i = (np.arange(w.rows) % w.cols)[:, None]
+    j = np.arange(w.cols)[None, :]
+    assert np.all(gv[np.broadcast_to(j > i, gv.shape)] == 0)
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_workload_lmhead_softmax_f32_64x128256(q, mode):
+    w = synth.WORKLOADS["lmhead_softmax_f32_64x128256"]
+    say(w.name, mode)
+    g, r, d = _run(q, w.make(), mode, w.t)
+    assert_parity(g, r, d, "op", "%s mode %d" % (w.name, mode))
