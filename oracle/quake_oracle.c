@@ -113,6 +113,13 @@ static float quake_one(float x, float c0, float c1, int order) {
   return u2f(yi);
 }
 
+/*
+ * The exact exponential of the comparison (EXACT) operators: 2^s correctly
+ * rounded to binary32, the format the paper computes in (Sec. II-A), so it
+ * overflows to +inf like expf once 2^s exceeds the largest binary32 value.
+ */
+static float exp2_binary32(float s) { return (float)exp2((double)s); }
+
 /* ------------------------------------------------------------------------ */
 /* Format conversion (I/O only; the method computes in binary32).           */
 /* ------------------------------------------------------------------------ */
@@ -244,7 +251,7 @@ int qo_sigmoid(const void* x, void* y, int64_t n, int dt, int mode, int silu) {
   float c0e = (float)(-1.0 / LN2);
   for (int64_t i = 0; i < n; ++i) {
     float xv = load_el(x, i, dt);
-    double e = (mode == QO_EXACT) ? exp2((double)fmaf(xv, c0e, 0.0f))
+    double e = (mode == QO_EXACT) ? (double)exp2_binary32(fmaf(xv, c0e, 0.0f))
                                   : (double)quake_one(xv, c0, c1, mode);
     double num = silu ? (double)xv : 1.0;
     store_el(y, i, dt, num / (1.0 + e));
@@ -263,7 +270,7 @@ int qo_gelu(const void* x, void* y, int64_t n, int dt, int mode) {
     float xv = load_el(x, i, dt);
     float u = fmaf(xv, xv, A);      /* 1/0.044715 + x^2, one FMA */
     float w = xv * u;
-    double e = (mode == QO_EXACT) ? exp2((double)fmaf(w, c0e, 0.0f))
+    double e = (mode == QO_EXACT) ? (double)exp2_binary32(fmaf(w, c0e, 0.0f))
                                   : (double)quake_one(w, c0, c1, mode);
     store_el(y, i, dt, (double)xv / (1.0 + e));
   }
@@ -294,7 +301,7 @@ int qo_softmax(const void* x, void* y, int64_t rows, int64_t cols, int64_t ldx,
     if (mode == QO_EXACT) {
       float c1e = fmaf(-c0, m, 0.0f);
       for (int64_t j = 0; j < cols; ++j) {
-        tmp[j] = exp2((double)fmaf(load_el(x, bx + j, dt), c0, c1e));
+        tmp[j] = (double)exp2_binary32(fmaf(load_el(x, bx + j, dt), c0, c1e));
         sum += tmp[j];
       }
     } else {

@@ -53,3 +53,12 @@ def test_check_dispatch():
     g.view(np.uint32)[0] += 3
     assert check(g, r, "f32", "exp_exact") is not None
     assert check(g, r, "f32", "op") is None      # 3 ulp of 1.0 is inside 1e-6
+
+
+def test_bf16_subnormal_floor():
+    # bfloat16 subnormals (below 2^-126) may flush to zero; f16 has no such floor
+    r = np.array([0x001F, 0x0005, 0x807F], np.uint16)
+    g = np.zeros(3, np.uint16)
+    assert check_16(g, r, "bf16") is None
+    assert check_16(g, np.array([0x0081, 0x0005, 0x807F], np.uint16), "bf16") is not None
+    assert check_16(g, np.array([0x0003, 0, 0], np.uint16), "f16") is not None

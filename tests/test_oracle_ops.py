@@ -211,3 +211,15 @@ def test_folded_exp_equals_raw_quake(oracle):
     assert np.array_equal(oracle.sigmoid(x, "f32", 2),
                           (1.0 / (1.0 + oracle.quake(x, c["C0_NEG"], c["K127"], 2).astype(np.float64)))
                           .astype(np.float32))
+
+
+def test_exact_mode_exponential_is_binary32(oracle):
+    # reading: the comparison operators compute in single precision (Sec. II-A),
+    # so their exponential overflows to +inf once 2^s exceeds the binary32 range
+    # and the operator output is then exactly -0 / 0.
+    g = oracle.gelu(np.array([-10.4, -9.99], np.float32), "f32", 0)
+    assert g[0] == 0.0 and np.signbit(g[0])
+    assert g[1] < 0 and abs(float(g[1])) > 1e-37       # 2^125.6 is still finite
+    s = oracle.sigmoid(np.array([-89.0, -88.0], np.float32), "f32", 0, silu=True)
+    assert s[0] == 0.0 and np.signbit(s[0])
+    assert s[1] < 0
