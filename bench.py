@@ -118,6 +118,10 @@ def time_workload(q, w, mode, x_host, steps, warmup, launch_kind):
         try:
             s = torch.cuda.Stream()
             s.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(s):        # per-stream workspaces exist before capture
+                for i in range(nbuf):
+                    f(i)
+            s.synchronize()
             graph = torch.cuda.CUDAGraph()
             with torch.cuda.stream(s):
                 with torch.cuda.graph(graph, stream=s):

@@ -1,12 +1,14 @@
 // elementwise.hip — quake_exp, quake_gelu, quake_sigmoid (Logistic / SiLU).
 //
-// One streaming kernel per (format, operator, mode): every lane moves UNROLL
-// 16-byte vectors (4 binary32 or 8 binary16/bfloat16 elements each), all
-// loads issued before any arithmetic, with non-temporal loads and stores (the
-// data is touched once). A wave reads 1 KiB contiguous per load instruction.
-// Elements past the last whole vector are handled by the last workgroup's
-// first lanes with scalar accesses. Buffers that are not 16-byte aligned take
-// a scalar grid-stride kernel with the same per-element arithmetic.
+// Streaming kernels per (format, operator, mode) over 16-byte vectors (4
+// binary32 or 8 binary16/bfloat16 elements), with non-temporal loads and
+// stores (the data is touched once); a wave reads 1 KiB contiguous per load
+// instruction. Two launch shapes, chosen by size: a one-shot grid with one
+// vector per lane for large inputs, and a resident, software-pipelined
+// grid-stride loop for mid-size ones (where launch ramp and tail dominate).
+// Elements past the last whole vector are handled by one workgroup's first
+// lanes with scalar accesses. Buffers that are not 16-byte aligned take a
+// scalar grid-stride kernel with the same per-element arithmetic.
 //
 // Per-element arithmetic (Sec. III-A, III-B, III-D of arXiv:2412.00408):
 //   exp      y = QuAKEx(x; c0, c1)                     (Eq. 5, Alg. 1)
@@ -45,30 +47,70 @@ __device__ __forceinline__ float ew_op(float x, const EwParams& p) {
 
 constexpr int kEwBlock = 256;
 
-template <int DT, int OP, int MODE, int UNROLL>
-__global__ __launch_bounds__(kEwBlock) void ew_vec_kernel(const u32x4* __restrict__ x,
-                                                         u32x4* __restrict__ y, uint32_t nvec,
-                                                         uint32_t tail, EwParams p) {
+// Large inputs: one 16-byte vector per lane, one workgroup per 256 vectors.
+// Workgroups are retired and replaced continuously, which keeps the most
+// requests in flight once the grid is many times the resident capacity.
+template <int DT, int OP, int MODE>
+__global__ __launch_bounds__(kEwBlock) void ew_oneshot_kernel(const u32x4* __restrict__ x,
+                                                             u32x4* __restrict__ y, uint32_t nvec,
+                                                             uint32_t tail, EwParams p) {
   constexpr int V = kV<DT>;
-  const uint32_t base = blockIdx.x * (kEwBlock * UNROLL) + threadIdx.x;
-  u32x4 v[UNROLL];
+  const uint32_t i = blockIdx.x * kEwBlock + threadIdx.x;
+  if (i < nvec) {
+    const u32x4 v = __builtin_nontemporal_load(x + i);
+    float f[V];
+    unpack<DT>(v, f);
 #pragma unroll
-  for (int u = 0; u < UNROLL; ++u) {
-    const uint32_t i = base + u * kEwBlock;
-    if (i < nvec) v[u] = __builtin_nontemporal_load(x + i);
-  }
-#pragma unroll
-  for (int u = 0; u < UNROLL; ++u) {
-    const uint32_t i = base + u * kEwBlock;
-    if (i < nvec) {
-      float f[V];
-      unpack<DT>(v[u], f);
-#pragma unroll
-      for (int k = 0; k < V; ++k) f[k] = ew_op<OP, MODE>(f[k], p);
-      __builtin_nontemporal_store(pack<DT>(f), y + i);
-    }
+    for (int k = 0; k < V; ++k) f[k] = ew_op<OP, MODE>(f[k], p);
+    __builtin_nontemporal_store(pack<DT>(f), y + i);
   }
   if (tail && blockIdx.x == gridDim.x - 1 && threadIdx.x < tail) {
+    const int64_t e = (int64_t)nvec * V + threadIdx.x;
+    store1<DT>(y, e, ew_op<OP, MODE>(load1<DT>(x, e), p));
+  }
+}
+
+// Mid-size inputs: a resident grid (a few workgroups per CU) strides over the
+// vectors, two per lane per step, and issues the next step's loads before the
+// current step's arithmetic so every lane always has loads in flight.
+template <int DT, int OP, int MODE>
+__global__ __launch_bounds__(kEwBlock) void ew_pipe_kernel(const u32x4* __restrict__ x,
+                                                          u32x4* __restrict__ y, uint32_t nvec,
+                                                          uint32_t tail, EwParams p) {
+  constexpr int V = kV<DT>;
+  constexpr int U = 2;
+  const uint32_t step = gridDim.x * (kEwBlock * U);
+  uint32_t base = blockIdx.x * (kEwBlock * U) + threadIdx.x;
+  u32x4 cur[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const uint32_t i = base + u * kEwBlock;
+    if (i < nvec) cur[u] = __builtin_nontemporal_load(x + i);
+  }
+  while (base < nvec) {
+    const uint32_t nb = base + step;
+    u32x4 nxt[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t i = nb + u * kEwBlock;
+      if (i < nvec) nxt[u] = __builtin_nontemporal_load(x + i);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t i = base + u * kEwBlock;
+      if (i < nvec) {
+        float f[V];
+        unpack<DT>(cur[u], f);
+#pragma unroll
+        for (int k = 0; k < V; ++k) f[k] = ew_op<OP, MODE>(f[k], p);
+        __builtin_nontemporal_store(pack<DT>(f), y + i);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) cur[u] = nxt[u];
+    base = nb;
+  }
+  if (tail && blockIdx.x == 0 && threadIdx.x < tail) {
     const int64_t e = (int64_t)nvec * V + threadIdx.x;
     store1<DT>(y, e, ew_op<OP, MODE>(load1<DT>(x, e), p));
   }
@@ -82,15 +124,32 @@ __global__ __launch_bounds__(kEwBlock) void ew_scalar_kernel(const void* __restr
     store1<DT>(y, i, ew_op<OP, MODE>(load1<DT>(x, i), p));
 }
 
-constexpr int kEwUnroll = 2;
 // Elements per launch: a multiple of every vector width, below 2^31.
 constexpr int64_t kEwChunk = int64_t(1) << 30;
+// Resident workgroups per CU for the strided kernel.
+constexpr int kEwPipeBlocksPerCu = 8;
+// At or above this many vectors per CU the one-shot kernel is used.
+constexpr int64_t kEwOneShotVecPerCu = 64 * kEwBlock;
+
+static int device_cus() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+      cus = 256;
+    cached[dev] = cus;
+  }
+  return cached[dev];
+}
 
 template <int DT, int OP, int MODE>
 quake_status ew_launch(const void* x, void* y, int64_t n, const EwParams& p, hipStream_t s) {
   constexpr int V = kV<DT>;
   constexpr int64_t esz = kEsz<DT>;
   const bool vec = aligned16(x) && aligned16(y);
+  const int cus = device_cus();
   for (int64_t off = 0; off < n; off += kEwChunk) {
     const int64_t m = std::min(kEwChunk, n - off);
     const char* xc = static_cast<const char*>(x) + off * esz;
@@ -98,12 +157,19 @@ quake_status ew_launch(const void* x, void* y, int64_t n, const EwParams& p, hip
     if (vec) {
       const uint32_t nvec = (uint32_t)(m / V);
       const uint32_t tail = (uint32_t)(m % V);
-      const int64_t per_block = (int64_t)kEwBlock * kEwUnroll;
-      uint32_t grid = (uint32_t)((nvec + per_block - 1) / per_block);
-      if (grid == 0) grid = 1;
-      hipLaunchKernelGGL((ew_vec_kernel<DT, OP, MODE, kEwUnroll>), dim3(grid), dim3(kEwBlock), 0,
-                         s, reinterpret_cast<const u32x4*>(xc), reinterpret_cast<u32x4*>(yc),
-                         nvec, tail, p);
+      const u32x4* xv = reinterpret_cast<const u32x4*>(xc);
+      u32x4* yv = reinterpret_cast<u32x4*>(yc);
+      if ((int64_t)nvec >= kEwOneShotVecPerCu * cus) {
+        const uint32_t grid = (uint32_t)((nvec + kEwBlock - 1) / kEwBlock);
+        hipLaunchKernelGGL((ew_oneshot_kernel<DT, OP, MODE>), dim3(grid), dim3(kEwBlock), 0, s, xv,
+                           yv, nvec, tail, p);
+      } else {
+        const int64_t want = ((int64_t)nvec + 2 * kEwBlock - 1) / (2 * kEwBlock);
+        const uint32_t grid =
+            (uint32_t)std::max<int64_t>(1, std::min<int64_t>(want, (int64_t)kEwPipeBlocksPerCu * cus));
+        hipLaunchKernelGGL((ew_pipe_kernel<DT, OP, MODE>), dim3(grid), dim3(kEwBlock), 0, s, xv, yv,
+                           nvec, tail, p);
+      }
     } else {
       const int64_t want = (m + kEwBlock - 1) / kEwBlock;
       const uint32_t grid = (uint32_t)std::min<int64_t>(want, 65536);

@@ -7,7 +7,10 @@
 //   Eq. 2 (QuAKE)       result = bits of z
 //   Alg. 1 (QuAKE2)     a_m = (z & 0x007FFFFF) | 0x3F800000   (v_and_or_b32)
 //                       y_m = fma(a_m, a_m, 2) * fl(1/3)      (Eq. 6, a0=1/3, a2=2/3)
-//                       result = (z & 0xFF800000) + bits(y_m) - 0x3F800000 (v_and + v_add3)
+//                       result = (z & 0xFF800000) + bits(y_m) - 0x3F800000, which is
+//                       one v_bfi_b32: y_m lies in [1, 2), so bits(y_m) - 0x3F800000
+//                       is exactly y_m's mantissa field and the addition cannot
+//                       carry into z's sign/exponent field.
 // plus 16-byte vector I/O for binary32 / binary16 / bfloat16 and the 64-lane
 // DPP reductions used by the softmax kernels.
 #pragma once
@@ -45,7 +48,7 @@ __device__ __forceinline__ float quake_of_l(float l) {
   } else {
     const float am = as_f((z & kMantMask) | kExpB);
     const float ym = __builtin_fmaf(am, am, 2.0f) * kThird;
-    return as_f((z & kSignExpMask) + as_u(ym) - kExpB);
+    return as_f((z & kSignExpMask) | (as_u(ym) & kMantMask));
   }
 }
 
@@ -190,6 +193,14 @@ __device__ __forceinline__ float wave_max(float v) {
   v = fmaxf(v, dpp_f32<kDppMirror>(v));
   return fmaxf(fmaxf(readlane_f32(v, 0), readlane_f32(v, 16)),
                fmaxf(readlane_f32(v, 32), readlane_f32(v, 48)));
+}
+
+__device__ __forceinline__ float wave_sum_f32(float v) {
+  v += dpp_f32<kDppXor1>(v);
+  v += dpp_f32<kDppXor2>(v);
+  v += dpp_f32<kDppHalfMirror>(v);
+  v += dpp_f32<kDppMirror>(v);
+  return (readlane_f32(v, 0) + readlane_f32(v, 16)) + (readlane_f32(v, 32) + readlane_f32(v, 48));
 }
 
 __device__ __forceinline__ double wave_sum(double v) {

@@ -15,15 +15,16 @@
 //   sm_split<NV>          rows longer than a workgroup's registers: G
 //                         workgroups per row each hold one chunk in VGPRs and
 //                         exchange their chunk max, then their chunk sum,
-//                         through a small device workspace (two arrivals on a
-//                         per-row counter). The launch is cooperative, so all
-//                         workgroups are co-resident and every wait ends; each
-//                         wait is also bounded by a spin limit.
+//                         through sentinel slots of a small device workspace
+//                         (relaxed atomics, no fences). A launch never has more
+//                         workgroups than fit on the device at once, so every
+//                         wait ends; each wait is also bounded by a spin limit.
 //   sm_generic            any alignment / stride / length: one workgroup per
 //                         row, three passes (max, sum, normalise) with scalar
 //                         accesses; the re-reads are served by the caches.
-// Sums: fp32 within one 16-byte vector (at most 8 terms), then double across
-// vectors, lanes, waves and workgroups, in a fixed order.
+// Sums: fp32 within one 16-byte vector (at most 8 terms), then, in a fixed
+// order, double across vectors, lanes, waves and workgroups for binary32
+// outputs and fp32 for 16-bit outputs (double across split workgroups).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -37,6 +38,23 @@
 namespace qk {
 
 constexpr int kSmBlock = 256;
+
+// Row sums: binary32 outputs accumulate in double across vectors, lanes and
+// waves (the 1e-6 relative tolerance leaves no room for a long fp32 chain) and
+// divide in double; 16-bit outputs accumulate in fp32 (error below 2^-20
+// relative, far under half an ulp of the output) and take one v_rcp_f32.
+template <int DT>
+struct AccOf {
+  typedef float T;
+};
+template <>
+struct AccOf<F32> {
+  typedef double T;
+};
+__device__ __forceinline__ double wave_sum_acc(double v) { return wave_sum(v); }
+__device__ __forceinline__ float wave_sum_acc(float v) { return wave_sum_f32(v); }
+__device__ __forceinline__ float inv_total(double t) { return (float)(1.0 / t); }
+__device__ __forceinline__ float inv_total(float t) { return __builtin_amdgcn_rcpf(t); }
 
 // Per-row c1 of Algorithm 2: fma(-c0, m, 127*2^23) (EXACT: -c0*m in base 2).
 template <int MODE>
@@ -56,8 +74,9 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
   constexpr int V = kV<DT>;
   constexpr int LANES = 64 * WAVES;
   constexpr int ROWS_PER_BLOCK = kSmBlock / LANES;
+  using Acc = typename AccOf<DT>::T;
   __shared__ float s_max[4];
-  __shared__ double s_sum[4];
+  __shared__ Acc s_sum[4];
 
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
@@ -96,7 +115,7 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
   }
 
   const float c1 = row_c1<MODE>(c0, m);
-  double acc = 0.0;
+  Acc acc = 0;
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
     float part = 0.0f;
@@ -105,15 +124,15 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
       f[k][j] = qexp<MODE>(f[k][j], c0, c1);
       part += f[k][j];
     }
-    acc += (double)part;
+    acc += (Acc)part;
   }
-  double total = wave_sum(acc);
+  Acc total = wave_sum_acc(acc);
   if constexpr (WAVES > 1) {
     if (lane == 0) s_sum[wave] = total;
     __syncthreads();
     total = (s_sum[0] + s_sum[1]) + (s_sum[2] + s_sum[3]);
   }
-  const float r = (m == -INFINITY) ? 0.0f : (float)(1.0 / total);
+  const float r = (m == -INFINITY) ? 0.0f : inv_total(total);
 
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
@@ -128,28 +147,44 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
 
 // ---------------------------------------------------------------------------
 // Split rows: G workgroups per row, exchanging chunk max and chunk sum.
+//
+// Exchange without fences: every chunk owns one 32-bit slot for its max and
+// one 64-bit slot for its sum, both holding a sentinel between launches. A
+// workgroup publishes its value with a relaxed agent-scope atomic store and
+// polls the G slots of its row with relaxed agent-scope atomic loads until no
+// sentinel is left. The value is itself the atomic object, so no release /
+// acquire fence (and no L2 write-back or invalidate) is needed. After reading
+// both rounds each workgroup counts itself done; the last one of the row puts
+// the sentinels back, so the workspace is ready for the next launch (also on
+// graph replay). Launches use at most as many workgroups as can be resident
+// at once, so every polled value is eventually written; every wait is also
+// bounded by a spin limit and then flags an error instead of hanging.
 // ---------------------------------------------------------------------------
 struct SplitWs {
-  float* pmax;      // [slots]   chunk maxima, index rr * G + g
-  double* psum;     // [slots]   chunk sums
-  uint32_t* cnt;    // [slots]   per-row arrival counters (zero between launches)
-  uint32_t* err;    // [1]       set if a wait hit its spin limit
+  uint32_t* pmax;   // [kWsSlots]  chunk maxima (binary32 bits), index rr * G + g
+  uint64_t* psum;   // [kWsSlots]  chunk sums (binary64 bits)
+  uint32_t* done;   // [kWsSlots]  per-row count of finished workgroups
+  uint32_t* err;    // [1]         set if a wait hit its spin limit
 };
 
-constexpr uint32_t kWsSlots = 8192;          // max rows * G per launch
-constexpr uint32_t kSpinLimit = 1u << 20;    // about a second of polling; never reached when co-resident
-constexpr int kMaxG = kSmBlock;              // chunk exchange goes through one LDS slot per lane
+constexpr uint32_t kWsSlots = 8192;                 // max rows * G per launch
+constexpr uint32_t kSpinLimit = 1u << 20;           // about a second of polling
+constexpr int kMaxG = kSmBlock;                     // one polling lane per chunk
+constexpr uint32_t kSent32 = 0xFFFFFFFFu;           // a NaN never published
+constexpr uint64_t kSent64 = 0xFFFFFFFFFFFFFFFFull; // a NaN never published
 
-__device__ __forceinline__ void arrive_and_wait(uint32_t* cnt, uint32_t target, uint32_t* err) {
-  __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+template <typename T>
+__device__ __forceinline__ T poll_slot(T* slot, T sentinel, T fallback, uint32_t* err) {
+  T v;
   uint32_t spins = 0;
-  while (__hip_atomic_load(cnt, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < target) {
+  while ((v = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) == sentinel) {
     __builtin_amdgcn_s_sleep(1);
     if (++spins == kSpinLimit) {
       __hip_atomic_store(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      break;
+      return fallback;
     }
   }
+  return v;
 }
 
 template <int DT, int MODE, int NV>
@@ -168,7 +203,8 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
   const int lane = threadIdx.x & 63;
   const uint32_t rr = blockIdx.x / G;
   const uint32_t g = blockIdx.x - rr * G;
-  const uint32_t slot = rr * G + g;
+  uint32_t* pm = ws.pmax + rr * G;
+  uint64_t* ps = ws.psum + rr * G;
 
   const u32x4* xr = reinterpret_cast<const u32x4*>(x + (int64_t)rr * ldx_b);
   u32x4* yr = reinterpret_cast<u32x4*>(y + (int64_t)rr * ldy_b);
@@ -190,22 +226,22 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
       lmax = fmaxf(lmax, f[k][j]);
     }
   }
+
+  // round 1: chunk maxima
   float m = wave_max(lmax);
   if (lane == 0) s_max[wave] = m;
   __syncthreads();
   if (threadIdx.x == 0) {
     m = fmaxf(fmaxf(s_max[0], s_max[1]), fmaxf(s_max[2], s_max[3]));
-    __hip_atomic_store(&ws.pmax[slot], m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    arrive_and_wait(&ws.cnt[rr], G, ws.err);
+    const uint32_t mb = (m != m) ? as_u(-INFINITY) : as_u(m);
+    __hip_atomic_store(pm + g, mb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  __syncthreads();
-  if (threadIdx.x < G)
-    s_pmax[threadIdx.x] =
-        __hip_atomic_load(&ws.pmax[rr * G + threadIdx.x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (threadIdx.x < G) s_pmax[threadIdx.x] = as_f(poll_slot<uint32_t>(pm + threadIdx.x, kSent32, as_u(-INFINITY), ws.err));
   __syncthreads();
   m = -INFINITY;
   for (uint32_t q = 0; q < G; ++q) m = fmaxf(m, s_pmax[q]);
 
+  // round 2: chunk sums with the row's final max
   const float c1 = row_c1<MODE>(c0, m);
   double acc = 0.0;
 #pragma unroll
@@ -223,23 +259,23 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
   __syncthreads();
   if (threadIdx.x == 0) {
     total = (s_sum[0] + s_sum[1]) + (s_sum[2] + s_sum[3]);
-    __hip_atomic_store(reinterpret_cast<uint64_t*>(&ws.psum[slot]),
-                       __builtin_bit_cast(uint64_t, total), __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
-    arrive_and_wait(&ws.cnt[rr], 2 * G, ws.err);
+    const uint64_t tb = (total != total) ? 0x7FF8000000000000ull : __builtin_bit_cast(uint64_t, total);
+    __hip_atomic_store(ps + g, tb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  __syncthreads();
   if (threadIdx.x < G)
-    s_psum[threadIdx.x] = __builtin_bit_cast(
-        double, __hip_atomic_load(reinterpret_cast<uint64_t*>(&ws.psum[rr * G + threadIdx.x]),
-                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+    s_psum[threadIdx.x] = __builtin_bit_cast(double, poll_slot<uint64_t>(ps + threadIdx.x, kSent64, 0, ws.err));
   __syncthreads();
   if (threadIdx.x == 0) {
-    // third arrival: this workgroup has finished reading the workspace; the
-    // last one of the row returns the counter to zero for the next launch.
-    const uint32_t old = __hip_atomic_fetch_add(&ws.cnt[rr], 1u, __ATOMIC_RELAXED,
-                                                __HIP_MEMORY_SCOPE_AGENT);
-    if (old == 3 * G - 1) __hip_atomic_store(&ws.cnt[rr], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // This workgroup has read both rounds (the values are in LDS); the last
+    // workgroup of the row restores the sentinels for the next launch.
+    const uint32_t old = __hip_atomic_fetch_add(ws.done + rr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (old == G - 1) {
+      for (uint32_t q = 0; q < G; ++q) {
+        __hip_atomic_store(pm + q, kSent32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(ps + q, kSent64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      __hip_atomic_store(ws.done + rr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
   total = 0.0;
   for (uint32_t q = 0; q < G; ++q) total += s_psum[q];
@@ -256,8 +292,13 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
   }
 }
 
-__global__ void zero_u32_kernel(uint32_t* p, uint32_t n) {
-  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
+__global__ void split_ws_init_kernel(SplitWs w, uint32_t n) {
+  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+    w.pmax[i] = kSent32;
+    w.psum[i] = kSent64;
+    w.done[i] = 0;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) *w.err = 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -316,8 +357,9 @@ static std::mutex g_ws_mu;
 static std::map<WsKey, SplitWs> g_ws;
 
 // Workspace of the split kernel for (current device, stream): allocated and
-// zeroed on first use, kept until the process ends. Launches on one stream
-// are ordered, so they may share it; different streams get their own.
+// filled with sentinels on first use (on that stream), kept until the process
+// ends. Launches on one stream are ordered, so they may share it; different
+// streams get their own.
 static quake_status split_workspace(hipStream_t s, SplitWs* out) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return QUAKE_EHIP;
@@ -327,16 +369,16 @@ static quake_status split_workspace(hipStream_t s, SplitWs* out) {
     *out = it->second;
     return QUAKE_OK;
   }
-  const size_t n_pmax = kWsSlots * sizeof(float), n_psum = kWsSlots * sizeof(double);
-  const size_t n_cnt = (kWsSlots + 64) * sizeof(uint32_t);
+  const size_t n_psum = kWsSlots * sizeof(uint64_t), n_pmax = kWsSlots * sizeof(uint32_t);
+  const size_t n_done = kWsSlots * sizeof(uint32_t), n_err = 256;
   char* base = nullptr;
-  if (hipMalloc(&base, n_psum + n_pmax + n_cnt) != hipSuccess) return QUAKE_EHIP;
+  if (hipMalloc(&base, n_psum + n_pmax + n_done + n_err) != hipSuccess) return QUAKE_EHIP;
   SplitWs w;
-  w.psum = reinterpret_cast<double*>(base);
-  w.pmax = reinterpret_cast<float*>(base + n_psum);
-  w.cnt = reinterpret_cast<uint32_t*>(base + n_psum + n_pmax);
-  w.err = w.cnt + kWsSlots;
-  hipLaunchKernelGGL(zero_u32_kernel, dim3(8), dim3(256), 0, s, w.cnt, kWsSlots + 64);
+  w.psum = reinterpret_cast<uint64_t*>(base);
+  w.pmax = reinterpret_cast<uint32_t*>(base + n_psum);
+  w.done = reinterpret_cast<uint32_t*>(base + n_psum + n_pmax);
+  w.err = reinterpret_cast<uint32_t*>(base + n_psum + n_pmax + n_done);
+  hipLaunchKernelGGL(split_ws_init_kernel, dim3(8), dim3(256), 0, s, w, kWsSlots);
   if (hipGetLastError() != hipSuccess) return QUAKE_EHIP;
   g_ws.emplace(WsKey{dev, s}, w);
   *out = w;
@@ -410,18 +452,13 @@ static int launch_split(const SmArgs& a) {
   SplitWs ws;
   quake_status st = split_workspace(a.s, &ws);
   if (st != QUAKE_OK) return 1 + st;
+  // every workgroup of one launch fits on the device at once
   const int64_t rows_per_launch = cap / G;
   for (int64_t r0 = 0; r0 < a.rows; r0 += rows_per_launch) {
     const int64_t nr = std::min(rows_per_launch, a.rows - r0);
-    const char* xp = a.x + r0 * a.ldx_b;
-    char* yp = a.y + r0 * a.ldy_b;
-    int64_t ldx_b = a.ldx_b, ldy_b = a.ldy_b;
-    float c0 = a.c0;
-    uint32_t g = G;
-    void* args[] = {&xp, &yp, const_cast<uint32_t*>(&nvr), &ldx_b, &ldy_b, &c0, &g, &ws};
-    if (hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kern), dim3((uint32_t)(nr * G)),
-                                   dim3(kSmBlock), args, 0, a.s) != hipSuccess)
-      return 1 + QUAKE_EHIP;
+    hipLaunchKernelGGL((sm_split_kernel<DT, MODE, NV>), dim3((uint32_t)(nr * G)), dim3(kSmBlock), 0,
+                       a.s, a.x + r0 * a.ldx_b, a.y + r0 * a.ldy_b, nvr, a.ldx_b, a.ldy_b, a.c0, G,
+                       ws);
     st = launch_status();
     if (st != QUAKE_OK) return 1 + st;
   }
@@ -445,7 +482,8 @@ static quake_status sm_dispatch(const void* x, void* y, int64_t rows, int64_t co
   if (nvr <= 512) return launch_rows<DT, MODE, 8, 1>(a);
   if (nvr <= 1024) return launch_rows<DT, MODE, 4, 4>(a);
   if (nvr <= 2048) return launch_rows<DT, MODE, 8, 4>(a);
-  const int rc = launch_split<DT, MODE, 8>(a);
+  // 64 elements per lane per chunk: 16 vectors of binary32 or 8 of 16-bit
+  const int rc = launch_split<DT, MODE, (DT == F32 ? 16 : 8)>(a);
   if (rc >= 0) return rc == 0 ? QUAKE_OK : (quake_status)(rc - 1);
   return launch_generic<DT, MODE>(x, y, rows, cols, ldx, ldy, c0, s);
 }
