@@ -35,7 +35,7 @@ MODE_IDS = {"exact": 0, "quake1": 1, "quake2": 2}
 KERNEL_SOURCES = ["paper_2412_00408_amd/csrc/elementwise.hip",
                   "paper_2412_00408_amd/csrc/softmax.hip",
                   "paper_2412_00408_amd/csrc/quake_device.hpp"]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.md")
 
 
 def source_hash() -> str:
@@ -216,15 +216,21 @@ def cpu_baseline(w, x_host, cpu_seconds):
 
 
 def traffic_for(name, hash_now):
+    """HBM bytes per launch measured by rocprofv3 FETCH_SIZE / WRITE_SIZE passes
+    (profiles/traffic.md), or None if absent or taken on other kernel sources."""
     try:
         with open(TRAFFIC_FILE) as f:
-            t = json.load(f)
-    except (OSError, ValueError):
-        return None, None
-    e = t.get(name)
-    if not e or e.get("source_hash") != hash_now:
-        return None, e
-    return e.get("bytes_per_launch"), e
+            text = f.read()
+    except OSError:
+        return None
+    hashes = [ln.split(":", 1)[1].strip() for ln in text.splitlines() if ln.startswith("source_hash:")]
+    if not hashes or hashes[-1] != hash_now:
+        return None
+    for ln in text.splitlines():
+        cells = [c.strip() for c in ln.strip().strip("|").split("|")]
+        if len(cells) == 8 and cells[0] == name:
+            return int(cells[5])
+    return None
 
 
 def main():
@@ -256,7 +262,7 @@ def main():
                       launch=kind)
     head = res[a.mode]
     hnow = source_hash()
-    tb, tentry = traffic_for(w.name + ":" + a.mode, hnow)
+    tb = traffic_for(w.name + ":" + a.mode, hnow)
     line = {
         "metric": "GB/s of algorithmic HBM traffic (input read once + output written once) and "
                   "fraction of MI355X peak HBM bandwidth; speedup vs the exact-exp kernel",

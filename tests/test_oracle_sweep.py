@@ -119,7 +119,7 @@ def test_quake1_error_within_quoted_bound(sweep_q1):
     assert abs(lo - (2 ** -BETA - 1)) < 1e-9
     assert abs(sweep_q1["emax"] - hi) <= L_SLACK
     assert abs(sweep_q1["emin"] - lo) <= L_SLACK
-    assert max(abs(sweep_q1["emin"]), sweep_q1["emax"]) <= 0.043   # "about 4.3 %"
+    assert max(abs(sweep_q1["emin"]), sweep_q1["emax"]) <= 0.043   # the cited 4.3 % bound
 
 
 @pytest.mark.slow
