@@ -58,6 +58,8 @@ def parse():
                     help="time only --workload in --mode (for profiler passes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--no-table4", action="store_true",
+                    help="skip the fused-vs-unfused study (the paper's Table IV, on this GPU)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="also run torch copies of MIB MiB (reference kernel for counters)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -69,7 +71,7 @@ def parse():
 # GPU side
 # ---------------------------------------------------------------------------
 
-def make_launcher(q, w, mode, xs, ys):
+def make_launcher(q, w, mode, xs, ys, fused=True):
     """Returns f(i) that launches the operator on buffer pair i (raw C ABI)."""
     import torch
     L = q.lib
@@ -79,8 +81,10 @@ def make_launcher(q, w, mode, xs, ys):
     xp = [x.data_ptr() for x in xs]
     yp = [y.data_ptr() for y in ys]
     if w.op == "gelu":
+        g = L.quake_gelu if fused else L.quake_gelu_unfused
+
         def f(i):
-            return L.quake_gelu(xp[i], yp[i], n, dt, mode, stream())
+            return g(xp[i], yp[i], n, dt, mode, stream())
     elif w.op in ("sigmoid", "silu"):
         silu = int(w.op == "silu")
 
@@ -88,15 +92,16 @@ def make_launcher(q, w, mode, xs, ys):
             return L.quake_sigmoid(xp[i], yp[i], n, dt, mode, silu, stream())
     elif w.op == "softmax":
         rows, cols = w.rows, w.cols
+        sm = L.quake_softmax if fused else L.quake_softmax_unfused
 
         def f(i):
-            return L.quake_softmax(xp[i], yp[i], rows, cols, cols, cols, dt, mode, w.t, stream())
+            return sm(xp[i], yp[i], rows, cols, cols, cols, dt, mode, w.t, stream())
     else:
         raise KeyError(w.op)
     return f
 
 
-def time_workload(q, w, mode, x_host, steps, warmup, launch_kind):
+def time_workload(q, w, mode, x_host, steps, warmup, launch_kind, fused=True):
     import torch
     nbuf = min(64, max(2, math.ceil((1 << 30) / w.algo_bytes)))
     xs, ys = [], []
@@ -105,7 +110,7 @@ def time_workload(q, w, mode, x_host, steps, warmup, launch_kind):
         xs.append(x0.clone())
         ys.append(torch.empty_like(x0))
     del x0
-    f = make_launcher(q, w, mode, xs, ys)
+    f = make_launcher(q, w, mode, xs, ys, fused)
     for i in range(max(warmup, nbuf)):
         rc = f(i % nbuf)
         if rc != 0:
@@ -215,6 +220,36 @@ def cpu_baseline(w, x_host, cpu_seconds):
     }
 
 
+def table4(q, synth, w_head, x_head, a):
+    """The paper's fusion study (Sec. V-A, Table IV) on this GPU: the vanilla
+    operator (unfused, exact exp), QuAKE plugged in without folding, and the
+    fused QuAKE operators, on the paper's op-level shapes and on two workloads
+    above. Ratios are time(vanilla)/time(unfused QuAKE) ("without fusion") and
+    time(unfused)/time(fused) ("additional from fusion")."""
+    out = {}
+    cases = list(synth.TABLE4_WORKLOADS.values()) + [synth.WORKLOADS["gelu_bf16_4096x3072"],
+                                                     synth.WORKLOADS["attn_softmax_bf16_causal"]]
+    for w in cases:
+        xh = x_head if w.name == w_head.name else w.make()
+        steps = max(50, min(a.steps, int(2e8 / w.algo_bytes) * 10))
+        t = {}
+        for key, mode, fused in (("vanilla", 0, False), ("unfused_quake1", 1, False),
+                                 ("unfused_quake2", 2, False), ("fused_exact", 0, True),
+                                 ("fused_quake1", 1, True), ("fused_quake2", 2, True)):
+            t[key] = time_workload(q, w, mode, xh, steps, 10, a.launch, fused)[0]
+        out[w.name] = {
+            "ms": {k: round(v, 6) for k, v in t.items()},
+            "speedup_without_fusion": {"quake1": round(t["vanilla"] / t["unfused_quake1"], 4),
+                                       "quake2": round(t["vanilla"] / t["unfused_quake2"], 4)},
+            "additional_speedup_from_fusion": {
+                "quake1": round(t["unfused_quake1"] / t["fused_quake1"], 4),
+                "quake2": round(t["unfused_quake2"] / t["fused_quake2"], 4)},
+            "fused_quake2_gbps": round(w.algo_bytes / (t["fused_quake2"] * 1e-3) / 1e9, 2),
+        }
+        del xh
+    return out
+
+
 def traffic_for(name, hash_now):
     """HBM bytes per launch measured by rocprofv3 FETCH_SIZE / WRITE_SIZE passes
     (profiles/traffic.md), or None if absent or taken on other kernel sources."""
@@ -311,6 +346,8 @@ def main():
                          "launch": r2["quake2"][1]}
             del xh
         line["secondary"] = sec
+    if not a.no_table4 and not a.only:
+        line["table4"] = table4(q, synth, w, x_host, a)
     line["kernel_source_hash"] = hnow
     print(json.dumps(line), flush=True)
 

@@ -97,8 +97,9 @@ quake_status quake_exp(const void* x, void* y, int64_t n, quake_dtype dtype,
  * c1 = fmaf(-c0, m, 127 * 2^23); y[r, j] = QuAKEx(x[r, j]) / sum_j QuAKEx(x[r, j]).
  * Every exponent of a row is taken against the row's final maximum (QuAKE is
  * not multiplicative, so online rescaling of partial sums would change the
- * result); sums are accumulated in fp32 per vector and in double across lanes,
- * waves and workgroups.
+ * result). Sums are accumulated in fp32 within each 16-byte vector, then in
+ * double (binary32 outputs) or fp32 (16-bit outputs) across vectors, lanes and
+ * waves, and in double across the workgroups of a split row.
  *   x    : device, rows x cols elements, row r at x + r*ldx (elements).
  *   y    : device, row r at y + r*ldy (elements).
  *   ldx, ldy >= cols. cols >= 1 when rows >= 1.
@@ -134,6 +135,26 @@ quake_status quake_gelu(const void* x, void* y, int64_t n, quake_dtype dtype,
  */
 quake_status quake_sigmoid(const void* x, void* y, int64_t n, quake_dtype dtype,
                            quake_mode mode, int silu, void* stream);
+
+/*
+ * quake_softmax_unfused, quake_gelu_unfused — the same operators in the
+ * "plug-in" form of the paper's fusion study (Sec. V-A, Table IV): the
+ * affine input transform is not folded into the exponential's constants.
+ * Softmax computes s = (x - m) * t in binary32 (m the row max) and then the
+ * standard exponential e^s; GELU computes s = k * x * (1/0.044715 + x^2),
+ * k = fl32(2*0.044715*sqrt(2/pi)), and then e^-s. The standard exponential is
+ * QuAKEx with c0 = fl32(2^23/ln2), c1 = (127 - beta)*2^23 (beta as in
+ * quake_exp), or, in QUAKE_EXACT, the hardware exp2 of fl32(s * fl32(1/ln2)) —
+ * the vanilla operator. Arguments, layout, errors and input contract are
+ * those of quake_softmax / quake_gelu. These exist to measure what the
+ * folding saves; results differ from the fused operators only by the
+ * binary32 rounding of the exponential's argument.
+ */
+quake_status quake_softmax_unfused(const void* x, void* y, int64_t rows, int64_t cols,
+                                   int64_t ldx, int64_t ldy, quake_dtype dtype,
+                                   quake_mode mode, float t, void* stream);
+quake_status quake_gelu_unfused(const void* x, void* y, int64_t n, quake_dtype dtype,
+                                quake_mode mode, void* stream);
 
 /* Static, human-readable name of a status code (never NULL). */
 const char* quake_status_str(quake_status s);

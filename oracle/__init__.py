@@ -68,10 +68,12 @@ def lib() -> ctypes.CDLL:
         L.qo_sigmoid.argtypes = [vp, vp, i64, ci, ci, ci]
         L.qo_gelu.argtypes = [vp, vp, i64, ci, ci]
         L.qo_softmax.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp]
+        L.qo_softmax_unfused.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp]
+        L.qo_gelu_unfused.argtypes = [vp, vp, i64, ci, ci]
         L.qo_round.argtypes = [vp, vp, i64, ci]
         L.qo_decode.argtypes = [vp, vp, i64, ci]
         for f in (L.qo_quake, L.qo_exp, L.qo_sigmoid, L.qo_gelu, L.qo_softmax,
-                  L.qo_round, L.qo_decode):
+                  L.qo_softmax_unfused, L.qo_gelu_unfused, L.qo_round, L.qo_decode):
             f.restype = ci
         _lib = L
     return _lib
@@ -158,7 +160,17 @@ def gelu(x, dt="f32", mode=Q2, threads=1):
     return _elementwise(lib().qo_gelu, x, dt, (mode,), threads)
 
 
-def softmax(x, dt="f32", mode=Q2, t=1.0, cols=None, ldx=None, ldy=None, threads=1):
+def gelu_unfused(x, dt="f32", mode=Q2, threads=1):
+    """GELU through Eq. 7 with the standard exponential plugged in (Table IV study)."""
+    return _elementwise(lib().qo_gelu_unfused, x, dt, (mode,), threads)
+
+
+def softmax_unfused(x, dt="f32", mode=Q2, t=1.0, cols=None, ldx=None, ldy=None, threads=1):
+    """Row softmax with (v - m) * t computed before a standard exponential (Table IV study)."""
+    return softmax(x, dt, mode, t, cols, ldx, ldy, threads, _fn="qo_softmax_unfused")
+
+
+def softmax(x, dt="f32", mode=Q2, t=1.0, cols=None, ldx=None, ldy=None, threads=1, _fn="qo_softmax"):
     """Row softmax of t*x (Algorithm 2). x: 2-D array (rows, ldx) of elements.
 
     If cols < ldx only the first cols elements of each row are used; the
@@ -178,8 +190,8 @@ def softmax(x, dt="f32", mode=Q2, t=1.0, cols=None, ldx=None, ldy=None, threads=
     def run(rng):
         s, e = rng
         tmp = np.empty(max(cols, 1), np.float64)
-        _check(lib().qo_softmax(xb + s * ldx * isz, yb + s * ldy * isz, e - s, cols, ldx,
-                                ldy, DTYPES[dt], mode, ctypes.c_float(t), _ptr(tmp)))
+        _check(getattr(lib(), _fn)(xb + s * ldx * isz, yb + s * ldy * isz, e - s, cols, ldx,
+                                   ldy, DTYPES[dt], mode, ctypes.c_float(t), _ptr(tmp)))
 
     if rows == 0:
         return y

@@ -18,6 +18,11 @@
  *   qo_softmax    Sec. III-C, Algorithm 2 (SoftMax-QuAKEx).
  *   qo_gelu       Sec. II-C Eq. 4 rewritten as Sec. III-D Eq. 7.
  *   qo_sigmoid    Sec. III-D logistic function (and SiLU = x * logistic).
+ *   qo_softmax_unfused, qo_gelu_unfused
+ *                 the operators of Sec. V-A's fusion study (Table IV) with the
+ *                 standard exponential plugged in: softmax computes (v - m) * t
+ *                 and then e^s; GELU computes k * x * (1/0.044715 + x^2) and then
+ *                 e^-s; EXACT mode is the vanilla operator with exp.
  *   qo_round      IEEE-754 round-to-nearest-even from double to binary32,
  *                 binary16 and bfloat16 (the output formats).
  *
@@ -312,6 +317,64 @@ int qo_softmax(const void* x, void* y, int64_t rows, int64_t cols, int64_t ldx,
       }
     }
     for (int64_t j = 0; j < cols; ++j) store_el(y, by + j, dt, tmp[j] / sum);
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Unfused ("plug-in") operators of the fusion study (Sec. V-A, Table IV).  */
+/* ------------------------------------------------------------------------ */
+
+/* The standard natural exponential of a binary32 argument: QuAKE with
+ * c0 = 2^23 log2 e and c1 = (127 - beta) 2^23 (Sec. III-A), or the vanilla
+ * exp in binary32 (EXACT: 2^(s * fl(log2 e)), the product rounded to binary32). */
+static float std_exp(float s, int mode) {
+  if (mode == QO_EXACT) return exp2_binary32(s * (float)(1.0 / LN2));
+  return quake_one(s, c0_of(1.0), c1_of(0.0, mode), mode);
+}
+
+/* Softmax without folding: s_j = (v_j - m) * t in binary32, then e^s_j. */
+int qo_softmax_unfused(const void* x, void* y, int64_t rows, int64_t cols, int64_t ldx,
+                       int64_t ldy, int dt, int mode, float t, double* tmp) {
+  int err = bad_args(dt, mode);
+  if (err) return err;
+  for (int64_t r = 0; r < rows; ++r) {
+    const int64_t bx = r * ldx, by = r * ldy;
+    float m = -INFINITY;
+    for (int64_t j = 0; j < cols; ++j) {
+      float v = load_el(x, bx + j, dt);
+      if (v > m) m = v;
+    }
+    if (m == -INFINITY) {
+      for (int64_t j = 0; j < cols; ++j) store_el(y, by + j, dt, 0.0);
+      continue;
+    }
+    double sum = 0.0;
+    for (int64_t j = 0; j < cols; ++j) {
+      float d = load_el(x, bx + j, dt) - m;   /* max subtraction */
+      float s = d * t;                        /* temperature     */
+      tmp[j] = (double)std_exp(s, mode);
+      sum += tmp[j];
+    }
+    for (int64_t j = 0; j < cols; ++j) store_el(y, by + j, dt, tmp[j] / sum);
+  }
+  return 0;
+}
+
+/* GELU through Eq. 7 without folding its constants into the exponential:
+ * s = k * (x * (1/0.044715 + x^2)), y = x / (1 + e^-s). */
+int qo_gelu_unfused(const void* x, void* y, int64_t n, int dt, int mode) {
+  int err = bad_args(dt, mode);
+  if (err) return err;
+  float A = a_gelu();
+  float k = (float)k_gelu();
+  for (int64_t i = 0; i < n; ++i) {
+    float xv = load_el(x, i, dt);
+    float u = fmaf(xv, xv, A);
+    float w = xv * u;
+    float s = w * k;
+    double e = (double)std_exp(-s, mode);
+    store_el(y, i, dt, (double)xv / (1.0 + e));
   }
   return 0;
 }

@@ -15,6 +15,8 @@
 //   GELU     u = fma(x, x, 1/0.044715); w = x*u; e = QuAKEx(w); y = x/(1+e)   (Eq. 7)
 //   Logistic e = QuAKEx(x; -2^23/ln2, c1); y = 1/(1+e)
 //   SiLU     y = x/(1+e)
+//   GELU, unfused (the fusion study of Sec. V-A / Table IV): s = k*w with
+//            k = 2*0.044715*sqrt(2/pi), e = e^-s through the standard constants
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -24,10 +26,12 @@
 
 namespace qk {
 
-enum Op : int { OP_EXP = 0, OP_GELU = 1, OP_SIGMOID = 2, OP_SILU = 3 };
+enum Op : int { OP_EXP = 0, OP_GELU = 1, OP_SIGMOID = 2, OP_SILU = 3, OP_GELU_UNFUSED = 4 };
 
 struct EwParams {
-  float c0, c1, a;  // folded constants; `a` is the FMA addend of GELU
+  float c0, c1;  // constants of the exponential (folded, or the standard e^s)
+  float a;       // FMA addend of GELU, 1/0.044715
+  float k;       // unfused GELU only: scale 2*0.044715*sqrt(2/pi) applied before e^-s
 };
 
 template <int OP, int MODE>
@@ -40,8 +44,14 @@ __device__ __forceinline__ float ew_op(float x, const EwParams& p) {
     return div_one_plus(x, qexp<MODE>(w, p.c0, p.c1));
   } else if constexpr (OP == OP_SIGMOID) {
     return __builtin_amdgcn_rcpf(1.0f + qexp<MODE>(x, p.c0, p.c1));
-  } else {
+  } else if constexpr (OP == OP_SILU) {
     return div_one_plus(x, qexp<MODE>(x, p.c0, p.c1));
+  } else {
+    // plug-in form of the fusion study: s = k * w, then the standard e^-s
+    const float u = __builtin_fmaf(x, x, p.a);
+    const float w = x * u;
+    const float sk = w * p.k;
+    return div_one_plus(x, qexp<MODE>(-sk, p.c0, p.c1));
   }
 }
 
@@ -214,7 +224,7 @@ extern "C" quake_status quake_exp(const void* x, void* y, int64_t n, quake_dtype
   const Affine af = exp_affine(a, b, mode);
   if (!std::isfinite(af.c0) || !std::isfinite(af.c1)) return QUAKE_EINVAL;
   if (n == 0) return QUAKE_OK;
-  return ew_dispatch<OP_EXP>(x, y, n, dtype, mode, EwParams{af.c0, af.c1, 0.0f},
+  return ew_dispatch<OP_EXP>(x, y, n, dtype, mode, EwParams{af.c0, af.c1, 0.0f, 0.0f},
                              static_cast<hipStream_t>(stream));
 }
 
@@ -223,8 +233,18 @@ extern "C" quake_status quake_gelu(const void* x, void* y, int64_t n, quake_dtyp
   quake_status st = ew_check(x, y, n, dtype, mode);
   if (st != QUAKE_OK || n == 0) return st;
   const Affine af = gelu_affine(mode);
-  return ew_dispatch<OP_GELU>(x, y, n, dtype, mode, EwParams{af.c0, af.c1, gelu_a()},
+  return ew_dispatch<OP_GELU>(x, y, n, dtype, mode, EwParams{af.c0, af.c1, gelu_a(), 0.0f},
                               static_cast<hipStream_t>(stream));
+}
+
+extern "C" quake_status quake_gelu_unfused(const void* x, void* y, int64_t n, quake_dtype dtype,
+                                           quake_mode mode, void* stream) {
+  quake_status st = ew_check(x, y, n, dtype, mode);
+  if (st != QUAKE_OK || n == 0) return st;
+  const Affine af = exp_affine(1.0, 0.0, mode);   // the standard e^s
+  return ew_dispatch<OP_GELU_UNFUSED>(x, y, n, dtype, mode,
+                                      EwParams{af.c0, af.c1, gelu_a(), (float)gelu_k()},
+                                      static_cast<hipStream_t>(stream));
 }
 
 extern "C" quake_status quake_sigmoid(const void* x, void* y, int64_t n, quake_dtype dtype,
@@ -232,7 +252,7 @@ extern "C" quake_status quake_sigmoid(const void* x, void* y, int64_t n, quake_d
   quake_status st = ew_check(x, y, n, dtype, mode);
   if (st != QUAKE_OK || n == 0) return st;
   const Affine af = sigmoid_affine(mode);
-  const EwParams p{af.c0, af.c1, 0.0f};
+  const EwParams p{af.c0, af.c1, 0.0f, 0.0f};
   hipStream_t s = static_cast<hipStream_t>(stream);
   return silu ? ew_dispatch<OP_SILU>(x, y, n, dtype, mode, p, s)
               : ew_dispatch<OP_SIGMOID>(x, y, n, dtype, mode, p, s);

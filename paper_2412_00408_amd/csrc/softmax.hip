@@ -10,8 +10,8 @@
 //   sm_rows<NV, WAVES=1>  one wave per row, the row held in VGPRs as NV
 //                         16-byte vectors per lane (rows up to 64*NV vectors);
 //                         4 rows per 256-thread workgroup, no LDS, no barrier.
-//   sm_rows<NV, WAVES=4>  one workgroup per row (rows up to 256*NV vectors),
-//                         cross-wave max/sum through LDS.
+//   sm_rows<NV, WAVES=4>  one workgroup per row (rows up to 256*NV vectors, i.e.
+//                         16384 elements), cross-wave max/sum through LDS.
 //   sm_split<NV>          rows longer than a workgroup's registers: G
 //                         workgroups per row each hold one chunk in VGPRs and
 //                         exchange their chunk max, then their chunk sum,
@@ -63,14 +63,44 @@ __device__ __forceinline__ float row_c1(float c0, float m) {
   return __builtin_fmaf(-c0, m, MODE == EXACT ? 0.0f : kK127);
 }
 
+// Constants of one softmax call. Fused (Algorithm 2): c0 = 2^23 t / ln2 and
+// the per-row c1. Unfused (the plug-in form of the fusion study, Sec. V-A /
+// Table IV): s = (v - m) * t in binary32, then the standard exponential with
+// c0 = 2^23 / ln2, c1 = c1s (EXACT: c0 = fl(1/ln2), c1 = 0).
+struct SmConst {
+  float c0, c1s, t;
+};
+
+template <int MODE, bool FUSE>
+struct RowExp {
+  float c0, c1, m, t;
+  __device__ __forceinline__ float operator()(float v) const {
+    if constexpr (FUSE) {
+      return qexp<MODE>(v, c0, c1);
+    } else {
+      const float d = v - m;
+      return qexp<MODE>(d * t, c0, c1);
+    }
+  }
+};
+
+template <int MODE, bool FUSE>
+__device__ __forceinline__ RowExp<MODE, FUSE> row_exp(const SmConst& k, float m) {
+  if constexpr (FUSE) {
+    return RowExp<MODE, FUSE>{k.c0, row_c1<MODE>(k.c0, m), 0.0f, 0.0f};
+  } else {
+    return RowExp<MODE, FUSE>{k.c0, k.c1s, m == -INFINITY ? 0.0f : m, k.t};
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Register-resident rows: one wave (WAVES = 1) or one workgroup (WAVES = 4).
 // ---------------------------------------------------------------------------
-template <int DT, int MODE, int NV, int WAVES>
+template <int DT, int MODE, bool FUSE, int NV, int WAVES>
 __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restrict__ x,
                                                           char* __restrict__ y, uint32_t rows,
                                                           uint32_t nvr, int64_t ldx_b,
-                                                          int64_t ldy_b, float c0) {
+                                                          int64_t ldy_b, SmConst kc) {
   constexpr int V = kV<DT>;
   constexpr int LANES = 64 * WAVES;
   constexpr int ROWS_PER_BLOCK = kSmBlock / LANES;
@@ -114,14 +144,14 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
     m = fmaxf(fmaxf(s_max[0], s_max[1]), fmaxf(s_max[2], s_max[3]));
   }
 
-  const float c1 = row_c1<MODE>(c0, m);
+  const RowExp<MODE, FUSE> ex = row_exp<MODE, FUSE>(kc, m);
   Acc acc = 0;
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
     float part = 0.0f;
 #pragma unroll
     for (int j = 0; j < V; ++j) {
-      f[k][j] = qexp<MODE>(f[k][j], c0, c1);
+      f[k][j] = ex(f[k][j]);
       part += f[k][j];
     }
     acc += (Acc)part;
@@ -187,11 +217,11 @@ __device__ __forceinline__ T poll_slot(T* slot, T sentinel, T fallback, uint32_t
   return v;
 }
 
-template <int DT, int MODE, int NV>
+template <int DT, int MODE, bool FUSE, int NV>
 __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restrict__ x,
                                                            char* __restrict__ y, uint32_t nvr,
-                                                           int64_t ldx_b, int64_t ldy_b, float c0,
-                                                           uint32_t G, SplitWs ws) {
+                                                           int64_t ldx_b, int64_t ldy_b,
+                                                           SmConst kc, uint32_t G, SplitWs ws) {
   constexpr int V = kV<DT>;
   constexpr int CHV = kSmBlock * NV;   // vectors per chunk
   __shared__ float s_max[4];
@@ -242,14 +272,14 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
   for (uint32_t q = 0; q < G; ++q) m = fmaxf(m, s_pmax[q]);
 
   // round 2: chunk sums with the row's final max
-  const float c1 = row_c1<MODE>(c0, m);
+  const RowExp<MODE, FUSE> ex = row_exp<MODE, FUSE>(kc, m);
   double acc = 0.0;
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
     float part = 0.0f;
 #pragma unroll
     for (int j = 0; j < V; ++j) {
-      f[k][j] = qexp<MODE>(f[k][j], c0, c1);
+      f[k][j] = ex(f[k][j]);
       part += f[k][j];
     }
     acc += (double)part;
@@ -318,11 +348,11 @@ __device__ __forceinline__ double block_sum(double v, double* s) {
   return (s[0] + s[1]) + (s[2] + s[3]);
 }
 
-template <int DT, int MODE>
+template <int DT, int MODE, bool FUSE>
 __global__ __launch_bounds__(kSmBlock) void sm_generic_kernel(const void* __restrict__ x,
                                                              void* __restrict__ y, int64_t rows,
                                                              int64_t cols, int64_t ldx,
-                                                             int64_t ldy, float c0) {
+                                                             int64_t ldy, SmConst kc) {
   __shared__ float s_max[4];
   __shared__ double s_sum[4];
   for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
@@ -330,14 +360,13 @@ __global__ __launch_bounds__(kSmBlock) void sm_generic_kernel(const void* __rest
     float lm = -INFINITY;
     for (int64_t j = threadIdx.x; j < cols; j += kSmBlock) lm = fmaxf(lm, load1<DT>(x, bx + j));
     const float m = block_max(lm, s_max);
-    const float c1 = row_c1<MODE>(c0, m);
+    const RowExp<MODE, FUSE> ex = row_exp<MODE, FUSE>(kc, m);
     double acc = 0.0;
-    for (int64_t j = threadIdx.x; j < cols; j += kSmBlock)
-      acc += (double)qexp<MODE>(load1<DT>(x, bx + j), c0, c1);
+    for (int64_t j = threadIdx.x; j < cols; j += kSmBlock) acc += (double)ex(load1<DT>(x, bx + j));
     const double total = block_sum(acc, s_sum);
     const float r = (m == -INFINITY) ? 0.0f : (float)(1.0 / total);
     for (int64_t j = threadIdx.x; j < cols; j += kSmBlock)
-      store1<DT>(y, by + j, qexp<MODE>(load1<DT>(x, bx + j), c0, c1) * r);
+      store1<DT>(y, by + j, ex(load1<DT>(x, bx + j)) * r);
     __syncthreads();   // s_max / s_sum are rewritten for the next row
   }
 }
@@ -399,13 +428,13 @@ struct SmArgs {
   const char* x;
   char* y;
   int64_t rows, cols, ldx_b, ldy_b;
-  float c0;
+  SmConst kc;
   hipStream_t s;
 };
 
 constexpr int64_t kRowChunk = int64_t(1) << 28;   // rows per launch (grid stays < 2^31)
 
-template <int DT, int MODE, int NV, int WAVES>
+template <int DT, int MODE, bool FUSE, int NV, int WAVES>
 static quake_status launch_rows(const SmArgs& a) {
   constexpr int V = kV<DT>;
   constexpr int RPB = kSmBlock / (64 * WAVES);
@@ -413,33 +442,33 @@ static quake_status launch_rows(const SmArgs& a) {
   for (int64_t r0 = 0; r0 < a.rows; r0 += kRowChunk) {
     const int64_t nr = std::min(kRowChunk, a.rows - r0);
     const uint32_t grid = (uint32_t)((nr + RPB - 1) / RPB);
-    hipLaunchKernelGGL((sm_rows_kernel<DT, MODE, NV, WAVES>), dim3(grid), dim3(kSmBlock), 0, a.s,
-                       a.x + r0 * a.ldx_b, a.y + r0 * a.ldy_b, (uint32_t)nr, nvr, a.ldx_b, a.ldy_b,
-                       a.c0);
+    hipLaunchKernelGGL((sm_rows_kernel<DT, MODE, FUSE, NV, WAVES>), dim3(grid), dim3(kSmBlock), 0,
+                       a.s, a.x + r0 * a.ldx_b, a.y + r0 * a.ldy_b, (uint32_t)nr, nvr, a.ldx_b,
+                       a.ldy_b, a.kc);
     const quake_status st = launch_status();
     if (st != QUAKE_OK) return st;
   }
   return QUAKE_OK;
 }
 
-template <int DT, int MODE>
+template <int DT, int MODE, bool FUSE>
 static quake_status launch_generic(const void* x, void* y, int64_t rows, int64_t cols, int64_t ldx,
-                                   int64_t ldy, float c0, hipStream_t s) {
+                                   int64_t ldy, const SmConst& kc, hipStream_t s) {
   const uint32_t grid = (uint32_t)std::min<int64_t>(rows, int64_t(1) << 20);
-  hipLaunchKernelGGL((sm_generic_kernel<DT, MODE>), dim3(grid), dim3(kSmBlock), 0, s, x, y, rows,
-                     cols, ldx, ldy, c0);
+  hipLaunchKernelGGL((sm_generic_kernel<DT, MODE, FUSE>), dim3(grid), dim3(kSmBlock), 0, s, x, y,
+                     rows, cols, ldx, ldy, kc);
   return launch_status();
 }
 
 // Returns QUAKE_OK on success, or 1 + status on failure; -1 if the split path
 // cannot be used (too many chunks per row) and the caller should fall back.
-template <int DT, int MODE, int NV>
+template <int DT, int MODE, bool FUSE, int NV>
 static int launch_split(const SmArgs& a) {
   constexpr int V = kV<DT>;
   constexpr int CHV = kSmBlock * NV;
   const uint32_t nvr = (uint32_t)(a.cols / V);
   const uint32_t G = (nvr + CHV - 1) / CHV;
-  auto kern = sm_split_kernel<DT, MODE, NV>;
+  auto kern = sm_split_kernel<DT, MODE, FUSE, NV>;
   static int cached[64] = {0};   // per device; a benign race only recomputes it
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 1 + QUAKE_EHIP;
@@ -456,36 +485,64 @@ static int launch_split(const SmArgs& a) {
   const int64_t rows_per_launch = cap / G;
   for (int64_t r0 = 0; r0 < a.rows; r0 += rows_per_launch) {
     const int64_t nr = std::min(rows_per_launch, a.rows - r0);
-    hipLaunchKernelGGL((sm_split_kernel<DT, MODE, NV>), dim3((uint32_t)(nr * G)), dim3(kSmBlock), 0,
-                       a.s, a.x + r0 * a.ldx_b, a.y + r0 * a.ldy_b, nvr, a.ldx_b, a.ldy_b, a.c0, G,
-                       ws);
+    hipLaunchKernelGGL((sm_split_kernel<DT, MODE, FUSE, NV>), dim3((uint32_t)(nr * G)),
+                       dim3(kSmBlock), 0, a.s, a.x + r0 * a.ldx_b, a.y + r0 * a.ldy_b, nvr, a.ldx_b,
+                       a.ldy_b, a.kc, G, ws);
     st = launch_status();
     if (st != QUAKE_OK) return 1 + st;
   }
   return QUAKE_OK;
 }
 
-template <int DT, int MODE>
+template <int DT, int MODE, bool FUSE>
 static quake_status sm_dispatch(const void* x, void* y, int64_t rows, int64_t cols, int64_t ldx,
-                                int64_t ldy, float c0, hipStream_t s) {
+                                int64_t ldy, const SmConst& kc, hipStream_t s) {
   constexpr int V = kV<DT>;
   constexpr int64_t esz = kEsz<DT>;
   const bool vec = aligned16(x) && aligned16(y) && (ldx * esz) % 16 == 0 && (ldy * esz) % 16 == 0 &&
                    cols % V == 0 && cols / V < (int64_t(1) << 30);
-  if (!vec) return launch_generic<DT, MODE>(x, y, rows, cols, ldx, ldy, c0, s);
+  if (!vec) return launch_generic<DT, MODE, FUSE>(x, y, rows, cols, ldx, ldy, kc, s);
   const SmArgs a{static_cast<const char*>(x), static_cast<char*>(y), rows, cols, ldx * esz,
-                 ldy * esz, c0, s};
+                 ldy * esz, kc, s};
   const int64_t nvr = cols / V;
-  if (nvr <= 64) return launch_rows<DT, MODE, 1, 1>(a);
-  if (nvr <= 128) return launch_rows<DT, MODE, 2, 1>(a);
-  if (nvr <= 256) return launch_rows<DT, MODE, 4, 1>(a);
-  if (nvr <= 512) return launch_rows<DT, MODE, 8, 1>(a);
-  if (nvr <= 1024) return launch_rows<DT, MODE, 4, 4>(a);
-  if (nvr <= 2048) return launch_rows<DT, MODE, 8, 4>(a);
+  if (nvr <= 64) return launch_rows<DT, MODE, FUSE, 1, 1>(a);
+  if (nvr <= 128) return launch_rows<DT, MODE, FUSE, 2, 1>(a);
+  if (nvr <= 256) return launch_rows<DT, MODE, FUSE, 4, 1>(a);
+  if (nvr <= 512) return launch_rows<DT, MODE, FUSE, 8, 1>(a);
+  if (nvr <= 1024) return launch_rows<DT, MODE, FUSE, 4, 4>(a);
+  if (nvr <= 2048) return launch_rows<DT, MODE, FUSE, 8, 4>(a);
+  if (DT == F32 && nvr <= 4096) return launch_rows<DT, MODE, FUSE, 16, 4>(a);
   // 64 elements per lane per chunk: 16 vectors of binary32 or 8 of 16-bit
-  const int rc = launch_split<DT, MODE, (DT == F32 ? 16 : 8)>(a);
+  const int rc = launch_split<DT, MODE, FUSE, (DT == F32 ? 16 : 8)>(a);
   if (rc >= 0) return rc == 0 ? QUAKE_OK : (quake_status)(rc - 1);
-  return launch_generic<DT, MODE>(x, y, rows, cols, ldx, ldy, c0, s);
+  return launch_generic<DT, MODE, FUSE>(x, y, rows, cols, ldx, ldy, kc, s);
+}
+
+template <bool FUSE>
+static quake_status softmax_entry(const void* x, void* y, int64_t rows, int64_t cols, int64_t ldx,
+                                  int64_t ldy, int dtype, int mode, float t, void* stream) {
+  if (!valid_dtype(dtype)) return QUAKE_EDTYPE;
+  if (!valid_mode(mode)) return QUAKE_EMODE;
+  if (rows < 0 || cols < 0 || ldx < 0 || ldy < 0) return QUAKE_EINVAL;
+  if (rows == 0) return QUAKE_OK;
+  if (cols == 0 || ldx < cols || ldy < cols || x == nullptr || y == nullptr) return QUAKE_EINVAL;
+  if (!std::isfinite(t) || !(t > 0.0f)) return QUAKE_EINVAL;
+  SmConst kc;
+  if (FUSE) {
+    kc = SmConst{softmax_c0(t, mode), 0.0f, t};
+    if (!std::isfinite(kc.c0) || kc.c0 == 0.0f) return QUAKE_EINVAL;
+  } else {
+    const Affine af = exp_affine(1.0, 0.0, mode);   // the standard e^s
+    kc = SmConst{af.c0, af.c1, t};
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+#define QK_SM_CASE(D, M) \
+  if (dtype == D && mode == M) return sm_dispatch<D, M, FUSE>(x, y, rows, cols, ldx, ldy, kc, s);
+  QK_SM_CASE(F32, EXACT) QK_SM_CASE(F32, Q1) QK_SM_CASE(F32, Q2)
+  QK_SM_CASE(F16, EXACT) QK_SM_CASE(F16, Q1) QK_SM_CASE(F16, Q2)
+  QK_SM_CASE(BF16, EXACT) QK_SM_CASE(BF16, Q1) QK_SM_CASE(BF16, Q2)
+#undef QK_SM_CASE
+  return QUAKE_EMODE;
 }
 
 }  // namespace qk
@@ -495,20 +552,11 @@ using namespace qk;
 extern "C" quake_status quake_softmax(const void* x, void* y, int64_t rows, int64_t cols,
                                       int64_t ldx, int64_t ldy, quake_dtype dtype,
                                       quake_mode mode, float t, void* stream) {
-  if (!valid_dtype(dtype)) return QUAKE_EDTYPE;
-  if (!valid_mode(mode)) return QUAKE_EMODE;
-  if (rows < 0 || cols < 0 || ldx < 0 || ldy < 0) return QUAKE_EINVAL;
-  if (rows == 0) return QUAKE_OK;
-  if (cols == 0 || ldx < cols || ldy < cols || x == nullptr || y == nullptr) return QUAKE_EINVAL;
-  if (!std::isfinite(t) || !(t > 0.0f)) return QUAKE_EINVAL;
-  const float c0 = softmax_c0(t, mode);
-  if (!std::isfinite(c0) || c0 == 0.0f) return QUAKE_EINVAL;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-#define QK_SM_CASE(D, M) \
-  if ((int)dtype == D && (int)mode == M) return sm_dispatch<D, M>(x, y, rows, cols, ldx, ldy, c0, s);
-  QK_SM_CASE(F32, EXACT) QK_SM_CASE(F32, Q1) QK_SM_CASE(F32, Q2)
-  QK_SM_CASE(F16, EXACT) QK_SM_CASE(F16, Q1) QK_SM_CASE(F16, Q2)
-  QK_SM_CASE(BF16, EXACT) QK_SM_CASE(BF16, Q1) QK_SM_CASE(BF16, Q2)
-#undef QK_SM_CASE
-  return QUAKE_EMODE;
+  return softmax_entry<true>(x, y, rows, cols, ldx, ldy, dtype, mode, t, stream);
+}
+
+extern "C" quake_status quake_softmax_unfused(const void* x, void* y, int64_t rows, int64_t cols,
+                                              int64_t ldx, int64_t ldy, quake_dtype dtype,
+                                              quake_mode mode, float t, void* stream) {
+  return softmax_entry<false>(x, y, rows, cols, ldx, ldy, dtype, mode, t, stream);
 }

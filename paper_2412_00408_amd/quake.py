@@ -38,8 +38,11 @@ def _load() -> ctypes.CDLL:
     L.quake_exp.argtypes = [vp, vp, i64, ci, ci, cf, cf, vp]
     L.quake_softmax.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp]
     L.quake_gelu.argtypes = [vp, vp, i64, ci, ci, vp]
+    L.quake_softmax_unfused.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp]
+    L.quake_gelu_unfused.argtypes = [vp, vp, i64, ci, ci, vp]
     L.quake_sigmoid.argtypes = [vp, vp, i64, ci, ci, ci, vp]
-    for f in (L.quake_exp, L.quake_softmax, L.quake_gelu, L.quake_sigmoid):
+    for f in (L.quake_exp, L.quake_softmax, L.quake_gelu, L.quake_sigmoid,
+              L.quake_softmax_unfused, L.quake_gelu_unfused):
         f.restype = ci
     L.quake_status_str.argtypes = [ci]
     L.quake_status_str.restype = ctypes.c_char_p
@@ -102,6 +105,15 @@ def quake_gelu(x, y=None, mode=QUAKE_2, stream=None):
     return y
 
 
+def quake_gelu_unfused(x, y=None, mode=QUAKE_2, stream=None):
+    """GELU with the standard exponential plugged in (fusion study, Table IV)."""
+    y = _check_io(x, y)
+    _raise("quake_gelu_unfused", lib.quake_gelu_unfused(x.data_ptr(), y.data_ptr(), x.numel(),
+                                                        DTYPES[x.dtype], MODES[mode],
+                                                        _stream(x, stream)))
+    return y
+
+
 def quake_sigmoid(x, y=None, mode=QUAKE_2, silu=False, stream=None):
     """Logistic sigma(x), or SiLU x*sigma(x) with silu=True."""
     y = _check_io(x, y)
@@ -122,7 +134,12 @@ def _rows_view(t: torch.Tensor, what: str):
     raise ValueError("%s must be contiguous, or 2-D with a contiguous last dimension" % what)
 
 
-def quake_softmax(x, y=None, mode=QUAKE_2, t=1.0, stream=None):
+def quake_softmax_unfused(x, y=None, mode=QUAKE_2, t=1.0, stream=None):
+    """Softmax with (x - m) * t computed before a standard exponential (Table IV)."""
+    return quake_softmax(x, y, mode, t, stream, _fn="quake_softmax_unfused")
+
+
+def quake_softmax(x, y=None, mode=QUAKE_2, t=1.0, stream=None, _fn="quake_softmax"):
     """Softmax of t*x over the last dimension (Algorithm 2)."""
     if x.dim() == 0:
         raise ValueError("softmax needs at least one dimension")
@@ -133,6 +150,6 @@ def quake_softmax(x, y=None, mode=QUAKE_2, t=1.0, stream=None):
         raise ValueError("output must match the input's dtype, device and shape")
     rows, cols, ldx = _rows_view(x, "input")
     _, _, ldy = _rows_view(y, "output")
-    _raise("quake_softmax", lib.quake_softmax(x.data_ptr(), y.data_ptr(), rows, cols, ldx, ldy,
-                                              DTYPES[x.dtype], MODES[mode], t, _stream(x, stream)))
+    _raise(_fn, getattr(lib, _fn)(x.data_ptr(), y.data_ptr(), rows, cols, ldx, ldy,
+                                  DTYPES[x.dtype], MODES[mode], t, _stream(x, stream)))
     return y

@@ -15,6 +15,9 @@ Workloads (name -> operator, I/O format, shape, distribution):
                             Bernoulli(0.01) positions set to +-80 (sign p = 1/2)
   lmhead_softmax_f32_64x128256  softmax, f32, [64,128256], 3*N(0,1) with 16
                             distinct random columns per row set to +20
+and the two op-level shapes of the fusion study (TABLE4_WORKLOADS):
+  softmax_f32_16384x16384   softmax, f32, [16384,16384], 4*N(0,1), t = 1
+  gelu_f32_260k             GELU, f32, [260000], N(0, 1.5^2)
 
 Every generator is numpy PCG64 seeded with SEED_BASE + k, so a given call is
 reproducible across machines. `rows`/`n` arguments shrink a workload to a
@@ -147,8 +150,24 @@ class Workload:
         if self.name == "lmhead_softmax_f32_64x128256":
             r = self.rows if rows is None else rows
             return spiked_logits(r, self.cols, 3.0, 16, 20.0, self.dt, self.seed)
+        if self.name == "softmax_f32_16384x16384":
+            r = self.rows if rows is None else rows
+            return normal((r, self.cols), 4.0, self.dt, self.seed)
+        if self.name == "gelu_f32_260k":
+            m = self.numel if n is None else n
+            return normal((m,), 1.5, self.dt, self.seed)
         raise KeyError(self.name)
 
+
+# The op-level shapes of the paper's fusion study (Sec. V-A, Table IV): a
+# row softmax of a 16384 x 16384 matrix and GELU of a 260k-element vector, both
+# binary32 (values 4*N(0,1) and N(0, 1.5^2)).
+TABLE4_WORKLOADS = {
+    w.name: w for w in [
+        Workload("softmax_f32_16384x16384", "softmax", "f32", (16384, 16384), 16384, 16384, 1.0, 6),
+        Workload("gelu_f32_260k", "gelu", "f32", (260000,), 0, 0, 1.0, 7),
+    ]
+}
 
 WORKLOADS = {
     w.name: w for w in [

@@ -37,6 +37,9 @@ def run_elementwise(q, op: str, x_cpu: torch.Tensor, mode: int, **kw):
     elif op == "gelu":
         yg = q.quake_gelu(xg, mode=mode)
         ref = oracle.gelu(xb, dt, mode, threads=THREADS)
+    elif op == "gelu_unfused":
+        yg = q.quake_gelu_unfused(xg, mode=mode)
+        ref = oracle.gelu_unfused(xb, dt, mode, threads=THREADS)
     elif op in ("sigmoid", "silu"):
         yg = q.quake_sigmoid(xg, mode=mode, silu=(op == "silu"))
         ref = oracle.sigmoid(xb, dt, mode, silu=(op == "silu"), threads=THREADS)

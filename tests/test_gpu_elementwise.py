@@ -71,7 +71,7 @@ def test_exp_affine(q, dt, mode, ab):
     assert_parity(g, r, d, kind_of("exp", mode), "exp %s %s %s" % (dt, mode, ab))
 
 
-@pytest.mark.parametrize("op", ["gelu", "sigmoid", "silu"])
+@pytest.mark.parametrize("op", ["gelu", "sigmoid", "silu", "gelu_unfused"])
 @pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
 @pytest.mark.parametrize("mode", MODES)
 def test_operators_random(q, op, dt, mode):
@@ -81,12 +81,12 @@ def test_operators_random(q, op, dt, mode):
     assert_parity(g, r, d, "op", "%s %s %s" % (op, dt, mode))
 
 
-@pytest.mark.parametrize("op", ["exp", "gelu", "sigmoid", "silu"])
+@pytest.mark.parametrize("op", ["exp", "gelu", "sigmoid", "silu", "gelu_unfused"])
 @pytest.mark.parametrize("mode", MODES)
 def test_special_values(q, op, mode):
     vals = [0.0, -0.0, 1e-40, -1e-40, 1e-30, 5.0, -5.0, 10.0, -9.99, -10.2, -10.5, 20.0, -20.0,
             80.0, -80.0, 87.0, -87.0, 88.7, 89.0, -104.0, 1e4, -1e4, 3e38, -3e38]
-    if op != "gelu":
+    if not op.startswith("gelu"):
         vals += [np.inf, -np.inf]
     x = torch.tensor(vals, dtype=torch.float32)
     say("special", op, mode)
@@ -98,7 +98,7 @@ def test_special_values(q, op, mode):
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 def test_ragged_lengths(q, n, dt):
     x = synth.normal((n,), 3.0, dt, 102)
-    for op in ("exp", "gelu", "sigmoid", "silu"):
+    for op in ("exp", "gelu", "sigmoid", "silu", "gelu_unfused"):
         say("ragged", op, dt, n)
         g, r, d = run_elementwise(q, op, x, 2)
         assert_parity(g, r, d, kind_of(op, 2), "ragged %s %s %d" % (op, dt, n))
@@ -198,3 +198,12 @@ def test_streams(q):
     s.synchronize()
     torch.cuda.synchronize()
     assert check_bits(host_bits(y), host_bits(ref)) is None
+
+
+@pytest.mark.parametrize("op", ["gelu", "gelu_unfused"])
+@pytest.mark.parametrize("mode", MODES)
+def test_workload_table4_gelu_f32_260k(q, op, mode):
+    w = synth.TABLE4_WORKLOADS["gelu_f32_260k"]
+    say(w.name, op, mode)
+    g, r, d = run_elementwise(q, op, w.make(), mode)
+    assert_parity(g, r, d, "op", "%s %s mode %d" % (w.name, op, mode))

@@ -23,7 +23,7 @@ def q():
     return quake
 
 
-def _run(q, x_cpu, mode, t, ld_pad=0, offset=0):
+def _run(q, x_cpu, mode, t, ld_pad=0, offset=0, fused=True):
     """Softmax of a [rows, cols] CPU tensor on the GPU and in the oracle.
 
     ld_pad > 0 stores rows with stride cols + ld_pad (input and output);
@@ -40,7 +40,7 @@ def _run(q, x_cpu, mode, t, ld_pad=0, offset=0):
         xg = gx[offset:offset + rows * ld].view(rows, ld)[:, :cols]
         gy = torch.full_like(gx, 7.0)
         yg = gy[offset:offset + rows * ld].view(rows, ld)[:, :cols]
-        q.quake_softmax(xg, yg, mode=mode, t=t)
+        (q.quake_softmax if fused else q.quake_softmax_unfused)(xg, yg, mode=mode, t=t)
         torch.cuda.synchronize()
         out = gy.cpu()
         # padding around the rows must be untouched
@@ -50,15 +50,16 @@ def _run(q, x_cpu, mode, t, ld_pad=0, offset=0):
         g = host_bits(out[offset:offset + rows * ld].view(rows, ld)[:, :cols].contiguous())
     else:
         xg = x_cpu.to("cuda:0")
-        yg = q.quake_softmax(xg, mode=mode, t=t)
+        yg = (q.quake_softmax if fused else q.quake_softmax_unfused)(xg, mode=mode, t=t)
         torch.cuda.synchronize()
         g = host_bits(yg)
-    ref = oracle.softmax(xb.reshape(rows, cols), dt, mode, t=t, threads=THREADS)
+    fn = oracle.softmax if fused else oracle.softmax_unfused
+    ref = fn(xb.reshape(rows, cols), dt, mode, t=t, threads=THREADS)
     return g, ref, dt
 
 
 COLS_F32 = [1, 2, 3, 4, 100, 128, 252, 256, 260, 512, 1000, 1024, 2048, 4096, 8188, 8192, 8196,
-            10000, 65536, 128256, 200000]
+            10000, 16384, 16388, 65536, 128256, 200000]
 COLS_16 = [1, 8, 24, 512, 1000, 1024, 2048, 4096, 8192, 16384, 16392, 32768, 128256]
 
 
@@ -191,3 +192,40 @@ def test_workload_lmhead_softmax_f32_64x128256(q, mode):
     say(w.name, mode)
     g, r, d = _run(q, w.make(), mode, w.t)
     assert_parity(g, r, d, "op", "%s mode %d" % (w.name, mode))
+
+
+# ------------------------------------------- unfused form (Table IV study)
+
+@pytest.mark.parametrize("cols,dt", [(128, "f32"), (512, "bf16"), (1001, "f32"), (4096, "f32"),
+                                     (16384, "f32"), (16384, "bf16"), (128256, "f32"),
+                                     (50000, "f16")])
+@pytest.mark.parametrize("mode", MODES)
+def test_unfused(q, cols, dt, mode):
+    rows = 6 if cols > 20000 else 33
+    x = synth.normal((rows, cols), 2.5, dt, 900 + cols % 83)
+    for t in (1.0, 0.125):
+        say("softmax unfused", dt, rows, cols, mode, t)
+        g, r, d = _run(q, x, mode, t, fused=False)
+        assert_parity(g, r, d, "op", "unfused %s %dx%d mode %d t %g" % (dt, rows, cols, mode, t))
+
+
+def test_unfused_masked_and_strided(q):
+    r = np.random.default_rng(11)
+    v = r.standard_normal((10, 3000)).astype(np.float32)
+    v[r.random((10, 3000)) < 0.5] = -np.inf
+    v[4] = -np.inf
+    x = synth.to_format(v, "bf16")
+    for mode in MODES:
+        say("softmax unfused masked", mode)
+        g, ref, d = _run(q, x, mode, 0.5, fused=False)
+        assert_parity(g, ref, d, "op", "unfused masked mode %d" % mode)
+        g, ref, d = _run(q, x, mode, 0.5, ld_pad=5, offset=1, fused=False)
+        assert_parity(g, ref, d, "op", "unfused masked strided mode %d" % mode)
+
+
+@pytest.mark.parametrize("fused,mode", [(True, 0), (True, 1), (True, 2), (False, 0), (False, 2)])
+def test_workload_table4_softmax_f32_16384x16384(q, fused, mode):
+    w = synth.TABLE4_WORKLOADS["softmax_f32_16384x16384"]
+    say(w.name, "fused" if fused else "unfused", mode)
+    g, r, d = _run(q, w.make(), mode, w.t, fused=fused)
+    assert_parity(g, r, d, "op", "%s fused=%s mode %d" % (w.name, fused, mode))

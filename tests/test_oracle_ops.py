@@ -223,3 +223,57 @@ def test_exact_mode_exponential_is_binary32(oracle):
     s = oracle.sigmoid(np.array([-89.0, -88.0], np.float32), "f32", 0, silu=True)
     assert s[0] == 0.0 and np.signbit(s[0])
     assert s[1] < 0
+
+
+# ------------------------- unfused operators (Table IV study) ----------------
+
+@pytest.mark.parametrize("mode", [0, 1, 2])
+@pytest.mark.parametrize("t", [1.0, 0.125, 2.5])
+def test_unfused_softmax_against_exact(oracle, mode, t):
+    x = _rows(21, 24, 300, 3.0)
+    y = oracle.softmax_unfused(x, "f32", mode, t=t).astype(np.float64)
+    ref = sp_softmax(t * x.astype(np.float64), axis=1)
+    big = ref > 1e-30
+    rel = np.abs(y / ref - 1)[big]
+    if mode == 0:
+        arg = (t * (x.max(axis=1, keepdims=True) - x).astype(np.float64))[big]
+        assert np.all(rel <= 4 * 2.0 ** -24 * (1 + arg) + 2e-7)
+    else:
+        assert rel.max() <= RATIO[mode]
+    s = y.sum(axis=1)
+    assert np.all(np.abs(s - 1) <= 300 * 2.0 ** -24)
+
+
+def test_unfused_softmax_matches_fused_quake2(oracle):
+    # folding (v - m) * t into c0, c1 changes only the binary32 rounding of l
+    x = _rows(22, 16, 500, 2.0)
+    for t in (1.0, 0.125, 3.0):
+        a = oracle.softmax(x, "f32", 2, t=t).astype(np.float64)
+        b = oracle.softmax_unfused(x, "f32", 2, t=t).astype(np.float64)
+        assert np.max(np.abs(a / b - 1)) < 2e-4
+        assert not np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("mode", [0, 1, 2])
+def test_unfused_softmax_masking(oracle, mode):
+    v = _rows(23, 6, 40, 2.0)
+    v[:, 5:17] = -np.inf
+    v[2] = -np.inf
+    y = oracle.softmax_unfused(v, "f32", mode)
+    assert np.all(y[:, 5:17] == 0) and np.all(y[2] == 0)
+
+
+@pytest.mark.parametrize("mode", [0, 1, 2])
+def test_unfused_gelu_against_eq4_and_fused(oracle, mode):
+    x = np.linspace(-12, 12, 200001).astype(np.float32)
+    y = oracle.gelu_unfused(x, "f32", mode).astype(np.float64)
+    ref = _gelu_tanh(x)
+    xa = np.abs(x.astype(np.float64))
+    if mode == 0:
+        # e^s overflows binary32 once s > 88.72 (R20), leaving at most |x| 2^-127
+        assert np.all(np.abs(y - ref) <= 3e-5 * np.abs(ref) + xa * 2.0 ** -127 + 1e-40)
+    else:
+        eps = EPS[mode]
+        assert np.all(np.abs(y - ref) <= xa * (eps / (4 * (1 - eps)) + 2.0 ** -23) + 1e-37)
+        f = oracle.gelu(x, "f32", mode).astype(np.float64)
+        assert np.all(np.abs(y - f) <= 1e-5 * xa + 1e-37)
