@@ -137,6 +137,27 @@ quake_status quake_sigmoid(const void* x, void* y, int64_t n, quake_dtype dtype,
                            quake_mode mode, int silu, void* stream);
 
 /*
+ * quake_softmax_causal — quake_softmax with an implicit causal mask, as in
+ * attention scores: entry (r, j) takes part iff j <= (r mod period) + shift;
+ * masked entries are NOT read and their outputs are exactly 0, which is what
+ * quake_softmax gives for -inf entries at those positions (Algorithm 2 with
+ * the clamp of l). A row with no live entry gives zeros. For self-attention
+ * with rows = batch*heads*seq and cols = seq, use period = seq, shift = 0;
+ * for queries aligned to the end of a longer key range, shift = cols - seq.
+ *   period       : 1 <= period <= 2^31 - 1; |shift| <= 2^40; otherwise QUAKE_EINVAL.
+ *   write_masked : nonzero writes 0 to every masked output; zero leaves
+ *                  masked outputs that lie in 16-byte vectors without live
+ *                  entries unwritten (for consumers that never read them, such
+ *                  as a causal P*V product), so only about half the outputs
+ *                  are stored.
+ * Other arguments as quake_softmax. Only the live entries are read from HBM.
+ */
+quake_status quake_softmax_causal(const void* x, void* y, int64_t rows, int64_t cols,
+                                  int64_t ldx, int64_t ldy, int64_t period, int64_t shift,
+                                  int write_masked, quake_dtype dtype, quake_mode mode, float t,
+                                  void* stream);
+
+/*
  * quake_softmax_unfused, quake_gelu_unfused — the same operators in the
  * "plug-in" form of the paper's fusion study (Sec. V-A, Table IV): the
  * affine input transform is not folded into the exponential's constants.

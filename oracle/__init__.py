@@ -69,11 +69,13 @@ def lib() -> ctypes.CDLL:
         L.qo_gelu.argtypes = [vp, vp, i64, ci, ci]
         L.qo_softmax.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp]
         L.qo_softmax_unfused.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp]
+        L.qo_softmax_causal.argtypes = [vp, vp, i64, i64, i64, i64, i64, i64, ci, ci, cf, vp]
         L.qo_gelu_unfused.argtypes = [vp, vp, i64, ci, ci]
         L.qo_round.argtypes = [vp, vp, i64, ci]
         L.qo_decode.argtypes = [vp, vp, i64, ci]
         for f in (L.qo_quake, L.qo_exp, L.qo_sigmoid, L.qo_gelu, L.qo_softmax,
-                  L.qo_softmax_unfused, L.qo_gelu_unfused, L.qo_round, L.qo_decode):
+                  L.qo_softmax_unfused, L.qo_gelu_unfused, L.qo_softmax_causal, L.qo_round,
+                  L.qo_decode):
             f.restype = ci
         _lib = L
     return _lib
@@ -200,6 +202,36 @@ def softmax(x, dt="f32", mode=Q2, t=1.0, cols=None, ldx=None, ldy=None, threads=
     else:
         with ThreadPoolExecutor(threads) as ex:
             list(ex.map(run, _split(rows, threads)))
+    return y
+
+
+def softmax_causal(x, period, shift=0, dt="f32", mode=Q2, t=1.0, threads=1):
+    """Row softmax where entry (r, j) is used iff j <= r mod period + shift
+    (the others are not read and give 0). x: 2-D contiguous array."""
+    x = _prep(x, dt)
+    rows, cols = x.shape
+    y = np.zeros((rows, cols), dtype=x.dtype)
+    isz = x.itemsize
+    xb, yb = _ptr(x), _ptr(y)
+
+    def run(rng):
+        s, e = rng
+        tmp = np.empty(max(cols, 1), np.float64)
+        # chunks start at multiples of period, so r mod period is the global one
+        _check(lib().qo_softmax_causal(xb + s * cols * isz, yb + s * cols * isz, e - s, cols, cols,
+                                       cols, period, shift, DTYPES[dt], mode, ctypes.c_float(t),
+                                       _ptr(tmp)))
+
+    if rows == 0:
+        return y
+    step = period * max(1, -(-rows // (period * max(1, threads))))
+    ranges = [(s0, min(rows, s0 + step)) for s0 in range(0, rows, step)]
+    if threads <= 1 or len(ranges) == 1:
+        for rg in ranges:
+            run(rg)
+    else:
+        with ThreadPoolExecutor(threads) as ex:
+            list(ex.map(run, ranges))
     return y
 
 

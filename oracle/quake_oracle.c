@@ -18,6 +18,10 @@
  *   qo_softmax    Sec. III-C, Algorithm 2 (SoftMax-QuAKEx).
  *   qo_gelu       Sec. II-C Eq. 4 rewritten as Sec. III-D Eq. 7.
  *   qo_sigmoid    Sec. III-D logistic function (and SiLU = x * logistic).
+ *   qo_softmax_causal
+ *                 Algorithm 2 on rows whose entries past a causal limit are
+ *                 masked: entry (r, j) takes part iff j <= r mod period + shift;
+ *                 masked entries are not read and give 0 (as -inf inputs would).
  *   qo_softmax_unfused, qo_gelu_unfused
  *                 the operators of Sec. V-A's fusion study (Table IV) with the
  *                 standard exponential plugged in: softmax computes (v - m) * t
@@ -317,6 +321,47 @@ int qo_softmax(const void* x, void* y, int64_t rows, int64_t cols, int64_t ldx,
       }
     }
     for (int64_t j = 0; j < cols; ++j) store_el(y, by + j, dt, tmp[j] / sum);
+  }
+  return 0;
+}
+
+/*
+ * Softmax with an implicit causal mask: row r uses only its first
+ * L = min(cols, r mod period + shift + 1) entries; the others are treated as
+ * -inf without being read (exactly what explicit -inf entries give under
+ * Algorithm 2 with the clamp of l), and their outputs are 0.
+ */
+int qo_softmax_causal(const void* x, void* y, int64_t rows, int64_t cols, int64_t ldx,
+                      int64_t ldy, int64_t period, int64_t shift, int dt, int mode, float t,
+                      double* tmp) {
+  int err = bad_args(dt, mode);
+  if (err) return err;
+  if (period <= 0) return 1;
+  float c0 = qo_softmax_c0(t, mode);
+  for (int64_t r = 0; r < rows; ++r) {
+    const int64_t bx = r * ldx, by = r * ldy;
+    int64_t L = r % period + shift + 1;
+    if (L > cols) L = cols;
+    if (L < 0) L = 0;
+    float m = -INFINITY;
+    for (int64_t j = 0; j < L; ++j) {
+      float v = load_el(x, bx + j, dt);
+      if (v > m) m = v;
+    }
+    for (int64_t j = L; j < cols; ++j) store_el(y, by + j, dt, 0.0);
+    if (m == -INFINITY) {
+      for (int64_t j = 0; j < L; ++j) store_el(y, by + j, dt, 0.0);
+      continue;
+    }
+    double sum = 0.0;
+    float c1 = (mode == QO_EXACT) ? fmaf(-c0, m, 0.0f) : fmaf(-c0, m, k127());
+    for (int64_t j = 0; j < L; ++j) {
+      float v = load_el(x, bx + j, dt);
+      tmp[j] = (mode == QO_EXACT) ? (double)exp2_binary32(fmaf(v, c0, c1))
+                                  : (double)quake_one(v, c0, c1, mode);
+      sum += tmp[j];
+    }
+    for (int64_t j = 0; j < L; ++j) store_el(y, by + j, dt, tmp[j] / sum);
   }
   return 0;
 }

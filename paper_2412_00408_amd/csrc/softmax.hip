@@ -93,14 +93,36 @@ __device__ __forceinline__ RowExp<MODE, FUSE> row_exp(const SmConst& k, float m)
   }
 }
 
+// Implicit causal mask: row r (global index) uses only its first
+// L = clamp(r mod period + shift + 1, 0, cols) entries; the rest are not
+// read and give 0, exactly what -inf entries give. row0_mod = (index of the
+// launch's first row) mod period, so r mod period = (row0_mod + local) mod period.
+struct CausalArg {
+  uint32_t row0_mod, period;
+  int64_t shift;
+  uint32_t write_masked;   // 0: masked outputs are not stored
+};
+
+template <bool CAUSAL>
+__device__ __forceinline__ int64_t live_len(const CausalArg& ca, uint32_t local_row, int64_t cols) {
+  if constexpr (!CAUSAL) {
+    return cols;
+  } else {
+    const int64_t r = (int64_t)((ca.row0_mod + local_row) % ca.period);
+    const int64_t L = r + ca.shift + 1;
+    return L < 0 ? 0 : (L > cols ? cols : L);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Register-resident rows: one wave (WAVES = 1) or one workgroup (WAVES = 4).
 // ---------------------------------------------------------------------------
-template <int DT, int MODE, bool FUSE, int NV, int WAVES>
+template <int DT, int MODE, bool FUSE, bool CAUSAL, int NV, int WAVES>
 __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restrict__ x,
                                                           char* __restrict__ y, uint32_t rows,
                                                           uint32_t nvr, int64_t ldx_b,
-                                                          int64_t ldy_b, SmConst kc) {
+                                                          int64_t ldy_b, SmConst kc,
+                                                          CausalArg ca) {
   constexpr int V = kV<DT>;
   constexpr int LANES = 64 * WAVES;
   constexpr int ROWS_PER_BLOCK = kSmBlock / LANES;
@@ -120,18 +142,22 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
   // Every lane loads (vectors past the row end re-read the row's last vector,
   // which stays in one cache line) and padding lanes select -inf: no branch
   // around the loads, so the whole row stays in registers without merges.
+  // With the causal mask only vectors holding live entries are read.
+  const uint32_t L = (uint32_t)live_len<CAUSAL>(ca, row, (int64_t)nvr * V);
+  const uint32_t nvl = CAUSAL ? (L + V - 1) / V : nvr;
+  const uint32_t vlast = (nvl > 0 ? nvl : 1) - 1;
   u32x4 raw[NV];
 #pragma unroll
-  for (int k = 0; k < NV; ++k)
-    raw[k] = __builtin_nontemporal_load(xr + umin32(k * LANES + lid, nvr - 1));
+  for (int k = 0; k < NV; ++k) raw[k] = __builtin_nontemporal_load(xr + umin32(k * LANES + lid, vlast));
   float f[NV][V];
   float lmax = -INFINITY;
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
     unpack<DT>(raw[k], f[k]);
-    const bool valid = k * LANES + lid < nvr;
+    const uint32_t vi = k * LANES + lid;
 #pragma unroll
     for (int j = 0; j < V; ++j) {
+      const bool valid = CAUSAL ? (vi * V + j < L) : (vi < nvr);
       f[k][j] = valid ? f[k][j] : -INFINITY;
       lmax = fmaxf(lmax, f[k][j]);
     }
@@ -167,7 +193,7 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
     const uint32_t vi = k * LANES + lid;
-    if (vi < nvr) {
+    if (vi < nvr && (!CAUSAL || ca.write_masked || vi < nvl)) {
 #pragma unroll
       for (int j = 0; j < V; ++j) f[k][j] *= r;
       __builtin_nontemporal_store(pack<DT>(f[k]), yr + vi);
@@ -217,11 +243,12 @@ __device__ __forceinline__ T poll_slot(T* slot, T sentinel, T fallback, uint32_t
   return v;
 }
 
-template <int DT, int MODE, bool FUSE, int NV>
+template <int DT, int MODE, bool FUSE, bool CAUSAL, int NV>
 __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restrict__ x,
                                                            char* __restrict__ y, uint32_t nvr,
                                                            int64_t ldx_b, int64_t ldy_b,
-                                                           SmConst kc, uint32_t G, SplitWs ws) {
+                                                           SmConst kc, CausalArg ca, uint32_t G,
+                                                           SplitWs ws) {
   constexpr int V = kV<DT>;
   constexpr int CHV = kSmBlock * NV;   // vectors per chunk
   __shared__ float s_max[4];
@@ -240,18 +267,22 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
   u32x4* yr = reinterpret_cast<u32x4*>(y + (int64_t)rr * ldy_b);
   const uint32_t v0 = g * CHV;
 
+  const uint32_t L = (uint32_t)live_len<CAUSAL>(ca, rr, (int64_t)nvr * V);
+  const uint32_t nvl = CAUSAL ? (L + V - 1) / V : nvr;
+  const uint32_t vlast = (nvl > 0 ? nvl : 1) - 1;
   u32x4 raw[NV];
 #pragma unroll
   for (int k = 0; k < NV; ++k)
-    raw[k] = __builtin_nontemporal_load(xr + umin32(v0 + k * kSmBlock + threadIdx.x, nvr - 1));
+    raw[k] = __builtin_nontemporal_load(xr + umin32(v0 + k * kSmBlock + threadIdx.x, vlast));
   float f[NV][V];
   float lmax = -INFINITY;
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
     unpack<DT>(raw[k], f[k]);
-    const bool valid = v0 + k * kSmBlock + threadIdx.x < nvr;
+    const uint32_t vi = v0 + k * kSmBlock + threadIdx.x;
 #pragma unroll
     for (int j = 0; j < V; ++j) {
+      const bool valid = CAUSAL ? (vi * V + j < L) : (vi < nvr);
       f[k][j] = valid ? f[k][j] : -INFINITY;
       lmax = fmaxf(lmax, f[k][j]);
     }
@@ -314,7 +345,7 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
     const uint32_t vi = v0 + k * kSmBlock + threadIdx.x;
-    if (vi < nvr) {
+    if (vi < nvr && (!CAUSAL || ca.write_masked || vi < nvl)) {
 #pragma unroll
       for (int j = 0; j < V; ++j) f[k][j] *= r;
       __builtin_nontemporal_store(pack<DT>(f[k]), yr + vi);
@@ -348,25 +379,28 @@ __device__ __forceinline__ double block_sum(double v, double* s) {
   return (s[0] + s[1]) + (s[2] + s[3]);
 }
 
-template <int DT, int MODE, bool FUSE>
+template <int DT, int MODE, bool FUSE, bool CAUSAL>
 __global__ __launch_bounds__(kSmBlock) void sm_generic_kernel(const void* __restrict__ x,
                                                              void* __restrict__ y, int64_t rows,
                                                              int64_t cols, int64_t ldx,
-                                                             int64_t ldy, SmConst kc) {
+                                                             int64_t ldy, SmConst kc,
+                                                             CausalArg ca) {
   __shared__ float s_max[4];
   __shared__ double s_sum[4];
   for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
     const int64_t bx = row * ldx, by = row * ldy;
+    const int64_t L = live_len<CAUSAL>(ca, (uint32_t)row, cols);
     float lm = -INFINITY;
-    for (int64_t j = threadIdx.x; j < cols; j += kSmBlock) lm = fmaxf(lm, load1<DT>(x, bx + j));
+    for (int64_t j = threadIdx.x; j < L; j += kSmBlock) lm = fmaxf(lm, load1<DT>(x, bx + j));
     const float m = block_max(lm, s_max);
     const RowExp<MODE, FUSE> ex = row_exp<MODE, FUSE>(kc, m);
     double acc = 0.0;
-    for (int64_t j = threadIdx.x; j < cols; j += kSmBlock) acc += (double)ex(load1<DT>(x, bx + j));
+    for (int64_t j = threadIdx.x; j < L; j += kSmBlock) acc += (double)ex(load1<DT>(x, bx + j));
     const double total = block_sum(acc, s_sum);
     const float r = (m == -INFINITY) ? 0.0f : (float)(1.0 / total);
-    for (int64_t j = threadIdx.x; j < cols; j += kSmBlock)
-      store1<DT>(y, by + j, ex(load1<DT>(x, bx + j)) * r);
+    const int64_t jend = (CAUSAL && !ca.write_masked) ? L : cols;
+    for (int64_t j = threadIdx.x; j < jend; j += kSmBlock)
+      store1<DT>(y, by + j, j < L ? ex(load1<DT>(x, bx + j)) * r : 0.0f);
     __syncthreads();   // s_max / s_sum are rewritten for the next row
   }
 }
@@ -429,12 +463,19 @@ struct SmArgs {
   char* y;
   int64_t rows, cols, ldx_b, ldy_b;
   SmConst kc;
+  int64_t period, shift;   // causal mask (unused otherwise)
+  uint32_t write_masked;
   hipStream_t s;
 };
 
+static CausalArg causal_at(const SmArgs& a, int64_t r0) {
+  if (a.period <= 0) return CausalArg{0, 1, 0, 1};
+  return CausalArg{(uint32_t)(r0 % a.period), (uint32_t)a.period, a.shift, a.write_masked};
+}
+
 constexpr int64_t kRowChunk = int64_t(1) << 28;   // rows per launch (grid stays < 2^31)
 
-template <int DT, int MODE, bool FUSE, int NV, int WAVES>
+template <int DT, int MODE, bool FUSE, bool CAUSAL, int NV, int WAVES>
 static quake_status launch_rows(const SmArgs& a) {
   constexpr int V = kV<DT>;
   constexpr int RPB = kSmBlock / (64 * WAVES);
@@ -442,33 +483,42 @@ static quake_status launch_rows(const SmArgs& a) {
   for (int64_t r0 = 0; r0 < a.rows; r0 += kRowChunk) {
     const int64_t nr = std::min(kRowChunk, a.rows - r0);
     const uint32_t grid = (uint32_t)((nr + RPB - 1) / RPB);
-    hipLaunchKernelGGL((sm_rows_kernel<DT, MODE, FUSE, NV, WAVES>), dim3(grid), dim3(kSmBlock), 0,
-                       a.s, a.x + r0 * a.ldx_b, a.y + r0 * a.ldy_b, (uint32_t)nr, nvr, a.ldx_b,
-                       a.ldy_b, a.kc);
+    hipLaunchKernelGGL((sm_rows_kernel<DT, MODE, FUSE, CAUSAL, NV, WAVES>), dim3(grid),
+                       dim3(kSmBlock), 0, a.s, a.x + r0 * a.ldx_b, a.y + r0 * a.ldy_b,
+                       (uint32_t)nr, nvr, a.ldx_b, a.ldy_b, a.kc, causal_at(a, r0));
     const quake_status st = launch_status();
     if (st != QUAKE_OK) return st;
   }
   return QUAKE_OK;
 }
 
-template <int DT, int MODE, bool FUSE>
-static quake_status launch_generic(const void* x, void* y, int64_t rows, int64_t cols, int64_t ldx,
-                                   int64_t ldy, const SmConst& kc, hipStream_t s) {
-  const uint32_t grid = (uint32_t)std::min<int64_t>(rows, int64_t(1) << 20);
-  hipLaunchKernelGGL((sm_generic_kernel<DT, MODE, FUSE>), dim3(grid), dim3(kSmBlock), 0, s, x, y,
-                     rows, cols, ldx, ldy, kc);
-  return launch_status();
+template <int DT, int MODE, bool FUSE, bool CAUSAL>
+static quake_status launch_generic(const void* x, void* y, const SmArgs& a, int64_t ldx,
+                                   int64_t ldy) {
+  constexpr int64_t esz = kEsz<DT>;
+  constexpr int64_t kGenericRows = int64_t(1) << 30;   // rows per launch (32-bit row index)
+  for (int64_t r0 = 0; r0 < a.rows; r0 += kGenericRows) {
+    const int64_t nr = std::min(kGenericRows, a.rows - r0);
+    const uint32_t grid = (uint32_t)std::min<int64_t>(nr, int64_t(1) << 20);
+    hipLaunchKernelGGL((sm_generic_kernel<DT, MODE, FUSE, CAUSAL>), dim3(grid), dim3(kSmBlock), 0,
+                       a.s, static_cast<const char*>(x) + r0 * ldx * esz,
+                       static_cast<char*>(y) + r0 * ldy * esz, nr, a.cols, ldx, ldy, a.kc,
+                       causal_at(a, r0));
+    const quake_status st = launch_status();
+    if (st != QUAKE_OK) return st;
+  }
+  return QUAKE_OK;
 }
 
 // Returns QUAKE_OK on success, or 1 + status on failure; -1 if the split path
 // cannot be used (too many chunks per row) and the caller should fall back.
-template <int DT, int MODE, bool FUSE, int NV>
+template <int DT, int MODE, bool FUSE, bool CAUSAL, int NV>
 static int launch_split(const SmArgs& a) {
   constexpr int V = kV<DT>;
   constexpr int CHV = kSmBlock * NV;
   const uint32_t nvr = (uint32_t)(a.cols / V);
   const uint32_t G = (nvr + CHV - 1) / CHV;
-  auto kern = sm_split_kernel<DT, MODE, FUSE, NV>;
+  auto kern = sm_split_kernel<DT, MODE, FUSE, CAUSAL, NV>;
   static int cached[64] = {0};   // per device; a benign race only recomputes it
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 1 + QUAKE_EHIP;
@@ -485,45 +535,54 @@ static int launch_split(const SmArgs& a) {
   const int64_t rows_per_launch = cap / G;
   for (int64_t r0 = 0; r0 < a.rows; r0 += rows_per_launch) {
     const int64_t nr = std::min(rows_per_launch, a.rows - r0);
-    hipLaunchKernelGGL((sm_split_kernel<DT, MODE, FUSE, NV>), dim3((uint32_t)(nr * G)),
+    hipLaunchKernelGGL((sm_split_kernel<DT, MODE, FUSE, CAUSAL, NV>), dim3((uint32_t)(nr * G)),
                        dim3(kSmBlock), 0, a.s, a.x + r0 * a.ldx_b, a.y + r0 * a.ldy_b, nvr, a.ldx_b,
-                       a.ldy_b, a.kc, G, ws);
+                       a.ldy_b, a.kc, causal_at(a, r0), G, ws);
     st = launch_status();
     if (st != QUAKE_OK) return 1 + st;
   }
   return QUAKE_OK;
 }
 
-template <int DT, int MODE, bool FUSE>
-static quake_status sm_dispatch(const void* x, void* y, int64_t rows, int64_t cols, int64_t ldx,
-                                int64_t ldy, const SmConst& kc, hipStream_t s) {
+template <int DT, int MODE, bool FUSE, bool CAUSAL>
+static quake_status sm_dispatch(const void* x, void* y, int64_t ldx, int64_t ldy, const SmArgs& ain) {
   constexpr int V = kV<DT>;
   constexpr int64_t esz = kEsz<DT>;
+  const int64_t cols = ain.cols;
   const bool vec = aligned16(x) && aligned16(y) && (ldx * esz) % 16 == 0 && (ldy * esz) % 16 == 0 &&
-                   cols % V == 0 && cols / V < (int64_t(1) << 30);
-  if (!vec) return launch_generic<DT, MODE, FUSE>(x, y, rows, cols, ldx, ldy, kc, s);
-  const SmArgs a{static_cast<const char*>(x), static_cast<char*>(y), rows, cols, ldx * esz,
-                 ldy * esz, kc, s};
+                   cols % V == 0 && cols < (int64_t(1) << 31) - 16;
+  if (!vec) return launch_generic<DT, MODE, FUSE, CAUSAL>(x, y, ain, ldx, ldy);
+  SmArgs a = ain;
+  a.x = static_cast<const char*>(x);
+  a.y = static_cast<char*>(y);
+  a.ldx_b = ldx * esz;
+  a.ldy_b = ldy * esz;
   const int64_t nvr = cols / V;
-  if (nvr <= 64) return launch_rows<DT, MODE, FUSE, 1, 1>(a);
-  if (nvr <= 128) return launch_rows<DT, MODE, FUSE, 2, 1>(a);
-  if (nvr <= 256) return launch_rows<DT, MODE, FUSE, 4, 1>(a);
-  if (nvr <= 512) return launch_rows<DT, MODE, FUSE, 8, 1>(a);
-  if (nvr <= 1024) return launch_rows<DT, MODE, FUSE, 4, 4>(a);
-  if (nvr <= 2048) return launch_rows<DT, MODE, FUSE, 8, 4>(a);
-  if (DT == F32 && nvr <= 4096) return launch_rows<DT, MODE, FUSE, 16, 4>(a);
+  if (nvr <= 64) return launch_rows<DT, MODE, FUSE, CAUSAL, 1, 1>(a);
+  if (nvr <= 128) return launch_rows<DT, MODE, FUSE, CAUSAL, 2, 1>(a);
+  if (nvr <= 256) return launch_rows<DT, MODE, FUSE, CAUSAL, 4, 1>(a);
+  if (nvr <= 512) return launch_rows<DT, MODE, FUSE, CAUSAL, 8, 1>(a);
+  if (nvr <= 1024) return launch_rows<DT, MODE, FUSE, CAUSAL, 4, 4>(a);
+  if (nvr <= 2048) return launch_rows<DT, MODE, FUSE, CAUSAL, 8, 4>(a);
+  if constexpr (DT == F32) {
+    if (nvr <= 4096) return launch_rows<DT, MODE, FUSE, CAUSAL, 16, 4>(a);
+  }
   // 64 elements per lane per chunk: 16 vectors of binary32 or 8 of 16-bit
-  const int rc = launch_split<DT, MODE, FUSE, (DT == F32 ? 16 : 8)>(a);
+  const int rc = launch_split<DT, MODE, FUSE, CAUSAL, (DT == F32 ? 16 : 8)>(a);
   if (rc >= 0) return rc == 0 ? QUAKE_OK : (quake_status)(rc - 1);
-  return launch_generic<DT, MODE, FUSE>(x, y, rows, cols, ldx, ldy, kc, s);
+  return launch_generic<DT, MODE, FUSE, CAUSAL>(x, y, ain, ldx, ldy);
 }
 
-template <bool FUSE>
+template <bool FUSE, bool CAUSAL>
 static quake_status softmax_entry(const void* x, void* y, int64_t rows, int64_t cols, int64_t ldx,
-                                  int64_t ldy, int dtype, int mode, float t, void* stream) {
+                                  int64_t ldy, int dtype, int mode, float t, int64_t period,
+                                  int64_t shift, int write_masked, void* stream) {
   if (!valid_dtype(dtype)) return QUAKE_EDTYPE;
   if (!valid_mode(mode)) return QUAKE_EMODE;
   if (rows < 0 || cols < 0 || ldx < 0 || ldy < 0) return QUAKE_EINVAL;
+  if (CAUSAL && (period <= 0 || period > INT32_MAX || shift < -(int64_t(1) << 40) ||
+                 shift > (int64_t(1) << 40)))
+    return QUAKE_EINVAL;
   if (rows == 0) return QUAKE_OK;
   if (cols == 0 || ldx < cols || ldy < cols || x == nullptr || y == nullptr) return QUAKE_EINVAL;
   if (!std::isfinite(t) || !(t > 0.0f)) return QUAKE_EINVAL;
@@ -535,9 +594,11 @@ static quake_status softmax_entry(const void* x, void* y, int64_t rows, int64_t 
     const Affine af = exp_affine(1.0, 0.0, mode);   // the standard e^s
     kc = SmConst{af.c0, af.c1, t};
   }
-  hipStream_t s = static_cast<hipStream_t>(stream);
+  const SmArgs a{static_cast<const char*>(x), static_cast<char*>(y), rows, cols, 0, 0, kc,
+                 CAUSAL ? period : 0, shift, (uint32_t)(write_masked != 0),
+                 static_cast<hipStream_t>(stream)};
 #define QK_SM_CASE(D, M) \
-  if (dtype == D && mode == M) return sm_dispatch<D, M, FUSE>(x, y, rows, cols, ldx, ldy, kc, s);
+  if (dtype == D && mode == M) return sm_dispatch<D, M, FUSE, CAUSAL>(x, y, ldx, ldy, a);
   QK_SM_CASE(F32, EXACT) QK_SM_CASE(F32, Q1) QK_SM_CASE(F32, Q2)
   QK_SM_CASE(F16, EXACT) QK_SM_CASE(F16, Q1) QK_SM_CASE(F16, Q2)
   QK_SM_CASE(BF16, EXACT) QK_SM_CASE(BF16, Q1) QK_SM_CASE(BF16, Q2)
@@ -552,11 +613,19 @@ using namespace qk;
 extern "C" quake_status quake_softmax(const void* x, void* y, int64_t rows, int64_t cols,
                                       int64_t ldx, int64_t ldy, quake_dtype dtype,
                                       quake_mode mode, float t, void* stream) {
-  return softmax_entry<true>(x, y, rows, cols, ldx, ldy, dtype, mode, t, stream);
+  return softmax_entry<true, false>(x, y, rows, cols, ldx, ldy, dtype, mode, t, 0, 0, 1, stream);
 }
 
 extern "C" quake_status quake_softmax_unfused(const void* x, void* y, int64_t rows, int64_t cols,
                                               int64_t ldx, int64_t ldy, quake_dtype dtype,
                                               quake_mode mode, float t, void* stream) {
-  return softmax_entry<false>(x, y, rows, cols, ldx, ldy, dtype, mode, t, stream);
+  return softmax_entry<false, false>(x, y, rows, cols, ldx, ldy, dtype, mode, t, 0, 0, 1, stream);
+}
+
+extern "C" quake_status quake_softmax_causal(const void* x, void* y, int64_t rows, int64_t cols,
+                                             int64_t ldx, int64_t ldy, int64_t period,
+                                             int64_t shift, int write_masked, quake_dtype dtype,
+                                             quake_mode mode, float t, void* stream) {
+  return softmax_entry<true, true>(x, y, rows, cols, ldx, ldy, dtype, mode, t, period, shift,
+                                   write_masked, stream);
 }

@@ -40,9 +40,10 @@ def _load() -> ctypes.CDLL:
     L.quake_gelu.argtypes = [vp, vp, i64, ci, ci, vp]
     L.quake_softmax_unfused.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp]
     L.quake_gelu_unfused.argtypes = [vp, vp, i64, ci, ci, vp]
+    L.quake_softmax_causal.argtypes = [vp, vp, i64, i64, i64, i64, i64, i64, ci, ci, ci, cf, vp]
     L.quake_sigmoid.argtypes = [vp, vp, i64, ci, ci, ci, vp]
     for f in (L.quake_exp, L.quake_softmax, L.quake_gelu, L.quake_sigmoid,
-              L.quake_softmax_unfused, L.quake_gelu_unfused):
+              L.quake_softmax_unfused, L.quake_gelu_unfused, L.quake_softmax_causal):
         f.restype = ci
     L.quake_status_str.argtypes = [ci]
     L.quake_status_str.restype = ctypes.c_char_p
@@ -152,4 +153,26 @@ def quake_softmax(x, y=None, mode=QUAKE_2, t=1.0, stream=None, _fn="quake_softma
     _, _, ldy = _rows_view(y, "output")
     _raise(_fn, getattr(lib, _fn)(x.data_ptr(), y.data_ptr(), rows, cols, ldx, ldy,
                                   DTYPES[x.dtype], MODES[mode], t, _stream(x, stream)))
+    return y
+
+
+def quake_softmax_causal(x, y=None, period=None, shift=0, mode=QUAKE_2, t=1.0, write_masked=True,
+                         stream=None):
+    """Softmax of t*x over the last dimension where entry (r, j) is used iff
+    j <= r mod period + shift (default period: the row length); masked
+    entries are not read and give 0 (left unwritten where a whole 16-byte
+    vector is masked, if write_masked is False)."""
+    if x.dim() == 0:
+        raise ValueError("softmax needs at least one dimension")
+    _check_io(x, None, contiguous=False)
+    if y is None:
+        y = torch.empty_like(x, memory_format=torch.contiguous_format)
+    if y.dtype != x.dtype or y.device != x.device or y.shape != x.shape:
+        raise ValueError("output must match the input's dtype, device and shape")
+    rows, cols, ldx = _rows_view(x, "input")
+    _, _, ldy = _rows_view(y, "output")
+    period = cols if period is None else period
+    _raise("quake_softmax_causal", lib.quake_softmax_causal(
+        x.data_ptr(), y.data_ptr(), rows, cols, ldx, ldy, period, shift, int(bool(write_masked)),
+        DTYPES[x.dtype], MODES[mode], t, _stream(x, stream)))
     return y

@@ -229,3 +229,71 @@ def test_workload_table4_softmax_f32_16384x16384(q, fused, mode):
     say(w.name, "fused" if fused else "unfused", mode)
     g, r, d = _run(q, w.make(), mode, w.t, fused=fused)
     assert_parity(g, r, d, "op", "%s fused=%s mode %d" % (w.name, fused, mode))
+
+
+# ------------------------------------------------------- implicit causal mask
+
+def _run_causal(q, x_cpu, mode, t, period, shift):
+    dt = {torch.float32: "f32", torch.float16: "f16", torch.bfloat16: "bf16"}[x_cpu.dtype]
+    xg = x_cpu.to("cuda:0")
+    yg = q.quake_softmax_causal(xg, period=period, shift=shift, mode=mode, t=t)
+    torch.cuda.synchronize()
+    ref = oracle.softmax_causal(host_bits(x_cpu), period, shift, dt, mode, t=t, threads=THREADS)
+    return host_bits(yg), ref, dt
+
+
+@pytest.mark.parametrize("cols,dt", [(64, "f32"), (512, "bf16"), (1000, "bf16"), (4096, "f32"),
+                                     (16384, "f32"), (40000, "f32"), (32768, "bf16")])
+@pytest.mark.parametrize("mode", MODES)
+def test_causal(q, cols, dt, mode):
+    rows = min(2 * cols, 96) if cols <= 4096 else 9
+    x = synth.normal((rows, cols), 2.0, dt, 1000 + cols % 71)
+    for period, shift in [(cols, 0), (rows, cols - rows), (7, 3), (5, -2)]:
+        say("softmax causal", dt, rows, cols, mode, period, shift)
+        g, r, d = _run_causal(q, x, mode, 0.6, period, shift)
+        assert_parity(g, r, d, "op", "causal %s %dx%d mode %d p %d s %d" % (dt, rows, cols, mode,
+                                                                            period, shift))
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_workload_attn_implicit_causal(q, mode):
+    """The attention workload with the mask implied instead of read: equal to
+    the oracle, and bit-identical to the explicit -inf input on the GPU; poison
+    in the masked half changes nothing."""
+    w = synth.WORKLOADS["attn_softmax_bf16_causal"]
+    x = w.make()
+    say(w.name, "implicit", mode)
+    g, r, d = _run_causal(q, x, mode, w.t, w.cols, 0)
+    assert_parity(g, r, d, "op", "implicit causal mode %d" % mode)
+    xg = x.to("cuda:0")
+    explicit = q.quake_softmax(xg, mode=mode, t=w.t)
+    poisoned = xg.clone()
+    i = (torch.arange(w.rows, device="cuda:0") % w.cols)[:, None]
+    j = torch.arange(w.cols, device="cuda:0")[None, :]
+    poisoned[j > i] = float("nan")
+    implicit = q.quake_softmax_causal(poisoned, period=w.cols, shift=0, mode=mode, t=w.t)
+    torch.cuda.synchronize()
+    assert check_bits(host_bits(implicit), host_bits(explicit)) is None
+
+
+@pytest.mark.parametrize("cols,dt", [(512, "bf16"), (4096, "f32"), (40000, "f32"), (1000, "bf16")])
+def test_causal_without_masked_writes(q, cols, dt):
+    rows = 64 if cols <= 4096 else 6
+    x = synth.normal((rows, cols), 2.0, dt, 1100 + cols % 61)
+    ref = oracle.softmax_causal(host_bits(x), cols, 0, dt, 2, t=1.0, threads=THREADS)
+    xg = x.to("cuda:0")
+    y = torch.full_like(xg, 7.0)
+    say("softmax causal no masked writes", dt, rows, cols)
+    q.quake_softmax_causal(xg, y, period=cols, shift=0, mode=2, write_masked=False)
+    torch.cuda.synchronize()
+    g = host_bits(y)
+    vec = 4 if dt == "f32" else 8
+    i = np.arange(rows)[:, None] % cols
+    j = np.arange(cols)[None, :]
+    live = j <= i
+    written = (j // vec) <= (i // vec) if cols % vec == 0 else live
+    # live outputs match the oracle; untouched outputs keep their old value
+    assert_parity(g[live], ref[live], dt, "op", "causal no-writes %s %d" % (dt, cols))
+    gv = oracle.decode(g.reshape(-1), dt).reshape(rows, cols)
+    assert np.all(gv[~written] == 7.0)
+    assert np.all(gv[written & ~live] == 0.0)

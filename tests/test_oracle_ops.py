@@ -277,3 +277,30 @@ def test_unfused_gelu_against_eq4_and_fused(oracle, mode):
         assert np.all(np.abs(y - ref) <= xa * (eps / (4 * (1 - eps)) + 2.0 ** -23) + 1e-37)
         f = oracle.gelu(x, "f32", mode).astype(np.float64)
         assert np.all(np.abs(y - f) <= 1e-5 * xa + 1e-37)
+
+
+# ------------------------------ implicit causal mask ------------------------
+
+@pytest.mark.parametrize("mode", [0, 1, 2])
+@pytest.mark.parametrize("period,shift", [(16, 0), (16, 3), (10, -2), (7, 100)])
+def test_causal_equals_explicit_mask(oracle, mode, period, shift):
+    # the implicit mask gives exactly what -inf entries give under Algorithm 2
+    rows, cols = 3 * period + 1, 24
+    x = _rows(30, rows, cols, 2.0)
+    i = (np.arange(rows) % period)[:, None] + shift
+    j = np.arange(cols)[None, :]
+    xm = np.where(j > i, -np.inf, x).astype(np.float32)
+    a = oracle.softmax_causal(x, period, shift, "f32", mode, t=0.7, threads=3)
+    b = oracle.softmax(xm, "f32", mode, t=0.7)
+    assert np.array_equal(a, b)
+    # masked entries are never read: poisoning them changes nothing
+    xp = np.where(j > i, np.float32(1e30), x).astype(np.float32)
+    assert np.array_equal(oracle.softmax_causal(xp, period, shift, "f32", mode, t=0.7), a)
+
+
+def test_causal_fully_masked_rows_are_zero(oracle):
+    x = _rows(31, 8, 12, 1.0)
+    y = oracle.softmax_causal(x, 4, -3, "f32", 2)
+    # L = r mod 4 - 2: rows with r mod 4 in {0, 1, 2} have no live entry, r mod 4 = 3 one
+    assert np.all(y[0::4] == 0) and np.all(y[1::4] == 0) and np.all(y[2::4] == 0)
+    assert np.all(y[3::4, 0] == 1.0) and np.all(y[3::4, 1:] == 0)
