@@ -105,3 +105,19 @@ def test_binding_rejects_host_tensors(q):
         q.quake_gelu(torch.zeros(4))
     with pytest.raises(ValueError):
         q.quake_softmax(torch.zeros(2, 4))
+
+
+def test_causal_and_unfused_validation(q):
+    L = q.lib
+    # quake_softmax_causal(x, y, rows, cols, ldx, ldy, period, shift, write_masked, dt, mode, t, s)
+    assert L.quake_softmax_causal(FAKE, FAKE, 0, 8, 8, 8, 4, 0, 1, 0, 2, 1.0, None) == q.OK
+    assert L.quake_softmax_causal(FAKE, FAKE, 4, 8, 8, 8, 0, 0, 1, 0, 2, 1.0, None) == q.EINVAL
+    assert L.quake_softmax_causal(FAKE, FAKE, 4, 8, 8, 8, -3, 0, 1, 0, 2, 1.0, None) == q.EINVAL
+    assert L.quake_softmax_causal(FAKE, FAKE, 4, 8, 8, 8, 1 << 31, 0, 1, 0, 2, 1.0, None) == q.EINVAL
+    assert L.quake_softmax_causal(FAKE, FAKE, 4, 8, 8, 8, 4, 1 << 41, 1, 0, 2, 1.0, None) == q.EINVAL
+    assert L.quake_softmax_causal(FAKE, FAKE, 4, 8, 7, 8, 4, 0, 1, 0, 2, 1.0, None) == q.EINVAL
+    assert L.quake_softmax_causal(FAKE, FAKE, 4, 8, 8, 8, 4, 0, 1, 9, 2, 1.0, None) == q.EDTYPE
+    assert L.quake_softmax_unfused(FAKE, FAKE, 4, 8, 8, 8, 0, 2, 0.0, None) == q.EINVAL
+    assert L.quake_softmax_unfused(FAKE, FAKE, 0, 8, 8, 8, 0, 2, 1.0, None) == q.OK
+    assert L.quake_gelu_unfused(FAKE, FAKE, -1, 0, 2, None) == q.EINVAL
+    assert L.quake_gelu_unfused(FAKE, FAKE, 10, 0, 5, None) == q.EMODE
