@@ -177,6 +177,26 @@ quake_status quake_softmax_unfused(const void* x, void* y, int64_t rows, int64_t
 quake_status quake_gelu_unfused(const void* x, void* y, int64_t n, quake_dtype dtype,
                                 quake_mode mode, void* stream);
 
+/*
+ * quake_softmax_split_timeouts — number of exchange waits of the split-row
+ * softmax path (rows longer than one workgroup holds) that gave up at their
+ * spin limit on `stream` since the previous call, which then resets it. Every
+ * such wait is bounded so the kernel always finishes; a nonzero count means
+ * the affected rows' outputs are not valid. With every workgroup of a launch
+ * resident at once (the library sizes launches so), the count stays 0.
+ * Synchronises `stream`. count: host pointer, non-NULL (else QUAKE_EINVAL).
+ */
+quake_status quake_softmax_split_timeouts(void* stream, int64_t* count);
+
+/*
+ * quake_test_split_fault — test hook for the bounded waits above: while on,
+ * split-row launches withhold chunk 0's exchange in every row, so every wait
+ * of those rows runs to a short spin limit and is counted by
+ * quake_softmax_split_timeouts; their outputs are invalid. Returns the
+ * previous setting. Not for production use.
+ */
+int quake_test_split_fault(int on);
+
 /* Static, human-readable name of a status code (never NULL). */
 const char* quake_status_str(quake_status s);
 

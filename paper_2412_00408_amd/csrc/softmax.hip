@@ -28,6 +28,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <map>
 #include <mutex>
 #include <utility>
@@ -217,26 +218,29 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
 // bounded by a spin limit and then flags an error instead of hanging.
 // ---------------------------------------------------------------------------
 struct SplitWs {
-  uint32_t* pmax;   // [kWsSlots]  chunk maxima (binary32 bits), index rr * G + g
-  uint64_t* psum;   // [kWsSlots]  chunk sums (binary64 bits)
-  uint32_t* done;   // [kWsSlots]  per-row count of finished workgroups
-  uint32_t* err;    // [1]         set if a wait hit its spin limit
+  uint32_t* pmax;        // [kWsSlots]  chunk maxima (binary32 bits), index rr * G + g
+  uint64_t* psum;        // [kWsSlots]  chunk sums (binary64 bits)
+  uint32_t* done;        // [kWsSlots]  per-row count of finished workgroups
+  uint32_t* err;         // [1]         number of waits that hit their spin limit
+  uint32_t spin_limit;   // polls before a wait gives up
+  uint32_t withhold;     // test hook: chunk 0 of every row never publishes
 };
 
 constexpr uint32_t kWsSlots = 8192;                 // max rows * G per launch
 constexpr uint32_t kSpinLimit = 1u << 20;           // about a second of polling
+constexpr uint32_t kTestSpinLimit = 1u << 12;       // short limit while a fault is injected
 constexpr int kMaxG = kSmBlock;                     // one polling lane per chunk
 constexpr uint32_t kSent32 = 0xFFFFFFFFu;           // a NaN never published
 constexpr uint64_t kSent64 = 0xFFFFFFFFFFFFFFFFull; // a NaN never published
 
 template <typename T>
-__device__ __forceinline__ T poll_slot(T* slot, T sentinel, T fallback, uint32_t* err) {
+__device__ __forceinline__ T poll_slot(T* slot, T sentinel, T fallback, const SplitWs& ws) {
   T v;
   uint32_t spins = 0;
   while ((v = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) == sentinel) {
     __builtin_amdgcn_s_sleep(1);
-    if (++spins == kSpinLimit) {
-      __hip_atomic_store(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (++spins >= ws.spin_limit) {
+      __hip_atomic_fetch_add(ws.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       return fallback;
     }
   }
@@ -292,12 +296,14 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
   float m = wave_max(lmax);
   if (lane == 0) s_max[wave] = m;
   __syncthreads();
-  if (threadIdx.x == 0) {
+  const bool publish = !(ws.withhold && g == 0);
+  if (threadIdx.x == 0 && publish) {
     m = fmaxf(fmaxf(s_max[0], s_max[1]), fmaxf(s_max[2], s_max[3]));
     const uint32_t mb = (m != m) ? as_u(-INFINITY) : as_u(m);
     __hip_atomic_store(pm + g, mb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  if (threadIdx.x < G) s_pmax[threadIdx.x] = as_f(poll_slot<uint32_t>(pm + threadIdx.x, kSent32, as_u(-INFINITY), ws.err));
+  if (threadIdx.x < G)
+    s_pmax[threadIdx.x] = as_f(poll_slot<uint32_t>(pm + threadIdx.x, kSent32, as_u(-INFINITY), ws));
   __syncthreads();
   m = -INFINITY;
   for (uint32_t q = 0; q < G; ++q) m = fmaxf(m, s_pmax[q]);
@@ -318,13 +324,13 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
   double total = wave_sum(acc);
   if (lane == 0) s_sum[wave] = total;
   __syncthreads();
-  if (threadIdx.x == 0) {
+  if (threadIdx.x == 0 && publish) {
     total = (s_sum[0] + s_sum[1]) + (s_sum[2] + s_sum[3]);
     const uint64_t tb = (total != total) ? 0x7FF8000000000000ull : __builtin_bit_cast(uint64_t, total);
     __hip_atomic_store(ps + g, tb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   if (threadIdx.x < G)
-    s_psum[threadIdx.x] = __builtin_bit_cast(double, poll_slot<uint64_t>(ps + threadIdx.x, kSent64, 0, ws.err));
+    s_psum[threadIdx.x] = __builtin_bit_cast(double, poll_slot<uint64_t>(ps + threadIdx.x, kSent64, 0, ws));
   __syncthreads();
   if (threadIdx.x == 0) {
     // This workgroup has read both rounds (the values are in LDS); the last
@@ -418,6 +424,7 @@ struct WsKey {
 
 static std::mutex g_ws_mu;
 static std::map<WsKey, SplitWs> g_ws;
+static std::atomic<int> g_test_fault{0};
 
 // Workspace of the split kernel for (current device, stream): allocated and
 // filled with sentinels on first use (on that stream), kept until the process
@@ -427,9 +434,12 @@ static quake_status split_workspace(hipStream_t s, SplitWs* out) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return QUAKE_EHIP;
   std::lock_guard<std::mutex> lk(g_ws_mu);
+  const bool fault = g_test_fault.load(std::memory_order_relaxed) != 0;
   auto it = g_ws.find(WsKey{dev, s});
   if (it != g_ws.end()) {
     *out = it->second;
+    out->withhold = fault ? 1u : 0u;
+    out->spin_limit = fault ? kTestSpinLimit : kSpinLimit;
     return QUAKE_OK;
   }
   const size_t n_psum = kWsSlots * sizeof(uint64_t), n_pmax = kWsSlots * sizeof(uint32_t);
@@ -441,10 +451,36 @@ static quake_status split_workspace(hipStream_t s, SplitWs* out) {
   w.pmax = reinterpret_cast<uint32_t*>(base + n_psum);
   w.done = reinterpret_cast<uint32_t*>(base + n_psum + n_pmax);
   w.err = reinterpret_cast<uint32_t*>(base + n_psum + n_pmax + n_done);
+  w.spin_limit = kSpinLimit;
+  w.withhold = 0;
   hipLaunchKernelGGL(split_ws_init_kernel, dim3(8), dim3(256), 0, s, w, kWsSlots);
   if (hipGetLastError() != hipSuccess) return QUAKE_EHIP;
   g_ws.emplace(WsKey{dev, s}, w);
   *out = w;
+  out->withhold = fault ? 1u : 0u;
+  out->spin_limit = fault ? kTestSpinLimit : kSpinLimit;
+  return QUAKE_OK;
+}
+
+static quake_status split_timeouts(hipStream_t s, int64_t* count) {
+  *count = 0;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return QUAKE_EHIP;
+  uint32_t* err = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    auto it = g_ws.find(WsKey{dev, s});
+    if (it == g_ws.end()) return QUAKE_OK;   // no split-row launch on this stream yet
+    err = it->second.err;
+  }
+  uint32_t v = 0;
+  if (hipStreamSynchronize(s) != hipSuccess) return QUAKE_EHIP;
+  if (hipMemcpy(&v, err, sizeof(v), hipMemcpyDeviceToHost) != hipSuccess) return QUAKE_EHIP;
+  if (v != 0) {
+    const uint32_t zero = 0;
+    if (hipMemcpy(err, &zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess) return QUAKE_EHIP;
+  }
+  *count = v;
   return QUAKE_OK;
 }
 
@@ -628,4 +664,13 @@ extern "C" quake_status quake_softmax_causal(const void* x, void* y, int64_t row
                                              quake_mode mode, float t, void* stream) {
   return softmax_entry<true, true>(x, y, rows, cols, ldx, ldy, dtype, mode, t, period, shift,
                                    write_masked, stream);
+}
+
+extern "C" quake_status quake_softmax_split_timeouts(void* stream, int64_t* count) {
+  if (count == nullptr) return QUAKE_EINVAL;
+  return split_timeouts(static_cast<hipStream_t>(stream), count);
+}
+
+extern "C" int quake_test_split_fault(int on) {
+  return g_test_fault.exchange(on ? 1 : 0);
 }

@@ -45,6 +45,10 @@ def _load() -> ctypes.CDLL:
     for f in (L.quake_exp, L.quake_softmax, L.quake_gelu, L.quake_sigmoid,
               L.quake_softmax_unfused, L.quake_gelu_unfused, L.quake_softmax_causal):
         f.restype = ci
+    L.quake_softmax_split_timeouts.argtypes = [vp, ctypes.POINTER(i64)]
+    L.quake_softmax_split_timeouts.restype = ci
+    L.quake_test_split_fault.argtypes = [ci]
+    L.quake_test_split_fault.restype = ci
     L.quake_status_str.argtypes = [ci]
     L.quake_status_str.restype = ctypes.c_char_p
     L.quake_abi_version.argtypes = []
@@ -61,6 +65,16 @@ def status_str(code: int) -> str:
 
 def abi_version() -> int:
     return lib.quake_abi_version()
+
+
+def softmax_split_timeouts(stream=None) -> int:
+    """Waits of the split-row softmax that hit their spin limit on the stream
+    since the last query (0 in normal operation); synchronises the stream."""
+    c = ctypes.c_int64(0)
+    s = int(torch.cuda.current_stream().cuda_stream) if stream is None else int(
+        getattr(stream, "cuda_stream", stream))
+    _raise("quake_softmax_split_timeouts", lib.quake_softmax_split_timeouts(s, ctypes.byref(c)))
+    return c.value
 
 
 def _stream(t: torch.Tensor, stream) -> int:

@@ -1,0 +1,98 @@
+"""GPU robustness: HIP-graph replay of every kernel family, and the bounded
+waits of the split-row softmax forced to time out from the host."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from compare import check_bits
+from gpu_util import THREADS, assert_parity, host_bits, say
+from paper_2412_00408_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def q():
+    assert torch.cuda.is_available(), "GPU tests need cuda:0"
+    from paper_2412_00408_amd import quake
+    return quake
+
+
+def _ops(q, bufs):
+    """One call of each kernel family on preallocated buffers."""
+    q.quake_gelu(bufs["gelu_x"], bufs["gelu_y"], mode=2)                       # pipelined stride
+    q.quake_sigmoid(bufs["sig_x"], bufs["sig_y"], mode=2, silu=True)           # one-shot
+    q.quake_softmax(bufs["attn_x"], bufs["attn_y"], mode=2, t=0.125)           # wave per row
+    q.quake_softmax(bufs["lm_x"], bufs["lm_y"], mode=2)                        # split rows
+    q.quake_softmax_causal(bufs["attn_x"], bufs["causal_y"], period=512, mode=2, t=0.125)
+    q.quake_softmax(bufs["gen_x"], bufs["gen_y"], mode=1)                      # generic
+
+
+def _bufs():
+    b = {
+        "gelu_x": synth.WORKLOADS["gelu_bf16_4096x3072"].make(n=1 << 22).to("cuda:0"),
+        "sig_x": synth.WORKLOADS["silu_f16_2p28"].make(n=1 << 26).to("cuda:0"),
+        "attn_x": synth.WORKLOADS["attn_softmax_bf16_causal"].make(rows=4096).to("cuda:0"),
+        "lm_x": synth.WORKLOADS["lmhead_softmax_f32_64x128256"].make(rows=16).to("cuda:0"),
+        "gen_x": synth.normal((37, 1001), 2.0, "f32", 1200).to("cuda:0"),
+    }
+    for k in ("gelu", "sig", "attn", "lm", "gen"):
+        b[k + "_y"] = torch.empty_like(b[k + "_x"])
+    b["causal_y"] = torch.empty_like(b["attn_x"])
+    return b
+
+
+def test_graph_replay_matches_eager(q):
+    bufs = _bufs()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):          # eager reference, and per-stream workspaces before capture
+        _ops(q, bufs)
+    s.synchronize()
+    ref = {k: v.clone() for k, v in bufs.items() if k.endswith("_y")}
+    g = torch.cuda.CUDAGraph()
+    for k in ref:
+        bufs[k].zero_()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g, stream=s):
+        _ops(q, bufs)
+    torch.cuda.synchronize()
+    scratch = torch.zeros(1 << 20, device="cuda:0")
+    for rep in range(5):
+        say("graph replay", rep)
+        for k in ref:
+            bufs[k].fill_(7.0)
+        scratch.add_(1.0)                       # the program's own eager work between replays
+        _ = q.quake_gelu(bufs["gelu_x"], mode=0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k, v in ref.items():
+            msg = check_bits(host_bits(bufs[k]), host_bits(v), name="replay %d %s" % (rep, k))
+            assert msg is None, msg
+    assert q.softmax_split_timeouts(s) == 0
+
+
+def test_split_waits_forced_to_time_out_then_recover(q):
+    w = synth.WORKLOADS["lmhead_softmax_f32_64x128256"]
+    x = w.make(rows=8)
+    xg = x.to("cuda:0")
+    ref = oracle.softmax(host_bits(x), "f32", 2, threads=THREADS)
+    y = q.quake_softmax(xg, mode=2)
+    assert q.softmax_split_timeouts() == 0
+    assert_parity(host_bits(y), ref, "f32", "op", "split before fault")
+    say("forced split timeouts")
+    prev = q.lib.quake_test_split_fault(1)
+    try:
+        assert prev == 0
+        q.quake_softmax(xg, y, mode=2)          # every wait of every row gives up, kernel ends
+        n = q.softmax_split_timeouts()
+    finally:
+        q.lib.quake_test_split_fault(0)
+    assert n > 0
+    # the workspace is back in its initial state: the next call is exact again
+    y2 = q.quake_softmax(xg, mode=2)
+    torch.cuda.synchronize()
+    assert q.softmax_split_timeouts() == 0
+    assert_parity(host_bits(y2), ref, "f32", "op", "split after fault")
