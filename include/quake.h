@@ -85,7 +85,9 @@ typedef enum {
  * powers of two, Sec. III-B). QUAKE_EXACT computes exp2(fmaf(x, fl32(a/ln2),
  * fl32(b/ln2))) with the hardware exp2.
  *   x, y : device buffers of n elements of `dtype`, contiguous.
- *   a, b : finite; otherwise QUAKE_EINVAL.
+ *   a, b : finite, with c0 and c1 finite in binary32 (|a|, |b| below about
+ *          2.8e31 in QUAKE_1/QUAKE_2, 2.3e38 in QUAKE_EXACT); otherwise
+ *          QUAKE_EINVAL.
  * QUAKE_1 and QUAKE_2 outputs are bit-exact functions of the input.
  */
 quake_status quake_exp(const void* x, void* y, int64_t n, quake_dtype dtype,
@@ -103,9 +105,13 @@ quake_status quake_exp(const void* x, void* y, int64_t n, quake_dtype dtype,
  *   x    : device, rows x cols elements, row r at x + r*ldx (elements).
  *   y    : device, row r at y + r*ldy (elements).
  *   ldx, ldy >= cols. cols >= 1 when rows >= 1.
- *   t    : temperature, finite and > 0; otherwise QUAKE_EINVAL.
+ *   t    : temperature, finite and > 0, with c0 finite in binary32 (t below
+ *          about 2.8e31 in QUAKE_1/QUAKE_2); otherwise QUAKE_EINVAL.
  * Rows may hold -inf (masking); those entries give exactly 0, and a row that
  * is entirely -inf gives a row of zeros. +inf inputs are unspecified.
+ * Folding m into c1 (one binary32 rounding of c0*m) shifts every exponent's
+ * argument by up to |t*m| * 2^-24 (natural-log units); rows with |t*m| above
+ * about 1e9 are outside the folded form's range and may give NaN.
  * Rows longer than one workgroup's registers are split over several
  * workgroups that exchange (max, sum) through a small per-stream device
  * workspace the library allocates on first use and keeps until exit.

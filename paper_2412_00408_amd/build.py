@@ -19,6 +19,9 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libquake.so")
+C_CLIENT_SRC = os.path.join(ROOT, "tests", "c", "abi_smoke.c")
+C_CLIENT = os.path.join(ROOT, "tests", "c", "abi_smoke")
+ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 
 SOURCES = ["elementwise.hip", "softmax.hip", "abi.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -56,6 +59,24 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def build_c_client(verbose: bool = False) -> str:
+    """Compile the plain-C client of the ABI (gcc, include/quake.h and the HIP
+    runtime only) that checks the library from C, without Python or torch."""
+    cmd = ["gcc", "-std=c11", "-O2", "-Wall", "-D__HIP_PLATFORM_AMD__", "-I", INCLUDE,
+           "-I", os.path.join(ROCM, "include"), C_CLIENT_SRC, "-o", C_CLIENT + ".tmp",
+           "-L", HERE, "-lquake", "-L", os.path.join(ROCM, "lib"), "-lamdhip64", "-lm",
+           "-Wl,-rpath,$ORIGIN/../../paper_2412_00408_amd",
+           "-Wl,-rpath," + os.path.join(ROCM, "lib")]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("gcc failed for the C client:\n%s\n%s" % (r.stdout, r.stderr))
+    os.replace(C_CLIENT + ".tmp", C_CLIENT)
+    if verbose:
+        print("built", C_CLIENT)
+    return C_CLIENT
+
+
 if __name__ == "__main__":
     build(verbose=True)
+    build_c_client(verbose=True)
     sys.exit(0)

@@ -1,0 +1,98 @@
+/*
+ * Plain-C client of libquake: allocates device memory with the HIP runtime,
+ * calls the C ABI declared in include/quake.h, and checks properties that hold
+ * exactly or within a known bound (no Python, no torch involved).
+ *
+ * Built by paper_2412_00408_amd/build.py (build_c_client) with gcc against
+ * include/quake.h and the HIP runtime only; run by tests/test_gpu_c_client.py.
+ * Exit status 0 on success, 1 on a failed check, 2 on a HIP error; prints one
+ * line per check.
+ */
+#include <hip/hip_runtime_api.h>
+#include <math.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "quake.h"
+
+static int failures = 0;
+
+static void check(int ok, const char* what) {
+  printf("%s: %s\n", ok ? "ok  " : "FAIL", what);
+  if (!ok) failures++;
+}
+
+#define HIPCHECK(x)                                                   \
+  do {                                                                \
+    hipError_t e_ = (x);                                              \
+    if (e_ != hipSuccess) {                                           \
+      printf("FAIL: %s -> %s\n", #x, hipGetErrorString(e_));          \
+      return 2;                                                       \
+    }                                                                 \
+  } while (0)
+
+int main(void) {
+  int ndev = 0;
+  HIPCHECK(hipGetDeviceCount(&ndev));
+  if (ndev < 1) {
+    printf("FAIL: no GPU\n");
+    return 2;
+  }
+  check(quake_abi_version() == QUAKE_ABI_VERSION, "abi version matches the header");
+
+  /* softmax of 8 rows x 1000 binary32 values: rows sum to 1 */
+  const int rows = 8, cols = 1000;
+  float* hx = (float*)malloc(sizeof(float) * rows * cols);
+  float* hy = (float*)malloc(sizeof(float) * rows * cols);
+  uint32_t s = 12345u;
+  for (int i = 0; i < rows * cols; ++i) {
+    s = s * 1664525u + 1013904223u;
+    hx[i] = ((float)(s >> 8) / 16777216.0f - 0.5f) * 8.0f;
+  }
+  void *dx = NULL, *dy = NULL;
+  HIPCHECK(hipMalloc(&dx, sizeof(float) * rows * cols));
+  HIPCHECK(hipMalloc(&dy, sizeof(float) * rows * cols));
+  HIPCHECK(hipMemcpy(dx, hx, sizeof(float) * rows * cols, hipMemcpyHostToDevice));
+  quake_status st = quake_softmax(dx, dy, rows, cols, cols, cols, QUAKE_F32, QUAKE_2, 1.0f, NULL);
+  check(st == QUAKE_OK, "quake_softmax returns QUAKE_OK");
+  HIPCHECK(hipDeviceSynchronize());
+  HIPCHECK(hipMemcpy(hy, dy, sizeof(float) * rows * cols, hipMemcpyDeviceToHost));
+  int sums_ok = 1;
+  for (int r = 0; r < rows; ++r) {
+    double sum = 0.0;
+    for (int j = 0; j < cols; ++j) sum += hy[r * cols + j];
+    if (fabs(sum - 1.0) > cols * 6e-8) sums_ok = 0;
+  }
+  check(sums_ok, "every softmax row sums to 1 within n * 2^-24");
+
+  /* QuAKE2 is exact at integer powers of two (Sec. III-B): with a = fl32(ln2),
+   * c0 = fl32(2^23 * a / ln2) = 2^23 and c1 = 127 * 2^23, so l = (k + 127) * 2^23
+   * exactly, the mantissa field is 0, y_m = 1 and the result is exactly 2^k. */
+  float hk[64], he[64];
+  for (int k = 0; k < 64; ++k) hk[k] = (float)(k - 32);
+  HIPCHECK(hipMemcpy(dx, hk, sizeof(hk), hipMemcpyHostToDevice));
+  st = quake_exp(dx, dy, 64, QUAKE_F32, QUAKE_2, 0.693147180559945309f, 0.0f, NULL);
+  check(st == QUAKE_OK, "quake_exp returns QUAKE_OK");
+  HIPCHECK(hipDeviceSynchronize());
+  HIPCHECK(hipMemcpy(he, dy, sizeof(he), hipMemcpyDeviceToHost));
+  int pow_ok = 1;
+  for (int k = 0; k < 64; ++k)
+    if (he[k] != ldexpf(1.0f, k - 32)) pow_ok = 0;
+  check(pow_ok, "QuAKE2 of x = k with a = ln2 is exactly 2^k");
+
+  /* argument validation happens before any HIP call */
+  check(quake_gelu(NULL, NULL, 5, QUAKE_F32, QUAKE_2, NULL) == QUAKE_EINVAL, "NULL buffers rejected");
+  check(quake_sigmoid(dx, dy, 5, (quake_dtype)7, QUAKE_2, 0, NULL) == QUAKE_EDTYPE, "bad dtype rejected");
+  check(quake_softmax(dx, dy, 2, 8, 4, 8, QUAKE_F32, QUAKE_2, 1.0f, NULL) == QUAKE_EINVAL,
+        "ldx < cols rejected");
+  check(strncmp(quake_status_str(QUAKE_EMODE), "QUAKE_EMODE", 11) == 0, "status strings");
+
+  HIPCHECK(hipFree(dx));
+  HIPCHECK(hipFree(dy));
+  free(hx);
+  free(hy);
+  printf("%s\n", failures ? "abi smoke FAILED" : "abi smoke passed");
+  return failures ? 1 : 0;
+}

@@ -70,6 +70,9 @@ def test_elementwise_validation(q):
     assert L.quake_exp(FAKE, FAKE, 10, 0, 2, nan, 0.0, None) == q.EINVAL
     assert L.quake_exp(FAKE, FAKE, 10, 0, 2, 1.0, inf, None) == q.EINVAL
     assert L.quake_exp(FAKE, FAKE, 10, 0, 2, 3e38, 0.0, None) == q.EINVAL   # c0 overflows
+    assert L.quake_exp(FAKE, FAKE, 10, 0, 1, -2.9e31, 0.0, None) == q.EINVAL  # 2^23 a / ln2 > max
+    assert L.quake_exp(FAKE, FAKE, 10, 0, 2, 1.0, 2.9e31, None) == q.EINVAL   # c1 overflows
+    assert L.quake_exp(FAKE, FAKE, 10, 0, 0, 1.0, 2.4e38, None) == q.EINVAL   # b / ln2 > max
 
 
 def test_softmax_validation(q):

@@ -36,6 +36,7 @@ MUTANTS = {
     "unfused_no_temperature": ("float s = d * t;                        /* temperature     */",
                                "float s = d;"),
     "unfused_gelu_sign": ("double e = (double)std_exp(-s, mode);", "double e = (double)std_exp(s, mode);"),
+    "causal_off_by_one": ("int64_t L = r % period + shift + 1;", "int64_t L = r % period + shift;"),
     "unfused_no_max": ("float d = load_el(x, bx + j, dt) - m;   /* max subtraction */",
                        "float d = load_el(x, bx + j, dt);"),
 }
