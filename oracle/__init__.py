@@ -32,7 +32,7 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 # (see tests/test_oracle_mutants.py) to show that the pins catch the mistake.
 _OVERRIDE = os.environ.get("QUAKE_ORACLE_LIB")
 
-EXACT, Q1, Q2, Q2_DIV = 0, 1, 2, 3
+EXACT, Q1, Q2, Q2M, Q2_DIV = 0, 1, 2, 3, 4
 DTYPES = {"f32": 0, "f16": 1, "bf16": 2}
 
 CFLAGS = ["-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared"]
@@ -73,6 +73,8 @@ def lib() -> ctypes.CDLL:
         L.qo_gelu_unfused.argtypes = [vp, vp, i64, ci, ci]
         L.qo_round.argtypes = [vp, vp, i64, ci]
         L.qo_decode.argtypes = [vp, vp, i64, ci]
+        L.qo_q2m_coefficients.argtypes = [vp]
+        L.qo_q2m_coefficients.restype = None
         for f in (L.qo_quake, L.qo_exp, L.qo_sigmoid, L.qo_gelu, L.qo_softmax,
                   L.qo_softmax_unfused, L.qo_gelu_unfused, L.qo_softmax_causal, L.qo_round,
                   L.qo_decode):
@@ -115,12 +117,22 @@ def constants() -> dict:
     return dict(zip(names, out.tolist()))
 
 
+def q2m_coefficients() -> dict:
+    """Minimax coefficients of Eq. 6 (mode Q2M): a0, a1, a2 in double and as
+    the binary32 values the approximation uses, the worst-case relative error E
+    and the four equioscillation points in a_m."""
+    out = np.zeros(8, np.float64)
+    lib().qo_q2m_coefficients(_ptr(out))
+    a = out[:3].copy()
+    return dict(a=a, a_f32=a.astype(np.float32), err=float(out[3]), ref=out[4:8].copy())
+
+
 def softmax_c0(t: float, mode: int) -> float:
     return float(lib().qo_softmax_c0(t, mode))
 
 
 def quake(x: np.ndarray, c0: float, c1: float, order: int) -> np.ndarray:
-    """Raw QuAKE (order Q1) / QuAKE2 (Q2, Q2_DIV) of binary32 inputs."""
+    """Raw QuAKE (order Q1) / QuAKE2 (Q2, Q2M, Q2_DIV) of binary32 inputs."""
     x = np.ascontiguousarray(x, dtype=np.float32)
     y = np.empty_like(x)
     _check(lib().qo_quake(_ptr(x), _ptr(y), x.size, c0, c1, order))

@@ -14,6 +14,10 @@
  * What each function follows:
  *   qo_quake      Sec. II-B Eq. 2-3, Sec. III-A Eq. 5 (QuAKE), Sec. III-B Eq. 6
  *                 and Algorithm 1 (QuAKE2), with explicit constants c0, c1.
+ *                 Every operator takes mode QO_Q2M too: QuAKE2 with the
+ *                 coefficients of Eq. 6 that minimise the worst-case relative
+ *                 error (the grid-search optimum of Sec. III-B, here solved by
+ *                 the Remez exchange; qo_q2m_coefficients).
  *   qo_exp        Sec. III-A: e^(a x + b) with the affine map folded into c0, c1.
  *   qo_softmax    Sec. III-C, Algorithm 2 (SoftMax-QuAKEx).
  *   qo_gelu       Sec. II-C Eq. 4 rewritten as Sec. III-D Eq. 7.
@@ -45,7 +49,7 @@
 #include <string.h>
 
 /* ---- mode / dtype codes (same numeric values as the public ABI enums) ---- */
-enum { QO_EXACT = 0, QO_Q1 = 1, QO_Q2 = 2, QO_Q2_DIV = 3 };
+enum { QO_EXACT = 0, QO_Q1 = 1, QO_Q2 = 2, QO_Q2M = 3, QO_Q2_DIV = 4 };
 enum { QO_F32 = 0, QO_F16 = 1, QO_BF16 = 2 };
 
 /* ---- IEEE binary32 layout, Sec. II-A Eq. 1: l_e = 8, l_m = 23, B = 127 ---- */
@@ -85,6 +89,77 @@ static float c1_of(double b, int mode) {
 /* fl32(1/3): a0 = 1/3 of the continuity-constrained coefficients, Sec. III-B. */
 static float third(void) { return (float)(1.0 / 3.0); }
 
+/*
+ * Minimax coefficients of Eq. 6: the quadratic y(a) = a0 a^2 + a1 a + a2 that
+ * minimises the worst-case relative error |y(a) 2^(1-a) - 1| over a = a_m in
+ * [1, 2] (f = a - 1 in [0, 1)), the problem the paper solves by grid search
+ * (Sec. III-B). Solved here by the Remez exchange: the best quadratic's error
+ * takes its extreme value E with alternating signs at four points, both ends
+ * and the two interior roots of e'(a) = 0. With w(a) = 2^(1-a),
+ * e'(a) = w (y'(a) - ln2 y(a)), so the interior extrema are the roots of the
+ * quadratic ln2 a0 a^2 + (ln2 a1 - 2 a0) a + (ln2 a2 - a1). Each step solves
+ * the 4x4 linear system y(r_i) w(r_i) - (-1)^i E = 1 on the current points
+ * r_i and moves the interior points to those roots. Computed once in double
+ * when the library loads; each coefficient is then rounded once to binary32.
+ */
+static double q2m_c[3], q2m_e, q2m_ref[4];
+static float q2m_f[3];
+
+/* Gaussian elimination with partial pivoting on a 4x5 augmented matrix. */
+static void solve4(double m[4][5], double* out) {
+  for (int c = 0; c < 4; ++c) {
+    int piv = c;
+    for (int r = c + 1; r < 4; ++r)
+      if (fabs(m[r][c]) > fabs(m[piv][c])) piv = r;
+    for (int k = 0; k < 5; ++k) {
+      double t = m[c][k];
+      m[c][k] = m[piv][k];
+      m[piv][k] = t;
+    }
+    for (int r = 0; r < 4; ++r) {
+      if (r == c) continue;
+      double f = m[r][c] / m[c][c];
+      for (int k = c; k < 5; ++k) m[r][k] -= f * m[c][k];
+    }
+  }
+  for (int c = 0; c < 4; ++c) out[c] = m[c][4] / m[c][c];
+}
+
+static void q2m_remez(void) {
+  double r[4] = {1.0, 4.0 / 3.0, 5.0 / 3.0, 2.0};
+  double sol[4] = {1.0 / 3.0, 0.0, 2.0 / 3.0, 0.0};
+  for (int it = 0; it < 100; ++it) {
+    double m[4][5];
+    for (int i = 0; i < 4; ++i) {
+      double w = exp2(1.0 - r[i]);
+      m[i][0] = r[i] * r[i] * w;
+      m[i][1] = r[i] * w;
+      m[i][2] = w;
+      m[i][3] = (i % 2) ? 1.0 : -1.0;   /* -(-1)^i E */
+      m[i][4] = 1.0;
+    }
+    solve4(m, sol);
+    /* interior extrema: roots of A a^2 + B a + C */
+    double A = LN2 * sol[0], B = LN2 * sol[1] - 2.0 * sol[0], C = LN2 * sol[2] - sol[1];
+    double disc = sqrt(B * B - 4.0 * A * C);
+    double q = -0.5 * (B + (B >= 0 ? disc : -disc));
+    double x1 = q / A, x2 = C / q;
+    double lo = x1 < x2 ? x1 : x2, hi = x1 < x2 ? x2 : x1;
+    double moved = fabs(lo - r[1]) + fabs(hi - r[2]);
+    r[1] = lo;
+    r[2] = hi;
+    if (moved < 1e-15) break;
+  }
+  for (int k = 0; k < 3; ++k) {
+    q2m_c[k] = sol[k];
+    q2m_f[k] = (float)sol[k];
+  }
+  q2m_e = fabs(sol[3]);
+  for (int k = 0; k < 4; ++k) q2m_ref[k] = r[k];
+}
+
+__attribute__((constructor)) static void qo_init(void) { q2m_remez(); }
+
 /* 1/0.044715 of Eq. 7. */
 static float a_gelu(void) { return (float)(1.0 / 0.044715); }
 
@@ -102,6 +177,16 @@ static double k_gelu(void) { return 2.0 * 0.044715 * sqrt(2.0 / 3.14159265358979
  *                     exponent field set to B; y_m = (a_m^2 + 2)/3 (Eq. 6,
  *                     a0 = 1/3, a1 = 0, a2 = 2/3) as fmaf(a_m, a_m, 2) * fl(1/3);
  *                     result = z's sign+exponent field joined with y_m's mantissa.
+ *   order QO_Q2M    : as QO_Q2 with the minimax coefficients of Eq. 6 (above),
+ *                     y_m = fmaf(fmaf(a0, a_m, a1), a_m, a2) (Horner, two FMAs);
+ *                     y_m stays inside [1, 2), so the same join applies.
+ *                     Where a_m = 1 (z's mantissa field is 0: every integer
+ *                     exponent, and both ends of the clamp) y_m is taken as 1,
+ *                     the value 2^0 itself, so the result is z's bits: exact
+ *                     powers of two, 0 for l <= 0 (masked -inf entries) and
+ *                     +inf at the top of the clamp, as with the paper's
+ *                     coefficients (the optimum's y_m(1) = 1.0017 would join
+ *                     to a nonzero denormal at the bottom and NaN at the top).
  *   order QO_Q2_DIV : as QO_Q2 with the literal float expression (a*a + 2) / 3.
  */
 static float quake_one(float x, float c0, float c1, int order) {
@@ -115,10 +200,13 @@ static float quake_one(float x, float c0, float c1, int order) {
   float ym;
   if (order == QO_Q2_DIV) {
     ym = (am * am + 2.0f) / 3.0f;
+  } else if (order == QO_Q2M) {
+    ym = fmaf(fmaf(q2m_f[0], am, q2m_f[1]), am, q2m_f[2]);
   } else {
     ym = fmaf(am, am, 2.0f) * third();
   }
   uint32_t yi = ((uint32_t)z & MASK_SIGN_EXP) + f2u(ym) - EXP_B;
+  if (order == QO_Q2M && ((uint32_t)z & MASK_MANT) == 0) yi = (uint32_t)z;
   return u2f(yi);
 }
 
@@ -221,6 +309,14 @@ void qo_constants(float* out) {
   out[9] = (float)(-k_gelu() / LN2);   /* EXACT-mode GELU scale      */
 }
 
+/* The minimax coefficients of Eq. 6 (double), their worst-case relative
+ * error E and the four equioscillation points: out[0..2], out[3], out[4..7]. */
+void qo_q2m_coefficients(double* out) {
+  for (int k = 0; k < 3; ++k) out[k] = q2m_c[k];
+  out[3] = q2m_e;
+  for (int k = 0; k < 4; ++k) out[4 + k] = q2m_ref[k];
+}
+
 /* c0 of the softmax for temperature t (Algorithm 2): 2^23 t / ln2. */
 float qo_softmax_c0(float t, int mode) {
   if (mode == QO_EXACT) return (float)((double)t / LN2);
@@ -229,7 +325,7 @@ float qo_softmax_c0(float t, int mode) {
 
 /* Raw QuAKE with explicit constants, binary32 in and out. */
 int qo_quake(const float* x, float* y, int64_t n, float c0, float c1, int order) {
-  if (order != QO_Q1 && order != QO_Q2 && order != QO_Q2_DIV) return 3;
+  if (order != QO_Q1 && order != QO_Q2 && order != QO_Q2M && order != QO_Q2_DIV) return 3;
   for (int64_t i = 0; i < n; ++i) y[i] = quake_one(x[i], c0, c1, order);
   return 0;
 }

@@ -76,7 +76,7 @@ static void elementwise(void) {
     float* dec = (float*)malloc(n * 4);
     float* out = (float*)malloc(n * 4);
     EXPECT(qo_decode(x, dec, n, dt) == 0, "decode dt=%d", dt);
-    for (int mode = 0; mode < 4; ++mode) {
+    for (int mode = 0; mode < 5; ++mode) {
       const float ab[][2] = {{1.0f, 0.0f}, {-1.0f, 0.0f}, {0.5f, -3.0f}, {1e30f, 0.0f},
                              {1e-30f, 5.0f}};
       for (size_t k = 0; k < sizeof(ab) / sizeof(ab[0]); ++k) {
@@ -131,7 +131,7 @@ static void softmax(void) {
   x[6 * ld + 9] = NAN;
   for (int64_t i = 0; i < rows * ld; ++i) xh[i] = (uint16_t)(s = s * 1664525u + 1013904223u) ;
   const float temps[] = {1.4e-45f, 1e-30f, 0.125f, 1.0f, 1e10f, 2.8e31f};
-  for (int mode = 0; mode < 4; ++mode) {
+  for (int mode = 0; mode < 5; ++mode) {
     for (size_t k = 0; k < sizeof(temps) / sizeof(temps[0]); ++k) {
       const float t = temps[k];
       if (!isfinite(qo_softmax_c0(t, mode))) continue;

@@ -37,6 +37,10 @@ MUTANTS = {
                                "float s = d;"),
     "unfused_gelu_sign": ("double e = (double)std_exp(-s, mode);", "double e = (double)std_exp(s, mode);"),
     "causal_off_by_one": ("int64_t L = r % period + shift + 1;", "int64_t L = r % period + shift;"),
+    "q2m_no_alternation": ("m[i][3] = (i % 2) ? 1.0 : -1.0;   /* -(-1)^i E */", "m[i][3] = -1.0;"),
+    "q2m_horner_swap": ("ym = fmaf(fmaf(q2m_f[0], am, q2m_f[1]), am, q2m_f[2]);",
+                        "ym = fmaf(fmaf(q2m_f[0], am, q2m_f[2]), am, q2m_f[1]);"),
+    "q2m_integer_rule_missing": ("  if (order == QO_Q2M && ((uint32_t)z & MASK_MANT) == 0) yi = (uint32_t)z;\n", ""),
     "unfused_no_max": ("float d = load_el(x, bx + j, dt) - m;   /* max subtraction */",
                        "float d = load_el(x, bx + j, dt);"),
 }
@@ -60,7 +64,8 @@ def test_pins_catch_mutant(name, tmp_path):
     env = dict(os.environ, QUAKE_ORACLE_LIB=str(so))
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                         os.path.join(HERE, "test_oracle_scalar.py"),
-                        os.path.join(HERE, "test_oracle_ops.py")],
+                        os.path.join(HERE, "test_oracle_ops.py"),
+                        os.path.join(HERE, "test_oracle_q2m.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, "mutant %s survived the pins:\n%s" % (name, r.stdout[-2000:])
     assert "failed" in r.stdout or "error" in r.stdout.lower()
