@@ -40,6 +40,15 @@
  *                refined with y_m = (a_m^2 + 2)/3 (Eq. 6 with a0 = 1/3, a1 = 0,
  *                a2 = 2/3), evaluated as fmaf(a_m, a_m, 2) * fl(1/3), and joined
  *                to the exponent field of z.
+ *   QUAKE_2M     QuAKE2 with the coefficients of Eq. 6 that minimise the
+ *                worst-case relative error over [0, 1) (the optimum of the
+ *                paper's grid search, Sec. III-B; solved exactly by the Remez
+ *                exchange: a0 = 0.33718944, a1 = -0.016742593, a2 = 0.68127793
+ *                in binary32, worst case 0.1725 %): y_m = fmaf(fmaf(a0, a_m,
+ *                a1), a_m, a2), joined as in QUAKE_2. Where a_m = 1 (integer
+ *                exponents, both clamp ends) the result is z's bits, so 0, +inf
+ *                and exact powers of two are kept. Half QuAKE2's worst-case
+ *                error, not continuous at binade edges, monotone.
  *   Before convert_to_int, l is clamped to [0, 255 * 2^23] (our reading of the
  *   v_min clamp of Algorithm 2, applied to every operator): inputs whose result
  *   underflows give 0 (or a denormal ramp), +inf or overflowing inputs give
@@ -54,7 +63,7 @@
 extern "C" {
 #endif
 
-#define QUAKE_ABI_VERSION 1
+#define QUAKE_ABI_VERSION 2
 
 typedef enum {
   QUAKE_F32 = 0,  /* IEEE binary32 */
@@ -65,7 +74,8 @@ typedef enum {
 typedef enum {
   QUAKE_EXACT = 0,
   QUAKE_1 = 1,
-  QUAKE_2 = 2
+  QUAKE_2 = 2,
+  QUAKE_2M = 3
 } quake_mode;
 
 typedef enum {
@@ -81,14 +91,14 @@ typedef enum {
  * Sec. III-A, Eq. 5: the affine map is folded into the constants,
  *   c0 = fl32(2^23 * a / ln2),  c1 = fl32(2^23 * (127 - beta + b / ln2)),
  * each evaluated in double and rounded once. beta is the Schraudolph bias
- * 0.0436 in QUAKE_1 (Sec. III-A) and 0 in QUAKE_2 (QuAKE2 is exact at integer
- * powers of two, Sec. III-B). QUAKE_EXACT computes exp2(fmaf(x, fl32(a/ln2),
+ * 0.0436 in QUAKE_1 (Sec. III-A) and 0 in QUAKE_2 and QUAKE_2M (QuAKE2 is
+ * exact at integer powers of two, Sec. III-B). QUAKE_EXACT computes exp2(fmaf(x, fl32(a/ln2),
  * fl32(b/ln2))) with the hardware exp2.
  *   x, y : device buffers of n elements of `dtype`, contiguous.
  *   a, b : finite, with c0 and c1 finite in binary32 (|a|, |b| below about
  *          2.8e31 in QUAKE_1/QUAKE_2, 2.3e38 in QUAKE_EXACT); otherwise
  *          QUAKE_EINVAL.
- * QUAKE_1 and QUAKE_2 outputs are bit-exact functions of the input.
+ * QUAKE_1, QUAKE_2 and QUAKE_2M outputs are bit-exact functions of the input.
  */
 quake_status quake_exp(const void* x, void* y, int64_t n, quake_dtype dtype,
                        quake_mode mode, float a, float b, void* stream);

@@ -197,9 +197,9 @@ quake_status ew_dispatch(const void* x, void* y, int64_t n, int dt, int mode, co
                          hipStream_t s) {
 #define QK_EW_CASE(D, M) \
   if (dt == D && mode == M) return ew_launch<D, OP, M>(x, y, n, p, s);
-  QK_EW_CASE(F32, EXACT) QK_EW_CASE(F32, Q1) QK_EW_CASE(F32, Q2)
-  QK_EW_CASE(F16, EXACT) QK_EW_CASE(F16, Q1) QK_EW_CASE(F16, Q2)
-  QK_EW_CASE(BF16, EXACT) QK_EW_CASE(BF16, Q1) QK_EW_CASE(BF16, Q2)
+  QK_EW_CASE(F32, EXACT) QK_EW_CASE(F32, Q1) QK_EW_CASE(F32, Q2) QK_EW_CASE(F32, Q2M)
+  QK_EW_CASE(F16, EXACT) QK_EW_CASE(F16, Q1) QK_EW_CASE(F16, Q2) QK_EW_CASE(F16, Q2M)
+  QK_EW_CASE(BF16, EXACT) QK_EW_CASE(BF16, Q1) QK_EW_CASE(BF16, Q2) QK_EW_CASE(BF16, Q2M)
 #undef QK_EW_CASE
   return QUAKE_EMODE;
 }

@@ -6,6 +6,7 @@
 //   Eq. 3               z = convert_to_int(l), one v_cvt_i32_f32 (truncating)
 //   Eq. 2 (QuAKE)       result = bits of z
 //   Alg. 1 (QuAKE2)     a_m = (z & 0x007FFFFF) | 0x3F800000   (v_and_or_b32)
+//                       (QuAKE2M: the same with the minimax coefficients of Eq. 6)
 //                       y_m = fma(a_m, a_m, 2) * fl(1/3)      (Eq. 6, a0=1/3, a2=2/3)
 //                       result = (z & 0xFF800000) + bits(y_m) - 0x3F800000, which is
 //                       one v_bfi_b32: y_m lies in [1, 2), so bits(y_m) - 0x3F800000
@@ -20,7 +21,7 @@
 
 namespace qk {
 
-enum Mode : int { EXACT = 0, Q1 = 1, Q2 = 2 };
+enum Mode : int { EXACT = 0, Q1 = 1, Q2 = 2, Q2M = 3 };
 enum Dt : int { F32 = 0, F16 = 1, BF16 = 2 };
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -32,6 +33,13 @@ constexpr float kThird = (float)(1.0 / 3.0);          // fl32(1/3)
 constexpr uint32_t kMantMask = 0x007FFFFFu;           // Alg. 1: keep mantissa
 constexpr uint32_t kSignExpMask = 0xFF800000u;        // Alg. 1: keep sign + exponent
 constexpr uint32_t kExpB = 0x3F800000u;               // Alg. 1: exponent field := B
+// Coefficients of Eq. 6 minimising max |y_m(a) 2^(1-a) - 1| over a in [1, 2]
+// (the grid-search optimum of Sec. III-B): the Remez solution in double,
+// 0.33718943461968731, -0.016742593503297265, 0.68127792209835503 (worst case
+// 0.17247632 %), each rounded once to binary32.
+constexpr float kQ2mA0 = 0x1.594830p-2f;
+constexpr float kQ2mA1 = -0x1.124f86p-6f;
+constexpr float kQ2mA2 = 0x1.5cd076p-1f;
 
 __device__ __forceinline__ uint32_t umin32(uint32_t a, uint32_t b) { return a < b ? a : b; }
 
@@ -45,10 +53,19 @@ __device__ __forceinline__ float quake_of_l(float l) {
   const uint32_t z = (uint32_t)(int32_t)l;
   if constexpr (MODE == Q1) {
     return as_f(z);
-  } else {
+  } else if constexpr (MODE == Q2) {
     const float am = as_f((z & kMantMask) | kExpB);
     const float ym = __builtin_fmaf(am, am, 2.0f) * kThird;
     return as_f((z & kSignExpMask) | (as_u(ym) & kMantMask));
+  } else {
+    // minimax coefficients, Horner form; y_m in [1.0017, 1.9966) so the same
+    // join applies. At a_m = 1 the result is z itself (y_m := 1): exact powers
+    // of two, and 0 / +inf at the two ends of the clamp.
+    const uint32_t mz = z & kMantMask;
+    const float am = as_f(mz | kExpB);
+    const float ym = __builtin_fmaf(__builtin_fmaf(kQ2mA0, am, kQ2mA1), am, kQ2mA2);
+    const uint32_t j = (z & kSignExpMask) | (as_u(ym) & kMantMask);
+    return as_f(mz == 0 ? z : j);
   }
 }
 
@@ -89,16 +106,19 @@ __device__ __forceinline__ float f16_hi(uint32_t w) {
   return (float)__builtin_bit_cast(_Float16, (uint16_t)(w >> 16));
 }
 
-// Round-to-nearest-even narrowing (v_cvt_pk_bf16_f32 / v_cvt_f16_f32).
+// Round-to-nearest-even narrowing of two binary32 values into one dword, one
+// instruction each (v_cvt_pk_bf16_f32 / v_cvt_pk_f16_f32); converting the
+// halves separately costs two conversions plus a shift-and-or per pair.
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
-  const uint32_t lo = __builtin_bit_cast(uint16_t, (__bf16)a);
-  const uint32_t hi = __builtin_bit_cast(uint16_t, (__bf16)b);
-  return lo | (hi << 16);
+  const f32x2_t v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 __device__ __forceinline__ uint32_t pack_f16(float a, float b) {
-  const uint32_t lo = __builtin_bit_cast(uint16_t, (_Float16)a);
-  const uint32_t hi = __builtin_bit_cast(uint16_t, (_Float16)b);
-  return lo | (hi << 16);
+  const f32x2_t v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, f16x2_t));
 }
 
 template <int DT>

@@ -51,7 +51,9 @@ inline float softmax_c0(double t, int mode) {
 }
 
 inline bool valid_dtype(int d) { return d == QUAKE_F32 || d == QUAKE_F16 || d == QUAKE_BF16; }
-inline bool valid_mode(int m) { return m == QUAKE_EXACT || m == QUAKE_1 || m == QUAKE_2; }
+inline bool valid_mode(int m) {
+  return m == QUAKE_EXACT || m == QUAKE_1 || m == QUAKE_2 || m == QUAKE_2M;
+}
 inline int64_t elem_size(int d) { return d == QUAKE_F32 ? 4 : 2; }
 
 inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }

@@ -635,9 +635,9 @@ static quake_status softmax_entry(const void* x, void* y, int64_t rows, int64_t 
                  static_cast<hipStream_t>(stream)};
 #define QK_SM_CASE(D, M) \
   if (dtype == D && mode == M) return sm_dispatch<D, M, FUSE, CAUSAL>(x, y, ldx, ldy, a);
-  QK_SM_CASE(F32, EXACT) QK_SM_CASE(F32, Q1) QK_SM_CASE(F32, Q2)
-  QK_SM_CASE(F16, EXACT) QK_SM_CASE(F16, Q1) QK_SM_CASE(F16, Q2)
-  QK_SM_CASE(BF16, EXACT) QK_SM_CASE(BF16, Q1) QK_SM_CASE(BF16, Q2)
+  QK_SM_CASE(F32, EXACT) QK_SM_CASE(F32, Q1) QK_SM_CASE(F32, Q2) QK_SM_CASE(F32, Q2M)
+  QK_SM_CASE(F16, EXACT) QK_SM_CASE(F16, Q1) QK_SM_CASE(F16, Q2) QK_SM_CASE(F16, Q2M)
+  QK_SM_CASE(BF16, EXACT) QK_SM_CASE(BF16, Q1) QK_SM_CASE(BF16, Q2) QK_SM_CASE(BF16, Q2M)
 #undef QK_SM_CASE
   return QUAKE_EMODE;
 }

@@ -16,9 +16,9 @@ import torch
 
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libquake.so")
 
-EXACT, QUAKE_1, QUAKE_2 = 0, 1, 2
-MODES = {"exact": EXACT, "quake1": QUAKE_1, "quake2": QUAKE_2, EXACT: EXACT, QUAKE_1: QUAKE_1,
-         QUAKE_2: QUAKE_2}
+EXACT, QUAKE_1, QUAKE_2, QUAKE_2M = 0, 1, 2, 3
+MODES = {"exact": EXACT, "quake1": QUAKE_1, "quake2": QUAKE_2, "quake2m": QUAKE_2M, EXACT: EXACT,
+         QUAKE_1: QUAKE_1, QUAKE_2: QUAKE_2, QUAKE_2M: QUAKE_2M}
 DTYPES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
 OK, EINVAL, EDTYPE, EMODE, EHIP = 0, 1, 2, 3, 4
 

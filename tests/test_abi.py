@@ -64,7 +64,8 @@ def test_elementwise_validation(q):
         assert call(FAKE, None, 10, 0, 2) == q.EINVAL
         assert call(FAKE, FAKE, 10, 3, 2) == q.EDTYPE
         assert call(FAKE, FAKE, 10, -1, 2) == q.EDTYPE
-        assert call(FAKE, FAKE, 10, 0, 3) == q.EMODE
+        assert call(FAKE, FAKE, 10, 0, 4) == q.EMODE
+        assert call(FAKE, FAKE, 10, 0, -1) == q.EMODE
         assert call(FAKE, FAKE, 0, 7, 2) == q.EDTYPE        # enums are checked first
     nan, inf = float("nan"), float("inf")
     assert L.quake_exp(FAKE, FAKE, 10, 0, 2, nan, 0.0, None) == q.EINVAL

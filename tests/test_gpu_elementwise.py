@@ -11,7 +11,7 @@ from paper_2412_00408_amd import synth
 
 pytestmark = pytest.mark.gpu
 
-MODES = [0, 1, 2]
+MODES = [0, 1, 2, 3]
 DT = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
 
 
@@ -22,7 +22,7 @@ def q():
     return quake
 
 
-@pytest.mark.parametrize("mode", [1, 2])
+@pytest.mark.parametrize("mode", [1, 2, 3])
 def test_exp_f32_bit_exact_every_input(q, mode):
     """QuAKE / QuAKE2 exp of every binary32 bit pattern (NaN inputs excluded)."""
     chunk = 1 << 26

@@ -13,7 +13,7 @@ from paper_2412_00408_amd import synth
 
 pytestmark = pytest.mark.gpu
 
-MODES = [0, 1, 2]
+MODES = [0, 1, 2, 3]
 
 
 @pytest.fixture(scope="module")
