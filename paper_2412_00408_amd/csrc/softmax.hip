@@ -203,6 +203,119 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
 }
 
 // ---------------------------------------------------------------------------
+// Square causal blocks (period = cols = P, shift = 0): row r of a block has
+// r + 1 live entries, so a wave that owns one row leaves most lanes idle in
+// the block's upper rows. Here a wave owns two rows whose live vectors fit its
+// 64 lanes together: r and M - 1 - r, with M = P - K and K = max(0, P - 63 V)
+// (then ceil((r+1)/V) + ceil((M-r)/V) <= 64). Lanes [0, nA) hold row A's live
+// vectors and lanes [nA, nA + nB) row B's; max and sum are reduced per row
+// over its own lanes (the other lanes contribute the identity). Row B's
+// partial sums are first rotated down by nA lanes (ds_bpermute), so both rows
+// are summed over lanes 0, 1, ... in the one-row kernel's reduction tree and
+// the results are bit-identical to it. Rows M .. P-1, and the middle row
+// when M is odd, take a wave alone. Masked entries are neither read nor
+// computed; with write_masked their outputs are stored as zeros.
+// ---------------------------------------------------------------------------
+// v of lane (lane + k) mod 64, for every lane (ds_bpermute).
+__device__ __forceinline__ float lane_rotate(float v, uint32_t k) {
+  const int src = (int)((((uint32_t)(threadIdx.x & 63) + k) & 63u) << 2);
+  return as_f((uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)as_u(v)));
+}
+__device__ __forceinline__ double lane_rotate(double v, uint32_t k) {
+  const int src = (int)((((uint32_t)(threadIdx.x & 63) + k) & 63u) << 2);
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)(uint32_t)u);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)(uint32_t)(u >> 32));
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+struct PairArg {
+  uint32_t P;        // rows per block = cols
+  uint32_t M;        // rows [0, M) are paired r <-> M - 1 - r
+  uint32_t J;        // jobs (waves) per block: M / 2 + (M & 1) + (P - M)
+  uint32_t jobs;     // jobs in this launch (whole blocks)
+  uint32_t write_masked;
+};
+
+template <int DT, int MODE, bool FUSE>
+__global__ __launch_bounds__(kSmBlock) void sm_causal_pair_kernel(const char* __restrict__ x,
+                                                                 char* __restrict__ y,
+                                                                 int64_t ldx_b, int64_t ldy_b,
+                                                                 SmConst kc, PairArg pa) {
+  constexpr int V = kV<DT>;
+  using Acc = typename AccOf<DT>::T;
+  const int lane = threadIdx.x & 63;
+  const uint32_t job = blockIdx.x * (kSmBlock / 64) + (threadIdx.x >> 6);
+  if (job >= pa.jobs) return;   // uniform per wave
+
+  const uint32_t blk = job / pa.J;
+  const uint32_t j = job - blk * pa.J;
+  const uint32_t npairs = pa.M / 2;
+  uint32_t rA, rB = 0;
+  const bool pair = j < npairs;
+  if (pair) {
+    rA = j;
+    rB = pa.M - 1 - j;
+  } else {
+    const uint32_t s = j - npairs;
+    rA = (pa.M & 1) ? (s == 0 ? npairs : pa.M + s - 1) : pa.M + s;
+  }
+  const uint32_t nvr = pa.P / V;
+  const uint32_t LA = rA + 1, LB = pair ? rB + 1 : 0;
+  const uint32_t nA = (LA + V - 1) / V, nB = (LB + V - 1) / V;
+  const bool inA = (uint32_t)lane < nA;
+  const bool inB = !inA && (uint32_t)lane - nA < nB;
+  // idle lanes re-read row A's last live vector (in bounds, no branch)
+  const uint32_t row = inB ? rB : rA;
+  const uint32_t vi = inA ? (uint32_t)lane : (inB ? (uint32_t)lane - nA : nA - 1);
+  const uint32_t Lrow = inB ? LB : ((inA) ? LA : 0);
+
+  const int64_t grow = (int64_t)blk * pa.P + row;
+  const u32x4* xr = reinterpret_cast<const u32x4*>(x + grow * ldx_b);
+  const u32x4 raw = __builtin_nontemporal_load(xr + vi);
+  float f[V];
+  unpack<DT>(raw, f);
+  float lmax = -INFINITY;
+#pragma unroll
+  for (int e = 0; e < V; ++e) {
+    f[e] = (vi * V + e < Lrow) ? f[e] : -INFINITY;
+    lmax = fmaxf(lmax, f[e]);
+  }
+  const float mA = wave_max(inA ? lmax : -INFINITY);
+  const float mB = pair ? wave_max(inB ? lmax : -INFINITY) : -INFINITY;
+  const float m = inB ? mB : mA;
+
+  const RowExp<MODE, FUSE> ex = row_exp<MODE, FUSE>(kc, m);
+  float part = 0.0f;
+#pragma unroll
+  for (int e = 0; e < V; ++e) {
+    f[e] = ex(f[e]);
+    part += f[e];
+  }
+  const Acc acc = (Acc)part;
+  const Acc tA = wave_sum_acc(inA ? acc : (Acc)0);
+  const Acc tB = pair ? wave_sum_acc(lane_rotate(inB ? acc : (Acc)0, nA)) : (Acc)0;
+  const float r = (m == -INFINITY) ? 0.0f : inv_total(inB ? tB : tA);
+
+  if (inA || inB) {
+    u32x4* yr = reinterpret_cast<u32x4*>(y + grow * ldy_b);
+#pragma unroll
+    for (int e = 0; e < V; ++e) f[e] *= r;
+    __builtin_nontemporal_store(pack<DT>(f), yr + vi);
+  }
+  if (pa.write_masked) {
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    const int64_t gA = (int64_t)blk * pa.P + rA;
+    if (nA + lane < nvr)
+      __builtin_nontemporal_store(z, reinterpret_cast<u32x4*>(y + gA * ldy_b) + nA + lane);
+    if (pair && nB + lane < nvr) {
+      const int64_t gB = (int64_t)blk * pa.P + rB;
+      __builtin_nontemporal_store(z, reinterpret_cast<u32x4*>(y + gB * ldy_b) + nB + lane);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Split rows: G workgroups per row, exchanging chunk max and chunk sum.
 //
 // Exchange without fences: every chunk owns one 32-bit slot for its max and
@@ -528,6 +641,42 @@ static quake_status launch_rows(const SmArgs& a) {
   return QUAKE_OK;
 }
 
+// Square causal blocks with rows of at most 64 vectors: the paired kernel on
+// whole blocks. Returns false (nothing launched) when the shape does not apply.
+template <int DT, int MODE, bool FUSE>
+static bool pair_applies(const SmArgs& a) {
+  constexpr int V = kV<DT>;
+  return a.period == a.cols && a.shift == 0 && a.cols % V == 0 && a.cols / V <= 64 &&
+         a.rows >= a.period;
+}
+
+template <int DT, int MODE, bool FUSE>
+static quake_status launch_causal_pair(const SmArgs& a, int64_t* rows_done) {
+  constexpr int V = kV<DT>;
+  const uint32_t P = (uint32_t)a.cols;
+  const uint32_t K = P > 63u * V ? P - 63u * V : 0u;
+  PairArg pa;
+  pa.P = P;
+  pa.M = P - K;
+  pa.J = pa.M / 2 + (pa.M & 1) + K;
+  pa.write_masked = a.write_masked;
+  const int64_t nblocks = a.rows / P;
+  // blocks per launch: keep the job count (and the grid) below 2^31
+  const int64_t per = std::max<int64_t>(1, (int64_t(1) << 30) / pa.J);
+  for (int64_t b0 = 0; b0 < nblocks; b0 += per) {
+    const int64_t nb = std::min(per, nblocks - b0);
+    pa.jobs = (uint32_t)(nb * pa.J);
+    const uint32_t grid = (pa.jobs + (kSmBlock / 64) - 1) / (kSmBlock / 64);
+    const int64_t r0 = b0 * P;
+    hipLaunchKernelGGL((sm_causal_pair_kernel<DT, MODE, FUSE>), dim3(grid), dim3(kSmBlock), 0, a.s,
+                       a.x + r0 * a.ldx_b, a.y + r0 * a.ldy_b, a.ldx_b, a.ldy_b, a.kc, pa);
+    const quake_status st = launch_status();
+    if (st != QUAKE_OK) return st;
+  }
+  *rows_done = nblocks * P;
+  return QUAKE_OK;
+}
+
 template <int DT, int MODE, bool FUSE, bool CAUSAL>
 static quake_status launch_generic(const void* x, void* y, const SmArgs& a, int64_t ldx,
                                    int64_t ldy) {
@@ -594,6 +743,19 @@ static quake_status sm_dispatch(const void* x, void* y, int64_t ldx, int64_t ldy
   a.ldx_b = ldx * esz;
   a.ldy_b = ldy * esz;
   const int64_t nvr = cols / V;
+  if constexpr (CAUSAL) {
+    if (pair_applies<DT, MODE, FUSE>(a)) {
+      int64_t done = 0;
+      const quake_status st = launch_causal_pair<DT, MODE, FUSE>(a, &done);
+      if (st != QUAKE_OK || done == a.rows) return st;
+      // rows after the last whole block: the one-row kernel (r0 is a multiple of P)
+      SmArgs rest = a;
+      rest.x = a.x + done * a.ldx_b;
+      rest.y = a.y + done * a.ldy_b;
+      rest.rows = a.rows - done;
+      return launch_rows<DT, MODE, FUSE, CAUSAL, 1, 1>(rest);
+    }
+  }
   if (nvr <= 64) return launch_rows<DT, MODE, FUSE, CAUSAL, 1, 1>(a);
   if (nvr <= 128) return launch_rows<DT, MODE, FUSE, CAUSAL, 2, 1>(a);
   if (nvr <= 256) return launch_rows<DT, MODE, FUSE, CAUSAL, 4, 1>(a);

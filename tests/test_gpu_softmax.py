@@ -297,3 +297,41 @@ def test_causal_without_masked_writes(q, cols, dt):
     gv = oracle.decode(g.reshape(-1), dt).reshape(rows, cols)
     assert np.all(gv[~written] == 7.0)
     assert np.all(gv[written & ~live] == 0.0)
+
+
+# Square causal blocks (period = cols, shift = 0, at most 64 vectors per row)
+# take the paired-row kernel: two rows per wave, r and M - 1 - r. Shapes cover
+# K = 0 and K > 0 (P above 63 vectors), odd M, one-vector rows, a trailing
+# partial block (handled by the one-row kernel) and padded row strides.
+@pytest.mark.parametrize("P,dt,rows,pad", [(512, "bf16", 2 * 512 + 37, 0), (504, "bf16", 504, 8),
+                                           (256, "f32", 2 * 256 + 3, 0), (252, "f32", 252, 4),
+                                           (200, "f16", 401, 0), (8, "bf16", 40, 0),
+                                           (4, "f32", 13, 4), (72, "bf16", 3 * 72, 0)])
+@pytest.mark.parametrize("mode", MODES)
+def test_causal_paired_rows(q, P, dt, rows, pad, mode):
+    ld = P + pad
+    x = synth.normal((rows, ld), 2.0, dt, 1200 + P)
+    xg = x.to("cuda:0")[:, :P]
+    say("softmax causal paired", dt, rows, P, pad, mode)
+    for wm in (True, False):
+        y = torch.full((rows, ld), 5.0, dtype=xg.dtype, device="cuda:0")[:, :P]
+        q.quake_softmax_causal(xg, y, period=P, shift=0, mode=mode, t=0.7, write_masked=wm)
+        torch.cuda.synchronize()
+        g = host_bits(y)
+        ref = oracle.softmax_causal(host_bits(x[:, :P]), P, 0, dt, mode, t=0.7, threads=THREADS)
+        i = np.arange(rows)[:, None] % P
+        j = np.arange(P)[None, :]
+        live = j <= i
+        vec = 4 if dt == "f32" else 8
+        written = live | ((j // vec) <= (i // vec)) if not wm else np.ones_like(live)
+        assert_parity(g[written], ref[written], dt, "op", "paired %s P %d wm %d" % (dt, P, wm))
+        if not wm:
+            gv = oracle.decode(g.reshape(-1), dt).reshape(rows, P)
+            assert np.all(gv[~written] == 5.0)
+        # bit-identical to the one-row kernel reading explicit -inf entries
+        xm = xg.clone()
+        xm[torch.from_numpy(~live).to("cuda:0")] = float("-inf")
+        e = q.quake_softmax(xm, mode=mode, t=0.7)
+        torch.cuda.synchronize()
+        eb = host_bits(e)
+        assert check_bits(g[written], eb[written]) is None
