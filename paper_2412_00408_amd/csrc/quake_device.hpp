@@ -149,6 +149,14 @@ __device__ __forceinline__ u32x4 pack(const float* f) {
   return v;
 }
 
+// A 16-byte vector of -inf in each format (masked lanes of a softmax row).
+template <int DT>
+__device__ __forceinline__ u32x4 neg_inf_vec() {
+  constexpr uint32_t w = (DT == F32) ? 0xFF800000u : (DT == F16 ? 0xFC00FC00u : 0xFF80FF80u);
+  const u32x4 v = {w, w, w, w};
+  return v;
+}
+
 template <int DT>
 __device__ __forceinline__ float load1(const void* p, int64_t i) {
   if constexpr (DT == F32) {
@@ -206,13 +214,34 @@ __device__ __forceinline__ double readlane_f64(double v, int lane) {
   return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
 }
 
+// The wave maximum runs on order-preserving integer images of the values: a
+// binary32 pattern with its magnitude bits flipped when negative compares as a
+// signed int32 exactly as the floats compare (NaN aside), so each step is one
+// v_max_i32 with a DPP operand and the last combination runs on the scalar
+// unit. A float max would need the DPP value quieted (IEEE mode) first.
+__device__ __forceinline__ int32_t ord_key(float v) {
+  const int32_t u = (int32_t)as_u(v);
+  return u ^ (int32_t)((uint32_t)(u >> 31) >> 1);
+}
+__device__ __forceinline__ float ord_val(int32_t k) {
+  return as_f((uint32_t)(k ^ (int32_t)((uint32_t)(k >> 31) >> 1)));
+}
+template <int CTRL>
+__device__ __forceinline__ int32_t dpp_max_i32(int32_t k) {
+  const int32_t o = __builtin_amdgcn_update_dpp(INT32_MIN, k, CTRL, 0xF, 0xF, false);
+  return k > o ? k : o;
+}
+
 __device__ __forceinline__ float wave_max(float v) {
-  v = fmaxf(v, dpp_f32<kDppXor1>(v));
-  v = fmaxf(v, dpp_f32<kDppXor2>(v));
-  v = fmaxf(v, dpp_f32<kDppHalfMirror>(v));
-  v = fmaxf(v, dpp_f32<kDppMirror>(v));
-  return fmaxf(fmaxf(readlane_f32(v, 0), readlane_f32(v, 16)),
-               fmaxf(readlane_f32(v, 32), readlane_f32(v, 48)));
+  int32_t k = ord_key(v);
+  k = dpp_max_i32<kDppXor1>(k);
+  k = dpp_max_i32<kDppXor2>(k);
+  k = dpp_max_i32<kDppHalfMirror>(k);
+  k = dpp_max_i32<kDppMirror>(k);
+  const int32_t a = __builtin_amdgcn_readlane(k, 0), b = __builtin_amdgcn_readlane(k, 16);
+  const int32_t c = __builtin_amdgcn_readlane(k, 32), d = __builtin_amdgcn_readlane(k, 48);
+  const int32_t ab = a > b ? a : b, cd = c > d ? c : d;
+  return ord_val(ab > cd ? ab : cd);
 }
 
 __device__ __forceinline__ float wave_sum_f32(float v) {

@@ -154,12 +154,14 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
   float lmax = -INFINITY;
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
-    unpack<DT>(raw[k], f[k]);
     const uint32_t vi = k * LANES + lid;
+    // whole vectors past the row end become -inf before widening (one select
+    // per word); only the causal boundary needs a per-element mask
+    if (!CAUSAL && vi >= nvr) raw[k] = neg_inf_vec<DT>();
+    unpack<DT>(raw[k], f[k]);
 #pragma unroll
     for (int j = 0; j < V; ++j) {
-      const bool valid = CAUSAL ? (vi * V + j < L) : (vi < nvr);
-      f[k][j] = valid ? f[k][j] : -INFINITY;
+      if constexpr (CAUSAL) f[k][j] = (vi * V + j < L) ? f[k][j] : -INFINITY;
       lmax = fmaxf(lmax, f[k][j]);
     }
   }
@@ -395,12 +397,12 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
   float lmax = -INFINITY;
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
-    unpack<DT>(raw[k], f[k]);
     const uint32_t vi = v0 + k * kSmBlock + threadIdx.x;
+    if (!CAUSAL && vi >= nvr) raw[k] = neg_inf_vec<DT>();
+    unpack<DT>(raw[k], f[k]);
 #pragma unroll
     for (int j = 0; j < V; ++j) {
-      const bool valid = CAUSAL ? (vi * V + j < L) : (vi < nvr);
-      f[k][j] = valid ? f[k][j] : -INFINITY;
+      if constexpr (CAUSAL) f[k][j] = (vi * V + j < L) ? f[k][j] : -INFINITY;
       lmax = fmaxf(lmax, f[k][j]);
     }
   }
