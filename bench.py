@@ -235,7 +235,47 @@ def cpu_baseline(w, x_host, cpu_seconds):
         "sample": "%d of %d elements of %s, quake2, %d passes over %.1f s wall" % (
             elems, w.numel, w.name, reps, wall),
         "single_thread_value": round(one, 3),
+        "single_thread_mode_ratios": cpu_mode_ratios(w, xb),
     }
+
+
+def cpu_mode_ratios(w, xb):
+    """The oracle's own operators timed on one host core (the paper's protocol:
+    single thread, scalar code) in every mode, on the first 2^20 elements (or
+    the rows holding them), median of three passes: the host-CPU counterpart
+    of the QuAKE-versus-exp comparison. EXACT here is the oracle's reference
+    exponential (binary32 result of a double exp2), the plug-in exp of the
+    unfused operator is the 'vanilla' form of the fusion study."""
+    import oracle
+    n = min(xb.size, 1 << 20)
+    xs = xb.reshape(-1)[:n] if w.op != "softmax" else xb[:max(1, n // w.cols)]
+
+    def op(mode, fused=True):
+        if w.op == "gelu":
+            (oracle.gelu if fused else oracle.gelu_unfused)(xs, w.dt, mode, threads=1)
+        elif w.op in ("sigmoid", "silu"):
+            oracle.sigmoid(xs, w.dt, mode, silu=(w.op == "silu"), threads=1)
+        else:
+            (oracle.softmax if fused else oracle.softmax_unfused)(
+                xs.reshape(-1, w.cols), w.dt, mode, t=w.t, threads=1)
+
+    def med(fn):
+        ts = []
+        for _ in range(3):
+            t0 = time.perf_counter()
+            fn()
+            ts.append(time.perf_counter() - t0)
+        return sorted(ts)[1]
+
+    t = {m: med(lambda m=m: op(MODE_IDS[m])) for m in ("exact", "quake1", "quake2", "quake2m")}
+    out = {"elements": int(xs.size), "ns_per_element": {m: round(v / xs.size * 1e9, 2)
+                                                       for m, v in t.items()},
+           "speedup_vs_exact": {m: round(t["exact"] / v, 3) for m, v in t.items() if m != "exact"}}
+    if w.op in ("gelu", "softmax"):
+        van = med(lambda: op(0, fused=False))
+        out["speedup_vs_unfused_exact"] = {m: round(van / t[m], 3)
+                                           for m in ("quake1", "quake2", "quake2m")}
+    return out
 
 
 def implicit_causal(q, synth, a):
