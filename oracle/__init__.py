@@ -73,6 +73,8 @@ def lib() -> ctypes.CDLL:
         L.qo_gelu_unfused.argtypes = [vp, vp, i64, ci, ci]
         L.qo_round.argtypes = [vp, vp, i64, ci]
         L.qo_decode.argtypes = [vp, vp, i64, ci]
+        L.qo_exp16.argtypes = [vp, vp, i64, ci, ci, cf, cf]
+        L.qo_exp16.restype = ci
         L.qo_q2m_coefficients.argtypes = [vp]
         L.qo_q2m_coefficients.restype = None
         for f in (L.qo_quake, L.qo_exp, L.qo_sigmoid, L.qo_gelu, L.qo_softmax,
@@ -244,6 +246,26 @@ def softmax_causal(x, period, shift=0, dt="f32", mode=Q2, t=1.0, threads=1):
     else:
         with ThreadPoolExecutor(threads) as ex:
             list(ex.map(run, ranges))
+    return y
+
+
+def exp16(x: np.ndarray, dt: str, mode: int, a: float = 1.0, b: float = 0.0,
+          threads: int = 1) -> np.ndarray:
+    """e^(a x + b) with QuAKE / QuAKE2 built in the 16-bit format's own layout
+    (dt "f16" or "bf16"; uint16 raw bits in and out; modes Q1, Q2)."""
+    if dt not in ("f16", "bf16"):
+        raise ValueError(dt)
+    x = _prep(x, dt)
+    y = np.empty(x.shape, np.uint16)
+    xf = x.reshape(-1).view(np.uint16)
+    yf = y.reshape(-1)
+
+    def work(r):
+        lo, hi = r
+        _check(lib().qo_exp16(_ptr(xf[lo:]), _ptr(yf[lo:]), hi - lo, DTYPES[dt], mode, a, b))
+
+    with ThreadPoolExecutor(max(1, threads)) as ex:
+        list(ex.map(work, _split(xf.size, threads)))
     return y
 
 

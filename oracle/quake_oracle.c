@@ -31,6 +31,9 @@
  *                 standard exponential plugged in: softmax computes (v - m) * t
  *                 and then e^s; GELU computes k * x * (1/0.044715 + x^2) and then
  *                 e^-s; EXACT mode is the vanilla operator with exp.
+ *   qo_exp16      Sec. II-A/II-B in a 16-bit format's own layout: Eq. 3 with
+ *                 the l_m and B of binary16 / bfloat16, Algorithm 1 with the
+ *                 16-bit masks and the refinement in that format's arithmetic.
  *   qo_round      IEEE-754 round-to-nearest-even from double to binary32,
  *                 binary16 and bfloat16 (the output formats).
  *
@@ -517,6 +520,68 @@ int qo_gelu_unfused(const void* x, void* y, int64_t n, int dt, int mode) {
     double e = (double)std_exp(-s, mode);
     store_el(y, i, dt, (double)xv / (1.0 + e));
   }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* QuAKE built in a 16-bit format's own layout (Sec. II-A, II-B).           */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * e^(a x + b) for binary16 / bfloat16 inputs and outputs, with Eq. 3 taken in
+ * the output format itself: z = (x/ln2 + B) 2^l_m is the 16-bit pattern of
+ * the result (binary16: l_e = 5, l_m = 10, B = 15; bfloat16: l_e = 8,
+ * l_m = 7, B = 127), no binary32 result and no narrowing.
+ *   l = fmaf(x, c0, c1) in binary32 (x widened exactly), c0 = fl32(2^l_m a/ln2),
+ *       c1 = fl32(2^l_m (B - beta + b/ln2)), beta = 0.0436 for QuAKE only;
+ *   l clamped to [0, (2^l_e - 1) 2^l_m] (the top is the pattern of +inf);
+ *   z = (int) l, truncating: the 16-bit result of QuAKE (Eq. 2, 3);
+ *   QuAKE2 (Algorithm 1 with the 16-bit masks): a_m = (z & (2^l_m - 1)) |
+ *       (B << l_m) in [1, 2); y_m = (a_m^2 + 2) / 3 in the format's own
+ *       arithmetic, each operation rounded to nearest even once:
+ *         binary16: t = fl16(a_m a_m + 2) (one fused operation), y_m = fl16(t fl16(1/3));
+ *         bfloat16: t = a_m a_m + 2 (exact in binary32), y_m = fl_bf16(fl32(t fl32(1/3)))
+ *       (bfloat16 arithmetic is binary32 arithmetic rounded to bfloat16);
+ *       result = z's sign and exponent fields joined with y_m's mantissa.
+ * x and y hold raw 16-bit patterns. Modes QO_Q1, QO_Q2 only.
+ */
+static uint16_t quake16_one(float x, float c0, float c1, int dt, int order) {
+  const int lm = (dt == QO_F16) ? 10 : 7;
+  const int bias = (dt == QO_F16) ? 15 : 127;
+  const int le = (dt == QO_F16) ? 5 : 8;
+  const uint32_t mant = (1u << lm) - 1u;
+  const float top = (float)(((1 << le) - 1) * (1 << lm));
+  float l = fmaf(x, c0, c1);
+  if (!(l > 0.0f)) l = 0.0f;
+  if (l > top) l = top;
+  const uint32_t z = (uint32_t)(int32_t)l;
+  if (order == QO_Q1) return (uint16_t)z;
+  const uint32_t am_bits = (z & mant) | ((uint32_t)bias << lm);
+  uint32_t ym_bits;
+  if (dt == QO_F16) {
+    const double am = (double)dec_f16((uint16_t)am_bits);
+    const double third16 = (double)dec_f16(enc_f16(1.0 / 3.0));
+    const double t = (double)dec_f16(enc_f16(am * am + 2.0));   /* exact in double, rounded once */
+    ym_bits = enc_f16(t * third16);                             /* exact in double, rounded once */
+  } else {
+    const float am = dec_bf16((uint16_t)am_bits);
+    const float t = fmaf(am, am, 2.0f);                         /* exact in binary32 */
+    const float p = t * (float)(1.0 / 3.0);                     /* binary32 rounding */
+    ym_bits = enc_bf16((double)p);
+  }
+  return (uint16_t)((z & ~mant & 0xFFFFu) | (ym_bits & mant));
+}
+
+int qo_exp16(const void* x, void* y, int64_t n, int dt, int mode, float a, float b) {
+  if (dt != QO_F16 && dt != QO_BF16) return 2;
+  if (mode != QO_Q1 && mode != QO_Q2) return 3;
+  const double two_lm = (dt == QO_F16) ? 1024.0 : 128.0;
+  const double bias = (dt == QO_F16) ? 15.0 : 127.0;
+  const double beta = (mode == QO_Q1) ? 0.0436 : 0.0;
+  const float c0 = (float)(((double)a / LN2) * two_lm);
+  const float c1 = (float)(((bias - beta) + (double)b / LN2) * two_lm);
+  for (int64_t i = 0; i < n; ++i)
+    ((uint16_t*)y)[i] = quake16_one(load_el(x, i, dt), c0, c1, dt, mode);
   return 0;
 }
 

@@ -29,6 +29,7 @@ int qo_softmax_unfused(const void* x, void* y, int64_t rows, int64_t cols, int64
 int qo_softmax_causal(const void* x, void* y, int64_t rows, int64_t cols, int64_t ldx,
                       int64_t ldy, int64_t period, int64_t shift, int dt, int mode, float t,
                       double* tmp);
+int qo_exp16(const void* x, void* y, int64_t n, int dt, int mode, float a, float b);
 int qo_round(const double* v, void* out, int64_t n, int dt);
 int qo_decode(const void* in, float* out, int64_t n, int dt);
 float qo_softmax_c0(float t, int mode);
@@ -93,6 +94,11 @@ static void elementwise(void) {
       EXPECT(qo_sigmoid(x, y, n, dt, mode, 1) == 0, "silu");
       EXPECT(qo_gelu(x, y, n, dt, mode) == 0, "gelu");
       EXPECT(qo_gelu_unfused(x, y, n, dt, mode) == 0, "gelu unfused");
+      if (dt > 0 && (mode == 1 || mode == 2)) {
+        const float ab16[][2] = {{1.0f, 0.0f}, {-1.0f, 0.0f}, {3e4f, 0.0f}, {1e-30f, -7.0f}};
+        for (size_t k = 0; k < 4; ++k)
+          EXPECT(qo_exp16(x, y, n, dt, mode, ab16[k][0], ab16[k][1]) == 0, "exp16");
+      }
       if (mode > 0) {
         float* fy = (float*)y;
         EXPECT(qo_quake(dec, fy, n, 12102203.0f, 1065353216.0f, mode) == 0, "quake");

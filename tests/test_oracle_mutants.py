@@ -41,6 +41,10 @@ MUTANTS = {
     "q2m_horner_swap": ("ym = fmaf(fmaf(q2m_f[0], am, q2m_f[1]), am, q2m_f[2]);",
                         "ym = fmaf(fmaf(q2m_f[0], am, q2m_f[2]), am, q2m_f[1]);"),
     "q2m_integer_rule_missing": ("  if (order == QO_Q2M && ((uint32_t)z & MASK_MANT) == 0) yi = (uint32_t)z;\n", ""),
+    "exp16_f16_bias": ("const int bias = (dt == QO_F16) ? 15 : 127;", "const int bias = (dt == QO_F16) ? 16 : 127;"),
+    "exp16_mask": ("const uint32_t mant = (1u << lm) - 1u;", "const uint32_t mant = (1u << (lm - 1)) - 1u;"),
+    "exp16_third_unrounded": ("const double third16 = (double)dec_f16(enc_f16(1.0 / 3.0));",
+                              "const double third16 = 1.0 / 3.0;"),
     "unfused_no_max": ("float d = load_el(x, bx + j, dt) - m;   /* max subtraction */",
                        "float d = load_el(x, bx + j, dt);"),
 }
@@ -65,7 +69,8 @@ def test_pins_catch_mutant(name, tmp_path):
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                         os.path.join(HERE, "test_oracle_scalar.py"),
                         os.path.join(HERE, "test_oracle_ops.py"),
-                        os.path.join(HERE, "test_oracle_q2m.py")],
+                        os.path.join(HERE, "test_oracle_q2m.py"),
+                        os.path.join(HERE, "test_oracle_native16.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, "mutant %s survived the pins:\n%s" % (name, r.stdout[-2000:])
     assert "failed" in r.stdout or "error" in r.stdout.lower()
