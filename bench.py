@@ -95,6 +95,11 @@ def make_launcher(q, w, mode, xs, ys, fused=True):
 
         def f(i):
             return L.quake_sigmoid(xp[i], yp[i], n, dt, mode, silu, stream())
+    elif w.op in ("exp", "exp16"):
+        e = L.quake_exp16 if w.op == "exp16" else L.quake_exp
+
+        def f(i):
+            return e(xp[i], yp[i], n, dt, mode, 1.0, 0.0, stream())
     elif w.op == "softmax":
         rows, cols = w.rows, w.cols
         sm = L.quake_softmax if fused else L.quake_softmax_unfused
@@ -278,6 +283,26 @@ def cpu_mode_ratios(w, xb):
     return out
 
 
+def native16(q, synth, a):
+    """e^x over 2^28 binary16 elements: the binary32 path (quake_exp: binary32
+    arithmetic, result narrowed) against the construction in binary16's own
+    layout (quake_exp16), QuAKE and QuAKE2; both read and write 2 bytes per
+    element."""
+    import dataclasses
+    w = synth.EXTRA_WORKLOADS["exp_f16_2p28"]
+    xh = w.make()
+    steps = max(100, min(a.steps, int(1e12 / w.algo_bytes)))
+    out = {"algo_bytes": w.algo_bytes}
+    for path, wop in (("binary32_path", w), ("native16", dataclasses.replace(w, op="exp16"))):
+        for m in ("quake1", "quake2"):
+            ms = time_workload(q, wop, MODE_IDS[m], xh, steps, a.warmup, a.launch)[0]
+            out["%s_%s_ms" % (path, m)] = ms
+            out["%s_%s_gbps" % (path, m)] = round(w.algo_bytes / (ms * 1e-3) / 1e9, 2)
+    out["native16_speedup"] = {m: round(out["binary32_path_%s_ms" % m] / out["native16_%s_ms" % m], 4)
+                               for m in ("quake1", "quake2")}
+    return out
+
+
 def implicit_causal(q, synth, a):
     """The attention workload with the causal mask implied (quake_softmax_causal):
     only live entries are read, so its algorithmic bytes are the live inputs
@@ -454,6 +479,7 @@ def main():
                          "quake2m_speedup_vs_exact": round(r2["exact"][0] / r2["quake2m"][0], 4),
                          "launch": r2["quake2"][1]}
             del xh
+        sec["exp_f16_2p28"] = native16(q, synth, a)
         imp = implicit_causal(q, synth, a)
         imp["no_masked_writes"]["speedup_vs_explicit_mask_input"] = round(
             sec["attn_softmax_bf16_causal"]["quake2_ms"] / imp["no_masked_writes"]["quake2_ms"], 4)

@@ -194,6 +194,30 @@ quake_status quake_gelu_unfused(const void* x, void* y, int64_t n, quake_dtype d
                                 quake_mode mode, void* stream);
 
 /*
+ * quake_exp16 — y[i] = e^(a*x[i] + b) with QuAKE / QuAKE2 built directly in
+ * the 16-bit format's own layout (Sec. II-A notes the construction holds for
+ * any IEEE-style format; Eq. 3 with that format's l_m and B, Algorithm 1 with
+ * its masks): binary16 (l_e = 5, l_m = 10, B = 15) or bfloat16 (l_e = 8,
+ * l_m = 7, B = 127). No binary32 result is formed and nothing is narrowed:
+ *   l = fmaf(x, c0, c1) in binary32, c0 = fl32(2^l_m a / ln2),
+ *   c1 = fl32(2^l_m (B - beta + b / ln2)) (beta as in quake_exp);
+ *   l clamped to [0, (2^l_e - 1) 2^l_m]; z = (int) l is the 16-bit result of
+ *   QUAKE_1; QUAKE_2 sets z's mantissa to that of y_m = (a_m^2 + 2)/3,
+ *   a_m = (z & (2^l_m - 1)) | (B << l_m), evaluated in the format's own
+ *   arithmetic: binary16 fl16(fl16(a_m a_m + 2) fl16(1/3)); bfloat16
+ *   fl_bf16(fl32((a_m a_m + 2) fl32(1/3))).
+ * The mantissa carries l_m bits, so results are coarser than quake_exp's
+ * (QUAKE_2 worst case about 0.38 % in binary16, 1 % in bfloat16, over normal
+ * results). Outputs are bit-exact functions of the input.
+ *   x, y  : device buffers of n contiguous elements of `dtype`.
+ *   dtype : QUAKE_F16 or QUAKE_BF16 (else QUAKE_EDTYPE).
+ *   mode  : QUAKE_1 or QUAKE_2 (else QUAKE_EMODE).
+ *   a, b  : finite, with c0, c1 finite; otherwise QUAKE_EINVAL.
+ */
+quake_status quake_exp16(const void* x, void* y, int64_t n, quake_dtype dtype, quake_mode mode,
+                         float a, float b, void* stream);
+
+/*
  * quake_softmax_split_timeouts — number of exchange waits of the split-row
  * softmax path (rows longer than one workgroup holds) that gave up at their
  * spin limit on `stream` since the previous call, which then resets it. Every

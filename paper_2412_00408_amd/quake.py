@@ -36,13 +36,14 @@ def _load() -> ctypes.CDLL:
     L = ctypes.CDLL(_LIB_PATH)
     vp, i64, ci, cf = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float
     L.quake_exp.argtypes = [vp, vp, i64, ci, ci, cf, cf, vp]
+    L.quake_exp16.argtypes = [vp, vp, i64, ci, ci, cf, cf, vp]
     L.quake_softmax.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp]
     L.quake_gelu.argtypes = [vp, vp, i64, ci, ci, vp]
     L.quake_softmax_unfused.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp]
     L.quake_gelu_unfused.argtypes = [vp, vp, i64, ci, ci, vp]
     L.quake_softmax_causal.argtypes = [vp, vp, i64, i64, i64, i64, i64, i64, ci, ci, ci, cf, vp]
     L.quake_sigmoid.argtypes = [vp, vp, i64, ci, ci, ci, vp]
-    for f in (L.quake_exp, L.quake_softmax, L.quake_gelu, L.quake_sigmoid,
+    for f in (L.quake_exp, L.quake_exp16, L.quake_softmax, L.quake_gelu, L.quake_sigmoid,
               L.quake_softmax_unfused, L.quake_gelu_unfused, L.quake_softmax_causal):
         f.restype = ci
     L.quake_softmax_split_timeouts.argtypes = [vp, ctypes.POINTER(i64)]
@@ -109,6 +110,14 @@ def quake_exp(x, y=None, mode=QUAKE_2, a=1.0, b=0.0, stream=None):
     y = _check_io(x, y)
     _raise("quake_exp", lib.quake_exp(x.data_ptr(), y.data_ptr(), x.numel(), DTYPES[x.dtype],
                                       MODES[mode], a, b, _stream(x, stream)))
+    return y
+
+
+def quake_exp16(x, y=None, mode=QUAKE_2, a=1.0, b=0.0, stream=None):
+    """y = e^(a x + b) with the approximation built in x's own 16-bit layout."""
+    y = _check_io(x, y)
+    _raise("quake_exp16", lib.quake_exp16(x.data_ptr(), y.data_ptr(), x.numel(), DTYPES[x.dtype],
+                                          MODES[mode], a, b, _stream(x, stream)))
     return y
 
 

@@ -144,7 +144,7 @@ class Workload:
         if self.name == "attn_softmax_bf16_causal":
             return causal_scores(self.shape[0] * self.shape[1], self.cols, self.dt, self.seed,
                                  rows=rows)
-        if self.name in ("sigmoid_f16_2p28", "silu_f16_2p28"):
+        if self.name in ("sigmoid_f16_2p28", "silu_f16_2p28", "exp_f16_2p28"):
             m = self.numel if n is None else n
             return uniform_with_outliers(m, -12.0, 12.0, 0.01, 80.0, self.dt, self.seed)
         if self.name == "lmhead_softmax_f32_64x128256":
@@ -166,6 +166,14 @@ TABLE4_WORKLOADS = {
     w.name: w for w in [
         Workload("softmax_f32_16384x16384", "softmax", "f32", (16384, 16384), 16384, 16384, 1.0, 6),
         Workload("gelu_f32_260k", "gelu", "f32", (260000,), 0, 0, 1.0, 7),
+    ]
+}
+
+# The exponential alone on the Logistic input (e^x in the binary32 path against
+# the construction in binary16's own layout, quake_exp16).
+EXTRA_WORKLOADS = {
+    w.name: w for w in [
+        Workload("exp_f16_2p28", "exp", "f16", (1 << 28,), 0, 0, 1.0, 4),
     ]
 }
 

@@ -125,3 +125,19 @@ def test_causal_and_unfused_validation(q):
     assert L.quake_softmax_unfused(FAKE, FAKE, 0, 8, 8, 8, 0, 2, 1.0, None) == q.OK
     assert L.quake_gelu_unfused(FAKE, FAKE, -1, 0, 2, None) == q.EINVAL
     assert L.quake_gelu_unfused(FAKE, FAKE, 10, 0, 5, None) == q.EMODE
+
+
+def test_exp16_validation(q):
+    L = q.lib
+    # quake_exp16(x, y, n, dtype, mode, a, b, stream)
+    assert L.quake_exp16(FAKE, FAKE, 0, 1, 2, 1.0, 0.0, None) == q.OK
+    assert L.quake_exp16(None, None, 0, 2, 1, 1.0, 0.0, None) == q.OK
+    assert L.quake_exp16(FAKE, FAKE, 10, 0, 2, 1.0, 0.0, None) == q.EDTYPE     # binary32
+    assert L.quake_exp16(FAKE, FAKE, 10, 3, 2, 1.0, 0.0, None) == q.EDTYPE
+    assert L.quake_exp16(FAKE, FAKE, 10, 1, 0, 1.0, 0.0, None) == q.EMODE      # EXACT
+    assert L.quake_exp16(FAKE, FAKE, 10, 1, 3, 1.0, 0.0, None) == q.EMODE      # QUAKE_2M
+    assert L.quake_exp16(FAKE, FAKE, -1, 1, 2, 1.0, 0.0, None) == q.EINVAL
+    assert L.quake_exp16(None, FAKE, 10, 1, 2, 1.0, 0.0, None) == q.EINVAL
+    assert L.quake_exp16(FAKE, FAKE, 10, 1, 2, float("inf"), 0.0, None) == q.EINVAL
+    assert L.quake_exp16(FAKE, FAKE, 10, 2, 2, 1.0, float("nan"), None) == q.EINVAL
+    assert L.quake_exp16(FAKE, FAKE, 10, 1, 2, 3e38, 0.0, None) == q.EINVAL      # c0 overflows
