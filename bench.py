@@ -303,6 +303,55 @@ def native16(q, synth, a):
     return out
 
 
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix-core peak
+
+
+def linear_gelu(q, synth, a):
+    """GELU(x w^T) for the up-projection of a BERT-base MLP over 4096 tokens
+    (x [4096, 768], w [3072, 768], bf16): the fused kernel in every mode, the
+    same product without the GELU, the product followed by quake_gelu, and
+    torch.matmul (the vendor BLAS) for context. Eight rotating operand sets
+    (about 290 MB) keep the timed launches out of the 256 MB Infinity Cache."""
+    import torch
+    m, n, k = 4096, 3072, 768
+    nb = 8
+    xs = [synth.normal((m, k), 1.0, "bf16", 1900 + i).to("cuda:0") for i in range(nb)]
+    ws = [synth.normal((n, k), 0.05, "bf16", 1950 + i).to("cuda:0") for i in range(nb)]
+    ys = [torch.empty((m, n), dtype=torch.bfloat16, device="cuda:0") for _ in range(nb)]
+    wts = [w.t().contiguous() for w in ws]
+    flop = 2.0 * m * n * k
+    iters = max(50, min(a.steps, 2000))
+
+    def timeit(fn):
+        for i in range(max(a.warmup, nb)):
+            fn(i % nb)
+        torch.cuda.synchronize()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for i in range(iters):
+            fn(i % nb)
+        e.record()
+        torch.cuda.synchronize()
+        return s.elapsed_time(e) / iters
+
+    out = {"shape_mnk": [m, n, k], "flop": flop, "peak_tflops": PEAK_BF16_TFLOPS}
+    for mname in ("exact", "quake1", "quake2", "quake2m"):
+        ms = timeit(lambda i, md=MODE_IDS[mname]: q.quake_linear_gelu(xs[i], ws[i], ys[i], mode=md))
+        out["fused_%s_ms" % mname] = ms
+    ms0 = timeit(lambda i: q.quake_linear_gelu(xs[i], ws[i], ys[i], mode=2, gelu=False))
+    msg = timeit(lambda i: q.quake_gelu(ys[i], ys[i], mode=2))
+    mst = timeit(lambda i: torch.matmul(xs[i], wts[i], out=ys[i]))
+    out.update({"product_only_ms": ms0, "quake_gelu_ms": msg, "torch_matmul_ms": mst})
+    out["fused_quake2_tflops"] = round(flop / (out["fused_quake2_ms"] * 1e-3) / 1e12, 1)
+    out["product_only_tflops"] = round(flop / (ms0 * 1e-3) / 1e12, 1)
+    out["product_only_frac_of_peak"] = round(out["product_only_tflops"] / PEAK_BF16_TFLOPS, 4)
+    out["fused_vs_product_then_gelu"] = round((ms0 + msg) / out["fused_quake2_ms"], 4)
+    out["epilogue_ms_over_product"] = {mm: round(out["fused_%s_ms" % mm] - ms0, 5)
+                                       for mm in ("exact", "quake1", "quake2", "quake2m")}
+    del xs, ws, ys, wts
+    return out
+
+
 def implicit_causal(q, synth, a):
     """The attention workload with the causal mask implied (quake_softmax_causal):
     only live entries are read, so its algorithmic bytes are the live inputs
@@ -480,6 +529,7 @@ def main():
                          "launch": r2["quake2"][1]}
             del xh
         sec["exp_f16_2p28"] = native16(q, synth, a)
+        sec["linear_gelu_bf16_4096x3072x768"] = linear_gelu(q, synth, a)
         imp = implicit_causal(q, synth, a)
         imp["no_masked_writes"]["speedup_vs_explicit_mask_input"] = round(
             sec["attn_softmax_bf16_causal"]["quake2_ms"] / imp["no_masked_writes"]["quake2_ms"], 4)

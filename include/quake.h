@@ -218,6 +218,27 @@ quake_status quake_exp16(const void* x, void* y, int64_t n, quake_dtype dtype, q
                          float a, float b, void* stream);
 
 /*
+ * quake_linear_gelu — y = GELU(x w^T), or y = x w^T when gelu == 0: the
+ * up-projection of a transformer MLP with its activation fused. The GELU is
+ * Eq. 7 with the exponential of `mode` (Sec. III-D, as quake_gelu), applied
+ * to the binary32 accumulators in the epilogue of a matrix-core product; the
+ * paper applies QuAKE to standalone operators, this is the same operator
+ * fused into its producer.
+ *   x : device, m x k bfloat16, row r at x + r*ldx (elements), 16-byte aligned.
+ *   w : device, n x k bfloat16 (a linear layer's weight), row r at w + r*ldw,
+ *       16-byte aligned.
+ *   y : device, m x n bfloat16, row r at y + r*ldy.
+ *   k, ldx, ldw: multiples of 8; ldx, ldw >= k; ldy >= n.
+ *   dtype : QUAKE_BF16 only (else QUAKE_EDTYPE); mode: any quake_mode.
+ * Products are accumulated in binary32 (order unspecified), then the GELU of
+ * each accumulator is rounded to bfloat16. m == 0 or n == 0 launches nothing;
+ * other bad sizes, strides or alignments return QUAKE_EINVAL.
+ */
+quake_status quake_linear_gelu(const void* x, const void* w, void* y, int64_t m, int64_t n,
+                               int64_t k, int64_t ldx, int64_t ldw, int64_t ldy,
+                               quake_dtype dtype, quake_mode mode, int gelu, void* stream);
+
+/*
  * quake_softmax_split_timeouts — number of exchange waits of the split-row
  * softmax path (rows longer than one workgroup holds) that gave up at their
  * spin limit on `stream` since the previous call, which then resets it. Every

@@ -73,6 +73,8 @@ def lib() -> ctypes.CDLL:
         L.qo_gelu_unfused.argtypes = [vp, vp, i64, ci, ci]
         L.qo_round.argtypes = [vp, vp, i64, ci]
         L.qo_decode.argtypes = [vp, vp, i64, ci]
+        L.qo_gelu_f32in.argtypes = [vp, vp, i64, ci, ci]
+        L.qo_gelu_f32in.restype = ci
         L.qo_exp16.argtypes = [vp, vp, i64, ci, ci, cf, cf]
         L.qo_exp16.restype = ci
         L.qo_q2m_coefficients.argtypes = [vp]
@@ -247,6 +249,29 @@ def softmax_causal(x, period, shift=0, dt="f32", mode=Q2, t=1.0, threads=1):
         with ThreadPoolExecutor(threads) as ex:
             list(ex.map(run, ranges))
     return y
+
+
+def linear_gelu(x: np.ndarray, w: np.ndarray, mode: int, gelu: bool = True, dt: str = "bf16",
+                threads: int = 1) -> np.ndarray:
+    """GELU(x w^T) of 16-bit matrices x [m, k] and w [n, k] (raw bits): the
+    product in float64 (every product of two bfloat16 / binary16 values is
+    exact there and the sum keeps far more than binary32's precision), rounded
+    once to binary32, then GELU of Eq. 7 (or nothing) and rounding to dt."""
+    xd = decode(np.ascontiguousarray(x).reshape(-1), dt).astype(np.float64).reshape(x.shape)
+    wd = decode(np.ascontiguousarray(w).reshape(-1), dt).astype(np.float64).reshape(w.shape)
+    acc = (xd @ wd.T).astype(np.float32)
+    if not gelu:
+        return round_to(acc.astype(np.float64), dt)
+    flat = np.ascontiguousarray(acc).reshape(-1)
+    y = np.empty(flat.size, np.uint16)
+
+    def work(r):
+        lo, hi = r
+        _check(lib().qo_gelu_f32in(_ptr(flat[lo:]), _ptr(y[lo:]), hi - lo, DTYPES[dt], mode))
+
+    with ThreadPoolExecutor(max(1, threads)) as ex:
+        list(ex.map(work, _split(flat.size, threads)))
+    return y.reshape(acc.shape)
 
 
 def exp16(x: np.ndarray, dt: str, mode: int, a: float = 1.0, b: float = 0.0,

@@ -31,6 +31,8 @@
  *                 standard exponential plugged in: softmax computes (v - m) * t
  *                 and then e^s; GELU computes k * x * (1/0.044715 + x^2) and then
  *                 e^-s; EXACT mode is the vanilla operator with exp.
+ *   qo_gelu_f32in qo_gelu on binary32 inputs with output in any format (the
+ *                 epilogue of a matrix product: GELU of the binary32 sums).
  *   qo_exp16      Sec. II-A/II-B in a 16-bit format's own layout: Eq. 3 with
  *                 the l_m and B of binary16 / bfloat16, Algorithm 1 with the
  *                 16-bit masks and the refinement in that format's arithmetic.
@@ -501,6 +503,25 @@ int qo_softmax_unfused(const void* x, void* y, int64_t rows, int64_t cols, int64
       sum += tmp[j];
     }
     for (int64_t j = 0; j < cols; ++j) store_el(y, by + j, dt, tmp[j] / sum);
+  }
+  return 0;
+}
+
+/* GELU via Eq. 7 of binary32 inputs (e.g. the binary32 accumulators of a
+ * matrix product), output rounded once to format dt. */
+int qo_gelu_f32in(const float* x, void* y, int64_t n, int dt, int mode) {
+  int err = bad_args(dt, mode);
+  if (err) return err;
+  float A = a_gelu();
+  float c0 = (float)(-(k_gelu() / LN2) * TWO_LM), c1 = c1_of(0.0, mode);
+  float c0e = (float)(-k_gelu() / LN2);
+  for (int64_t i = 0; i < n; ++i) {
+    float xv = x[i];
+    float u = fmaf(xv, xv, A);
+    float w = xv * u;
+    double e = (mode == QO_EXACT) ? (double)exp2_binary32(fmaf(w, c0e, 0.0f))
+                                  : (double)quake_one(w, c0, c1, mode);
+    store_el(y, i, dt, (double)xv / (1.0 + e));
   }
   return 0;
 }

@@ -39,9 +39,7 @@ __device__ __forceinline__ float ew_op(float x, const EwParams& p) {
   if constexpr (OP == OP_EXP) {
     return qexp<MODE>(x, p.c0, p.c1);
   } else if constexpr (OP == OP_GELU) {
-    const float u = __builtin_fmaf(x, x, p.a);
-    const float w = x * u;
-    return div_one_plus(x, qexp<MODE>(w, p.c0, p.c1));
+    return gelu_q<MODE>(x, p.c0, p.c1, p.a);
   } else if constexpr (OP == OP_SIGMOID) {
     return __builtin_amdgcn_rcpf(1.0f + qexp<MODE>(x, p.c0, p.c1));
   } else if constexpr (OP == OP_SILU) {

@@ -1,0 +1,182 @@
+// gemm.hip — quake_linear_gelu: y = GELU(x w^T) for bfloat16 x [m, k] and
+// w [n, k] (both k-contiguous, the layout of a linear layer's input and
+// weight), binary32 accumulation on the matrix cores, the GELU of Eq. 7 with
+// QuAKE / QuAKE2 / EXACT applied to the binary32 accumulators in the
+// epilogue, bfloat16 output. This is QuAKE inside a fused consumer: the GELU
+// costs no HBM traffic of its own, and its VALU work runs beside the MFMAs.
+//
+// Tiling: a workgroup (4 waves) computes a 128 x 128 tile of y, each wave a
+// 64 x 64 quarter as 2 x 2 blocks of v_mfma_f32_32x32x16_bf16. K advances in
+// slabs of 64: the next slab is loaded from HBM into registers while the
+// current one is multiplied out of LDS (rows padded by 16 bytes so the
+// 16-byte fragment reads of 8 consecutive rows hit distinct banks).
+// Operand lane layout of the 32x32x16 bf16 MFMA (checked on the device):
+// lane l holds row (l mod 32) and k = 8 (l / 32) .. +7 of A, and column
+// (l mod 32), the same k, of B; accumulator r of lane l is row
+// 8 (r / 4) + 4 (l / 32) + (r mod 4), column l mod 32.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+
+#include "quake_device.hpp"
+#include "quake_host.hpp"
+
+namespace qk {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int kBM = 128, kBN = 128, kBK = 64;
+constexpr int kLdsRow = kBK + 8;   // bf16 elements per LDS row (144 bytes)
+constexpr int kGemmThreads = 256;
+
+struct GemmArgs {
+  const uint16_t* x;
+  const uint16_t* w;
+  uint16_t* y;
+  int32_t m, n, k;
+  int64_t ldx, ldw, ldy;   // elements
+  float c0, c1, a;         // GELU constants (Eq. 7 folded into Eq. 5)
+  uint32_t tiles_m, tiles_n;
+  uint32_t xcd_split;      // tiles_m % 4 == 0 and tiles_n % 2 == 0
+};
+
+template <int MODE, bool GELU>
+__global__ __launch_bounds__(kGemmThreads, 3) void gemm_bf16_kernel(GemmArgs g) {
+  __shared__ __attribute__((aligned(16))) uint16_t sx[kBM * kLdsRow];
+  __shared__ __attribute__((aligned(16))) uint16_t sw[kBN * kLdsRow];
+  const int t = threadIdx.x;
+  const int lane = t & 63, wave = t >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  // Workgroups go to the 8 XCDs round-robin (blockIdx mod 8). When the tile
+  // grid splits into 4 x 2 equal blocks, XCD j gets block (j / 2, j mod 2),
+  // so the rows of x and w its tiles share stay in its own L2.
+  int tm, tn;
+  if (g.xcd_split) {
+    const uint32_t xcd = blockIdx.x & 7u, local = blockIdx.x >> 3;
+    const uint32_t bm = g.tiles_m >> 2, bn = g.tiles_n >> 1;
+    tm = (int)((xcd >> 1) * bm + local / bn);
+    tn = (int)((xcd & 1u) * bn + local % bn);
+  } else {
+    tm = (int)(blockIdx.x / g.tiles_n);
+    tn = (int)(blockIdx.x % g.tiles_n);
+  }
+  const int row0 = tm * kBM, col0 = tn * kBN;
+
+  // Slab loads: 1024 16-byte vectors per operand; thread t takes t + 256 i,
+  // i.e. row v / 8 and k-vector v mod 8. Rows past m (n) re-read the last
+  // row; k past the end reads zeros (k is a multiple of 8).
+  u32x4 rx[4], rw[4];
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+  auto load_slab = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int v = t + kGemmThreads * i;
+      const int r = v >> 3, kk = k0 + 8 * (v & 7);
+      const int gm = min(row0 + r, g.m - 1), gn = min(col0 + r, g.n - 1);
+      const bool in = kk < g.k;
+      const int kc = in ? kk : 0;
+      const u32x4 a = *reinterpret_cast<const u32x4*>(g.x + (int64_t)gm * g.ldx + kc);
+      const u32x4 b = *reinterpret_cast<const u32x4*>(g.w + (int64_t)gn * g.ldw + kc);
+      rx[i] = in ? a : zero;
+      rw[i] = in ? b : zero;
+    }
+  };
+  auto store_slab = [&]() {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int v = t + kGemmThreads * i;
+      const int r = v >> 3, c = 8 * (v & 7);
+      *reinterpret_cast<u32x4*>(sx + r * kLdsRow + c) = rx[i];
+      *reinterpret_cast<u32x4*>(sw + r * kLdsRow + c) = rw[i];
+    }
+  };
+
+  f32x16_t acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  const int nk = (g.k + kBK - 1) / kBK;
+  load_slab(0);
+  const int fr = lane & 31, fk = 8 * (lane >> 5);
+  for (int kt = 0; kt < nk; ++kt) {
+    __syncthreads();   // every wave is done reading the previous slab
+    store_slab();
+    __syncthreads();
+    if (kt + 1 < nk) load_slab((kt + 1) * kBK);   // in flight during the MFMAs
+#pragma unroll
+    for (int ks = 0; ks < kBK / 16; ++ks) {
+      bf16x8_t af[2], bf[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        af[i] = *reinterpret_cast<const bf16x8_t*>(sx + (wm * 64 + 32 * i + fr) * kLdsRow + ks * 16 + fk);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        bf[j] = *reinterpret_cast<const bf16x8_t*>(sw + (wn * 64 + 32 * j + fr) * kLdsRow + ks * 16 + fk);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+    }
+  }
+
+  // Epilogue: GELU on the binary32 accumulators, round to bfloat16, store.
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int col = col0 + wn * 64 + 32 * j + fr;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = row0 + wm * 64 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        float v = acc[i][j][r];
+        if constexpr (GELU) v = gelu_q<MODE>(v, g.c0, g.c1, g.a);
+        if (row < g.m && col < g.n)
+          g.y[(int64_t)row * g.ldy + col] = __builtin_bit_cast(uint16_t, (__bf16)v);
+      }
+    }
+}
+
+}  // namespace qk
+
+using namespace qk;
+
+extern "C" quake_status quake_linear_gelu(const void* x, const void* w, void* y, int64_t m,
+                                          int64_t n, int64_t k, int64_t ldx, int64_t ldw,
+                                          int64_t ldy, quake_dtype dtype, quake_mode mode,
+                                          int gelu, void* stream) {
+  if (dtype != QUAKE_BF16) return QUAKE_EDTYPE;
+  if (!valid_mode(mode)) return QUAKE_EMODE;
+  if (m < 0 || n < 0 || k < 0) return QUAKE_EINVAL;
+  if (m == 0 || n == 0) return QUAKE_OK;
+  if (k == 0 || k % 8 != 0 || x == nullptr || w == nullptr || y == nullptr) return QUAKE_EINVAL;
+  if (ldx < k || ldw < k || ldy < n || ldx % 8 != 0 || ldw % 8 != 0) return QUAKE_EINVAL;
+  if (!aligned16(x) || !aligned16(w)) return QUAKE_EINVAL;
+  if (m > INT32_MAX - kBM || n > INT32_MAX - kBN || k > INT32_MAX - kBK) return QUAKE_EINVAL;
+  const int64_t tiles_m = (m + kBM - 1) / kBM, tiles_n = (n + kBN - 1) / kBN;
+  if (tiles_m * tiles_n > INT32_MAX) return QUAKE_EINVAL;
+  const Affine af = gelu_affine(mode);
+  GemmArgs g{static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w),
+             static_cast<uint16_t*>(y), (int32_t)m, (int32_t)n, (int32_t)k, ldx, ldw, ldy,
+             af.c0, af.c1, gelu_a(), (uint32_t)tiles_m, (uint32_t)tiles_n,
+             (uint32_t)(tiles_m % 4 == 0 && tiles_n % 2 == 0)};
+  const dim3 grid((uint32_t)(tiles_m * tiles_n));
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+#define QK_GEMM_CASE(M)                                                                      \
+  if (mode == M) {                                                                           \
+    if (gelu)                                                                                \
+      hipLaunchKernelGGL((gemm_bf16_kernel<M, true>), grid, dim3(kGemmThreads), 0, s, g);    \
+    else                                                                                     \
+      hipLaunchKernelGGL((gemm_bf16_kernel<M, false>), grid, dim3(kGemmThreads), 0, s, g);   \
+    return launch_status();                                                                  \
+  }
+  QK_GEMM_CASE(EXACT) QK_GEMM_CASE(Q1) QK_GEMM_CASE(Q2) QK_GEMM_CASE(Q2M)
+#undef QK_GEMM_CASE
+  return QUAKE_EMODE;
+}

@@ -89,6 +89,15 @@ __device__ __forceinline__ float div_one_plus(float num, float e) {
   return (num * 0.25f) * __builtin_amdgcn_rcpf(__builtin_fmaf(e, 0.25f, 0.25f));
 }
 
+// GELU through Eq. 7: u = fma(x, x, 1/0.044715), w = x u, y = x / (1 + QuAKEx(w))
+// with the folded constants c0 = -2^23 2 0.044715 sqrt(2/pi) / ln2 and c1.
+template <int MODE>
+__device__ __forceinline__ float gelu_q(float x, float c0, float c1, float a) {
+  const float u = __builtin_fmaf(x, x, a);
+  const float w = x * u;
+  return div_one_plus(x, qexp<MODE>(w, c0, c1));
+}
+
 // ---------------------------------------------------------------------------
 // Element formats. A 16-byte vector holds kV<DT> elements.
 // ---------------------------------------------------------------------------

@@ -37,13 +37,15 @@ def _load() -> ctypes.CDLL:
     vp, i64, ci, cf = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float
     L.quake_exp.argtypes = [vp, vp, i64, ci, ci, cf, cf, vp]
     L.quake_exp16.argtypes = [vp, vp, i64, ci, ci, cf, cf, vp]
+    L.quake_linear_gelu.argtypes = [vp, vp, vp, i64, i64, i64, i64, i64, i64, ci, ci, ci, vp]
     L.quake_softmax.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp]
     L.quake_gelu.argtypes = [vp, vp, i64, ci, ci, vp]
     L.quake_softmax_unfused.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp]
     L.quake_gelu_unfused.argtypes = [vp, vp, i64, ci, ci, vp]
     L.quake_softmax_causal.argtypes = [vp, vp, i64, i64, i64, i64, i64, i64, ci, ci, ci, cf, vp]
     L.quake_sigmoid.argtypes = [vp, vp, i64, ci, ci, ci, vp]
-    for f in (L.quake_exp, L.quake_exp16, L.quake_softmax, L.quake_gelu, L.quake_sigmoid,
+    for f in (L.quake_exp, L.quake_exp16, L.quake_linear_gelu, L.quake_softmax, L.quake_gelu,
+              L.quake_sigmoid,
               L.quake_softmax_unfused, L.quake_gelu_unfused, L.quake_softmax_causal):
         f.restype = ci
     L.quake_softmax_split_timeouts.argtypes = [vp, ctypes.POINTER(i64)]
@@ -156,6 +158,30 @@ def _rows_view(t: torch.Tensor, what: str):
     if t.dim() == 2 and (t.stride(1) == 1 or cols == 1):
         return t.shape[0], cols, t.stride(0)
     raise ValueError("%s must be contiguous, or 2-D with a contiguous last dimension" % what)
+
+
+def quake_linear_gelu(x, w, y=None, mode=QUAKE_2, gelu=True, stream=None):
+    """y = GELU(x w^T) (or x w^T with gelu=False): bfloat16 x [m, k] and
+    w [n, k] with contiguous rows, binary32 accumulation, bfloat16 y [m, n]."""
+    if not (x.is_cuda and w.is_cuda):
+        raise ValueError("libquake takes device tensors")
+    if x.dim() != 2 or w.dim() != 2 or x.shape[1] != w.shape[1]:
+        raise ValueError("x [m, k] and w [n, k] with the same k")
+    m, k = x.shape
+    n = w.shape[0]
+    for t, what in ((x, "x"), (w, "w")):
+        if t.dtype not in DTYPES:
+            raise TypeError("libquake takes float32, float16 or bfloat16 tensors, got %s" % t.dtype)
+        if t.stride(1) != 1:
+            raise ValueError("%s must have a contiguous last dimension" % what)
+    if y is None:
+        y = torch.empty((m, n), dtype=x.dtype, device=x.device)
+    if y.shape != (m, n) or y.dtype != x.dtype or y.stride(1) != 1:
+        raise ValueError("y must be [m, n] of x's dtype with a contiguous last dimension")
+    _raise("quake_linear_gelu", lib.quake_linear_gelu(
+        x.data_ptr(), w.data_ptr(), y.data_ptr(), m, n, k, x.stride(0), w.stride(0), y.stride(0),
+        DTYPES[x.dtype], MODES[mode], int(bool(gelu)), _stream(x, stream)))
+    return y
 
 
 def quake_softmax_unfused(x, y=None, mode=QUAKE_2, t=1.0, stream=None):

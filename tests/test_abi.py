@@ -141,3 +141,23 @@ def test_exp16_validation(q):
     assert L.quake_exp16(FAKE, FAKE, 10, 1, 2, float("inf"), 0.0, None) == q.EINVAL
     assert L.quake_exp16(FAKE, FAKE, 10, 2, 2, 1.0, float("nan"), None) == q.EINVAL
     assert L.quake_exp16(FAKE, FAKE, 10, 1, 2, 3e38, 0.0, None) == q.EINVAL      # c0 overflows
+
+
+def test_linear_gelu_validation(q):
+    L = q.lib
+    A = 0x10000   # 16-byte aligned, never dereferenced
+
+    def call(m=256, n=256, k=64, ldx=64, ldw=64, ldy=256, dt=2, mode=2, x=A, w=A, y=A):
+        return L.quake_linear_gelu(x, w, y, m, n, k, ldx, ldw, ldy, dt, mode, 1, None)
+    assert call(m=0) == q.OK and call(n=0) == q.OK
+    assert call(dt=0) == q.EDTYPE and call(dt=1) == q.EDTYPE
+    assert call(mode=7) == q.EMODE
+    assert call(k=0) == q.EINVAL
+    assert call(k=60, ldx=64, ldw=64) == q.EINVAL         # k not a multiple of 8
+    assert call(ldx=32) == q.EINVAL                        # ldx < k
+    assert call(ldx=68) == q.EINVAL                        # ldx not a multiple of 8
+    assert call(ldy=255) == q.EINVAL
+    assert call(x=A + 2) == q.EINVAL                       # misaligned x
+    assert call(w=A + 8) == q.EINVAL
+    assert call(y=0) == q.EINVAL
+    assert call(m=-1) == q.EINVAL

@@ -1,0 +1,86 @@
+"""GPU parity of quake_linear_gelu (matrix-core product with the GELU of Eq. 7
+in its epilogue) against the oracle's float64 product rounded to binary32
+followed by the oracle's GELU.
+
+Tolerance per element (derived, written here): the GPU sums in binary32 in
+its own order, so its accumulator differs from the binary32-rounded exact sum
+by at most k * 2^-24 * sum_i |x_i w_i| (plus that rounding); GELU with any of
+the exponentials here changes by at most 2x a change of its argument (slope of
+x * sigma(.) at most 1.13, QuAKE's piecewise slope at most 1.44 times e^x's),
+and each side rounds once to bfloat16: |gpu - ref| <= ulp_bf16(ref) +
+2 * (k + 1) * 2^-24 * sum|x||w| + 2^-126."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import THREADS, host_bits, say
+from paper_2412_00408_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def q():
+    assert torch.cuda.is_available(), "GPU tests need cuda:0"
+    from paper_2412_00408_amd import quake
+    return quake
+
+
+def _ulp_bf16(v):
+    a = np.abs(v)
+    e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
+    return np.where(a >= 2.0 ** -126, np.ldexp(1.0, (e - 7).astype(int)), 2.0 ** -133)
+
+
+def _check(g_bits, r_bits, xb, wb, k, lip, name):
+    g = oracle.decode(g_bits.reshape(-1), "bf16").astype(np.float64)
+    r = oracle.decode(r_bits.reshape(-1), "bf16").astype(np.float64)
+    xa = np.abs(oracle.decode(xb.reshape(-1), "bf16").astype(np.float64)).reshape(xb.shape)
+    wa = np.abs(oracle.decode(wb.reshape(-1), "bf16").astype(np.float64)).reshape(wb.shape)
+    s = (xa @ wa.T).reshape(-1)
+    bound = _ulp_bf16(r) + lip * (k + 1) * 2.0 ** -24 * s + 2.0 ** -126
+    err = np.abs(g - r)
+    bad = ~(err <= bound)
+    assert not bad.any(), "%s: %d of %d outside the bound, worst at %d: gpu %r ref %r bound %r" % (
+        name, int(bad.sum()), bad.size, int(np.argmax(err - bound)), g[np.argmax(err - bound)],
+        r[np.argmax(err - bound)], bound[np.argmax(err - bound)])
+    return err
+
+
+def _run(q, m, n, k, mode, gelu, seed, pad=0):
+    x = synth.normal((m, k + pad), 1.0, "bf16", seed)
+    w = synth.normal((n, k + pad), 0.05, "bf16", seed + 1)
+    xg, wg = x.to("cuda:0"), w.to("cuda:0")
+    y = q.quake_linear_gelu(xg[:, :k], wg[:, :k], mode=mode, gelu=gelu)
+    torch.cuda.synchronize()
+    xb, wb = host_bits(x)[:, :k].copy(), host_bits(w)[:, :k].copy()
+    ref = oracle.linear_gelu(xb, wb, mode, gelu=gelu, threads=THREADS)
+    return host_bits(y), ref, xb, wb
+
+
+@pytest.mark.parametrize("m,n,k", [(128, 128, 64), (256, 384, 768), (200, 130, 72), (1, 1, 8),
+                                   (129, 257, 136), (64, 1000, 32)])
+@pytest.mark.parametrize("mode", [0, 1, 2, 3])
+def test_shapes_and_modes(q, m, n, k, mode):
+    for gelu in (True, False):
+        say("linear gelu", m, n, k, mode, gelu)
+        g, r, xb, wb = _run(q, m, n, k, mode, gelu, 1600 + m % 7 + n % 5)
+        _check(g, r, xb, wb, k, 2.0 if gelu else 1.0, "linear %dx%dx%d mode %d gelu %d" % (m, n, k, mode, gelu))
+
+
+def test_strided_rows(q):
+    say("linear gelu strided")
+    g, r, xb, wb = _run(q, 256, 256, 768, 2, True, 1700, pad=24)
+    _check(g, r, xb, wb, 768, 2.0, "strided")
+
+
+@pytest.mark.parametrize("mode", [0, 2])
+def test_bert_mlp_shape(q, mode):
+    """The up-projection of a BERT-base MLP over 4096 tokens, [4096, 768] x [3072, 768]^T,
+    the producer of the GELU workload's input."""
+    say("linear gelu 4096x3072x768", mode)
+    g, r, xb, wb = _run(q, 4096, 3072, 768, mode, True, 1800)
+    err = _check(g, r, xb, wb, 768, 2.0, "bert mlp mode %d" % mode)
+    # most outputs are the oracle's bfloat16 value itself
+    assert np.count_nonzero(err == 0) > 0.95 * err.size
