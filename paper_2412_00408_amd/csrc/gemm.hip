@@ -66,7 +66,10 @@ __global__ __launch_bounds__(kGemmThreads, 3) void gemm_bf16_kernel(GemmArgs g) 
 
   // Slab loads: 1024 16-byte vectors per operand; thread t takes t + 256 i,
   // i.e. row v / 8 and k-vector v mod 8. Rows past m (n) re-read the last
-  // row; k past the end reads zeros (k is a multiple of 8).
+  // row; k past the end re-reads k-vector 0 and is replaced by zeros when the
+  // slab is written to LDS (k is a multiple of 8). Nothing consumes the loaded
+  // registers before that write, so the loads stay in flight during the
+  // previous slab's MFMAs.
   u32x4 rx[4], rw[4];
   const u32x4 zero = {0u, 0u, 0u, 0u};
   auto load_slab = [&](int k0) {
@@ -75,21 +78,19 @@ __global__ __launch_bounds__(kGemmThreads, 3) void gemm_bf16_kernel(GemmArgs g) 
       const int v = t + kGemmThreads * i;
       const int r = v >> 3, kk = k0 + 8 * (v & 7);
       const int gm = min(row0 + r, g.m - 1), gn = min(col0 + r, g.n - 1);
-      const bool in = kk < g.k;
-      const int kc = in ? kk : 0;
-      const u32x4 a = *reinterpret_cast<const u32x4*>(g.x + (int64_t)gm * g.ldx + kc);
-      const u32x4 b = *reinterpret_cast<const u32x4*>(g.w + (int64_t)gn * g.ldw + kc);
-      rx[i] = in ? a : zero;
-      rw[i] = in ? b : zero;
+      const int kc = kk < g.k ? kk : 0;
+      rx[i] = *reinterpret_cast<const u32x4*>(g.x + (int64_t)gm * g.ldx + kc);
+      rw[i] = *reinterpret_cast<const u32x4*>(g.w + (int64_t)gn * g.ldw + kc);
     }
   };
-  auto store_slab = [&]() {
+  auto store_slab = [&](int k0) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int v = t + kGemmThreads * i;
       const int r = v >> 3, c = 8 * (v & 7);
-      *reinterpret_cast<u32x4*>(sx + r * kLdsRow + c) = rx[i];
-      *reinterpret_cast<u32x4*>(sw + r * kLdsRow + c) = rw[i];
+      const bool in = k0 + c < g.k;
+      *reinterpret_cast<u32x4*>(sx + r * kLdsRow + c) = in ? rx[i] : zero;
+      *reinterpret_cast<u32x4*>(sw + r * kLdsRow + c) = in ? rw[i] : zero;
     }
   };
 
@@ -106,7 +107,7 @@ __global__ __launch_bounds__(kGemmThreads, 3) void gemm_bf16_kernel(GemmArgs g) 
   const int fr = lane & 31, fk = 8 * (lane >> 5);
   for (int kt = 0; kt < nk; ++kt) {
     __syncthreads();   // every wave is done reading the previous slab
-    store_slab();
+    store_slab(kt * kBK);
     __syncthreads();
     if (kt + 1 < nk) load_slab((kt + 1) * kBK);   // in flight during the MFMAs
 #pragma unroll
