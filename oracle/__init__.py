@@ -73,6 +73,8 @@ def lib() -> ctypes.CDLL:
         L.qo_gelu_unfused.argtypes = [vp, vp, i64, ci, ci]
         L.qo_round.argtypes = [vp, vp, i64, ci]
         L.qo_decode.argtypes = [vp, vp, i64, ci]
+        L.qo_softmax_numerators.argtypes = [vp, vp, vp, i64, i64, ci, cf]
+        L.qo_softmax_numerators.restype = ci
         L.qo_gelu_f32in.argtypes = [vp, vp, i64, ci, ci]
         L.qo_gelu_f32in.restype = ci
         L.qo_exp16.argtypes = [vp, vp, i64, ci, ci, cf, cf]
@@ -249,6 +251,50 @@ def softmax_causal(x, period, shift=0, dt="f32", mode=Q2, t=1.0, threads=1):
         with ThreadPoolExecutor(threads) as ex:
             list(ex.map(run, ranges))
     return y
+
+
+def softmax_numerators(s: np.ndarray, mode: int, t: float = 1.0, threads: int = 1):
+    """Algorithm 2 without the division, on binary32 rows: (p, sums) with p the
+    binary32 exponentials against each row's max and sums their float64 sums."""
+    s = np.ascontiguousarray(s, dtype=np.float32)
+    rows, cols = s.shape
+    p = np.empty_like(s)
+    sums = np.empty(rows, np.float64)
+
+    def work(r):
+        lo, hi = r
+        _check(lib().qo_softmax_numerators(_ptr(s[lo:]), _ptr(p[lo:]), _ptr(sums[lo:]), hi - lo,
+                                           cols, mode, t))
+
+    with ThreadPoolExecutor(max(1, threads)) as ex:
+        list(ex.map(work, _split(rows, threads)))
+    return p, sums
+
+
+def attention(q: np.ndarray, k: np.ndarray, vt: np.ndarray, mode: int, t: float,
+              causal: bool = True, threads: int = 1) -> np.ndarray:
+    """softmax(t q k^T) v per head with the softmax of Algorithm 2, for bfloat16
+    q, k [h, s, d] and vt [h, d, >= s] (v transposed, raw bits; columns past s
+    are ignored). Scores: float64 products of the
+    bfloat16 inputs rounded once to binary32, causal entries (key > query) set
+    to -inf; numerators and sums as softmax_numerators; the numerators rounded
+    to bfloat16 for the second product (its operands are bfloat16), that product
+    in float64, divided by the float64 sum, rounded to bfloat16."""
+    h, s_len, d = q.shape
+    qd = decode(np.ascontiguousarray(q).reshape(-1), "bf16").astype(np.float64).reshape(h, s_len, d)
+    kd = decode(np.ascontiguousarray(k).reshape(-1), "bf16").astype(np.float64).reshape(h, s_len, d)
+    vd = decode(np.ascontiguousarray(vt[:, :, :s_len]).reshape(-1), "bf16").astype(
+        np.float64).reshape(h, d, s_len)
+    scores = np.matmul(qd, np.transpose(kd, (0, 2, 1))).astype(np.float32)
+    if causal:
+        mask = np.arange(s_len)[None, :] > np.arange(s_len)[:, None]
+        scores[:, mask] = -np.inf
+    p, sums = softmax_numerators(scores.reshape(h * s_len, s_len), mode, t, threads)
+    pb = decode(round_to(p.astype(np.float64).reshape(-1), "bf16"), "bf16").astype(np.float64)
+    o = np.matmul(pb.reshape(h, s_len, s_len), np.transpose(vd, (0, 2, 1)))
+    with np.errstate(invalid="ignore", divide="ignore"):
+        o = np.where(sums.reshape(h, s_len, 1) > 0, o / sums.reshape(h, s_len, 1), 0.0)
+    return round_to(o.reshape(-1), "bf16").reshape(h, s_len, d)
 
 
 def linear_gelu(x: np.ndarray, w: np.ndarray, mode: int, gelu: bool = True, dt: str = "bf16",

@@ -31,6 +31,9 @@
  *                 standard exponential plugged in: softmax computes (v - m) * t
  *                 and then e^s; GELU computes k * x * (1/0.044715 + x^2) and then
  *                 e^-s; EXACT mode is the vanilla operator with exp.
+ *   qo_softmax_numerators
+ *                 Algorithm 2 without the final division: the exponentials of
+ *                 a binary32 row against its max, and the row sum (attention).
  *   qo_gelu_f32in qo_gelu on binary32 inputs with output in any format (the
  *                 epilogue of a matrix product: GELU of the binary32 sums).
  *   qo_exp16      Sec. II-A/II-B in a 16-bit format's own layout: Eq. 3 with
@@ -503,6 +506,44 @@ int qo_softmax_unfused(const void* x, void* y, int64_t rows, int64_t cols, int64
       sum += tmp[j];
     }
     for (int64_t j = 0; j < cols; ++j) store_el(y, by + j, dt, tmp[j] / sum);
+  }
+  return 0;
+}
+
+/*
+ * Algorithm 2 up to the normalisation, for binary32 score rows (the scores of
+ * an attention head): p[r, j] = QuAKEx(s[r, j]) with c1 from the row max (the
+ * EXACT mode exponentiates the same base-2 argument), and sums[r] = sum_j p[r, j]
+ * in double. -inf entries give 0; an all -inf row gives zeros and sum 0.
+ */
+int qo_softmax_numerators(const float* s, float* p, double* sums, int64_t rows, int64_t cols,
+                          int mode, float t) {
+  int err = bad_args(QO_F32, mode);
+  if (err) return err;
+  float c0 = qo_softmax_c0(t, mode);
+  for (int64_t r = 0; r < rows; ++r) {
+    const float* sr = s + r * cols;
+    float* pr = p + r * cols;
+    float m = -INFINITY;
+    for (int64_t j = 0; j < cols; ++j)
+      if (sr[j] > m) m = sr[j];
+    double sum = 0.0;
+    if (m == -INFINITY) {
+      for (int64_t j = 0; j < cols; ++j) pr[j] = 0.0f;
+    } else if (mode == QO_EXACT) {
+      float c1e = fmaf(-c0, m, 0.0f);
+      for (int64_t j = 0; j < cols; ++j) {
+        pr[j] = exp2_binary32(fmaf(sr[j], c0, c1e));
+        sum += pr[j];
+      }
+    } else {
+      float c1 = fmaf(-c0, m, k127());
+      for (int64_t j = 0; j < cols; ++j) {
+        pr[j] = quake_one(sr[j], c0, c1, mode);
+        sum += pr[j];
+      }
+    }
+    sums[r] = sum;
   }
   return 0;
 }
