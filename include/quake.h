@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define QUAKE_ABI_VERSION 2
+#define QUAKE_ABI_VERSION 3
 
 typedef enum {
   QUAKE_F32 = 0,  /* IEEE binary32 */
@@ -237,6 +237,33 @@ quake_status quake_exp16(const void* x, void* y, int64_t n, quake_dtype dtype, q
 quake_status quake_linear_gelu(const void* x, const void* w, void* y, int64_t m, int64_t n,
                                int64_t k, int64_t ldx, int64_t ldw, int64_t ldy,
                                quake_dtype dtype, quake_mode mode, int gelu, void* stream);
+
+/*
+ * quake_attention — o = softmax(t q k^T) v for every head: scaled dot-product
+ * attention whose softmax is Algorithm 2 (Sec. III-C) with the exponential of
+ * `mode`, fused with both products. Each query's exponentials are taken
+ * against the max of its whole score row (no online rescaling), so the
+ * probabilities are the ones quake_softmax gives for those scores; they are
+ * rounded to bfloat16 before the second product, and the row sum (of the
+ * binary32 exponentials) divides the binary32 result, rounded to bfloat16.
+ *   q, k : device, [heads, seq, dim] bfloat16, contiguous, 16-byte aligned.
+ *   vt   : device, v transposed: [heads, dim, ldv] bfloat16, element
+ *          (h, d, j) = v[h, j, d]; ldv >= seq, 2-byte aligned. Columns
+ *          seq .. ldv-1 may hold anything (they do not affect o). With vt
+ *          16-byte aligned and ldv a multiple of 8 the rows are read as
+ *          16-byte vectors, else element by element.
+ *   o    : device, [heads, seq, dim] bfloat16, contiguous, 8-byte aligned.
+ *   dim == 64 and seq <= 512 (the keys of a row stay in registers);
+ *   t > 0 finite (1/sqrt(dim) for the usual scaling); causal != 0 lets query
+ *   i use keys j <= i only (masked keys are neither loaded nor multiplied).
+ *   dtype : QUAKE_BF16 only (else QUAKE_EDTYPE); mode: any quake_mode.
+ * Scores are binary32 sums of the bfloat16 products (order unspecified).
+ * heads == 0 or seq == 0 launches nothing; other bad sizes, strides,
+ * alignments or t return QUAKE_EINVAL.
+ */
+quake_status quake_attention(const void* q, const void* k, const void* vt, void* o, int64_t heads,
+                             int64_t seq, int64_t dim, int64_t ldv, quake_dtype dtype,
+                             quake_mode mode, float t, int causal, void* stream);
 
 /*
  * quake_softmax_split_timeouts — number of exchange waits of the split-row

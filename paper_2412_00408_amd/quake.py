@@ -44,8 +44,9 @@ def _load() -> ctypes.CDLL:
     L.quake_gelu_unfused.argtypes = [vp, vp, i64, ci, ci, vp]
     L.quake_softmax_causal.argtypes = [vp, vp, i64, i64, i64, i64, i64, i64, ci, ci, ci, cf, vp]
     L.quake_sigmoid.argtypes = [vp, vp, i64, ci, ci, ci, vp]
+    L.quake_attention.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, ci, ci, cf, ci, vp]
     for f in (L.quake_exp, L.quake_exp16, L.quake_linear_gelu, L.quake_softmax, L.quake_gelu,
-              L.quake_sigmoid,
+              L.quake_sigmoid, L.quake_attention,
               L.quake_softmax_unfused, L.quake_gelu_unfused, L.quake_softmax_causal):
         f.restype = ci
     L.quake_softmax_split_timeouts.argtypes = [vp, ctypes.POINTER(i64)]
@@ -182,6 +183,52 @@ def quake_linear_gelu(x, w, y=None, mode=QUAKE_2, gelu=True, stream=None):
         x.data_ptr(), w.data_ptr(), y.data_ptr(), m, n, k, x.stride(0), w.stride(0), y.stride(0),
         DTYPES[x.dtype], MODES[mode], int(bool(gelu)), _stream(x, stream)))
     return y
+
+
+def _vt_row_stride(shape, strides) -> int:
+    """Row stride (ldv) of v^T [..., dim, seq]: the last dimension contiguous,
+    rows ldv apart, heads dim * ldv apart one after another."""
+    dim, seq = shape[-2], shape[-1]
+    if seq > 1 and strides[-1] != 1:
+        raise ValueError("vt must have a contiguous last dimension")
+    ldv = strides[-2] if dim > 1 else seq
+    want = [ldv, 1]
+    for i in range(len(shape) - 3, -1, -1):
+        want.insert(0, want[0] * shape[i + 1])
+    if any(n > 1 and st != w for n, st, w in zip(shape, strides, want)):
+        raise ValueError("vt must be [..., dim, seq] with a contiguous last dimension and "
+                         "rows (possibly padded) packed head after head")
+    return ldv
+
+
+def quake_attention(q, k, vt, o=None, mode=QUAKE_2, t=None, causal=True, stream=None):
+    """softmax(t q k^T) v per head with Algorithm 2's softmax: bfloat16 q, k
+    [..., seq, 64] and vt = v transposed [..., 64, seq] (or a view of wider,
+    padded rows with a contiguous last dimension); returns
+    bfloat16 o [..., seq, 64]. t defaults to 1/sqrt(64)."""
+    for a, what in ((q, "q"), (k, "k"), (vt, "vt")):
+        if not a.is_cuda:
+            raise ValueError("libquake takes device tensors")
+        if a.dtype not in DTYPES:
+            raise TypeError("libquake takes float32, float16 or bfloat16 tensors, got %s" % a.dtype)
+        if a.dim() < 2:
+            raise ValueError("%s needs [..., rows, cols]" % what)
+    if not (q.is_contiguous() and k.is_contiguous()) or q.shape != k.shape:
+        raise ValueError("q and k must be contiguous and of the same shape")
+    seq, dim = q.shape[-2], q.shape[-1]
+    heads = q.numel() // max(seq * dim, 1)
+    if tuple(vt.shape[:-2]) != tuple(q.shape[:-2]) or tuple(vt.shape[-2:]) != (dim, seq):
+        raise ValueError("vt must be [..., dim, seq]")
+    ldv = _vt_row_stride(tuple(vt.shape), tuple(vt.stride()))
+    if o is None:
+        o = torch.empty_like(q)
+    if o.shape != q.shape or o.dtype != q.dtype or not o.is_contiguous():
+        raise ValueError("o must be contiguous and shaped like q")
+    t = 1.0 / dim ** 0.5 if t is None else t
+    _raise("quake_attention", lib.quake_attention(
+        q.data_ptr(), k.data_ptr(), vt.data_ptr(), o.data_ptr(), heads, seq, dim, ldv,
+        DTYPES[q.dtype], MODES[mode], t, int(bool(causal)), _stream(q, stream)))
+    return o
 
 
 def quake_softmax_unfused(x, y=None, mode=QUAKE_2, t=1.0, stream=None):

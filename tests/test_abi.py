@@ -161,3 +161,39 @@ def test_linear_gelu_validation(q):
     assert call(w=A + 8) == q.EINVAL
     assert call(y=0) == q.EINVAL
     assert call(m=-1) == q.EINVAL
+
+
+def test_attention_validation(q):
+    L = q.lib
+    A = 0x10000   # 16-byte aligned, never dereferenced
+
+    def call(h=4, s=128, d=64, ldv=128, dt=2, mode=2, t=0.125, qp=A, kp=A, vp=A, op=A):
+        return L.quake_attention(qp, kp, vp, op, h, s, d, ldv, dt, mode, t, 1, None)
+    assert call(h=0) == q.OK and call(s=0, ldv=0) == q.OK
+    assert call(h=0, qp=None, kp=None, vp=None, op=None) == q.OK
+    assert call(dt=0) == q.EDTYPE and call(dt=1) == q.EDTYPE
+    assert call(mode=9) == q.EMODE
+    assert call(d=128) == q.EINVAL                         # head dimension 64 only
+    assert call(s=520, ldv=520) == q.EINVAL                # longer than 512
+    assert call(s=130, ldv=128) == q.EINVAL                # ldv < seq
+    assert call(t=0.0) == q.EINVAL and call(t=float("nan")) == q.EINVAL
+    assert call(t=1e38) == q.EINVAL                        # c0 overflows
+    assert call(qp=A + 8) == q.EINVAL and call(vp=A + 1) == q.EINVAL
+    assert call(op=A + 2) == q.EINVAL
+    assert call(kp=None) == q.EINVAL
+    assert call(h=-1) == q.EINVAL
+
+
+def test_attention_vt_row_stride(q):
+    import torch
+    f = q._vt_row_stride
+    vt = torch.empty((2, 3, 64, 40))
+    assert f(tuple(vt.shape), vt.stride()) == 40
+    padded = torch.empty((2, 3, 64, 48))[..., :40]
+    assert f(tuple(padded.shape), padded.stride()) == 48
+    with pytest.raises(ValueError):
+        t = torch.empty((2, 3, 40, 64)).transpose(-1, -2)       # v, not v^T, in memory
+        f(tuple(t.shape), t.stride())
+    with pytest.raises(ValueError):
+        t = torch.empty((3, 2, 64, 40)).transpose(0, 1)         # heads out of order
+        f(tuple(t.shape), t.stride())

@@ -1,0 +1,164 @@
+"""GPU parity of quake_attention (both products on the matrix cores, the
+softmax of Algorithm 2 between them, all in one kernel) against the oracle's
+attention on the same seeded bfloat16 q, k and transposed v.
+
+Tolerance per output element (derived, written here). The GPU sums the 64
+products of a score in binary32 in its own order, the oracle rounds the exact
+sum once: |dS| <= 65 * 2^-24 * sum_i |q_i k_i| =: ds per score, and the row max
+moves by at most the same. An exponential of (s - m) t changes by a relative
+1.5 t (|ds| + |dm|) at most (QuAKE's piecewise slope is at most 1.44 times
+e^x's; EXACT's v_exp_f32 adds 2^-23), so each probability moves by at most
+rp = 3 t ds_max + 2^-22 before its rounding to bfloat16, which can then land on
+the neighbouring value (one bfloat16 ulp, at most 2^-7 relative). The second
+product and the row sum add (seq + 4) 2^-24 relative in binary32, and each side
+rounds the result once to bfloat16:
+  |gpu - ref| <= ulp_bf16(ref) + (2^-7 + 2.2 rp + (seq + 4) 2^-24) * pv
+with pv = sum_k p_k |v_k| / sum_k p_k (textbook probabilities, times 1.1 to
+cover QuAKE's <= 3 % error). Further, at least 99 % of the elements must be
+within one bfloat16 ulp of the oracle (probability roundings rarely flip).
+Cases: every mode, causal and not, one to several 32-query tiles, a ragged
+last tile, ragged key blocks, the longest sequence (512), a single key, a
+padded v^T row whose padding is NaN, and the full 96-head x 512 workload in
+the launch configuration the benchmark times, compared element by element."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import THREADS, host_bits, say
+from paper_2412_00408_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+T = 0.125
+
+
+@pytest.fixture(scope="module")
+def q():
+    assert torch.cuda.is_available(), "GPU tests need cuda:0"
+    from paper_2412_00408_amd import quake
+    return quake
+
+
+def _ulp_bf16(v):
+    a = np.abs(v)
+    e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
+    return np.where(a >= 2.0 ** -126, np.ldexp(1.0, (e - 7).astype(int)), 2.0 ** -133)
+
+
+def _dec(b):
+    return oracle.decode(np.ascontiguousarray(b).reshape(-1), "bf16").astype(np.float64).reshape(b.shape)
+
+
+def _bound(qb, kb, vtb, seq, causal, ref):
+    out = np.empty(ref.shape)
+    for h0 in range(0, ref.shape[0], 4):
+        sl = slice(h0, h0 + 4)
+        out[sl] = _bound_heads(qb[sl], kb[sl], vtb[sl], seq, causal, ref[sl])
+    return out
+
+
+def _bound_heads(qb, kb, vtb, seq, causal, ref):
+    qd, kd = _dec(qb), _dec(kb)
+    vd = _dec(vtb)[:, :, :seq]
+    sc = np.matmul(qd, np.transpose(kd, (0, 2, 1)))
+    sa = np.matmul(np.abs(qd), np.transpose(np.abs(kd), (0, 2, 1)))
+    if causal:
+        mask = np.triu(np.ones((seq, seq), bool), 1)
+        sc[:, mask] = -np.inf
+        sa[:, mask] = 0.0
+    ds_max = 65 * 2.0 ** -24 * sa.max(axis=2, keepdims=True)
+    rp = 3 * T * ds_max + 2.0 ** -22
+    p = np.exp(T * (sc - sc.max(axis=2, keepdims=True)))
+    pv = 1.1 * np.matmul(p, np.transpose(np.abs(vd), (0, 2, 1))) / p.sum(axis=2, keepdims=True)
+    return _ulp_bf16(ref) + (2.0 ** -7 + 2.2 * rp + (seq + 4) * 2.0 ** -24) * pv
+
+
+def _run(q, heads, seq, mode, causal, seed, ldv=None, pad=0.0):
+    say("attention heads=%d seq=%d ldv=%s mode=%d causal=%d seed=%d" % (heads, seq, ldv, mode,
+                                                                          causal, seed))
+    qc, kc, vtc = synth.attention_inputs(heads, seq, seed, ldv=ldv, pad=pad)
+    qg, kg, vtg = qc.to("cuda:0"), kc.to("cuda:0"), vtc.to("cuda:0")
+    o = torch.full((heads, seq, 64), float("nan"), dtype=torch.bfloat16, device="cuda:0")
+    if ldv is not None and ldv != seq:
+        vt_view = vtg[:, :, :seq]
+    else:
+        vt_view = vtg
+    q.quake_attention(qg, kg, vt_view, o, mode=mode, t=T, causal=causal)
+    torch.cuda.synchronize()
+    qb, kb, vtb = host_bits(qc), host_bits(kc), host_bits(vtc)
+    ref = oracle.attention(qb, kb, vtb, mode, T, causal, threads=THREADS)
+    return host_bits(o), ref, (qb, kb, vtb)
+
+
+def _check(g_bits, r_bits, ins, seq, causal, name):
+    g, r = _dec(g_bits), _dec(r_bits)
+    assert not np.isnan(g).any(), "%s: unwritten or NaN outputs" % name
+    bound = _bound(*ins, seq, causal, r)
+    err = np.abs(g - r)
+    bad = ~(err <= bound)
+    i = int(np.argmax((err - bound).reshape(-1)))
+    assert not bad.any(), "%s: %d of %d outside the bound, worst at %d: gpu %r ref %r bound %r" % (
+        name, int(bad.sum()), bad.size, i, g.reshape(-1)[i], r.reshape(-1)[i], bound.reshape(-1)[i])
+    within1 = np.mean(err <= _ulp_bf16(r))
+    assert within1 >= 0.99, "%s: only %.4f within one bfloat16 ulp" % (name, within1)
+    return err
+
+
+SHAPES = [(2, 64), (3, 40), (2, 96), (1, 512), (2, 33), (5, 8)]
+
+
+@pytest.mark.parametrize("mode", [0, 1, 2, 3])
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("heads,seq", SHAPES)
+def test_attention_matches_oracle(q, mode, causal, heads, seq):
+    g, r, ins = _run(q, heads, seq, mode, causal, 60 + seq)
+    _check(g, r, ins, seq, causal, "h%d s%d m%d c%d" % (heads, seq, mode, causal))
+
+
+@pytest.mark.parametrize("mode", [0, 2])
+def test_single_key_returns_v(q, mode):
+    g, r, ins = _run(q, 4, 1, mode, False, 61)
+    assert np.array_equal(g.reshape(4, 64), ins[2].reshape(4, 64))
+
+
+@pytest.mark.parametrize("ldv", [208, 203])     # vector rows; element-wise rows
+@pytest.mark.parametrize("causal", [True, False])
+def test_padded_vt_rows_with_nan_padding(q, causal, ldv):
+    g, r, ins = _run(q, 3, 200, 2, causal, 62, ldv=ldv, pad=float("nan"))
+    _check(g, r, ins, 200, causal, "padded")
+
+
+def test_full_workload_causal_quake2(q):
+    """96 heads x 512 keys, the configuration the benchmark times."""
+    g, r, ins = _run(q, 96, 512, 2, True, 63)
+    _check(g, r, ins, 512, True, "full")
+
+
+def test_full_workload_noncausal_exact(q):
+    g, r, ins = _run(q, 96, 512, 0, False, 64)
+    _check(g, r, ins, 512, False, "full exact")
+
+
+def test_deterministic_and_zero_sizes(q):
+    qc, kc, vtc = synth.attention_inputs(8, 128, 65)
+    qg, kg, vtg = qc.to("cuda:0"), kc.to("cuda:0"), vtc.to("cuda:0")
+    a = q.quake_attention(qg, kg, vtg, mode=2, t=T)
+    b = q.quake_attention(qg, kg, vtg, mode=2, t=T)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    e = torch.empty((0, 128, 64), dtype=torch.bfloat16, device="cuda:0")
+    et = torch.empty((0, 64, 128), dtype=torch.bfloat16, device="cuda:0")
+    assert q.quake_attention(e, e, et, mode=2).shape == (0, 128, 64)
+
+
+def test_bad_arguments_raise(q):
+    qc, kc, vtc = synth.attention_inputs(2, 64, 66)
+    qg, kg, vtg = qc.to("cuda:0"), kc.to("cuda:0"), vtc.to("cuda:0")
+    with pytest.raises(q.QuakeError):
+        q.quake_attention(qg, kg, vtg, t=-1.0)
+    with pytest.raises(q.QuakeError):
+        q.quake_attention(qg.float(), kg.float(), vtg.float())
+    big = torch.zeros((1, 520, 64), dtype=torch.bfloat16, device="cuda:0")
+    with pytest.raises(q.QuakeError):
+        q.quake_attention(big, big, torch.zeros((1, 64, 520), dtype=torch.bfloat16, device="cuda:0"))
