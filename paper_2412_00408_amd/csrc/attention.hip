@@ -52,6 +52,7 @@ struct AttnArgs {
   int32_t qblocks;   // ceil(s / 32)
   float c0;          // Algorithm 2: 2^23 t / ln2 (EXACT: t / ln2)
   uint32_t causal;
+  uint32_t xcd_group;   // grid size a multiple of 8: keep a head's tiles on one XCD
 };
 
 __device__ __forceinline__ u32x4_t ld16(const uint16_t* p) {
@@ -64,166 +65,260 @@ __device__ __forceinline__ float xor32(float v) {
   return as_f((threadIdx.x & 32) ? r[0] : r[1]);
 }
 
-// 8 keys key0 .. key0 + 7 of one V^T row; keys at or past s read as zero (their
-// probabilities are zero, and the padding of the row may hold anything).
-// VEC: rows 16-byte aligned (ldv a multiple of 8), one 16-byte load; else eight
-// 2-byte loads.
-template <bool VEC>
-__device__ __forceinline__ bf16x8_t load_v(const uint16_t* row, int key0, int s, bool tail) {
-  if constexpr (VEC) {
-    if (!tail) return __builtin_bit_cast(bf16x8_t, ld16(row + key0));
-    u32x4_t v = {0u, 0u, 0u, 0u};
-    const int nv = s - key0;
-    if (nv > 0) {
-      v = ld16(row + key0);
+// Operand staging. The matrix cores want lane (r, h) = (lane mod 32, lane / 32)
+// to hold 16 bytes of row r of a 32-row block; loaded straight from global
+// memory that is 32 rows per instruction. Instead each block is read with
+// whole rows per instruction (coalesced), written to the wave's own LDS slots
+// and read back in operand layout; 16-byte slots are XOR-swizzled so that
+// both the writes and the operand reads are free of bank conflicts. A wave
+// writes a block, reads it back and only then writes the next one, so one
+// buffer per wave suffices (LDS operations of a wave complete in order).
+//
+// K block: 32 keys x 128 B. Slot of (row r, chunk c): 8 r + (c ^ (r & 7)).
+// Load j of 4 covers rows 8 j .. 8 j + 7; lane l takes row 8 j + l / 8,
+// chunk l mod 8. Rows past s are clamped to row s - 1 (their scores are
+// masked afterwards).
+__device__ __forceinline__ void kblock_load(const uint16_t* k, int kbase, int s, int lane,
+                                            u32x4_t (&g)[4]) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (2 * i >= nv) v[i] = 0u;
-        else if (2 * i + 1 >= nv) v[i] &= 0xFFFFu;
-      }
-    }
-    return __builtin_bit_cast(bf16x8_t, v);
-  } else {
-    uint16_t e[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) e[i] = (!tail || key0 + i < s) ? row[key0 + i] : (uint16_t)0;
-    u32x4_t v;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = (uint32_t)e[2 * i] | ((uint32_t)e[2 * i + 1] << 16);
-    return __builtin_bit_cast(bf16x8_t, v);
+  for (int j = 0; j < 4; ++j) {
+    const int row = min(kbase + 8 * j + (lane >> 3), s - 1);
+    g[j] = ld16(k + (int64_t)row * kAttnD + 8 * (lane & 7));
   }
 }
+__device__ __forceinline__ void kblock_store(u32x4_t* buf, int lane, const u32x4_t (&g)[4]) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int r = 8 * j + (lane >> 3);
+    buf[8 * r + ((lane & 7) ^ (r & 7))] = g[j];
+  }
+}
+// A operands of S^T = K Q^T: 16-dim step ks, dims 16 ks + 8 h .. + 7 of key fr
+__device__ __forceinline__ void kblock_read(const u32x4_t* buf, int fr, int h, bf16x8_t (&a)[4]) {
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks)
+    a[ks] = __builtin_bit_cast(bf16x8_t, buf[8 * fr + ((2 * ks + h) ^ (fr & 7))]);
+}
 
-template <int MODE, bool VEC>
-__global__ __launch_bounds__(kAttnThreads) void attn_kernel(AttnArgs g) {
+// Layouts of V^T the kernel is built for: sequence a multiple of 32 with
+// 16-byte rows (no block reaches past s), any sequence with 16-byte rows, and
+// any sequence with rows of any alignment.
+enum VtKind { kVtFull = 0, kVtRagged = 1, kVtScalar = 2 };
+
+// V^T block: 64 dims x 32 keys (64 B). Slot of (row d, chunk c):
+// 4 d + (c ^ ((d >> 1) & 3)). Load j of 4 covers rows 16 j .. 16 j + 15; lane l
+// takes row 16 j + l / 4, keys kbase + 8 (l mod 4) .. + 7. In a block that
+// reaches past s (`tail`, uniform) keys at or past s read as zero without
+// leaving the row: their probabilities are zero, and the padding of the row
+// may hold anything.
+template <int VK>
+__device__ __forceinline__ void vblock_load(const uint16_t* vt, int ldv, int kbase, int s,
+                                            bool tail, int lane, u32x4_t (&g)[4]) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint16_t* row = vt + (int64_t)(16 * j + (lane >> 2)) * ldv;
+    const int key0 = kbase + 8 * (lane & 3);
+    u32x4_t v;
+    if constexpr (VK == kVtFull) {
+      v = ld16(row + key0);
+    } else if constexpr (VK == kVtRagged) {
+      const int nv = tail ? s - key0 : 8;
+      v = ld16(row + (nv > 0 ? key0 : 0));
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        v[i] = (2 * i + 1 < nv) ? v[i] : ((2 * i < nv) ? (v[i] & 0xFFFFu) : 0u);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int k0 = key0 + 2 * i, k1 = k0 + 1;
+        const uint32_t lo = (!tail || k0 < s) ? row[(!tail || k0 < s) ? k0 : 0] : 0u;
+        const uint32_t hi = (!tail || k1 < s) ? row[(!tail || k1 < s) ? k1 : 0] : 0u;
+        v[i] = lo | (hi << 16);
+      }
+    }
+    g[j] = v;
+  }
+}
+__device__ __forceinline__ void vblock_store(u32x4_t* buf, int lane, const u32x4_t (&g)[4]) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int d = 16 * j + (lane >> 2);
+    buf[4 * d + ((lane & 3) ^ ((d >> 1) & 3))] = g[j];
+  }
+}
+// A operands of O^T = V^T P: 16-key step ks, 32-dim half db; keys
+// 16 ks + 8 h .. + 7 of dim 32 db + fr
+__device__ __forceinline__ void vblock_read(const u32x4_t* buf, int fr, int h,
+                                            bf16x8_t (&a)[2][2]) {
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+    for (int db = 0; db < 2; ++db) {
+      const int d = 32 * db + fr;
+      a[ks][db] = __builtin_bit_cast(bf16x8_t, buf[4 * d + ((2 * ks + h) ^ ((d >> 1) & 3))]);
+    }
+}
+
+template <int MODE, int VK>
+__global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
   __shared__ float s_max[kAttnWaves][kAttnQ];
   __shared__ float s_sum[kAttnWaves][kAttnQ];
-  __shared__ float s_o[kAttnWaves][32 * 64];
+  // per wave: operand staging (4 KB), then its partial O^T (8 KB)
+  __shared__ u32x4_t s_buf[kAttnWaves][512];
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int bh = (int)(blockIdx.x / (uint32_t)g.qblocks);
-  const int qb = (int)(blockIdx.x % (uint32_t)g.qblocks);
+  const int lane = threadIdx.x & 63;
+  // uniform across the wave: every condition below that depends on it is a
+  // scalar branch
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // tiles of one head on one XCD (blockIdx round-robins over the 8 XCDs), so
+  // its K and V stay in that XCD's L2; within a head the longest causal rows
+  // first
+  uint32_t bid = blockIdx.x;
+  if (g.xcd_group) bid = (bid & 7u) * (gridDim.x >> 3) + (bid >> 3);
+  const int bh = (int)(bid / (uint32_t)g.qblocks);
+  const int qb = g.qblocks - 1 - (int)(bid % (uint32_t)g.qblocks);
   const int S = g.s;
   const int q0 = qb * kAttnQ;
   const int kblocks = (S + 31) >> 5;
   const int nkb = g.causal ? min(kblocks, qb + 1) : kblocks;   // live key blocks of the tile
+  // this wave's blocks are w, w + 4, ...: the first nlive of them are live
+  const int nlive = max(0, (nkb - wave + kAttnWaves - 1) / kAttnWaves);
   const int fr = lane & 31, fk = 8 * (lane >> 5);
   const int query = q0 + fr;
   const uint16_t* Q = g.q + (int64_t)bh * S * kAttnD;
   const uint16_t* K = g.k + (int64_t)bh * S * kAttnD;
   const uint16_t* Vt = g.vt + (int64_t)bh * kAttnD * g.ldv;
 
-  // S^T = K Q^T over the live key blocks of this wave
+  // S^T = K Q^T over the live key blocks, the next block's K in flight
   bf16x8_t qf[4];
   {
     const uint16_t* qr = Q + (int64_t)min(query, S - 1) * kAttnD + fk;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) qf[ks] = __builtin_bit_cast(bf16x8_t, ld16(qr + 16 * ks));
   }
+  u32x4_t* stage = s_buf[wave];
+  const int h = lane >> 5;
+  u32x4_t gk[4];
+  if (nlive > 0) kblock_load(K, 32 * wave, S, lane, gk);
   f32x16_t sacc[kAttnBlk];
+  float m = -INFINITY;
 #pragma unroll
   for (int i = 0; i < kAttnBlk; ++i) {
-    const int kbg = kAttnWaves * i + wave;
+    if (i < nlive) {
+      const int kbg = kAttnWaves * i + wave;
+      kblock_store(stage, lane, gk);
+      if (i + 1 < nlive) kblock_load(K, 32 * (kbg + kAttnWaves), S, lane, gk);
+      __builtin_amdgcn_wave_barrier();   // lanes read what other lanes wrote
+      bf16x8_t ka[4];
+      kblock_read(stage, fr, h, ka);
+      __builtin_amdgcn_wave_barrier();   // before the slots are written again
+      const f32x16_t zero = {};
+      sacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qf[0], zero, 0, 0, 0);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) sacc[i][r] = -INFINITY;
-    if (kbg < nkb) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[i][r] = 0.0f;
-      const uint16_t* kr = K + (int64_t)min(32 * kbg + fr, S - 1) * kAttnD + fk;
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
-        sacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            __builtin_bit_cast(bf16x8_t, ld16(kr + 16 * ks)), qf[ks], sacc[i], 0, 0, 0);
+      for (int ks = 1; ks < 4; ++ks)
+        sacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks], qf[ks], sacc[i], 0, 0, 0);
       const bool diag = g.causal && kbg == qb;
-      if (diag || 32 * kbg + 32 > S) {
+      if (diag || (VK != kVtFull && 32 * kbg + 32 > S)) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int key = 32 * kbg + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          const int key = 32 * kbg + 8 * (r >> 2) + 4 * h + (r & 3);
           if (key >= S || (diag && key > query)) sacc[i][r] = -INFINITY;
         }
       }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) m = fmaxf(m, sacc[i][r]);
     }
   }
+  // the first block of V^T in flight across the reductions
+  u32x4_t gv[4];
+  if (nlive > 0)
+    vblock_load<VK>(Vt, g.ldv, 32 * wave, S, VK != kVtFull && 32 * wave + 32 > S, lane, gv);
 
   // row (query) max: the lane's own values, lane l xor 32, the other waves
-  float m = -INFINITY;
-#pragma unroll
-  for (int i = 0; i < kAttnBlk; ++i)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) m = fmaxf(m, sacc[i][r]);
   m = fmaxf(m, xor32(m));
   if (lane < 32) s_max[wave][lane] = m;
   __syncthreads();
   m = fmaxf(fmaxf(s_max[0][fr], s_max[1][fr]), fmaxf(s_max[2][fr], s_max[3][fr]));
 
-  // Algorithm 2: exponentials against the row max (c1 folds it in), their sum
+  // Algorithm 2: exponentials against the row max (c1 folds it in), their
+  // sum; the probabilities rounded to bfloat16 pairs (keys 8 gi + 4 (lane / 32)
+  // + 0..3 of each block)
   const float c1 = (m == -INFINITY) ? 0.0f : __builtin_fmaf(-g.c0, m, MODE == EXACT ? 0.0f : kK127);
   float part = 0.0f;
+  uint32_t pk[kAttnBlk][4][2];
 #pragma unroll
   for (int i = 0; i < kAttnBlk; ++i) {
-    if (kAttnWaves * i + wave < nkb) {
+    if (i < nlive) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        sacc[i][r] = qexp<MODE>(sacc[i][r], g.c0, c1);
-        part += sacc[i][r];
+      for (int gi = 0; gi < 4; ++gi) {
+        float e[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          e[j] = qexp<MODE>(sacc[i][4 * gi + j], g.c0, c1);
+          part += e[j];
+        }
+        pk[i][gi][0] = pack_bf16(e[0], e[1]);
+        pk[i][gi][1] = pack_bf16(e[2], e[3]);
       }
     }
   }
   part += xor32(part);
   if (lane < 32) s_sum[wave][lane] = part;
 
-  // O^T = V^T P over this wave's live keys
-  f32x16_t oacc[2];
-#pragma unroll
-  for (int db = 0; db < 2; ++db)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) oacc[db][r] = 0.0f;
+  // O^T = V^T P over this wave's live keys, the next block's V in flight
+  f32x16_t oacc[2] = {};
 #pragma unroll
   for (int i = 0; i < kAttnBlk; ++i) {
-    const int kbg = kAttnWaves * i + wave;
-    if (kbg < nkb) {
-      const bool tail = 32 * kbg + 32 > S;
-      uint32_t gp[4][2];   // keys 8 gi + 4 (lane / 32) + 0..3 as two bfloat16 pairs
-#pragma unroll
-      for (int gi = 0; gi < 4; ++gi) {
-        gp[gi][0] = pack_bf16(sacc[i][4 * gi + 0], sacc[i][4 * gi + 1]);
-        gp[gi][1] = pack_bf16(sacc[i][4 * gi + 2], sacc[i][4 * gi + 3]);
+    if (i < nlive) {
+      const int kbg = kAttnWaves * i + wave;
+      vblock_store(stage, lane, gv);
+      if (i + 1 < nlive) {
+        const int nb = 32 * (kbg + kAttnWaves);
+        vblock_load<VK>(Vt, g.ldv, nb, S, VK != kVtFull && nb + 32 > S, lane, gv);
       }
+      __builtin_amdgcn_wave_barrier();
+      bf16x8_t va[2][2];
+      vblock_read(stage, fr, h, va);
+      __builtin_amdgcn_wave_barrier();
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         // lanes < 32 end with keys 16 ks + 0..7, lanes >= 32 with 16 ks + 8..15
-        const auto s0 = __builtin_amdgcn_permlane32_swap(gp[2 * ks][0], gp[2 * ks + 1][0], false, false);
-        const auto s1 = __builtin_amdgcn_permlane32_swap(gp[2 * ks][1], gp[2 * ks + 1][1], false, false);
+        const auto s0 = __builtin_amdgcn_permlane32_swap(pk[i][2 * ks][0], pk[i][2 * ks + 1][0], false, false);
+        const auto s1 = __builtin_amdgcn_permlane32_swap(pk[i][2 * ks][1], pk[i][2 * ks + 1][1], false, false);
         const u32x4_t bv = {s0[0], s1[0], s0[1], s1[1]};
         const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, bv);
-        const int key0 = 32 * kbg + 16 * ks + fk;
 #pragma unroll
-        for (int db = 0; db < 2; ++db) {
-          const bf16x8_t vf = load_v<VEC>(Vt + (int64_t)(32 * db + fr) * g.ldv, key0, S, tail);
-          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, oacc[db], 0, 0, 0);
-        }
+        for (int db = 0; db < 2; ++db)
+          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[ks][db], pf, oacc[db], 0, 0, 0);
       }
     }
   }
 
-  // the four partial O^T through LDS; wave w finishes dims 8 w + 4 (lane / 32)
-  // + 0..3 of both 32-dim halves
+  // the four partial O^T through LDS (each wave's own region, its staging
+  // reads done); wave w finishes dims 8 w + 4 (lane / 32) + 0..3 of both
+  // 32-dim halves
+  __builtin_amdgcn_wave_barrier();
+  float* po = reinterpret_cast<float*>(stage);
 #pragma unroll
   for (int db = 0; db < 2; ++db)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) s_o[wave][(db * 16 + r) * 64 + lane] = oacc[db][r];
+    for (int r = 0; r < 16; ++r) po[(db * 16 + r) * 64 + lane] = oacc[db][r];
   __syncthreads();
   if (query < S) {
     const float total = (s_sum[0][fr] + s_sum[1][fr]) + (s_sum[2][fr] + s_sum[3][fr]);
     const float inv = (m == -INFINITY || !(total > 0.0f)) ? 0.0f : 1.0f / total;
     uint16_t* orow = g.o + ((int64_t)bh * S + query) * kAttnD;
+    const float* p0 = reinterpret_cast<const float*>(s_buf[0]);
+    const float* p1 = reinterpret_cast<const float*>(s_buf[1]);
+    const float* p2 = reinterpret_cast<const float*>(s_buf[2]);
+    const float* p3 = reinterpret_cast<const float*>(s_buf[3]);
 #pragma unroll
     for (int db = 0; db < 2; ++db) {
       float v[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int idx = (db * 16 + 4 * wave + j) * 64 + lane;
-        v[j] = ((s_o[0][idx] + s_o[1][idx]) + (s_o[2][idx] + s_o[3][idx])) * inv;
+        v[j] = ((p0[idx] + p1[idx]) + (p2[idx] + p3[idx])) * inv;
       }
       uint2 w;
       w.x = pack_bf16(v[0], v[1]);
@@ -234,11 +329,13 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(AttnArgs g) {
 }
 
 template <int MODE>
-void launch_attn(bool vec, dim3 grid, hipStream_t s, const AttnArgs& g) {
-  if (vec)
-    hipLaunchKernelGGL((attn_kernel<MODE, true>), grid, dim3(kAttnThreads), 0, s, g);
+void launch_attn(int vk, dim3 grid, hipStream_t s, const AttnArgs& g) {
+  if (vk == kVtFull)
+    hipLaunchKernelGGL((attn_kernel<MODE, kVtFull>), grid, dim3(kAttnThreads), 0, s, g);
+  else if (vk == kVtRagged)
+    hipLaunchKernelGGL((attn_kernel<MODE, kVtRagged>), grid, dim3(kAttnThreads), 0, s, g);
   else
-    hipLaunchKernelGGL((attn_kernel<MODE, false>), grid, dim3(kAttnThreads), 0, s, g);
+    hipLaunchKernelGGL((attn_kernel<MODE, kVtScalar>), grid, dim3(kAttnThreads), 0, s, g);
 }
 
 }  // namespace qk
@@ -264,15 +361,17 @@ extern "C" quake_status quake_attention(const void* q, const void* k, const void
   if (heads > INT32_MAX / qblocks || heads * ldv * kAttnD > INT64_MAX / 4) return QUAKE_EINVAL;
   const AttnArgs g{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                    static_cast<const uint16_t*>(vt), static_cast<uint16_t*>(o), (int32_t)seq,
-                   (int32_t)ldv, (int32_t)qblocks, c0, (uint32_t)(causal != 0)};
+                   (int32_t)ldv, (int32_t)qblocks, c0, (uint32_t)(causal != 0),
+                   (uint32_t)((heads * qblocks) % 8 == 0)};
   const dim3 grid((uint32_t)(heads * qblocks));
   const hipStream_t s = static_cast<hipStream_t>(stream);
   const bool vec = aligned16(vt) && ldv % 8 == 0;
+  const int vk = !vec ? kVtScalar : (seq % 32 == 0 ? kVtFull : kVtRagged);
   switch (mode) {
-    case QUAKE_EXACT: launch_attn<EXACT>(vec, grid, s, g); break;
-    case QUAKE_1: launch_attn<Q1>(vec, grid, s, g); break;
-    case QUAKE_2: launch_attn<Q2>(vec, grid, s, g); break;
-    default: launch_attn<Q2M>(vec, grid, s, g); break;
+    case QUAKE_EXACT: launch_attn<EXACT>(vk, grid, s, g); break;
+    case QUAKE_1: launch_attn<Q1>(vk, grid, s, g); break;
+    case QUAKE_2: launch_attn<Q2>(vk, grid, s, g); break;
+    default: launch_attn<Q2M>(vk, grid, s, g); break;
   }
   return launch_status();
 }
