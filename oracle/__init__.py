@@ -275,11 +275,21 @@ def attention(q: np.ndarray, k: np.ndarray, vt: np.ndarray, mode: int, t: float,
               causal: bool = True, threads: int = 1) -> np.ndarray:
     """softmax(t q k^T) v per head with the softmax of Algorithm 2, for bfloat16
     q, k [h, s, d] and vt [h, d, >= s] (v transposed, raw bits; columns past s
-    are ignored). Scores: float64 products of the
-    bfloat16 inputs rounded once to binary32, causal entries (key > query) set
-    to -inf; numerators and sums as softmax_numerators; the numerators rounded
-    to bfloat16 for the second product (its operands are bfloat16), that product
-    in float64, divided by the float64 sum, rounded to bfloat16."""
+    are ignored). Heads are independent and are taken a few at a time."""
+    h, s_len, d = q.shape
+    out = np.empty((h, s_len, d), np.uint16)
+    for h0 in range(0, h, 4):
+        out[h0:h0 + 4] = _attention_heads(q[h0:h0 + 4], k[h0:h0 + 4], vt[h0:h0 + 4], mode, t,
+                                          causal, threads)
+    return out
+
+
+def _attention_heads(q, k, vt, mode, t, causal, threads):
+    """Scores: float64 products of the bfloat16 inputs rounded once to
+    binary32, causal entries (key > query) set to -inf; numerators and sums as
+    softmax_numerators; the numerators rounded to bfloat16 for the second
+    product (its operands are bfloat16), that product in float64, divided by
+    the float64 sum, rounded to bfloat16."""
     h, s_len, d = q.shape
     qd = decode(np.ascontiguousarray(q).reshape(-1), "bf16").astype(np.float64).reshape(h, s_len, d)
     kd = decode(np.ascontiguousarray(k).reshape(-1), "bf16").astype(np.float64).reshape(h, s_len, d)

@@ -70,11 +70,14 @@ __device__ __forceinline__ float xor32(float v) {
 // memory that is 32 rows per instruction. Instead each block is read with
 // whole rows per instruction (coalesced), written to the wave's own LDS slots
 // and read back in operand layout; 16-byte slots are XOR-swizzled so that
-// both the writes and the operand reads are free of bank conflicts. A wave
+// both the writes and the operand reads are free of bank conflicts (whether
+// the LDS serves 8 lanes of a 16-byte access per clock over 32 banks or 16
+// lanes over 64 banks). A wave
 // writes a block, reads it back and only then writes the next one, so one
 // buffer per wave suffices (LDS operations of a wave complete in order).
 //
-// K block: 32 keys x 128 B. Slot of (row r, chunk c): 8 r + (c ^ (r & 7)).
+// K block: 32 keys x 128 B. Slot of (row r, chunk c): 8 r + (c ^ fk(r)) with
+// fk(r) = (r mod 8) ^ ((r / 8) mod 2).
 // Load j of 4 covers rows 8 j .. 8 j + 7; lane l takes row 8 j + l / 8,
 // chunk l mod 8. Rows past s are clamped to row s - 1 (their scores are
 // masked afterwards).
@@ -86,18 +89,19 @@ __device__ __forceinline__ void kblock_load(const uint16_t* k, int kbase, int s,
     g[j] = ld16(k + (int64_t)row * kAttnD + 8 * (lane & 7));
   }
 }
+__device__ __forceinline__ int kswz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 __device__ __forceinline__ void kblock_store(u32x4_t* buf, int lane, const u32x4_t (&g)[4]) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int r = 8 * j + (lane >> 3);
-    buf[8 * r + ((lane & 7) ^ (r & 7))] = g[j];
+    buf[8 * r + ((lane & 7) ^ kswz(r))] = g[j];
   }
 }
 // A operands of S^T = K Q^T: 16-dim step ks, dims 16 ks + 8 h .. + 7 of key fr
 __device__ __forceinline__ void kblock_read(const u32x4_t* buf, int fr, int h, bf16x8_t (&a)[4]) {
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks)
-    a[ks] = __builtin_bit_cast(bf16x8_t, buf[8 * fr + ((2 * ks + h) ^ (fr & 7))]);
+    a[ks] = __builtin_bit_cast(bf16x8_t, buf[8 * fr + ((2 * ks + h) ^ kswz(fr))]);
 }
 
 // Layouts of V^T the kernel is built for: sequence a multiple of 32 with
@@ -106,7 +110,7 @@ __device__ __forceinline__ void kblock_read(const u32x4_t* buf, int fr, int h, b
 enum VtKind { kVtFull = 0, kVtRagged = 1, kVtScalar = 2 };
 
 // V^T block: 64 dims x 32 keys (64 B). Slot of (row d, chunk c):
-// 4 d + (c ^ ((d >> 1) & 3)). Load j of 4 covers rows 16 j .. 16 j + 15; lane l
+// 4 d + (c ^ fv(d)) with fv(d) = ((d / 2) ^ (d / 4)) mod 4. Load j of 4 covers rows 16 j .. 16 j + 15; lane l
 // takes row 16 j + l / 4, keys kbase + 8 (l mod 4) .. + 7. In a block that
 // reaches past s (`tail`, uniform) keys at or past s read as zero without
 // leaving the row: their probabilities are zero, and the padding of the row
@@ -139,11 +143,12 @@ __device__ __forceinline__ void vblock_load(const uint16_t* vt, int ldv, int kba
     g[j] = v;
   }
 }
+__device__ __forceinline__ int vswz(int d) { return ((d >> 1) ^ (d >> 2)) & 3; }
 __device__ __forceinline__ void vblock_store(u32x4_t* buf, int lane, const u32x4_t (&g)[4]) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int d = 16 * j + (lane >> 2);
-    buf[4 * d + ((lane & 3) ^ ((d >> 1) & 3))] = g[j];
+    buf[4 * d + ((lane & 3) ^ vswz(d))] = g[j];
   }
 }
 // A operands of O^T = V^T P: 16-key step ks, 32-dim half db; keys
@@ -155,7 +160,7 @@ __device__ __forceinline__ void vblock_read(const u32x4_t* buf, int fr, int h,
 #pragma unroll
     for (int db = 0; db < 2; ++db) {
       const int d = 32 * db + fr;
-      a[ks][db] = __builtin_bit_cast(bf16x8_t, buf[4 * d + ((2 * ks + h) ^ ((d >> 1) & 3))]);
+      a[ks][db] = __builtin_bit_cast(bf16x8_t, buf[4 * d + ((2 * ks + h) ^ vswz(d))]);
     }
 }
 

@@ -132,7 +132,8 @@ MUTANTS = {
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
 def test_pins_catch_attention_mutant(oracle, name):
-    src = textwrap.dedent(inspect.getsource(oracle.attention))
+    src = textwrap.dedent(inspect.getsource(oracle.attention)) + "\n" + textwrap.dedent(
+        inspect.getsource(oracle._attention_heads))
     old, new = MUTANTS[name]
     assert old in src, name
     ns = dict(vars(oracle))
