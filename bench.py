@@ -59,6 +59,9 @@ def parse():
     ap.add_argument("--launch", default="graph", choices=["graph", "eager"])
     ap.add_argument("--only", action="store_true",
                     help="time only --workload in --mode (for profiler passes)")
+    ap.add_argument("--attention-only", action="store_true",
+                    help="time only the fused attention (quake_attention) and print its JSON "
+                         "(for profiler passes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-table4", action="store_true",
@@ -561,8 +564,6 @@ def main():
     from paper_2412_00408_amd import quake as q, synth
 
     assert torch.cuda.is_available(), "bench.py needs cuda:0"
-    w = synth.WORKLOADS[a.workload]
-    x_host = w.make()
     if a.calibrate_copy:
         nb = a.calibrate_copy << 20
         src = torch.empty(nb // 4, dtype=torch.float32, device="cuda:0").fill_(1.0)
@@ -570,6 +571,19 @@ def main():
         for _ in range(5):
             dst.copy_(src)
         torch.cuda.synchronize()
+    if a.attention_only:
+        if a.prewarm > 0:
+            qc, kc, vtc = synth.attention_inputs(96, 512, 1)
+            qg, kg, vg = qc.to("cuda:0"), kc.to("cuda:0"), vtc.to("cuda:0")
+            t_end = time.time() + a.prewarm
+            while time.time() < t_end:
+                q.quake_attention(qg, kg, vg, mode=MODE_IDS[a.mode], t=0.125)
+            torch.cuda.synchronize()
+            del qg, kg, vg
+        print(json.dumps({"attention_bf16_96x512x64": fused_attention(q, synth, a)}), flush=True)
+        return
+    w = synth.WORKLOADS[a.workload]
+    x_host = w.make()
 
     if a.prewarm > 0:
         prewarm(q, w, x_host, a.prewarm, a.launch)
