@@ -59,9 +59,9 @@ def parse():
     ap.add_argument("--launch", default="graph", choices=["graph", "eager"])
     ap.add_argument("--only", action="store_true",
                     help="time only --workload in --mode (for profiler passes)")
-    ap.add_argument("--attention-only", action="store_true",
-                    help="time only the fused attention (quake_attention) and print its JSON "
-                         "(for profiler passes)")
+    ap.add_argument("--section", choices=["attention", "linear_gelu"],
+                    help="time only the fused attention (quake_attention) or the fused "
+                         "linear+GELU (quake_linear_gelu) and print its JSON (for profiler passes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-table4", action="store_true",
@@ -309,12 +309,46 @@ def native16(q, synth, a):
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix-core peak
 
 
+def graph_ms(f, nb, reps):
+    """Average ms per launch of f(i, stream) for i = 0 .. nb-1 (one launch on
+    operand set i, enqueued on `stream`), captured once in a HIP graph and
+    replayed `reps` times: the Python cost of a launch stays out of the timed
+    region."""
+    import torch
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        for i in range(nb):
+            f(i, s.cuda_stream)
+    s.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            for i in range(nb):
+                rc = f(i, s.cuda_stream)
+                if rc not in (0, None):
+                    raise RuntimeError("launch failed: %d" % rc)
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(st)
+    for _ in range(reps):
+        g.replay()
+    e1.record(st)
+    torch.cuda.synchronize()
+    del g
+    return e0.elapsed_time(e1) / (reps * nb)
+
+
 def linear_gelu(q, synth, a):
     """GELU(x w^T) for the up-projection of a BERT-base MLP over 4096 tokens
     (x [4096, 768], w [3072, 768], bf16): the fused kernel in every mode, the
     same product without the GELU, the product followed by quake_gelu, and
     torch.matmul (the vendor BLAS) for context. Eight rotating operand sets
-    (about 290 MB) keep the timed launches out of the 256 MB Infinity Cache."""
+    (about 290 MB) keep the timed launches out of the 256 MB Infinity Cache;
+    each variant is captured in a HIP graph over the eight sets and replayed."""
     import torch
     m, n, k = 4096, 3072, 768
     nb = 8
@@ -323,27 +357,28 @@ def linear_gelu(q, synth, a):
     ys = [torch.empty((m, n), dtype=torch.bfloat16, device="cuda:0") for _ in range(nb)]
     wts = [w.t().contiguous() for w in ws]
     flop = 2.0 * m * n * k
-    iters = max(50, min(a.steps, 2000))
+    reps = max(10, min(a.steps, 2000) // nb)
+    L = q.lib
 
-    def timeit(fn):
-        for i in range(max(a.warmup, nb)):
-            fn(i % nb)
-        torch.cuda.synchronize()
-        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        s.record()
-        for i in range(iters):
-            fn(i % nb)
-        e.record()
-        torch.cuda.synchronize()
-        return s.elapsed_time(e) / iters
+    def lin(mode, gelu):
+        def f(i, stream):
+            return L.quake_linear_gelu(xs[i].data_ptr(), ws[i].data_ptr(), ys[i].data_ptr(), m, n, k,
+                                       k, k, n, 2, mode, gelu, stream)
+        return f
 
-    out = {"shape_mnk": [m, n, k], "flop": flop, "peak_tflops": PEAK_BF16_TFLOPS}
+    def gelu_only(i, stream):
+        return L.quake_gelu(ys[i].data_ptr(), ys[i].data_ptr(), m * n, 2, 2, stream)
+
+    def vendor(i, stream):
+        torch.matmul(xs[i], wts[i], out=ys[i])
+
+    out = {"shape_mnk": [m, n, k], "flop": flop, "peak_tflops": PEAK_BF16_TFLOPS,
+           "launch": "graph (%d launches per replay)" % nb}
     for mname in ("exact", "quake1", "quake2", "quake2m"):
-        ms = timeit(lambda i, md=MODE_IDS[mname]: q.quake_linear_gelu(xs[i], ws[i], ys[i], mode=md))
-        out["fused_%s_ms" % mname] = ms
-    ms0 = timeit(lambda i: q.quake_linear_gelu(xs[i], ws[i], ys[i], mode=2, gelu=False))
-    msg = timeit(lambda i: q.quake_gelu(ys[i], ys[i], mode=2))
-    mst = timeit(lambda i: torch.matmul(xs[i], wts[i], out=ys[i]))
+        out["fused_%s_ms" % mname] = graph_ms(lin(MODE_IDS[mname], 1), nb, reps)
+    ms0 = graph_ms(lin(2, 0), nb, reps)
+    msg = graph_ms(gelu_only, nb, reps)
+    mst = graph_ms(vendor, nb, reps)
     out.update({"product_only_ms": ms0, "quake_gelu_ms": msg, "torch_matmul_ms": mst})
     out["fused_quake2_tflops"] = round(flop / (out["fused_quake2_ms"] * 1e-3) / 1e12, 1)
     out["product_only_tflops"] = round(flop / (ms0 * 1e-3) / 1e12, 1)
@@ -364,7 +399,8 @@ def fused_attention(q, synth, a):
     product (torch.bmm). Algorithmic bytes: q, k and v read once, o written
     once; useful flops: 4 d per (query, live key) pair. The fused launches are
     captured in a HIP graph over 12 rotating operand sets (about 300 MB, more
-    than the Infinity Cache holds) and replayed."""
+    than the Infinity Cache holds) and replayed; the explicit path is captured
+    the same way over two sets."""
     import torch
     heads, seq, d, t, nb = 96, 512, 64, 0.125, 12
     sets = []
@@ -376,32 +412,6 @@ def fused_attention(q, synth, a):
     algo = 4 * heads * seq * d * 2
     pairs = {1: heads * seq * (seq + 1) // 2, 0: heads * seq * seq}
     reps = max(20, min(a.steps, 20000) // nb)
-
-    def graph_ms(f):
-        s = torch.cuda.Stream()
-        s.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(s):
-            for i in range(nb):
-                f(i, s.cuda_stream)
-        s.synchronize()
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.stream(s):
-            with torch.cuda.graph(g, stream=s):
-                for i in range(nb):
-                    rc = f(i, s.cuda_stream)
-                    if rc != 0:
-                        raise RuntimeError(q.status_str(rc))
-        torch.cuda.synchronize()
-        g.replay()
-        torch.cuda.synchronize()
-        st = torch.cuda.current_stream()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(st)
-        for _ in range(reps):
-            g.replay()
-        e1.record(st)
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / (reps * nb)
 
     out = {"heads": heads, "seq": seq, "head_dim": d, "t": t, "algo_bytes": algo,
            "launch": "graph (%d launches per replay)" % nb}
@@ -417,33 +427,22 @@ def fused_attention(q, synth, a):
                 return L.quake_attention(qg.data_ptr(), kg.data_ptr(), vg.data_ptr(),
                                          og.data_ptr(), heads, seq, d, seq, 2, mid, t, causal,
                                          stream)
-            r[mname] = graph_ms(f)
+            r[mname] = graph_ms(f, nb, reps)
         flop = 4.0 * d * pairs[causal]
 
-        def explicit(i):
+        def explicit(i, stream):
             qg, _, _, og = sets[i]
             torch.bmm(qg, kts[i], out=scores)
-            st = int(torch.cuda.current_stream().cuda_stream)
             if causal:
                 rc = L.quake_softmax_causal(scores.data_ptr(), probs.data_ptr(), heads * seq, seq,
-                                            seq, seq, seq, 0, 1, 2, 2, t, st)
+                                            seq, seq, seq, 0, 1, 2, 2, t, stream)
             else:
                 rc = L.quake_softmax(scores.data_ptr(), probs.data_ptr(), heads * seq, seq, seq,
-                                     seq, 2, 2, t, st)
+                                     seq, 2, 2, t, stream)
             if rc != 0:
                 raise RuntimeError(q.status_str(rc))
             torch.bmm(probs, vs[i], out=og)
-        for i in range(20):
-            explicit(i % 2)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        n_ex = 200
-        e0.record()
-        for i in range(n_ex):
-            explicit(i % 2)
-        e1.record()
-        torch.cuda.synchronize()
-        ms_ex = e0.elapsed_time(e1) / n_ex
+        ms_ex = graph_ms(explicit, 2, 100)
         ms = r["quake2"]
         out[name] = {
             "fused_ms": {m: round(v, 6) for m, v in r.items()},
@@ -571,7 +570,7 @@ def main():
         for _ in range(5):
             dst.copy_(src)
         torch.cuda.synchronize()
-    if a.attention_only:
+    if a.section == "attention":
         if a.prewarm > 0:
             qc, kc, vtc = synth.attention_inputs(96, 512, 1)
             qg, kg, vg = qc.to("cuda:0"), kc.to("cuda:0"), vtc.to("cuda:0")
@@ -581,6 +580,17 @@ def main():
             torch.cuda.synchronize()
             del qg, kg, vg
         print(json.dumps({"attention_bf16_96x512x64": fused_attention(q, synth, a)}), flush=True)
+        return
+    if a.section == "linear_gelu":
+        if a.prewarm > 0:
+            xg = synth.normal((4096, 768), 1.0, "bf16", 1900).to("cuda:0")
+            wg = synth.normal((3072, 768), 0.05, "bf16", 1950).to("cuda:0")
+            t_end = time.time() + a.prewarm
+            while time.time() < t_end:
+                q.quake_linear_gelu(xg, wg, mode=MODE_IDS[a.mode])
+            torch.cuda.synchronize()
+            del xg, wg
+        print(json.dumps({"linear_gelu_bf16_4096x3072x768": linear_gelu(q, synth, a)}), flush=True)
         return
     w = synth.WORKLOADS[a.workload]
     x_host = w.make()
