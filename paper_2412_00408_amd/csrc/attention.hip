@@ -52,7 +52,7 @@ struct AttnArgs {
   int32_t qblocks;   // ceil(s / 32)
   float c0;          // Algorithm 2: 2^23 t / ln2 (EXACT: t / ln2)
   uint32_t causal;
-  uint32_t xcd_group;   // grid size a multiple of 8: keep a head's tiles on one XCD
+  uint32_t xcd_heads;   // heads a multiple of 8: heads per XCD, else 0
 };
 
 __device__ __forceinline__ u32x4_t ld16(const uint16_t* p) {
@@ -175,13 +175,21 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
   // uniform across the wave: every condition below that depends on it is a
   // scalar branch
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  // tiles of one head on one XCD (blockIdx round-robins over the 8 XCDs), so
-  // its K and V stay in that XCD's L2; within a head the longest causal rows
-  // first
-  uint32_t bid = blockIdx.x;
-  if (g.xcd_group) bid = (bid & 7u) * (gridDim.x >> 3) + (bid >> 3);
-  const int bh = (int)(bid / (uint32_t)g.qblocks);
-  const int qb = g.qblocks - 1 - (int)(bid % (uint32_t)g.qblocks);
+  // Tile order. blockIdx round-robins over the 8 XCDs; with the heads a
+  // multiple of 8, XCD x takes heads x H8 .. x H8 + H8 - 1 (H8 = heads / 8), so
+  // their K and V stay in that XCD's L2, and it starts its tiles longest causal
+  // rows first across all its heads (query tile qblocks - 1 of every head, then
+  // qblocks - 2, ...), which keeps the end of the launch from waiting on a few
+  // long tiles started late.
+  int bh, qb;
+  if (g.xcd_heads) {
+    const uint32_t x = blockIdx.x & 7u, slot = blockIdx.x >> 3;
+    bh = (int)(x * g.xcd_heads + slot % g.xcd_heads);
+    qb = g.qblocks - 1 - (int)(slot / g.xcd_heads);
+  } else {
+    bh = (int)(blockIdx.x / (uint32_t)g.qblocks);
+    qb = g.qblocks - 1 - (int)(blockIdx.x % (uint32_t)g.qblocks);
+  }
   const int S = g.s;
   const int q0 = qb * kAttnQ;
   const int kblocks = (S + 31) >> 5;
@@ -367,7 +375,7 @@ extern "C" quake_status quake_attention(const void* q, const void* k, const void
   const AttnArgs g{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                    static_cast<const uint16_t*>(vt), static_cast<uint16_t*>(o), (int32_t)seq,
                    (int32_t)ldv, (int32_t)qblocks, c0, (uint32_t)(causal != 0),
-                   (uint32_t)((heads * qblocks) % 8 == 0)};
+                   (uint32_t)(heads % 8 == 0 ? heads / 8 : 0)};
   const dim3 grid((uint32_t)(heads * qblocks));
   const hipStream_t s = static_cast<hipStream_t>(stream);
   const bool vec = aligned16(vt) && ldv % 8 == 0;
