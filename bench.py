@@ -197,6 +197,26 @@ def time_workload(q, w, mode, x_host, steps, warmup, launch_kind, fused=True):
 # CPU baseline: the oracle as it stands, on the host cores
 # ---------------------------------------------------------------------------
 
+def copy_ceiling(w, reps):
+    """A plain copy of the workload's input bytes (read numel elements, write
+    numel elements: the same algorithmic bytes as the operator) with torch's
+    copy kernel, over >= 1 GiB of rotating buffer pairs, graph-captured: the
+    bandwidth a kernel moving these bytes reaches on this machine."""
+    import torch
+    from paper_2412_00408_amd import synth
+    nb = min(64, max(2, math.ceil((1 << 30) / w.algo_bytes)))
+    n = w.numel * synth.ELEM_BYTES[w.dt] // 4
+    srcs = [torch.ones(n, dtype=torch.float32, device="cuda:0") for _ in range(nb)]
+    dsts = [torch.empty_like(srcs[0]) for _ in range(nb)]
+
+    def f(i, stream):
+        dsts[i].copy_(srcs[i])
+    ms = graph_ms(f, nb, max(10, reps // nb))
+    del srcs, dsts
+    return {"ms": ms, "gbps": round(w.algo_bytes / (ms * 1e-3) / 1e9, 2),
+            "kernel": "torch copy_ of %d bytes" % (n * 4)}
+
+
 def cpu_baseline(w, x_host, cpu_seconds):
     import oracle
     from paper_2412_00408_amd import synth
@@ -238,8 +258,18 @@ def cpu_baseline(w, x_host, cpu_seconds):
     t0 = time.perf_counter()
     run(1, sample)
     one = (2 * synth.ELEM_BYTES[w.dt] * elems) / (time.perf_counter() - t0) / 1e9
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    cpu = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {
         "value": round(gbps, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
+        "cpu_model": cpu,
         "sample": "%d of %d elements of %s, quake2, %d passes over %.1f s wall" % (
             elems, w.numel, w.name, reps, wall),
         "single_thread_value": round(one, 3),
@@ -630,6 +660,10 @@ def main():
         "modes": {m: {"ms_per_launch": r["ms"], "gbps": round(r["gbps"], 2),
                       "elements_per_s": w.numel / (r["ms"] * 1e-3)} for m, r in res.items()},
     }
+    if not a.only:
+        cc = copy_ceiling(w, a.steps)
+        line["copy_ceiling"] = dict(cc, frac=round(cc["gbps"] / PEAK_HBM_GBPS, 4),
+                                    value_over_copy=round(head["gbps"] / cc["gbps"], 4))
     if "exact" in res:
         line["speedup_vs_exact"] = {m: round(res["exact"]["ms"] / r["ms"], 4)
                                     for m, r in res.items() if m != "exact"}
