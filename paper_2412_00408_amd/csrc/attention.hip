@@ -8,16 +8,17 @@
 // One workgroup = 32 queries of one head, four waves; wave w takes the 32-key
 // blocks w, w + 4, w + 8, w + 12 (interleaved, so causal work stays balanced).
 // The scores are computed transposed, S^T = K Q^T, on the matrix cores
-// (v_mfma_f32_32x32x16_bf16; A = 32 keys x 16 dims straight from K's rows,
-// B = the 32 queries' dims straight from Q's rows), so that lane l holds one
-// query (l mod 32) and keys 8 g + 4 (l / 32) + i, g, i < 4, of each block:
+// (v_mfma_f32_32x32x16_bf16; A = 32 keys x 16 dims of K, staged through LDS as
+// described below, B = the 32 queries' dims read straight from Q's rows), so
+// that lane l holds one query (l mod 32) and keys 8 g + 4 (l / 32) + i,
+// g, i < 4, of each block:
 //   * the row max and the row sum reduce the lane's own values, exchange once
 //     with lane l xor 32 (v_permlane32_swap) and once across waves through LDS;
 //   * the exponentials, rounded to bfloat16, become the B operand of the second
 //     product O^T = V^T P after one v_permlane32_swap per dword pair (lane
 //     l < 32 takes keys 4-7 from its partner and gives it keys 8-11), without a
 //     trip through LDS. V is passed transposed ([head, dim, key]), so the A
-//     operand (32 dims x 16 keys) is 16 contiguous bytes per lane.
+//     operand (32 dims x 16 keys) is 16 contiguous bytes of a row of V^T.
 // Causal key blocks above a query block's diagonal are neither loaded nor
 // multiplied. The four partial O^T meet in LDS; wave w adds up, normalises by
 // 1 / sum and stores one quarter of the 32 x 64 output tile as bfloat16.
