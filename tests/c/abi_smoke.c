@@ -82,6 +82,55 @@ int main(void) {
     if (he[k] != ldexpf(1.0f, k - 32)) pow_ok = 0;
   check(pow_ok, "QuAKE2 of x = k with a = ln2 is exactly 2^k");
 
+  /* attention with all-zero queries: every score is 0, every probability
+   * exactly 1, so each output is the plain mean of the values the query may
+   * use (causal: keys 0..i). With v[j][d] = j + 1 (exact in bfloat16) the mean
+   * over keys 0..i is (i + 2) / 2, exact in bfloat16 for i < 255. */
+  {
+    const int heads = 2, seq = 40, dim = 64;
+    const size_t nq = (size_t)heads * seq * dim;
+    uint16_t* hq = (uint16_t*)calloc(nq, 2);
+    uint16_t* hv = (uint16_t*)malloc(nq * 2);
+    uint16_t* ho = (uint16_t*)malloc(nq * 2);
+    for (int h = 0; h < heads; ++h)
+      for (int d = 0; d < dim; ++d)
+        for (int j = 0; j < seq; ++j) {
+          float f = (float)(j + 1);
+          uint32_t b;
+          memcpy(&b, &f, 4);
+          hv[((size_t)h * dim + d) * seq + j] = (uint16_t)(b >> 16);   /* v^T, exact */
+        }
+    void *dq = NULL, *dv = NULL, *dout = NULL;
+    HIPCHECK(hipMalloc(&dq, nq * 2));
+    HIPCHECK(hipMalloc(&dv, nq * 2));
+    HIPCHECK(hipMalloc(&dout, nq * 2));
+    HIPCHECK(hipMemcpy(dq, hq, nq * 2, hipMemcpyHostToDevice));
+    HIPCHECK(hipMemcpy(dv, hv, nq * 2, hipMemcpyHostToDevice));
+    st = quake_attention(dq, dq, dv, dout, heads, seq, dim, seq, QUAKE_BF16, QUAKE_2, 0.125f, 1,
+                         NULL);
+    check(st == QUAKE_OK, "quake_attention returns QUAKE_OK");
+    HIPCHECK(hipDeviceSynchronize());
+    HIPCHECK(hipMemcpy(ho, dout, nq * 2, hipMemcpyDeviceToHost));
+    int mean_ok = 1;
+    for (int h = 0; h < heads; ++h)
+      for (int i = 0; i < seq; ++i)
+        for (int d = 0; d < dim; ++d) {
+          uint32_t b = (uint32_t)ho[((size_t)h * seq + i) * dim + d] << 16;
+          float f;
+          memcpy(&f, &b, 4);
+          if (f != 0.5f * (float)(i + 2)) mean_ok = 0;
+        }
+    check(mean_ok, "causal attention of equal scores is the mean of the allowed values");
+    check(quake_attention(dq, dq, dv, dout, heads, seq, 128, seq, QUAKE_BF16, QUAKE_2, 0.125f, 1,
+                          NULL) == QUAKE_EINVAL, "attention head dim other than 64 rejected");
+    HIPCHECK(hipFree(dq));
+    HIPCHECK(hipFree(dv));
+    HIPCHECK(hipFree(dout));
+    free(hq);
+    free(hv);
+    free(ho);
+  }
+
   /* argument validation happens before any HIP call */
   check(quake_gelu(NULL, NULL, 5, QUAKE_F32, QUAKE_2, NULL) == QUAKE_EINVAL, "NULL buffers rejected");
   check(quake_sigmoid(dx, dy, 5, (quake_dtype)7, QUAKE_2, 0, NULL) == QUAKE_EDTYPE, "bad dtype rejected");
