@@ -1,4 +1,5 @@
-"""GPU robustness: HIP-graph replay of every kernel family, and the bounded
+"""GPU robustness: HIP-graph replay of every kernel family (elementwise,
+softmax, the 16-bit construction, linear+GELU, fused attention), and the bounded
 waits of the split-row softmax forced to time out from the host."""
 import numpy as np
 import pytest
@@ -27,6 +28,10 @@ def _ops(q, bufs):
     q.quake_softmax(bufs["lm_x"], bufs["lm_y"], mode=2)                        # split rows
     q.quake_softmax_causal(bufs["attn_x"], bufs["causal_y"], period=512, mode=2, t=0.125)
     q.quake_softmax(bufs["gen_x"], bufs["gen_y"], mode=1)                      # generic
+    q.quake_exp16(bufs["e16_x"], bufs["e16_y"], mode=2)                        # 16-bit layout
+    q.quake_linear_gelu(bufs["lin_x"], bufs["lin_w"], bufs["lin_y"], mode=2)   # matrix cores
+    q.quake_attention(bufs["att_q"], bufs["att_k"], bufs["att_vt"], bufs["att_y"], mode=2,
+                      t=0.125, causal=True)                                    # fused attention
 
 
 def _bufs():
@@ -37,9 +42,16 @@ def _bufs():
         "lm_x": synth.WORKLOADS["lmhead_softmax_f32_64x128256"].make(rows=16).to("cuda:0"),
         "gen_x": synth.normal((37, 1001), 2.0, "f32", 1200).to("cuda:0"),
     }
-    for k in ("gelu", "sig", "attn", "lm", "gen"):
+    b["e16_x"] = synth.WORKLOADS["sigmoid_f16_2p28"].make(n=1 << 20).to("cuda:0")
+    b["lin_x"] = synth.normal((256, 768), 1.0, "bf16", 1201).to("cuda:0")
+    b["lin_w"] = synth.normal((512, 768), 0.05, "bf16", 1202).to("cuda:0")
+    qa, ka, va = synth.attention_inputs(4, 512, 1203)
+    b["att_q"], b["att_k"], b["att_vt"] = qa.to("cuda:0"), ka.to("cuda:0"), va.to("cuda:0")
+    for k in ("gelu", "sig", "attn", "lm", "gen", "e16"):
         b[k + "_y"] = torch.empty_like(b[k + "_x"])
     b["causal_y"] = torch.empty_like(b["attn_x"])
+    b["lin_y"] = torch.empty((256, 512), dtype=torch.bfloat16, device="cuda:0")
+    b["att_y"] = torch.empty_like(b["att_q"])
     return b
 
 
