@@ -5,11 +5,14 @@
 // epilogue, bfloat16 output. This is QuAKE inside a fused consumer: the GELU
 // costs no HBM traffic of its own, and its VALU work runs beside the MFMAs.
 //
-// Tiling: a workgroup (4 waves) computes a 128 x 128 tile of y, each wave a
-// 64 x 64 quarter as 2 x 2 blocks of v_mfma_f32_32x32x16_bf16. K advances in
-// slabs of 64: the next slab is loaded from HBM into registers while the
-// current one is multiplied out of LDS (rows padded by 16 bytes so the
-// 16-byte fragment reads of 8 consecutive rows hit distinct banks).
+// Tiling: a workgroup (4 waves) computes a 128 x BN tile of y (BN = 192 when
+// n is a multiple of 192, else 128), each wave a 64 x BN/2 quarter as
+// 2 x BN/64 blocks of v_mfma_f32_32x32x16_bf16. The wider tile reads 17 % fewer
+// LDS bytes per matrix-core operation (each A fragment feeds three blocks
+// instead of two), which is what bounds this loop. K advances in slabs of 64:
+// the next slab is loaded from HBM into registers while the current one is
+// multiplied out of LDS (rows padded by 16 bytes so the 16-byte fragment reads
+// of 8 consecutive rows hit distinct banks).
 // Operand lane layout of the 32x32x16 bf16 MFMA (checked on the device):
 // lane l holds row (l mod 32) and k = 8 (l / 32) .. +7 of A, and column
 // (l mod 32), the same k, of B; accumulator r of lane l is row
@@ -27,9 +30,10 @@ namespace qk {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-constexpr int kBM = 128, kBN = 128, kBK = 64;
+constexpr int kBM = 128, kBK = 64;
 constexpr int kLdsRow = kBK + 8;   // bf16 elements per LDS row (144 bytes)
 constexpr int kGemmThreads = 256;
+constexpr int kMaxBN = 192;
 
 struct GemmArgs {
   const uint16_t* x;
@@ -42,10 +46,16 @@ struct GemmArgs {
   uint32_t xcd_split;      // tiles_m % 4 == 0 and tiles_n % 2 == 0
 };
 
-template <int MODE, bool GELU>
-__global__ __launch_bounds__(kGemmThreads, 3) void gemm_bf16_kernel(GemmArgs g) {
+// OCC: workgroups per CU the register budget is set for (3 at BN = 128: at
+// most 168 VGPRs; 2 at BN = 192)
+template <int MODE, bool GELU, int BN, int OCC>
+__global__ __launch_bounds__(kGemmThreads, OCC) void gemm_bf16_kernel(GemmArgs g) {
+  constexpr int TN = BN / 64;                     // 32 x 32 blocks per wave along n
+  constexpr int VA = kBM * 8 / kGemmThreads;      // 16-byte vectors per thread per slab
+  constexpr int VB = BN * 8 / kGemmThreads;
+  static_assert(BN % 64 == 0 && BN <= kMaxBN && BN * 8 % kGemmThreads == 0, "tile width");
   __shared__ __attribute__((aligned(16))) uint16_t sx[kBM * kLdsRow];
-  __shared__ __attribute__((aligned(16))) uint16_t sw[kBN * kLdsRow];
+  __shared__ __attribute__((aligned(16))) uint16_t sw[BN * kLdsRow];
   const int t = threadIdx.x;
   const int lane = t & 63, wave = t >> 6;
   const int wm = wave >> 1, wn = wave & 1;
@@ -62,43 +72,54 @@ __global__ __launch_bounds__(kGemmThreads, 3) void gemm_bf16_kernel(GemmArgs g) 
     tm = (int)(blockIdx.x / g.tiles_n);
     tn = (int)(blockIdx.x % g.tiles_n);
   }
-  const int row0 = tm * kBM, col0 = tn * kBN;
+  const int row0 = tm * kBM, col0 = tn * BN;
 
-  // Slab loads: 1024 16-byte vectors per operand; thread t takes t + 256 i,
-  // i.e. row v / 8 and k-vector v mod 8. Rows past m (n) re-read the last
-  // row; k past the end re-reads k-vector 0 and is replaced by zeros when the
-  // slab is written to LDS (k is a multiple of 8). Nothing consumes the loaded
-  // registers before that write, so the loads stay in flight during the
-  // previous slab's MFMAs.
-  u32x4 rx[4], rw[4];
+  // Slab loads: 8 16-byte vectors per row of each operand; thread t takes
+  // vectors t + 256 i, i.e. row v / 8 and k-vector v mod 8. Rows past m (n)
+  // re-read the last row; k past the end re-reads k-vector 0 and is replaced
+  // by zeros when the slab is written to LDS (k is a multiple of 8). Nothing
+  // consumes the loaded registers before that write, so the loads stay in
+  // flight during the previous slab's MFMAs.
+  u32x4 rx[VA], rw[VB];
   const u32x4 zero = {0u, 0u, 0u, 0u};
   auto load_slab = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < VA; ++i) {
       const int v = t + kGemmThreads * i;
       const int r = v >> 3, kk = k0 + 8 * (v & 7);
-      const int gm = min(row0 + r, g.m - 1), gn = min(col0 + r, g.n - 1);
+      const int gm = min(row0 + r, g.m - 1);
       const int kc = kk < g.k ? kk : 0;
       rx[i] = *reinterpret_cast<const u32x4*>(g.x + (int64_t)gm * g.ldx + kc);
+    }
+#pragma unroll
+    for (int i = 0; i < VB; ++i) {
+      const int v = t + kGemmThreads * i;
+      const int r = v >> 3, kk = k0 + 8 * (v & 7);
+      const int gn = min(col0 + r, g.n - 1);
+      const int kc = kk < g.k ? kk : 0;
       rw[i] = *reinterpret_cast<const u32x4*>(g.w + (int64_t)gn * g.ldw + kc);
     }
   };
   auto store_slab = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < VA; ++i) {
       const int v = t + kGemmThreads * i;
       const int r = v >> 3, c = 8 * (v & 7);
-      const bool in = k0 + c < g.k;
-      *reinterpret_cast<u32x4*>(sx + r * kLdsRow + c) = in ? rx[i] : zero;
-      *reinterpret_cast<u32x4*>(sw + r * kLdsRow + c) = in ? rw[i] : zero;
+      *reinterpret_cast<u32x4*>(sx + r * kLdsRow + c) = (k0 + c < g.k) ? rx[i] : zero;
+    }
+#pragma unroll
+    for (int i = 0; i < VB; ++i) {
+      const int v = t + kGemmThreads * i;
+      const int r = v >> 3, c = 8 * (v & 7);
+      *reinterpret_cast<u32x4*>(sw + r * kLdsRow + c) = (k0 + c < g.k) ? rw[i] : zero;
     }
   };
 
-  f32x16_t acc[2][2];
+  f32x16_t acc[2][TN];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
@@ -112,17 +133,17 @@ __global__ __launch_bounds__(kGemmThreads, 3) void gemm_bf16_kernel(GemmArgs g) 
     if (kt + 1 < nk) load_slab((kt + 1) * kBK);   // in flight during the MFMAs
 #pragma unroll
     for (int ks = 0; ks < kBK / 16; ++ks) {
-      bf16x8_t af[2], bf[2];
+      bf16x8_t af[2], bf[TN];
 #pragma unroll
       for (int i = 0; i < 2; ++i)
         af[i] = *reinterpret_cast<const bf16x8_t*>(sx + (wm * 64 + 32 * i + fr) * kLdsRow + ks * 16 + fk);
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        bf[j] = *reinterpret_cast<const bf16x8_t*>(sw + (wn * 64 + 32 * j + fr) * kLdsRow + ks * 16 + fk);
+      for (int j = 0; j < TN; ++j)
+        bf[j] = *reinterpret_cast<const bf16x8_t*>(sw + (wn * 32 * TN + 32 * j + fr) * kLdsRow + ks * 16 + fk);
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
     }
   }
@@ -131,8 +152,8 @@ __global__ __launch_bounds__(kGemmThreads, 3) void gemm_bf16_kernel(GemmArgs g) 
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int col = col0 + wn * 64 + 32 * j + fr;
+    for (int j = 0; j < TN; ++j) {
+      const int col = col0 + wn * 32 * TN + 32 * j + fr;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = row0 + wm * 64 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
@@ -142,6 +163,14 @@ __global__ __launch_bounds__(kGemmThreads, 3) void gemm_bf16_kernel(GemmArgs g) 
           g.y[(int64_t)row * g.ldy + col] = __builtin_bit_cast(uint16_t, (__bf16)v);
       }
     }
+}
+
+template <int MODE, int BN, int OCC>
+void launch_gemm(int gelu, dim3 grid, hipStream_t s, const GemmArgs& g) {
+  if (gelu)
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, true, BN, OCC>), grid, dim3(kGemmThreads), 0, s, g);
+  else
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, false, BN, OCC>), grid, dim3(kGemmThreads), 0, s, g);
 }
 
 }  // namespace qk
@@ -159,8 +188,10 @@ extern "C" quake_status quake_linear_gelu(const void* x, const void* w, void* y,
   if (k == 0 || k % 8 != 0 || x == nullptr || w == nullptr || y == nullptr) return QUAKE_EINVAL;
   if (ldx < k || ldw < k || ldy < n || ldx % 8 != 0 || ldw % 8 != 0) return QUAKE_EINVAL;
   if (!aligned16(x) || !aligned16(w)) return QUAKE_EINVAL;
-  if (m > INT32_MAX - kBM || n > INT32_MAX - kBN || k > INT32_MAX - kBK) return QUAKE_EINVAL;
-  const int64_t tiles_m = (m + kBM - 1) / kBM, tiles_n = (n + kBN - 1) / kBN;
+  if (m > INT32_MAX - kBM || n > INT32_MAX - kMaxBN || k > INT32_MAX - kBK) return QUAKE_EINVAL;
+  const bool wide = n % 192 == 0;
+  const int64_t bn = wide ? 192 : 128;
+  const int64_t tiles_m = (m + kBM - 1) / kBM, tiles_n = (n + bn - 1) / bn;
   if (tiles_m * tiles_n > INT32_MAX) return QUAKE_EINVAL;
   const Affine af = gelu_affine(mode);
   GemmArgs g{static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w),
@@ -171,10 +202,10 @@ extern "C" quake_status quake_linear_gelu(const void* x, const void* w, void* y,
   const hipStream_t s = static_cast<hipStream_t>(stream);
 #define QK_GEMM_CASE(M)                                                                      \
   if (mode == M) {                                                                           \
-    if (gelu)                                                                                \
-      hipLaunchKernelGGL((gemm_bf16_kernel<M, true>), grid, dim3(kGemmThreads), 0, s, g);    \
+    if (wide)                                                                                \
+      launch_gemm<M, 192, 2>(gelu, grid, s, g);                                              \
     else                                                                                     \
-      hipLaunchKernelGGL((gemm_bf16_kernel<M, false>), grid, dim3(kGemmThreads), 0, s, g);   \
+      launch_gemm<M, 128, 3>(gelu, grid, s, g);                                              \
     return launch_status();                                                                  \
   }
   QK_GEMM_CASE(EXACT) QK_GEMM_CASE(Q1) QK_GEMM_CASE(Q2) QK_GEMM_CASE(Q2M)

@@ -59,8 +59,10 @@ def _run(q, m, n, k, mode, gelu, seed, pad=0):
     return host_bits(y), ref, xb, wb
 
 
+# n a multiple of 192 takes the 128 x 192 tile, other n the 128 x 128 tile
 @pytest.mark.parametrize("m,n,k", [(128, 128, 64), (256, 384, 768), (200, 130, 72), (1, 1, 8),
-                                   (129, 257, 136), (64, 1000, 32)])
+                                   (129, 257, 136), (64, 1000, 32), (200, 192, 72),
+                                   (129, 576, 136), (1, 192, 8)])
 @pytest.mark.parametrize("mode", [0, 1, 2, 3])
 def test_shapes_and_modes(q, m, n, k, mode):
     for gelu in (True, False):
