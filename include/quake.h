@@ -252,7 +252,8 @@ quake_status quake_linear_gelu(const void* x, const void* w, void* y, int64_t m,
  *          seq .. ldv-1 may hold anything (they do not affect o). With vt
  *          16-byte aligned and ldv a multiple of 8 the rows are read as
  *          16-byte vectors, else element by element.
- *   o    : device, [heads, seq, dim] bfloat16, contiguous, 8-byte aligned.
+ *   o    : device, [heads, seq, dim] bfloat16, contiguous, 8-byte aligned; it
+ *          must not overlap q, k or vt (other workgroups still read them).
  *   dim == 64 and seq <= 512 (the keys of a row stay in registers);
  *   t > 0 finite (1/sqrt(dim) for the usual scaling); causal != 0 lets query
  *   i use keys j <= i only (masked keys are neither loaded nor multiplied).
