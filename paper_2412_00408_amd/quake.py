@@ -185,6 +185,14 @@ def quake_linear_gelu(x, w, y=None, mode=QUAKE_2, gelu=True, stream=None):
     return y
 
 
+def _span(t: torch.Tensor):
+    """[first, last + 1) byte addresses a tensor view touches (empty: (0, 0))."""
+    if t.numel() == 0:
+        return 0, 0
+    last = sum((n - 1) * st for n, st in zip(t.shape, t.stride()))
+    return t.data_ptr(), t.data_ptr() + (last + 1) * t.element_size()
+
+
 def _vt_row_stride(shape, strides) -> int:
     """Row stride (ldv) of v^T [..., dim, seq]: the last dimension contiguous,
     rows ldv apart, heads dim * ldv apart one after another."""
@@ -224,6 +232,11 @@ def quake_attention(q, k, vt, o=None, mode=QUAKE_2, t=None, causal=True, stream=
         o = torch.empty_like(q)
     if o.shape != q.shape or o.dtype != q.dtype or not o.is_contiguous():
         raise ValueError("o must be contiguous and shaped like q")
+    o0, o1 = _span(o)
+    for a, what in ((q, "q"), (k, "k"), (vt, "vt")):
+        a0, a1 = _span(a)
+        if o0 < a1 and a0 < o1:
+            raise ValueError("o must not overlap %s" % what)
     t = 1.0 / dim ** 0.5 if t is None else t
     _raise("quake_attention", lib.quake_attention(
         q.data_ptr(), k.data_ptr(), vt.data_ptr(), o.data_ptr(), heads, seq, dim, ldv,

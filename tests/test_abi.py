@@ -197,3 +197,12 @@ def test_attention_vt_row_stride(q):
     with pytest.raises(ValueError):
         t = torch.empty((3, 2, 64, 40)).transpose(0, 1)         # heads out of order
         f(tuple(t.shape), t.stride())
+
+
+def test_span_of_views(q):
+    import torch
+    t = torch.empty((4, 10))
+    assert q._span(t) == (t.data_ptr(), t.data_ptr() + 160)
+    v = t[:, 2:5]
+    assert q._span(v) == (t.data_ptr() + 8, t.data_ptr() + 4 * (3 * 10 + 5))
+    assert q._span(torch.empty(0)) == (0, 0)

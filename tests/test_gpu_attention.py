@@ -159,6 +159,8 @@ def test_bad_arguments_raise(q):
         q.quake_attention(qg, kg, vtg, t=-1.0)
     with pytest.raises(q.QuakeError):
         q.quake_attention(qg.float(), kg.float(), vtg.float())
+    with pytest.raises(ValueError):
+        q.quake_attention(qg, kg, vtg, o=qg)            # output over an input
     big = torch.zeros((1, 520, 64), dtype=torch.bfloat16, device="cuda:0")
     with pytest.raises(q.QuakeError):
         q.quake_attention(big, big, torch.zeros((1, 64, 520), dtype=torch.bfloat16, device="cuda:0"))
