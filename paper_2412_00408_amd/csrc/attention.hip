@@ -37,7 +37,8 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kAttnD = 64;                     // head dimension
-constexpr int kAttnMaxS = 512;                 // longest sequence: 16 key blocks
+constexpr int kAttnMaxS = 512;         // longest sequence of the one-pass kernel: 16 key blocks
+constexpr int kAttnLongMaxS = 131072;  // longest sequence (two-pass kernel)
 constexpr int kAttnQ = 32;                     // queries per workgroup
 constexpr int kAttnWaves = 4;
 constexpr int kAttnThreads = 64 * kAttnWaves;
@@ -342,14 +343,191 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
   }
 }
 
-template <int MODE>
-void launch_attn(int vk, dim3 grid, hipStream_t s, const AttnArgs& g) {
-  if (vk == kVtFull)
-    hipLaunchKernelGGL((attn_kernel<MODE, kVtFull>), grid, dim3(kAttnThreads), 0, s, g);
-  else if (vk == kVtRagged)
-    hipLaunchKernelGGL((attn_kernel<MODE, kVtRagged>), grid, dim3(kAttnThreads), 0, s, g);
+// Sequences longer than 512 keys: the same tiles, waves and staging, but the
+// scores are not kept. Pass 1 computes them to find each query's row max;
+// pass 2 computes them again, block by block, and takes the exponentials
+// against that max (Algorithm 2 needs the final max before any exponential),
+// their sum and the second product. The scores, the max, the exponentials,
+// the sums and the products are computed by the same instructions in the same
+// order as in the one-pass kernel, so both give identical results.
+template <int MODE, int VK>
+__global__ __launch_bounds__(kAttnThreads, 3) void attn_long_kernel(AttnArgs g) {
+  __shared__ float s_max[kAttnWaves][kAttnQ];
+  __shared__ float s_sum[kAttnWaves][kAttnQ];
+  __shared__ u32x4_t s_buf[kAttnWaves][512];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  int bh, qb;
+  if (g.xcd_heads) {
+    const uint32_t x = blockIdx.x & 7u, slot = blockIdx.x >> 3;
+    bh = (int)(x * g.xcd_heads + slot % g.xcd_heads);
+    qb = g.qblocks - 1 - (int)(slot / g.xcd_heads);
+  } else {
+    bh = (int)(blockIdx.x / (uint32_t)g.qblocks);
+    qb = g.qblocks - 1 - (int)(blockIdx.x % (uint32_t)g.qblocks);
+  }
+  const int S = g.s;
+  const int q0 = qb * kAttnQ;
+  const int kblocks = (S + 31) >> 5;
+  const int nkb = g.causal ? min(kblocks, qb + 1) : kblocks;
+  const int nlive = max(0, (nkb - wave + kAttnWaves - 1) / kAttnWaves);
+  const int fr = lane & 31, fk = 8 * (lane >> 5), h = lane >> 5;
+  const int query = q0 + fr;
+  const uint16_t* Q = g.q + (int64_t)bh * S * kAttnD;
+  const uint16_t* K = g.k + (int64_t)bh * S * kAttnD;
+  const uint16_t* Vt = g.vt + (int64_t)bh * kAttnD * g.ldv;
+  u32x4_t* stage = s_buf[wave];
+
+  bf16x8_t qf[4];
+  {
+    const uint16_t* qr = Q + (int64_t)min(query, S - 1) * kAttnD + fk;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) qf[ks] = __builtin_bit_cast(bf16x8_t, ld16(qr + 16 * ks));
+  }
+  // one block of S^T = K Q^T from the staged K block gk (masked past s and,
+  // on the diagonal, above it)
+  auto scores = [&](const u32x4_t (&gk)[4], int kbg) {
+    kblock_store(stage, lane, gk);
+    __builtin_amdgcn_wave_barrier();   // lanes read what other lanes wrote
+    bf16x8_t ka[4];
+    kblock_read(stage, fr, h, ka);
+    __builtin_amdgcn_wave_barrier();   // before the slots are written again
+    const f32x16_t zero = {};
+    f32x16_t sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qf[0], zero, 0, 0, 0);
+#pragma unroll
+    for (int ks = 1; ks < 4; ++ks)
+      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks], qf[ks], sacc, 0, 0, 0);
+    const bool diag = g.causal && kbg == qb;
+    if (diag || (VK != kVtFull && 32 * kbg + 32 > S)) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = 32 * kbg + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (key >= S || (diag && key > query)) sacc[r] = -INFINITY;
+      }
+    }
+    return sacc;
+  };
+
+  // pass 1: the row max
+  u32x4_t gk[4], gv[4];
+  if (nlive > 0) kblock_load(K, 32 * wave, S, lane, gk);
+  float m = -INFINITY;
+  for (int i = 0; i < nlive; ++i) {
+    const int kbg = kAttnWaves * i + wave;
+    u32x4_t cur[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) cur[j] = gk[j];
+    if (i + 1 < nlive) kblock_load(K, 32 * (kbg + kAttnWaves), S, lane, gk);
+    const f32x16_t sacc = scores(cur, kbg);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) m = fmaxf(m, sacc[r]);
+  }
+  if (nlive > 0) {
+    kblock_load(K, 32 * wave, S, lane, gk);
+    vblock_load<VK>(Vt, g.ldv, 32 * wave, S, VK != kVtFull && 32 * wave + 32 > S, lane, gv);
+  }
+  m = fmaxf(m, xor32(m));
+  if (lane < 32) s_max[wave][lane] = m;
+  __syncthreads();
+  m = fmaxf(fmaxf(s_max[0][fr], s_max[1][fr]), fmaxf(s_max[2][fr], s_max[3][fr]));
+  const float c1 = (m == -INFINITY) ? 0.0f : __builtin_fmaf(-g.c0, m, MODE == EXACT ? 0.0f : kK127);
+
+  // pass 2: the scores again, their exponentials, the sum and O^T = V^T P
+  float part = 0.0f;
+  f32x16_t oacc[2] = {};
+  for (int i = 0; i < nlive; ++i) {
+    const int kbg = kAttnWaves * i + wave;
+    const int nb = 32 * (kbg + kAttnWaves);
+    u32x4_t curk[4], curv[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      curk[j] = gk[j];
+      curv[j] = gv[j];
+    }
+    if (i + 1 < nlive) {
+      kblock_load(K, nb, S, lane, gk);
+      vblock_load<VK>(Vt, g.ldv, nb, S, VK != kVtFull && nb + 32 > S, lane, gv);
+    }
+    const f32x16_t sacc = scores(curk, kbg);
+    uint32_t pk[4][2];
+#pragma unroll
+    for (int gi = 0; gi < 4; ++gi) {
+      float e[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        e[j] = qexp<MODE>(sacc[4 * gi + j], g.c0, c1);
+        part += e[j];
+      }
+      pk[gi][0] = pack_bf16(e[0], e[1]);
+      pk[gi][1] = pack_bf16(e[2], e[3]);
+    }
+    vblock_store(stage, lane, curv);
+    __builtin_amdgcn_wave_barrier();
+    bf16x8_t va[2][2];
+    vblock_read(stage, fr, h, va);
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const auto s0 = __builtin_amdgcn_permlane32_swap(pk[2 * ks][0], pk[2 * ks + 1][0], false, false);
+      const auto s1 = __builtin_amdgcn_permlane32_swap(pk[2 * ks][1], pk[2 * ks + 1][1], false, false);
+      const u32x4_t bv = {s0[0], s1[0], s0[1], s1[1]};
+      const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, bv);
+#pragma unroll
+      for (int db = 0; db < 2; ++db)
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[ks][db], pf, oacc[db], 0, 0, 0);
+    }
+  }
+  part += xor32(part);
+  if (lane < 32) s_sum[wave][lane] = part;
+
+  __builtin_amdgcn_wave_barrier();
+  float* po = reinterpret_cast<float*>(stage);
+#pragma unroll
+  for (int db = 0; db < 2; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) po[(db * 16 + r) * 64 + lane] = oacc[db][r];
+  __syncthreads();
+  if (query < S) {
+    const float total = (s_sum[0][fr] + s_sum[1][fr]) + (s_sum[2][fr] + s_sum[3][fr]);
+    const float inv = (m == -INFINITY || !(total > 0.0f)) ? 0.0f : 1.0f / total;
+    uint16_t* orow = g.o + ((int64_t)bh * S + query) * kAttnD;
+    const float* p0 = reinterpret_cast<const float*>(s_buf[0]);
+    const float* p1 = reinterpret_cast<const float*>(s_buf[1]);
+    const float* p2 = reinterpret_cast<const float*>(s_buf[2]);
+    const float* p3 = reinterpret_cast<const float*>(s_buf[3]);
+#pragma unroll
+    for (int db = 0; db < 2; ++db) {
+      float v[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int idx = (db * 16 + 4 * wave + j) * 64 + lane;
+        v[j] = ((p0[idx] + p1[idx]) + (p2[idx] + p3[idx])) * inv;
+      }
+      uint2 w;
+      w.x = pack_bf16(v[0], v[1]);
+      w.y = pack_bf16(v[2], v[3]);
+      *reinterpret_cast<uint2*>(orow + 32 * db + 8 * wave + 4 * (lane >> 5)) = w;
+    }
+  }
+}
+
+template <int MODE, int VK>
+void launch_attn_vk(bool one_pass, dim3 grid, hipStream_t s, const AttnArgs& g) {
+  if (one_pass)
+    hipLaunchKernelGGL((attn_kernel<MODE, VK>), grid, dim3(kAttnThreads), 0, s, g);
   else
-    hipLaunchKernelGGL((attn_kernel<MODE, kVtScalar>), grid, dim3(kAttnThreads), 0, s, g);
+    hipLaunchKernelGGL((attn_long_kernel<MODE, VK>), grid, dim3(kAttnThreads), 0, s, g);
+}
+
+template <int MODE>
+void launch_attn(int vk, bool one_pass, dim3 grid, hipStream_t s, const AttnArgs& g) {
+  if (vk == kVtFull)
+    launch_attn_vk<MODE, kVtFull>(one_pass, grid, s, g);
+  else if (vk == kVtRagged)
+    launch_attn_vk<MODE, kVtRagged>(one_pass, grid, s, g);
+  else
+    launch_attn_vk<MODE, kVtScalar>(one_pass, grid, s, g);
 }
 
 }  // namespace qk
@@ -362,7 +540,7 @@ extern "C" quake_status quake_attention(const void* q, const void* k, const void
                                         void* stream) {
   if (dtype != QUAKE_BF16) return QUAKE_EDTYPE;
   if (!valid_mode(mode)) return QUAKE_EMODE;
-  if (heads < 0 || seq < 0 || dim != kAttnD || seq > kAttnMaxS) return QUAKE_EINVAL;
+  if (heads < 0 || seq < 0 || dim != kAttnD || seq > kAttnLongMaxS) return QUAKE_EINVAL;
   if (ldv < seq || ldv > INT32_MAX) return QUAKE_EINVAL;
   if (!std::isfinite(t) || !(t > 0.0f)) return QUAKE_EINVAL;
   const float c0 = softmax_c0(t, mode);
@@ -381,11 +559,12 @@ extern "C" quake_status quake_attention(const void* q, const void* k, const void
   const hipStream_t s = static_cast<hipStream_t>(stream);
   const bool vec = aligned16(vt) && ldv % 8 == 0;
   const int vk = !vec ? kVtScalar : (seq % 32 == 0 ? kVtFull : kVtRagged);
+  const bool one_pass = seq <= kAttnMaxS;
   switch (mode) {
-    case QUAKE_EXACT: launch_attn<EXACT>(vk, grid, s, g); break;
-    case QUAKE_1: launch_attn<Q1>(vk, grid, s, g); break;
-    case QUAKE_2: launch_attn<Q2>(vk, grid, s, g); break;
-    default: launch_attn<Q2M>(vk, grid, s, g); break;
+    case QUAKE_EXACT: launch_attn<EXACT>(vk, one_pass, grid, s, g); break;
+    case QUAKE_1: launch_attn<Q1>(vk, one_pass, grid, s, g); break;
+    case QUAKE_2: launch_attn<Q2>(vk, one_pass, grid, s, g); break;
+    default: launch_attn<Q2M>(vk, one_pass, grid, s, g); break;
   }
   return launch_status();
 }

@@ -174,7 +174,7 @@ def test_attention_validation(q):
     assert call(dt=0) == q.EDTYPE and call(dt=1) == q.EDTYPE
     assert call(mode=9) == q.EMODE
     assert call(d=128) == q.EINVAL                         # head dimension 64 only
-    assert call(s=520, ldv=520) == q.EINVAL                # longer than 512
+    assert call(s=131073, ldv=131080) == q.EINVAL          # longer than 131072
     assert call(s=130, ldv=128) == q.EINVAL                # ldv < seq
     assert call(t=0.0) == q.EINVAL and call(t=float("nan")) == q.EINVAL
     assert call(t=1e38) == q.EINVAL                        # c0 overflows

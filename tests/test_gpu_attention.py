@@ -17,9 +17,10 @@ with pv = sum_k p_k |v_k| / sum_k p_k (textbook probabilities, times 1.1 to
 cover QuAKE's <= 3 % error). Further, at least 99 % of the elements must be
 within one bfloat16 ulp of the oracle (probability roundings rarely flip).
 Cases: every mode, causal and not, one to several 32-query tiles, a ragged
-last tile, ragged key blocks, the longest sequence (512), a single key, a
-padded v^T row whose padding is NaN, and the full 96-head x 512 workload in
-the launch configuration the benchmark times, compared element by element."""
+last tile, ragged key blocks, the longest one-pass sequence (512) and longer
+ones (513 to 2048 keys, the two-pass kernel), a single key, padded v^T rows
+whose padding is NaN, and the full 96-head x 512 workload in the launch
+configuration the benchmark times, compared element by element."""
 import numpy as np
 import pytest
 import torch
@@ -106,6 +107,8 @@ def _check(g_bits, r_bits, ins, seq, causal, name):
 
 
 SHAPES = [(2, 64), (3, 40), (2, 96), (1, 512), (2, 33), (5, 8)]
+# past 512 keys the two-pass kernel (scores computed twice, never stored)
+LONG_SHAPES = [(2, 513), (1, 1024), (1, 1000), (2, 2048)]
 
 
 @pytest.mark.parametrize("mode", [0, 1, 2, 3])
@@ -114,6 +117,20 @@ SHAPES = [(2, 64), (3, 40), (2, 96), (1, 512), (2, 33), (5, 8)]
 def test_attention_matches_oracle(q, mode, causal, heads, seq):
     g, r, ins = _run(q, heads, seq, mode, causal, 60 + seq)
     _check(g, r, ins, seq, causal, "h%d s%d m%d c%d" % (heads, seq, mode, causal))
+
+
+@pytest.mark.parametrize("mode", [0, 1, 2, 3])
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("heads,seq", LONG_SHAPES)
+def test_long_sequences_match_oracle(q, mode, causal, heads, seq):
+    g, r, ins = _run(q, heads, seq, mode, causal, 70 + seq)
+    _check(g, r, ins, seq, causal, "long h%d s%d m%d c%d" % (heads, seq, mode, causal))
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_long_sequence_padded_vt_element_rows(q, causal):
+    g, r, ins = _run(q, 1, 777, 2, causal, 71, ldv=781, pad=float("nan"))
+    _check(g, r, ins, 777, causal, "long padded")
 
 
 @pytest.mark.parametrize("mode", [0, 2])
@@ -161,6 +178,7 @@ def test_bad_arguments_raise(q):
         q.quake_attention(qg.float(), kg.float(), vtg.float())
     with pytest.raises(ValueError):
         q.quake_attention(qg, kg, vtg, o=qg)            # output over an input
-    big = torch.zeros((1, 520, 64), dtype=torch.bfloat16, device="cuda:0")
-    with pytest.raises(q.QuakeError):
-        q.quake_attention(big, big, torch.zeros((1, 64, 520), dtype=torch.bfloat16, device="cuda:0"))
+    big = torch.zeros((1, 131073, 64), dtype=torch.bfloat16, device="cuda:0")
+    with pytest.raises(q.QuakeError):                     # longer than 131072 keys
+        q.quake_attention(big, big, torch.zeros((1, 64, 131073), dtype=torch.bfloat16,
+                                                device="cuda:0"))
