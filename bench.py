@@ -420,9 +420,9 @@ def linear_gelu(q, synth, a):
     return out
 
 
-def fused_attention(q, synth, a):
+def fused_attention(q, synth, a, heads=96, seq=512):
     """softmax(t q k^T) v over the attention workload's heads (8 x 12 heads,
-    512 tokens, head dimension 64, bf16, t = 1/8) in one kernel
+    512 tokens, head dimension 64, bf16, t = 1/8; or another heads x seq) in one kernel
     (quake_attention), causal and not, in every mode, against the explicit
     path on the same inputs: the score product (torch.bmm, the vendor BLAS),
     quake_softmax_causal / quake_softmax over the bf16 scores, and the second
@@ -432,7 +432,7 @@ def fused_attention(q, synth, a):
     than the Infinity Cache holds) and replayed; the explicit path is captured
     the same way over two sets."""
     import torch
-    heads, seq, d, t, nb = 96, 512, 64, 0.125, 12
+    d, t, nb = 64, 0.125, 12
     sets = []
     for i in range(nb):
         qc, kc, vtc = synth.attention_inputs(heads, seq, 2000 + i)
@@ -441,7 +441,8 @@ def fused_attention(q, synth, a):
     L = q.lib
     algo = 4 * heads * seq * d * 2
     pairs = {1: heads * seq * (seq + 1) // 2, 0: heads * seq * seq}
-    reps = max(20, min(a.steps, 20000) // nb)
+    # about the same GPU time per configuration at every length
+    reps = max(10, min(a.steps, 20000) // nb * 512 * 512 // (seq * seq))
 
     out = {"heads": heads, "seq": seq, "head_dim": d, "t": t, "algo_bytes": algo,
            "launch": "graph (%d launches per replay)" % nb}
@@ -609,7 +610,9 @@ def main():
                 q.quake_attention(qg, kg, vg, mode=MODE_IDS[a.mode], t=0.125)
             torch.cuda.synchronize()
             del qg, kg, vg
-        print(json.dumps({"attention_bf16_96x512x64": fused_attention(q, synth, a)}), flush=True)
+        print(json.dumps({"attention_bf16_96x512x64": fused_attention(q, synth, a),
+                          "attention_bf16_32x2048x64": fused_attention(q, synth, a, 32, 2048)}),
+              flush=True)
         return
     if a.section == "linear_gelu":
         if a.prewarm > 0:
@@ -694,6 +697,7 @@ def main():
         sec["exp_f16_2p28"] = native16(q, synth, a)
         sec["linear_gelu_bf16_4096x3072x768"] = linear_gelu(q, synth, a)
         sec["attention_bf16_96x512x64"] = fused_attention(q, synth, a)
+        sec["attention_bf16_32x2048x64"] = fused_attention(q, synth, a, 32, 2048)
         imp = implicit_causal(q, synth, a)
         imp["no_masked_writes"]["speedup_vs_explicit_mask_input"] = round(
             sec["attn_softmax_bf16_causal"]["quake2_ms"] / imp["no_masked_writes"]["quake2_ms"], 4)
