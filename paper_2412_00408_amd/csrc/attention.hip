@@ -257,13 +257,19 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
 
   // Algorithm 2: exponentials against the row max (c1 folds it in), their
   // sum; the probabilities rounded to bfloat16 pairs (keys 8 gi + 4 (lane / 32)
-  // + 0..3 of each block)
+  // + 0..3 of each block) are consumed by the second product of the same
+  // block right away, so one block's exponentials (VALU) overlap the previous
+  // block's matrix-core work
   const float c1 = (m == -INFINITY) ? 0.0f : __builtin_fmaf(-g.c0, m, MODE == EXACT ? 0.0f : kK127);
   float part = 0.0f;
-  uint32_t pk[kAttnBlk][4][2];
+
+  // O^T = V^T P over this wave's live keys, the next block's V in flight
+  f32x16_t oacc[2] = {};
 #pragma unroll
   for (int i = 0; i < kAttnBlk; ++i) {
     if (i < nlive) {
+      const int kbg = kAttnWaves * i + wave;
+      uint32_t pk[4][2];
 #pragma unroll
       for (int gi = 0; gi < 4; ++gi) {
         float e[4];
@@ -272,20 +278,9 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
           e[j] = qexp<MODE>(sacc[i][4 * gi + j], g.c0, c1);
           part += e[j];
         }
-        pk[i][gi][0] = pack_bf16(e[0], e[1]);
-        pk[i][gi][1] = pack_bf16(e[2], e[3]);
+        pk[gi][0] = pack_bf16(e[0], e[1]);
+        pk[gi][1] = pack_bf16(e[2], e[3]);
       }
-    }
-  }
-  part += xor32(part);
-  if (lane < 32) s_sum[wave][lane] = part;
-
-  // O^T = V^T P over this wave's live keys, the next block's V in flight
-  f32x16_t oacc[2] = {};
-#pragma unroll
-  for (int i = 0; i < kAttnBlk; ++i) {
-    if (i < nlive) {
-      const int kbg = kAttnWaves * i + wave;
       vblock_store(stage, lane, gv);
       if (i + 1 < nlive) {
         const int nb = 32 * (kbg + kAttnWaves);
@@ -298,8 +293,8 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         // lanes < 32 end with keys 16 ks + 0..7, lanes >= 32 with 16 ks + 8..15
-        const auto s0 = __builtin_amdgcn_permlane32_swap(pk[i][2 * ks][0], pk[i][2 * ks + 1][0], false, false);
-        const auto s1 = __builtin_amdgcn_permlane32_swap(pk[i][2 * ks][1], pk[i][2 * ks + 1][1], false, false);
+        const auto s0 = __builtin_amdgcn_permlane32_swap(pk[2 * ks][0], pk[2 * ks + 1][0], false, false);
+        const auto s1 = __builtin_amdgcn_permlane32_swap(pk[2 * ks][1], pk[2 * ks + 1][1], false, false);
         const u32x4_t bv = {s0[0], s1[0], s0[1], s1[1]};
         const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, bv);
 #pragma unroll
@@ -308,6 +303,9 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
       }
     }
   }
+
+  part += xor32(part);
+  if (lane < 32) s_sum[wave][lane] = part;
 
   // the four partial O^T through LDS (each wave's own region, its staging
   // reads done); wave w finishes dims 8 w + 4 (lane / 32) + 0..3 of both
