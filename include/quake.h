@@ -224,14 +224,16 @@ quake_status quake_exp16(const void* x, void* y, int64_t n, quake_dtype dtype, q
  * to the binary32 accumulators in the epilogue of a matrix-core product; the
  * paper applies QuAKE to standalone operators, this is the same operator
  * fused into its producer.
- *   x : device, m x k bfloat16, row r at x + r*ldx (elements), 16-byte aligned.
- *   w : device, n x k bfloat16 (a linear layer's weight), row r at w + r*ldw,
+ *   x : device, m x k 16-bit (dtype), row r at x + r*ldx (elements),
  *       16-byte aligned.
- *   y : device, m x n bfloat16, row r at y + r*ldy.
+ *   w : device, n x k 16-bit (a linear layer's weight), row r at w + r*ldw,
+ *       16-byte aligned.
+ *   y : device, m x n 16-bit, row r at y + r*ldy.
  *   k, ldx, ldw: multiples of 8; ldx, ldw >= k; ldy >= n.
- *   dtype : QUAKE_BF16 only (else QUAKE_EDTYPE); mode: any quake_mode.
+ *   dtype : QUAKE_BF16 or QUAKE_F16 (binary16), the format of x, w and y
+ *       (else QUAKE_EDTYPE); mode: any quake_mode.
  * Products are accumulated in binary32 (order unspecified), then the GELU of
- * each accumulator is rounded to bfloat16. m == 0 or n == 0 launches nothing;
+ * each accumulator is rounded to the 16-bit format. m == 0 or n == 0 launches nothing;
  * other bad sizes, strides or alignments return QUAKE_EINVAL.
  */
 quake_status quake_linear_gelu(const void* x, const void* w, void* y, int64_t m, int64_t n,

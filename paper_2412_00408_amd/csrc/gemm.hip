@@ -1,8 +1,8 @@
-// gemm.hip — quake_linear_gelu: y = GELU(x w^T) for bfloat16 x [m, k] and
-// w [n, k] (both k-contiguous, the layout of a linear layer's input and
-// weight), binary32 accumulation on the matrix cores, the GELU of Eq. 7 with
-// QuAKE / QuAKE2 / EXACT applied to the binary32 accumulators in the
-// epilogue, bfloat16 output. This is QuAKE inside a fused consumer: the GELU
+// gemm.hip — quake_linear_gelu: y = GELU(x w^T) for bfloat16 or binary16
+// x [m, k] and w [n, k] (both k-contiguous, the layout of a linear layer's
+// input and weight), binary32 accumulation on the matrix cores, the GELU of
+// Eq. 7 with QuAKE / QuAKE2 / EXACT applied to the binary32 accumulators in
+// the epilogue, output in the input format. This is QuAKE inside a fused consumer: the GELU
 // costs no HBM traffic of its own, and its VALU work runs beside the MFMAs.
 //
 // Tiling: a workgroup (4 waves) computes a 128 x BN tile of y (BN = 192 when
@@ -28,7 +28,26 @@
 namespace qk {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+// one 32x32x16 matrix-core step on raw 16-bit operands of format DT
+template <int DT>
+__device__ __forceinline__ f32x16_t mfma16(u32x4 a, u32x4 b, f32x16_t c) {
+  if constexpr (DT == BF16)
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8_t, a),
+                                                  __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
+}
+template <int DT>
+__device__ __forceinline__ uint16_t narrow16(float v) {
+  if constexpr (DT == BF16)
+    return __builtin_bit_cast(uint16_t, (__bf16)v);
+  else
+    return __builtin_bit_cast(uint16_t, (_Float16)v);
+}
 
 constexpr int kBM = 128, kBK = 64;
 constexpr int kLdsRow = kBK + 8;   // bf16 elements per LDS row (144 bytes)
@@ -48,8 +67,8 @@ struct GemmArgs {
 
 // OCC: workgroups per CU the register budget is set for (3 at BN = 128: at
 // most 168 VGPRs; 2 at BN = 192)
-template <int MODE, bool GELU, int BN, int OCC>
-__global__ __launch_bounds__(kGemmThreads, OCC) void gemm_bf16_kernel(GemmArgs g) {
+template <int DT, int MODE, bool GELU, int BN, int OCC>
+__global__ __launch_bounds__(kGemmThreads, OCC) void gemm_kernel(GemmArgs g) {
   constexpr int TN = BN / 64;                     // 32 x 32 blocks per wave along n
   constexpr int VA = kBM * 8 / kGemmThreads;      // 16-byte vectors per thread per slab
   constexpr int VB = BN * 8 / kGemmThreads;
@@ -133,22 +152,22 @@ __global__ __launch_bounds__(kGemmThreads, OCC) void gemm_bf16_kernel(GemmArgs g
     if (kt + 1 < nk) load_slab((kt + 1) * kBK);   // in flight during the MFMAs
 #pragma unroll
     for (int ks = 0; ks < kBK / 16; ++ks) {
-      bf16x8_t af[2], bf[TN];
+      u32x4 af[2], bf[TN];
 #pragma unroll
       for (int i = 0; i < 2; ++i)
-        af[i] = *reinterpret_cast<const bf16x8_t*>(sx + (wm * 64 + 32 * i + fr) * kLdsRow + ks * 16 + fk);
+        af[i] = *reinterpret_cast<const u32x4*>(sx + (wm * 64 + 32 * i + fr) * kLdsRow + ks * 16 + fk);
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        bf[j] = *reinterpret_cast<const bf16x8_t*>(sw + (wn * 32 * TN + 32 * j + fr) * kLdsRow + ks * 16 + fk);
+        bf[j] = *reinterpret_cast<const u32x4*>(sw + (wn * 32 * TN + 32 * j + fr) * kLdsRow + ks * 16 + fk);
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = mfma16<DT>(af[i], bf[j], acc[i][j]);
     }
   }
 
-  // Epilogue: GELU on the binary32 accumulators, round to bfloat16, store.
+  // Epilogue: GELU on the binary32 accumulators, round to the 16-bit format, store.
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -160,17 +179,30 @@ __global__ __launch_bounds__(kGemmThreads, OCC) void gemm_bf16_kernel(GemmArgs g
         float v = acc[i][j][r];
         if constexpr (GELU) v = gelu_q<MODE>(v, g.c0, g.c1, g.a);
         if (row < g.m && col < g.n)
-          g.y[(int64_t)row * g.ldy + col] = __builtin_bit_cast(uint16_t, (__bf16)v);
+          g.y[(int64_t)row * g.ldy + col] = narrow16<DT>(v);
       }
     }
 }
 
-template <int MODE, int BN, int OCC>
+template <int DT, int MODE, int BN, int OCC>
 void launch_gemm(int gelu, dim3 grid, hipStream_t s, const GemmArgs& g) {
   if (gelu)
-    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, true, BN, OCC>), grid, dim3(kGemmThreads), 0, s, g);
+    hipLaunchKernelGGL((gemm_kernel<DT, MODE, true, BN, OCC>), grid, dim3(kGemmThreads), 0, s, g);
   else
-    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, false, BN, OCC>), grid, dim3(kGemmThreads), 0, s, g);
+    hipLaunchKernelGGL((gemm_kernel<DT, MODE, false, BN, OCC>), grid, dim3(kGemmThreads), 0, s, g);
+}
+
+template <int DT>
+void launch_gemm_dt(int mode, bool wide, int gelu, dim3 grid, hipStream_t s, const GemmArgs& g) {
+#define QK_GEMM_CASE(M)                                 \
+  if (mode == M) {                                      \
+    if (wide)                                           \
+      launch_gemm<DT, M, 192, 2>(gelu, grid, s, g);     \
+    else                                                \
+      launch_gemm<DT, M, 128, 3>(gelu, grid, s, g);     \
+  }
+  QK_GEMM_CASE(EXACT) QK_GEMM_CASE(Q1) QK_GEMM_CASE(Q2) QK_GEMM_CASE(Q2M)
+#undef QK_GEMM_CASE
 }
 
 }  // namespace qk
@@ -181,7 +213,7 @@ extern "C" quake_status quake_linear_gelu(const void* x, const void* w, void* y,
                                           int64_t n, int64_t k, int64_t ldx, int64_t ldw,
                                           int64_t ldy, quake_dtype dtype, quake_mode mode,
                                           int gelu, void* stream) {
-  if (dtype != QUAKE_BF16) return QUAKE_EDTYPE;
+  if (dtype != QUAKE_BF16 && dtype != QUAKE_F16) return QUAKE_EDTYPE;
   if (!valid_mode(mode)) return QUAKE_EMODE;
   if (m < 0 || n < 0 || k < 0) return QUAKE_EINVAL;
   if (m == 0 || n == 0) return QUAKE_OK;
@@ -200,15 +232,9 @@ extern "C" quake_status quake_linear_gelu(const void* x, const void* w, void* y,
              (uint32_t)(tiles_m % 4 == 0 && tiles_n % 2 == 0)};
   const dim3 grid((uint32_t)(tiles_m * tiles_n));
   const hipStream_t s = static_cast<hipStream_t>(stream);
-#define QK_GEMM_CASE(M)                                                                      \
-  if (mode == M) {                                                                           \
-    if (wide)                                                                                \
-      launch_gemm<M, 192, 2>(gelu, grid, s, g);                                              \
-    else                                                                                     \
-      launch_gemm<M, 128, 3>(gelu, grid, s, g);                                              \
-    return launch_status();                                                                  \
-  }
-  QK_GEMM_CASE(EXACT) QK_GEMM_CASE(Q1) QK_GEMM_CASE(Q2) QK_GEMM_CASE(Q2M)
-#undef QK_GEMM_CASE
-  return QUAKE_EMODE;
+  if (dtype == QUAKE_BF16)
+    launch_gemm_dt<BF16>(mode, wide, gelu, grid, s, g);
+  else
+    launch_gemm_dt<F16>(mode, wide, gelu, grid, s, g);
+  return launch_status();
 }

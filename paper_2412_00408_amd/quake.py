@@ -162,8 +162,9 @@ def _rows_view(t: torch.Tensor, what: str):
 
 
 def quake_linear_gelu(x, w, y=None, mode=QUAKE_2, gelu=True, stream=None):
-    """y = GELU(x w^T) (or x w^T with gelu=False): bfloat16 x [m, k] and
-    w [n, k] with contiguous rows, binary32 accumulation, bfloat16 y [m, n]."""
+    """y = GELU(x w^T) (or x w^T with gelu=False): bfloat16 or float16 x [m, k]
+    and w [n, k] with contiguous rows, binary32 accumulation, y [m, n] in the
+    same format."""
     if not (x.is_cuda and w.is_cuda):
         raise ValueError("libquake takes device tensors")
     if x.dim() != 2 or w.dim() != 2 or x.shape[1] != w.shape[1]:

@@ -150,7 +150,7 @@ def test_linear_gelu_validation(q):
     def call(m=256, n=256, k=64, ldx=64, ldw=64, ldy=256, dt=2, mode=2, x=A, w=A, y=A):
         return L.quake_linear_gelu(x, w, y, m, n, k, ldx, ldw, ldy, dt, mode, 1, None)
     assert call(m=0) == q.OK and call(n=0) == q.OK
-    assert call(dt=0) == q.EDTYPE and call(dt=1) == q.EDTYPE
+    assert call(dt=0) == q.EDTYPE and call(dt=3) == q.EDTYPE   # binary32, unknown
     assert call(mode=7) == q.EMODE
     assert call(k=0) == q.EINVAL
     assert call(k=60, ldx=64, ldw=64) == q.EINVAL         # k not a multiple of 8
