@@ -272,39 +272,40 @@ def softmax_numerators(s: np.ndarray, mode: int, t: float = 1.0, threads: int = 
 
 
 def attention(q: np.ndarray, k: np.ndarray, vt: np.ndarray, mode: int, t: float,
-              causal: bool = True, threads: int = 1) -> np.ndarray:
-    """softmax(t q k^T) v per head with the softmax of Algorithm 2, for bfloat16
-    q, k [h, s, d] and vt [h, d, >= s] (v transposed, raw bits; columns past s
-    are ignored). Heads are independent and are taken a few at a time."""
+              causal: bool = True, threads: int = 1, dt: str = "bf16") -> np.ndarray:
+    """softmax(t q k^T) v per head with the softmax of Algorithm 2, for 16-bit
+    (dt: "bf16" or "f16") q, k [h, s, d] and vt [h, d, >= s] (v transposed, raw
+    bits; columns past s are ignored). Heads are independent and are taken a
+    few at a time."""
     h, s_len, d = q.shape
     out = np.empty((h, s_len, d), np.uint16)
     for h0 in range(0, h, 4):
         out[h0:h0 + 4] = _attention_heads(q[h0:h0 + 4], k[h0:h0 + 4], vt[h0:h0 + 4], mode, t,
-                                          causal, threads)
+                                          causal, threads, dt)
     return out
 
 
-def _attention_heads(q, k, vt, mode, t, causal, threads):
-    """Scores: float64 products of the bfloat16 inputs rounded once to
+def _attention_heads(q, k, vt, mode, t, causal, threads, dt="bf16"):
+    """Scores: float64 products of the 16-bit inputs rounded once to
     binary32, causal entries (key > query) set to -inf; numerators and sums as
-    softmax_numerators; the numerators rounded to bfloat16 for the second
-    product (its operands are bfloat16), that product in float64, divided by
-    the float64 sum, rounded to bfloat16."""
+    softmax_numerators; the numerators rounded to the input format for the
+    second product (its operands are in that format), that product in float64,
+    divided by the float64 sum, rounded to the input format."""
     h, s_len, d = q.shape
-    qd = decode(np.ascontiguousarray(q).reshape(-1), "bf16").astype(np.float64).reshape(h, s_len, d)
-    kd = decode(np.ascontiguousarray(k).reshape(-1), "bf16").astype(np.float64).reshape(h, s_len, d)
-    vd = decode(np.ascontiguousarray(vt[:, :, :s_len]).reshape(-1), "bf16").astype(
+    qd = decode(np.ascontiguousarray(q).reshape(-1), dt).astype(np.float64).reshape(h, s_len, d)
+    kd = decode(np.ascontiguousarray(k).reshape(-1), dt).astype(np.float64).reshape(h, s_len, d)
+    vd = decode(np.ascontiguousarray(vt[:, :, :s_len]).reshape(-1), dt).astype(
         np.float64).reshape(h, d, s_len)
     scores = np.matmul(qd, np.transpose(kd, (0, 2, 1))).astype(np.float32)
     if causal:
         mask = np.arange(s_len)[None, :] > np.arange(s_len)[:, None]
         scores[:, mask] = -np.inf
     p, sums = softmax_numerators(scores.reshape(h * s_len, s_len), mode, t, threads)
-    pb = decode(round_to(p.astype(np.float64).reshape(-1), "bf16"), "bf16").astype(np.float64)
+    pb = decode(round_to(p.astype(np.float64).reshape(-1), dt), dt).astype(np.float64)
     o = np.matmul(pb.reshape(h, s_len, s_len), np.transpose(vd, (0, 2, 1)))
     with np.errstate(invalid="ignore", divide="ignore"):
         o = np.where(sums.reshape(h, s_len, 1) > 0, o / sums.reshape(h, s_len, 1), 0.0)
-    return round_to(o.reshape(-1), "bf16").reshape(h, s_len, d)
+    return round_to(o.reshape(-1), dt).reshape(h, s_len, d)
 
 
 def linear_gelu(x: np.ndarray, w: np.ndarray, mode: int, gelu: bool = True, dt: str = "bf16",

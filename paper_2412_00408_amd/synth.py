@@ -107,11 +107,11 @@ def spiked_logits(rows: int, cols: int, std: float, spikes: int, spike_val: floa
 
 
 def attention_inputs(heads: int, seq: int, k: int, dim: int = 64, ldv: int | None = None,
-                     pad: float = 0.0, heads_total: int | None = None):
-    """q, k [heads, seq, dim] and v transposed, vt [heads, dim, ldv], all
-    bfloat16 with N(0,1) entries (so with t = 1/sqrt(dim) the scaled scores are
-    about N(0,1)); vt's columns seq .. ldv-1 are set to `pad`. `heads` may be a
-    prefix of `heads_total` heads drawn by the same generator."""
+                     pad: float = 0.0, heads_total: int | None = None, dt: str = "bf16"):
+    """q, k [heads, seq, dim] and v transposed, vt [heads, dim, ldv], all in
+    16-bit format dt with N(0,1) entries (so with t = 1/sqrt(dim) the scaled
+    scores are about N(0,1)); vt's columns seq .. ldv-1 are set to `pad`.
+    `heads` may be a prefix of `heads_total` heads drawn by the same generator."""
     ldv = seq if ldv is None else ldv
     total = heads if heads_total is None else heads_total
     r = rng(k)
@@ -120,7 +120,7 @@ def attention_inputs(heads: int, seq: int, k: int, dim: int = 64, ldv: int | Non
     v = r.standard_normal((total, dim, seq), dtype=np.float32)[:heads]
     vt = np.full((heads, dim, ldv), np.float32(pad), np.float32)
     vt[:, :, :seq] = v
-    return to_format(q, "bf16"), to_format(kk, "bf16"), to_format(vt, "bf16")
+    return to_format(q, dt), to_format(kk, dt), to_format(vt, dt)
 
 
 # --------------------------------------------------------------------------

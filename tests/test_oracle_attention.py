@@ -21,51 +21,69 @@ def _np(t):
     return synth.bits(t)
 
 
-def _f64(bits16):
+def _f64(bits16, dt="bf16"):
     import oracle
-    return oracle.decode(np.ascontiguousarray(bits16).reshape(-1), "bf16").astype(
+    return oracle.decode(np.ascontiguousarray(bits16).reshape(-1), dt).astype(
         np.float64).reshape(bits16.shape)
 
 
-def _inputs(h, s, seed, ldv=None, pad=0.0):
-    q, k, vt = synth.attention_inputs(h, s, seed, ldv=ldv, pad=pad)
+def _inputs(h, s, seed, ldv=None, pad=0.0, dt="bf16"):
+    q, k, vt = synth.attention_inputs(h, s, seed, ldv=ldv, pad=pad, dt=dt)
     return _np(q), _np(k), _np(vt)
 
 
-def _textbook(q, k, vt, t, causal):
-    """float64 softmax(t q k^T) v with the standard exponential."""
+def _textbook(q, k, vt, t, causal, dt="bf16"):
+    """float64 softmax(t q k^T) v with the standard exponential; also
+    sum_k p_k |v_k| / sum_k p_k and sum_k |v_k| / sum_k p_k (allowed keys)."""
     s_len = q.shape[1]
-    sc = np.matmul(_f64(q), np.transpose(_f64(k), (0, 2, 1))) * t
+    sc = np.matmul(_f64(q, dt), np.transpose(_f64(k, dt), (0, 2, 1))) * t
+    allowed = np.ones((s_len, s_len), bool)
     if causal:
-        sc[:, np.triu(np.ones((s_len, s_len), bool), 1)] = -np.inf
+        allowed = ~np.triu(allowed, 1)
+        sc[:, ~allowed] = -np.inf
     sc -= sc.max(axis=2, keepdims=True)
     p = np.exp(sc)
-    ref = np.matmul(p, np.transpose(_f64(vt)[:, :, :s_len], (0, 2, 1))) / p.sum(axis=2, keepdims=True)
-    pv = np.matmul(p, np.transpose(np.abs(_f64(vt)[:, :, :s_len]), (0, 2, 1))) / p.sum(axis=2, keepdims=True)
-    return ref, pv
+    va = np.abs(_f64(vt, dt)[:, :, :s_len])
+    ref = np.matmul(p, np.transpose(_f64(vt, dt)[:, :, :s_len], (0, 2, 1))) / p.sum(axis=2, keepdims=True)
+    pv = np.matmul(p, np.transpose(va, (0, 2, 1))) / p.sum(axis=2, keepdims=True)
+    sv = np.matmul(allowed.astype(np.float64)[None], np.transpose(va, (0, 2, 1))) / p.sum(
+        axis=2, keepdims=True)
+    return ref, pv, sv
 
 
+# unit roundoff u of the format, and the absolute rounding floor of a value
+# below its normal range (binary16 probabilities can be subnormal)
+U = {"bf16": 2.0 ** -8, "f16": 2.0 ** -11}
+FLOOR = {"bf16": 2.0 ** -134, "f16": 2.0 ** -25}
+
+
+def _bound(ref, pv, sv, dt, rel):
+    return U[dt] * np.abs(ref) + (U[dt] + 2.0 ** -12 + rel) * pv + FLOOR[dt] * (sv + 1)
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
 @pytest.mark.parametrize("mode", [0, 1, 2, 3])
 @pytest.mark.parametrize("causal", [True, False])
-def test_single_key_returns_v(oracle, mode, causal):
-    q, k, vt = _inputs(3, 1, 40)
-    o = oracle.attention(q, k, vt, mode, 0.125, causal)
+def test_single_key_returns_v(oracle, mode, causal, dt):
+    q, k, vt = _inputs(3, 1, 40, dt=dt)
+    o = oracle.attention(q, k, vt, mode, 0.125, causal, dt=dt)
     assert np.array_equal(o, np.transpose(vt, (0, 2, 1)))
 
 
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
 @pytest.mark.parametrize("mode", [0, 1, 2, 3])
 @pytest.mark.parametrize("causal", [True, False])
-def test_equal_scores_give_the_mean_of_v(oracle, mode, causal):
+def test_equal_scores_give_the_mean_of_v(oracle, mode, causal, dt):
     h, s = 2, 37
-    _, k, vt = _inputs(h, s, 41)
+    _, k, vt = _inputs(h, s, 41, dt=dt)
     q = np.zeros((h, s, 64), np.uint16)                 # every score is 0: p = 1 exactly
-    o = _f64(oracle.attention(q, k, vt, mode, 0.125, causal))
-    v = np.transpose(_f64(vt), (0, 2, 1))
+    o = _f64(oracle.attention(q, k, vt, mode, 0.125, causal, dt=dt), dt)
+    v = np.transpose(_f64(vt, dt), (0, 2, 1))
     if causal:
         mean = np.cumsum(v, axis=1) / np.arange(1, s + 1)[None, :, None]
     else:
         mean = np.broadcast_to(v.mean(axis=1, keepdims=True), v.shape)
-    want = _f64(oracle.round_to(mean.reshape(-1), "bf16").reshape(mean.shape))
+    want = _f64(oracle.round_to(mean.reshape(-1), dt).reshape(mean.shape), dt)
     assert np.array_equal(o, want)
 
 
@@ -87,28 +105,29 @@ def test_numerators_reproduce_the_softmax_oracle(oracle, mode):
     assert np.all(p[9] == 0) and sums[9] == 0
 
 
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
 @pytest.mark.parametrize("causal", [True, False])
-def test_exact_mode_is_textbook_attention(oracle, causal):
-    q, k, vt = _inputs(3, 45, 44)
-    o = _f64(oracle.attention(q, k, vt, 0, 0.125, causal))
-    ref, pv = _textbook(q, k, vt, 0.125, causal)
-    # bfloat16 output rounding, bfloat16 probabilities (2^-8 relative each: 8 significant bits), the
-    # binary32 scores and exponent argument (far below 2^-12 relative here)
-    bound = 2.0 ** -8 * np.abs(ref) + (2.0 ** -8 + 2.0 ** -12) * pv
-    assert np.all(np.abs(o - ref) <= bound)
+def test_exact_mode_is_textbook_attention(oracle, causal, dt):
+    q, k, vt = _inputs(3, 45, 44, dt=dt)
+    o = _f64(oracle.attention(q, k, vt, 0, 0.125, causal, dt=dt), dt)
+    ref, pv, sv = _textbook(q, k, vt, 0.125, causal, dt)
+    # output rounding and probability rounding (unit roundoff u of the format
+    # each, plus the subnormal floor of binary16 probabilities), the binary32
+    # scores and exponent argument (far below 2^-12 relative here)
+    assert np.all(np.abs(o - ref) <= _bound(ref, pv, sv, dt, 0.0))
 
 
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
 @pytest.mark.parametrize("mode,err", [(1, 0.0299), (2, 0.00342), (3, 0.00173)])
-def test_quake_modes_within_their_error_range(oracle, mode, err):
+def test_quake_modes_within_their_error_range(oracle, mode, err, dt):
     # every exponential is within its mode's relative error range (pinned with
     # the scalar oracle: QuAKE1 2.99 %, QuAKE2 0.342 %, minimax 0.173 %), so
     # sum_j p_j v_j / sum_j p_j moves by at most (1 + err) / (1 - err) - 1,
     # below 2.2 err, times sum_j p_j |v_j| / sum_j p_j
-    q, k, vt = _inputs(2, 64, 45)
-    o = _f64(oracle.attention(q, k, vt, mode, 0.125, True))
-    ref, pv = _textbook(q, k, vt, 0.125, True)
-    bound = 2.0 ** -8 * np.abs(ref) + (2.0 ** -8 + 2.0 ** -12 + 2.2 * err) * pv
-    assert np.all(np.abs(o - ref) <= bound)
+    q, k, vt = _inputs(2, 64, 45, dt=dt)
+    o = _f64(oracle.attention(q, k, vt, mode, 0.125, True, dt=dt), dt)
+    ref, pv, sv = _textbook(q, k, vt, 0.125, True, dt)
+    assert np.all(np.abs(o - ref) <= _bound(ref, pv, sv, dt, 2.2 * err))
 
 
 def test_padding_of_vt_is_ignored(oracle):
@@ -119,6 +138,9 @@ def test_padding_of_vt_is_ignored(oracle):
 
 
 MUTANTS = {
+    "probabilities_always_bfloat16": (
+        'pb = decode(round_to(p.astype(np.float64).reshape(-1), dt), dt).astype(np.float64)',
+        'pb = decode(round_to(p.astype(np.float64).reshape(-1), "bf16"), "bf16").astype(np.float64)'),
     "causal_mask_includes_diagonal": ("np.arange(s_len)[None, :] > np.arange(s_len)[:, None]",
                                       "np.arange(s_len)[None, :] >= np.arange(s_len)[:, None]"),
     "v_not_transposed": ("o = np.matmul(pb.reshape(h, s_len, s_len), np.transpose(vd, (0, 2, 1)))",
@@ -140,14 +162,13 @@ def test_pins_catch_attention_mutant(oracle, name):
     exec(compile(src.replace(old, new), "<mutant %s>" % name, "exec"), ns)
     mut = ns["attention"]
     caught = []
-    for causal in (True, False):
-        q, k, vt = _inputs(2, 37, 47)
+    for causal, dt in ((True, "bf16"), (False, "bf16"), (True, "f16")):
+        q, k, vt = _inputs(2, 37, 47, dt=dt)
         try:
-            o = _f64(mut(q, k, vt, 0, 0.125, causal))
+            o = _f64(mut(q, k, vt, 0, 0.125, causal, dt=dt), dt)
         except ValueError:
             caught.append(True)
             continue
-        ref, pv = _textbook(q, k, vt, 0.125, causal)
-        bound = 2.0 ** -8 * np.abs(ref) + (2.0 ** -8 + 2.0 ** -12) * pv
-        caught.append(not np.all(np.abs(o - ref) <= bound))
+        ref, pv, sv = _textbook(q, k, vt, 0.125, causal, dt)
+        caught.append(not np.all(np.abs(o - ref) <= _bound(ref, pv, sv, dt, 0.0)))
     assert any(caught), name
