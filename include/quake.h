@@ -246,15 +246,16 @@ quake_status quake_linear_gelu(const void* x, const void* w, void* y, int64_t m,
  * `mode`, fused with both products. Each query's exponentials are taken
  * against the max of its whole score row (no online rescaling), so the
  * probabilities are the ones quake_softmax gives for those scores; they are
- * rounded to bfloat16 before the second product, and the row sum (of the
- * binary32 exponentials) divides the binary32 result, rounded to bfloat16.
- *   q, k : device, [heads, seq, dim] bfloat16, contiguous, 16-byte aligned.
- *   vt   : device, v transposed: [heads, dim, ldv] bfloat16, element
+ * rounded to the 16-bit format before the second product, and the row sum (of
+ * the binary32 exponentials) divides the binary32 result, rounded to the
+ * 16-bit format.
+ *   q, k : device, [heads, seq, dim] 16-bit (dtype), contiguous, 16-byte aligned.
+ *   vt   : device, v transposed: [heads, dim, ldv] 16-bit, element
  *          (h, d, j) = v[h, j, d]; ldv >= seq, 2-byte aligned. Columns
  *          seq .. ldv-1 may hold anything (they do not affect o). With vt
  *          16-byte aligned and ldv a multiple of 8 the rows are read as
  *          16-byte vectors, else element by element.
- *   o    : device, [heads, seq, dim] bfloat16, contiguous, 8-byte aligned; it
+ *   o    : device, [heads, seq, dim] 16-bit, contiguous, 8-byte aligned; it
  *          must not overlap q, k or vt (other workgroups still read them).
  *   dim == 64 and seq <= 131072. Up to 512 keys a query's scores stay in
  *   registers (one pass); longer sequences take two passes over the keys
@@ -262,8 +263,9 @@ quake_status quake_linear_gelu(const void* x, const void* w, void* y, int64_t m,
  *   second product), with results identical to what one pass would give;
  *   t > 0 finite (1/sqrt(dim) for the usual scaling); causal != 0 lets query
  *   i use keys j <= i only (masked keys are neither loaded nor multiplied).
- *   dtype : QUAKE_BF16 only (else QUAKE_EDTYPE); mode: any quake_mode.
- * Scores are binary32 sums of the bfloat16 products (order unspecified).
+ *   dtype : QUAKE_BF16 or QUAKE_F16, the format of q, k, vt and o (else
+ *   QUAKE_EDTYPE); mode: any quake_mode.
+ * Scores are binary32 sums of the exact 16-bit products (order unspecified).
  * heads == 0 or seq == 0 launches nothing; other bad sizes, strides,
  * alignments or t return QUAKE_EINVAL.
  */

@@ -33,6 +33,7 @@
 namespace qk {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
@@ -59,6 +60,25 @@ struct AttnArgs {
 
 __device__ __forceinline__ u32x4_t ld16(const uint16_t* p) {
   return *reinterpret_cast<const u32x4_t*>(p);
+}
+
+// One 32x32x16 matrix-core step on raw 16-bit operands of format DT
+// (bfloat16 or binary16), and two binary32 values rounded to a DT pair.
+template <int DT>
+__device__ __forceinline__ f32x16_t mma(u32x4_t a, u32x4_t b, f32x16_t c) {
+  if constexpr (DT == BF16)
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8_t, a),
+                                                  __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
+}
+template <int DT>
+__device__ __forceinline__ uint32_t pack16(float a, float b) {
+  if constexpr (DT == BF16)
+    return pack_bf16(a, b);
+  else
+    return pack_f16(a, b);
 }
 
 // the value held by lane l xor 32
@@ -100,10 +120,10 @@ __device__ __forceinline__ void kblock_store(u32x4_t* buf, int lane, const u32x4
   }
 }
 // A operands of S^T = K Q^T: 16-dim step ks, dims 16 ks + 8 h .. + 7 of key fr
-__device__ __forceinline__ void kblock_read(const u32x4_t* buf, int fr, int h, bf16x8_t (&a)[4]) {
+__device__ __forceinline__ void kblock_read(const u32x4_t* buf, int fr, int h, u32x4_t (&a)[4]) {
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks)
-    a[ks] = __builtin_bit_cast(bf16x8_t, buf[8 * fr + ((2 * ks + h) ^ kswz(fr))]);
+    a[ks] = buf[8 * fr + ((2 * ks + h) ^ kswz(fr))];
 }
 
 // Layouts of V^T the kernel is built for: sequence a multiple of 32 with
@@ -156,17 +176,17 @@ __device__ __forceinline__ void vblock_store(u32x4_t* buf, int lane, const u32x4
 // A operands of O^T = V^T P: 16-key step ks, 32-dim half db; keys
 // 16 ks + 8 h .. + 7 of dim 32 db + fr
 __device__ __forceinline__ void vblock_read(const u32x4_t* buf, int fr, int h,
-                                            bf16x8_t (&a)[2][2]) {
+                                            u32x4_t (&a)[2][2]) {
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
     for (int db = 0; db < 2; ++db) {
       const int d = 32 * db + fr;
-      a[ks][db] = __builtin_bit_cast(bf16x8_t, buf[4 * d + ((2 * ks + h) ^ vswz(d))]);
+      a[ks][db] = buf[4 * d + ((2 * ks + h) ^ vswz(d))];
     }
 }
 
-template <int MODE, int VK>
+template <int DT, int MODE, int VK>
 __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
   __shared__ float s_max[kAttnWaves][kAttnQ];
   __shared__ float s_sum[kAttnWaves][kAttnQ];
@@ -205,11 +225,11 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
   const uint16_t* Vt = g.vt + (int64_t)bh * kAttnD * g.ldv;
 
   // S^T = K Q^T over the live key blocks, the next block's K in flight
-  bf16x8_t qf[4];
+  u32x4_t qf[4];
   {
     const uint16_t* qr = Q + (int64_t)min(query, S - 1) * kAttnD + fk;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) qf[ks] = __builtin_bit_cast(bf16x8_t, ld16(qr + 16 * ks));
+    for (int ks = 0; ks < 4; ++ks) qf[ks] = ld16(qr + 16 * ks);
   }
   u32x4_t* stage = s_buf[wave];
   const int h = lane >> 5;
@@ -224,14 +244,14 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
       kblock_store(stage, lane, gk);
       if (i + 1 < nlive) kblock_load(K, 32 * (kbg + kAttnWaves), S, lane, gk);
       __builtin_amdgcn_wave_barrier();   // lanes read what other lanes wrote
-      bf16x8_t ka[4];
+      u32x4_t ka[4];
       kblock_read(stage, fr, h, ka);
       __builtin_amdgcn_wave_barrier();   // before the slots are written again
       const f32x16_t zero = {};
-      sacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qf[0], zero, 0, 0, 0);
+      sacc[i] = mma<DT>(ka[0], qf[0], zero);
 #pragma unroll
       for (int ks = 1; ks < 4; ++ks)
-        sacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks], qf[ks], sacc[i], 0, 0, 0);
+        sacc[i] = mma<DT>(ka[ks], qf[ks], sacc[i]);
       const bool diag = g.causal && kbg == qb;
       if (diag || (VK != kVtFull && 32 * kbg + 32 > S)) {
 #pragma unroll
@@ -278,8 +298,8 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
           e[j] = qexp<MODE>(sacc[i][4 * gi + j], g.c0, c1);
           part += e[j];
         }
-        pk[gi][0] = pack_bf16(e[0], e[1]);
-        pk[gi][1] = pack_bf16(e[2], e[3]);
+        pk[gi][0] = pack16<DT>(e[0], e[1]);
+        pk[gi][1] = pack16<DT>(e[2], e[3]);
       }
       vblock_store(stage, lane, gv);
       if (i + 1 < nlive) {
@@ -287,7 +307,7 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
         vblock_load<VK>(Vt, g.ldv, nb, S, VK != kVtFull && nb + 32 > S, lane, gv);
       }
       __builtin_amdgcn_wave_barrier();
-      bf16x8_t va[2][2];
+      u32x4_t va[2][2];
       vblock_read(stage, fr, h, va);
       __builtin_amdgcn_wave_barrier();
 #pragma unroll
@@ -296,10 +316,10 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
         const auto s0 = __builtin_amdgcn_permlane32_swap(pk[2 * ks][0], pk[2 * ks + 1][0], false, false);
         const auto s1 = __builtin_amdgcn_permlane32_swap(pk[2 * ks][1], pk[2 * ks + 1][1], false, false);
         const u32x4_t bv = {s0[0], s1[0], s0[1], s1[1]};
-        const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, bv);
+        
 #pragma unroll
         for (int db = 0; db < 2; ++db)
-          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[ks][db], pf, oacc[db], 0, 0, 0);
+          oacc[db] = mma<DT>(va[ks][db], bv, oacc[db]);
       }
     }
   }
@@ -334,8 +354,8 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
         v[j] = ((p0[idx] + p1[idx]) + (p2[idx] + p3[idx])) * inv;
       }
       uint2 w;
-      w.x = pack_bf16(v[0], v[1]);
-      w.y = pack_bf16(v[2], v[3]);
+      w.x = pack16<DT>(v[0], v[1]);
+      w.y = pack16<DT>(v[2], v[3]);
       *reinterpret_cast<uint2*>(orow + 32 * db + 8 * wave + 4 * (lane >> 5)) = w;
     }
   }
@@ -348,7 +368,7 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
 // their sum and the second product. The scores, the max, the exponentials,
 // the sums and the products are computed by the same instructions in the same
 // order as in the one-pass kernel, so both give identical results.
-template <int MODE, int VK>
+template <int DT, int MODE, int VK>
 __global__ __launch_bounds__(kAttnThreads, 3) void attn_long_kernel(AttnArgs g) {
   __shared__ float s_max[kAttnWaves][kAttnQ];
   __shared__ float s_sum[kAttnWaves][kAttnQ];
@@ -377,25 +397,25 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_long_kernel(AttnArgs g) 
   const uint16_t* Vt = g.vt + (int64_t)bh * kAttnD * g.ldv;
   u32x4_t* stage = s_buf[wave];
 
-  bf16x8_t qf[4];
+  u32x4_t qf[4];
   {
     const uint16_t* qr = Q + (int64_t)min(query, S - 1) * kAttnD + fk;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) qf[ks] = __builtin_bit_cast(bf16x8_t, ld16(qr + 16 * ks));
+    for (int ks = 0; ks < 4; ++ks) qf[ks] = ld16(qr + 16 * ks);
   }
   // one block of S^T = K Q^T from the staged K block gk (masked past s and,
   // on the diagonal, above it)
   auto scores = [&](const u32x4_t (&gk)[4], int kbg) {
     kblock_store(stage, lane, gk);
     __builtin_amdgcn_wave_barrier();   // lanes read what other lanes wrote
-    bf16x8_t ka[4];
+    u32x4_t ka[4];
     kblock_read(stage, fr, h, ka);
     __builtin_amdgcn_wave_barrier();   // before the slots are written again
     const f32x16_t zero = {};
-    f32x16_t sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0], qf[0], zero, 0, 0, 0);
+    f32x16_t sacc = mma<DT>(ka[0], qf[0], zero);
 #pragma unroll
     for (int ks = 1; ks < 4; ++ks)
-      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks], qf[ks], sacc, 0, 0, 0);
+      sacc = mma<DT>(ka[ks], qf[ks], sacc);
     const bool diag = g.causal && kbg == qb;
     if (diag || (VK != kVtFull && 32 * kbg + 32 > S)) {
 #pragma unroll
@@ -457,12 +477,12 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_long_kernel(AttnArgs g) 
         e[j] = qexp<MODE>(sacc[4 * gi + j], g.c0, c1);
         part += e[j];
       }
-      pk[gi][0] = pack_bf16(e[0], e[1]);
-      pk[gi][1] = pack_bf16(e[2], e[3]);
+      pk[gi][0] = pack16<DT>(e[0], e[1]);
+      pk[gi][1] = pack16<DT>(e[2], e[3]);
     }
     vblock_store(stage, lane, curv);
     __builtin_amdgcn_wave_barrier();
-    bf16x8_t va[2][2];
+    u32x4_t va[2][2];
     vblock_read(stage, fr, h, va);
     __builtin_amdgcn_wave_barrier();
 #pragma unroll
@@ -470,10 +490,10 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_long_kernel(AttnArgs g) 
       const auto s0 = __builtin_amdgcn_permlane32_swap(pk[2 * ks][0], pk[2 * ks + 1][0], false, false);
       const auto s1 = __builtin_amdgcn_permlane32_swap(pk[2 * ks][1], pk[2 * ks + 1][1], false, false);
       const u32x4_t bv = {s0[0], s1[0], s0[1], s1[1]};
-      const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, bv);
+      
 #pragma unroll
       for (int db = 0; db < 2; ++db)
-        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[ks][db], pf, oacc[db], 0, 0, 0);
+        oacc[db] = mma<DT>(va[ks][db], bv, oacc[db]);
     }
   }
   part += xor32(part);
@@ -503,29 +523,39 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_long_kernel(AttnArgs g) 
         v[j] = ((p0[idx] + p1[idx]) + (p2[idx] + p3[idx])) * inv;
       }
       uint2 w;
-      w.x = pack_bf16(v[0], v[1]);
-      w.y = pack_bf16(v[2], v[3]);
+      w.x = pack16<DT>(v[0], v[1]);
+      w.y = pack16<DT>(v[2], v[3]);
       *reinterpret_cast<uint2*>(orow + 32 * db + 8 * wave + 4 * (lane >> 5)) = w;
     }
   }
 }
 
-template <int MODE, int VK>
+template <int DT, int MODE, int VK>
 void launch_attn_vk(bool one_pass, dim3 grid, hipStream_t s, const AttnArgs& g) {
   if (one_pass)
-    hipLaunchKernelGGL((attn_kernel<MODE, VK>), grid, dim3(kAttnThreads), 0, s, g);
+    hipLaunchKernelGGL((attn_kernel<DT, MODE, VK>), grid, dim3(kAttnThreads), 0, s, g);
   else
-    hipLaunchKernelGGL((attn_long_kernel<MODE, VK>), grid, dim3(kAttnThreads), 0, s, g);
+    hipLaunchKernelGGL((attn_long_kernel<DT, MODE, VK>), grid, dim3(kAttnThreads), 0, s, g);
 }
 
-template <int MODE>
-void launch_attn(int vk, bool one_pass, dim3 grid, hipStream_t s, const AttnArgs& g) {
+template <int DT, int MODE>
+void launch_attn_mode(int vk, bool one_pass, dim3 grid, hipStream_t s, const AttnArgs& g) {
   if (vk == kVtFull)
-    launch_attn_vk<MODE, kVtFull>(one_pass, grid, s, g);
+    launch_attn_vk<DT, MODE, kVtFull>(one_pass, grid, s, g);
   else if (vk == kVtRagged)
-    launch_attn_vk<MODE, kVtRagged>(one_pass, grid, s, g);
+    launch_attn_vk<DT, MODE, kVtRagged>(one_pass, grid, s, g);
   else
-    launch_attn_vk<MODE, kVtScalar>(one_pass, grid, s, g);
+    launch_attn_vk<DT, MODE, kVtScalar>(one_pass, grid, s, g);
+}
+
+template <int DT>
+void launch_attn(int mode, int vk, bool one_pass, dim3 grid, hipStream_t s, const AttnArgs& g) {
+  switch (mode) {
+    case QUAKE_EXACT: launch_attn_mode<DT, EXACT>(vk, one_pass, grid, s, g); break;
+    case QUAKE_1: launch_attn_mode<DT, Q1>(vk, one_pass, grid, s, g); break;
+    case QUAKE_2: launch_attn_mode<DT, Q2>(vk, one_pass, grid, s, g); break;
+    default: launch_attn_mode<DT, Q2M>(vk, one_pass, grid, s, g); break;
+  }
 }
 
 }  // namespace qk
@@ -536,7 +566,7 @@ extern "C" quake_status quake_attention(const void* q, const void* k, const void
                                         int64_t heads, int64_t seq, int64_t dim, int64_t ldv,
                                         quake_dtype dtype, quake_mode mode, float t, int causal,
                                         void* stream) {
-  if (dtype != QUAKE_BF16) return QUAKE_EDTYPE;
+  if (dtype != QUAKE_BF16 && dtype != QUAKE_F16) return QUAKE_EDTYPE;
   if (!valid_mode(mode)) return QUAKE_EMODE;
   if (heads < 0 || seq < 0 || dim != kAttnD || seq > kAttnLongMaxS) return QUAKE_EINVAL;
   if (ldv < seq || ldv > INT32_MAX) return QUAKE_EINVAL;
@@ -558,11 +588,9 @@ extern "C" quake_status quake_attention(const void* q, const void* k, const void
   const bool vec = aligned16(vt) && ldv % 8 == 0;
   const int vk = !vec ? kVtScalar : (seq % 32 == 0 ? kVtFull : kVtRagged);
   const bool one_pass = seq <= kAttnMaxS;
-  switch (mode) {
-    case QUAKE_EXACT: launch_attn<EXACT>(vk, one_pass, grid, s, g); break;
-    case QUAKE_1: launch_attn<Q1>(vk, one_pass, grid, s, g); break;
-    case QUAKE_2: launch_attn<Q2>(vk, one_pass, grid, s, g); break;
-    default: launch_attn<Q2M>(vk, one_pass, grid, s, g); break;
-  }
+  if (dtype == QUAKE_BF16)
+    launch_attn<BF16>(mode, vk, one_pass, grid, s, g);
+  else
+    launch_attn<F16>(mode, vk, one_pass, grid, s, g);
   return launch_status();
 }

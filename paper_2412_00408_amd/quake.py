@@ -211,10 +211,10 @@ def _vt_row_stride(shape, strides) -> int:
 
 
 def quake_attention(q, k, vt, o=None, mode=QUAKE_2, t=None, causal=True, stream=None):
-    """softmax(t q k^T) v per head with Algorithm 2's softmax: bfloat16 q, k
-    [..., seq, 64] and vt = v transposed [..., 64, seq] (or a view of wider,
-    padded rows with a contiguous last dimension); returns
-    bfloat16 o [..., seq, 64]. t defaults to 1/sqrt(64)."""
+    """softmax(t q k^T) v per head with Algorithm 2's softmax: bfloat16 or
+    float16 q, k [..., seq, 64] and vt = v transposed [..., 64, seq] (or a view
+    of wider, padded rows with a contiguous last dimension); returns o
+    [..., seq, 64] in the same format. t defaults to 1/sqrt(64)."""
     for a, what in ((q, "q"), (k, "k"), (vt, "vt")):
         if not a.is_cuda:
             raise ValueError("libquake takes device tensors")
@@ -224,6 +224,8 @@ def quake_attention(q, k, vt, o=None, mode=QUAKE_2, t=None, causal=True, stream=
             raise ValueError("%s needs [..., rows, cols]" % what)
     if not (q.is_contiguous() and k.is_contiguous()) or q.shape != k.shape:
         raise ValueError("q and k must be contiguous and of the same shape")
+    if k.dtype != q.dtype or vt.dtype != q.dtype:
+        raise TypeError("q, k and vt must have the same dtype")
     seq, dim = q.shape[-2], q.shape[-1]
     heads = q.numel() // max(seq * dim, 1)
     if tuple(vt.shape[:-2]) != tuple(q.shape[:-2]) or tuple(vt.shape[-2:]) != (dim, seq):

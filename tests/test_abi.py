@@ -171,7 +171,7 @@ def test_attention_validation(q):
         return L.quake_attention(qp, kp, vp, op, h, s, d, ldv, dt, mode, t, 1, None)
     assert call(h=0) == q.OK and call(s=0, ldv=0) == q.OK
     assert call(h=0, qp=None, kp=None, vp=None, op=None) == q.OK
-    assert call(dt=0) == q.EDTYPE and call(dt=1) == q.EDTYPE
+    assert call(dt=0) == q.EDTYPE and call(dt=3) == q.EDTYPE   # binary32, unknown
     assert call(mode=9) == q.EMODE
     assert call(d=128) == q.EINVAL                         # head dimension 64 only
     assert call(s=131073, ldv=131080) == q.EINVAL          # longer than 131072

@@ -41,27 +41,29 @@ def q():
     return quake
 
 
-def _ulp_bf16(v):
+def _ulp(v, dt="bf16"):
     a = np.abs(v)
     e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
-    return np.where(a >= 2.0 ** -126, np.ldexp(1.0, (e - 7).astype(int)), 2.0 ** -133)
+    if dt == "bf16":
+        return np.where(a >= 2.0 ** -126, np.ldexp(1.0, (e - 7).astype(int)), 2.0 ** -133)
+    return np.where(a >= 2.0 ** -14, np.ldexp(1.0, (e - 10).astype(int)), 2.0 ** -24)
 
 
-def _dec(b):
-    return oracle.decode(np.ascontiguousarray(b).reshape(-1), "bf16").astype(np.float64).reshape(b.shape)
+def _dec(b, dt="bf16"):
+    return oracle.decode(np.ascontiguousarray(b).reshape(-1), dt).astype(np.float64).reshape(b.shape)
 
 
-def _bound(qb, kb, vtb, seq, causal, ref):
+def _bound(qb, kb, vtb, seq, causal, ref, dt="bf16"):
     out = np.empty(ref.shape)
     for h0 in range(0, ref.shape[0], 4):
         sl = slice(h0, h0 + 4)
-        out[sl] = _bound_heads(qb[sl], kb[sl], vtb[sl], seq, causal, ref[sl])
+        out[sl] = _bound_heads(qb[sl], kb[sl], vtb[sl], seq, causal, ref[sl], dt)
     return out
 
 
-def _bound_heads(qb, kb, vtb, seq, causal, ref):
-    qd, kd = _dec(qb), _dec(kb)
-    vd = _dec(vtb)[:, :, :seq]
+def _bound_heads(qb, kb, vtb, seq, causal, ref, dt):
+    qd, kd = _dec(qb, dt), _dec(kb, dt)
+    vd = _dec(vtb, dt)[:, :, :seq]
     sc = np.matmul(qd, np.transpose(kd, (0, 2, 1)))
     sa = np.matmul(np.abs(qd), np.transpose(np.abs(kd), (0, 2, 1)))
     if causal:
@@ -72,15 +74,22 @@ def _bound_heads(qb, kb, vtb, seq, causal, ref):
     rp = 3 * T * ds_max + 2.0 ** -22
     p = np.exp(T * (sc - sc.max(axis=2, keepdims=True)))
     pv = 1.1 * np.matmul(p, np.transpose(np.abs(vd), (0, 2, 1))) / p.sum(axis=2, keepdims=True)
-    return _ulp_bf16(ref) + (2.0 ** -7 + 2.2 * rp + (seq + 4) * 2.0 ** -24) * pv
+    if dt == "bf16":
+        return _ulp(ref, dt) + (2.0 ** -7 + 2.2 * rp + (seq + 4) * 2.0 ** -24) * pv
+    # binary16: a probability flip is one binary16 ulp (2^-10 relative, or
+    # 2^-24 absolute for subnormal probabilities), on any key
+    allowed = np.ones((seq, seq)) if not causal else np.tril(np.ones((seq, seq)))
+    sv = np.matmul(allowed[None], np.transpose(np.abs(vd), (0, 2, 1))) / p.sum(axis=2, keepdims=True)
+    return (_ulp(ref, dt) + (2.0 ** -10 + 2.2 * rp + (seq + 4) * 2.0 ** -24) * pv
+            + 2.0 ** -24 * sv)
 
 
-def _run(q, heads, seq, mode, causal, seed, ldv=None, pad=0.0):
-    say("attention heads=%d seq=%d ldv=%s mode=%d causal=%d seed=%d" % (heads, seq, ldv, mode,
-                                                                          causal, seed))
-    qc, kc, vtc = synth.attention_inputs(heads, seq, seed, ldv=ldv, pad=pad)
+def _run(q, heads, seq, mode, causal, seed, ldv=None, pad=0.0, dt="bf16"):
+    say("attention %s heads=%d seq=%d ldv=%s mode=%d causal=%d seed=%d" % (
+        dt, heads, seq, ldv, mode, causal, seed))
+    qc, kc, vtc = synth.attention_inputs(heads, seq, seed, ldv=ldv, pad=pad, dt=dt)
     qg, kg, vtg = qc.to("cuda:0"), kc.to("cuda:0"), vtc.to("cuda:0")
-    o = torch.full((heads, seq, 64), float("nan"), dtype=torch.bfloat16, device="cuda:0")
+    o = torch.full((heads, seq, 64), float("nan"), dtype=qc.dtype, device="cuda:0")
     if ldv is not None and ldv != seq:
         vt_view = vtg[:, :, :seq]
     else:
@@ -88,21 +97,21 @@ def _run(q, heads, seq, mode, causal, seed, ldv=None, pad=0.0):
     q.quake_attention(qg, kg, vt_view, o, mode=mode, t=T, causal=causal)
     torch.cuda.synchronize()
     qb, kb, vtb = host_bits(qc), host_bits(kc), host_bits(vtc)
-    ref = oracle.attention(qb, kb, vtb, mode, T, causal, threads=THREADS)
+    ref = oracle.attention(qb, kb, vtb, mode, T, causal, threads=THREADS, dt=dt)
     return host_bits(o), ref, (qb, kb, vtb)
 
 
-def _check(g_bits, r_bits, ins, seq, causal, name):
-    g, r = _dec(g_bits), _dec(r_bits)
+def _check(g_bits, r_bits, ins, seq, causal, name, dt="bf16"):
+    g, r = _dec(g_bits, dt), _dec(r_bits, dt)
     assert not np.isnan(g).any(), "%s: unwritten or NaN outputs" % name
-    bound = _bound(*ins, seq, causal, r)
+    bound = _bound(*ins, seq, causal, r, dt)
     err = np.abs(g - r)
     bad = ~(err <= bound)
     i = int(np.argmax((err - bound).reshape(-1)))
     assert not bad.any(), "%s: %d of %d outside the bound, worst at %d: gpu %r ref %r bound %r" % (
         name, int(bad.sum()), bad.size, i, g.reshape(-1)[i], r.reshape(-1)[i], bound.reshape(-1)[i])
-    within1 = np.mean(err <= _ulp_bf16(r))
-    assert within1 >= 0.99, "%s: only %.4f within one bfloat16 ulp" % (name, within1)
+    within1 = np.mean(err <= _ulp(r, dt))
+    assert within1 >= 0.99, "%s: only %.4f within one ulp" % (name, within1)
     return err
 
 
@@ -131,6 +140,19 @@ def test_long_sequences_match_oracle(q, mode, causal, heads, seq):
 def test_long_sequence_padded_vt_element_rows(q, causal):
     g, r, ins = _run(q, 1, 777, 2, causal, 71, ldv=781, pad=float("nan"))
     _check(g, r, ins, 777, causal, "long padded")
+
+
+@pytest.mark.parametrize("mode", [0, 1, 2, 3])
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("heads,seq", [(2, 64), (3, 40), (1, 512), (2, 1000)])
+def test_binary16_matches_oracle(q, mode, causal, heads, seq):
+    g, r, ins = _run(q, heads, seq, mode, causal, 80 + seq, dt="f16")
+    _check(g, r, ins, seq, causal, "f16 h%d s%d m%d c%d" % (heads, seq, mode, causal), "f16")
+
+
+def test_binary16_full_workload(q):
+    g, r, ins = _run(q, 96, 512, 2, True, 81, dt="f16")
+    _check(g, r, ins, 512, True, "f16 full", "f16")
 
 
 @pytest.mark.parametrize("mode", [0, 2])
