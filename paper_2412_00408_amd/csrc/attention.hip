@@ -1,27 +1,30 @@
 // attention.hip — quake_attention: O = softmax(t Q K^T) V per head (optionally
-// causal), with the softmax of Algorithm 2 (arXiv:2412.00408, Sec. III-C) taken
-// against each query's final row max. All scores of a query are in registers
-// before any exponential is taken, so there is no online rescaling: QuAKE is
-// not multiplicative (Q(a) Q(b) != Q(a + b)), and a flash-style running max
-// would change the results Algorithm 2 defines.
+// causal), bfloat16 or binary16, with the softmax of Algorithm 2
+// (arXiv:2412.00408, Sec. III-C) taken against each query's final row max.
+// Every exponential of a query waits for the max of its whole row, so there is
+// no online rescaling: QuAKE is not multiplicative (Q(a) Q(b) != Q(a + b)), and
+// a flash-style running max would change the results Algorithm 2 defines. Up
+// to 512 keys the scores of a query stay in registers (attn_kernel); longer
+// sequences compute them twice, once for the max and once for the
+// exponentials (attn_long_kernel).
 //
 // One workgroup = 32 queries of one head, four waves; wave w takes the 32-key
-// blocks w, w + 4, w + 8, w + 12 (interleaved, so causal work stays balanced).
+// blocks w, w + 4, w + 8, ... (interleaved, so causal work stays balanced).
 // The scores are computed transposed, S^T = K Q^T, on the matrix cores
-// (v_mfma_f32_32x32x16_bf16; A = 32 keys x 16 dims of K, staged through LDS as
-// described below, B = the 32 queries' dims read straight from Q's rows), so
-// that lane l holds one query (l mod 32) and keys 8 g + 4 (l / 32) + i,
-// g, i < 4, of each block:
+// (v_mfma_f32_32x32x16_bf16 / _f16; A = 32 keys x 16 dims of K, staged through
+// LDS as described below, B = the 32 queries' dims read straight from Q's
+// rows), so that lane l holds one query (l mod 32) and keys
+// 8 g + 4 (l / 32) + i, g, i < 4, of each block:
 //   * the row max and the row sum reduce the lane's own values, exchange once
 //     with lane l xor 32 (v_permlane32_swap) and once across waves through LDS;
-//   * the exponentials, rounded to bfloat16, become the B operand of the second
-//     product O^T = V^T P after one v_permlane32_swap per dword pair (lane
-//     l < 32 takes keys 4-7 from its partner and gives it keys 8-11), without a
-//     trip through LDS. V is passed transposed ([head, dim, key]), so the A
-//     operand (32 dims x 16 keys) is 16 contiguous bytes of a row of V^T.
+//   * the exponentials, rounded to the 16-bit format, become the B operand of
+//     the second product O^T = V^T P after one v_permlane32_swap per dword pair
+//     (lane l < 32 takes keys 4-7 from its partner and gives it keys 8-11),
+//     without a trip through LDS. V is passed transposed ([head, dim, key]), so
+//     the A operand (32 dims x 16 keys) is 16 contiguous bytes of a row of V^T.
 // Causal key blocks above a query block's diagonal are neither loaded nor
 // multiplied. The four partial O^T meet in LDS; wave w adds up, normalises by
-// 1 / sum and stores one quarter of the 32 x 64 output tile as bfloat16.
+// 1 / sum and stores one quarter of the 32 x 64 output tile.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -37,20 +40,20 @@ typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kAttnD = 64;                     // head dimension
-constexpr int kAttnMaxS = 512;         // longest sequence of the one-pass kernel: 16 key blocks
-constexpr int kAttnLongMaxS = 131072;  // longest sequence (two-pass kernel)
-constexpr int kAttnQ = 32;                     // queries per workgroup
+constexpr int kAttnD = 64;              // head dimension
+constexpr int kAttnMaxS = 512;          // longest sequence of the one-pass kernel: 16 key blocks
+constexpr int kAttnLongMaxS = 131072;   // longest sequence (two-pass kernel)
+constexpr int kAttnQ = 32;              // queries per workgroup
 constexpr int kAttnWaves = 4;
 constexpr int kAttnThreads = 64 * kAttnWaves;
-constexpr int kAttnBlk = kAttnMaxS / 32 / kAttnWaves;   // key blocks per wave
+constexpr int kAttnBlk = kAttnMaxS / 32 / kAttnWaves;   // key blocks per wave, one pass
 
 struct AttnArgs {
   const uint16_t* q;
   const uint16_t* k;
   const uint16_t* vt;
   uint16_t* o;
-  int32_t s;         // sequence length, 1 .. 512
+  int32_t s;         // sequence length, 1 .. 131072
   int32_t ldv;       // row stride of V^T in elements, >= s
   int32_t qblocks;   // ceil(s / 32)
   float c0;          // Algorithm 2: 2^23 t / ln2 (EXACT: t / ln2)
