@@ -204,3 +204,25 @@ def test_bad_arguments_raise(q):
     with pytest.raises(q.QuakeError):                     # longer than 131072 keys
         q.quake_attention(big, big, torch.zeros((1, 64, 131073), dtype=torch.bfloat16,
                                                 device="cuda:0"))
+
+
+def test_two_streams_at_once(q):
+    """Two launches in flight on two streams (no shared state in the kernel)."""
+    a = [x.to("cuda:0") for x in synth.attention_inputs(8, 512, 90)]
+    b = [x.to("cuda:0") for x in synth.attention_inputs(16, 256, 91)]
+    ref_a = q.quake_attention(*a, mode=2, t=T)
+    ref_b = q.quake_attention(*b, mode=1, t=T, causal=False)
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    s1.wait_stream(torch.cuda.current_stream())
+    s2.wait_stream(torch.cuda.current_stream())
+    outs_a, outs_b = [], []
+    for _ in range(4):
+        with torch.cuda.stream(s1):
+            outs_a.append(q.quake_attention(*a, mode=2, t=T))
+        with torch.cuda.stream(s2):
+            outs_b.append(q.quake_attention(*b, mode=1, t=T, causal=False))
+    torch.cuda.synchronize()
+    for oa, ob in zip(outs_a, outs_b):
+        assert torch.equal(oa.view(torch.int16), ref_a.view(torch.int16))
+        assert torch.equal(ob.view(torch.int16), ref_b.view(torch.int16))
