@@ -420,6 +420,33 @@ def linear_gelu(q, synth, a):
     return out
 
 
+def torch_sdpa_ms(sets, vs, causal, t, n):
+    """ms per call of torch.nn.functional.scaled_dot_product_attention on the
+    given (q, k, v^T, o) sets (v passed as vs, [heads, seq, d]) with only the
+    flash and memory-efficient backends allowed (no fallback to the math
+    path), launched eagerly back to back; None where neither is available."""
+    import torch
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    try:
+        with sdpa_kernel([SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION]):
+            def f(i):
+                qg, kg, _, _ = sets[i % len(sets)]
+                return torch.nn.functional.scaled_dot_product_attention(
+                    qg[None], kg[None], vs[i % len(vs)][None], is_causal=bool(causal), scale=t)
+            for i in range(10):
+                f(i)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for i in range(n):
+                f(i)
+            e1.record()
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / n
+    except RuntimeError:
+        return None
+
+
 def fused_attention(q, synth, a, heads=96, seq=512):
     """softmax(t q k^T) v over the attention workload's heads (8 x 12 heads,
     512 tokens, head dimension 64, bf16, t = 1/8; or another heads x seq) in one kernel
@@ -430,7 +457,10 @@ def fused_attention(q, synth, a, heads=96, seq=512):
     once; useful flops: 4 d per (query, live key) pair. The fused launches are
     captured in a HIP graph over 12 rotating operand sets (about 300 MB, more
     than the Infinity Cache holds) and replayed; the explicit path is captured
-    the same way over two sets."""
+    the same way over two sets. For context, torch's own fused attention
+    (scaled_dot_product_attention restricted to its flash / memory-efficient
+    kernels, exact exponential, so other numbers) is timed over the same 12
+    rotating sets with eager launches."""
     import torch
     d, t, nb = 64, 0.125, 12
     sets = []
@@ -450,6 +480,7 @@ def fused_attention(q, synth, a, heads=96, seq=512):
     probs = torch.empty_like(scores)
     kts = [kk.transpose(1, 2).contiguous() for _, kk, _, _ in sets[:2]]
     vs = [vt.transpose(1, 2).contiguous() for _, _, vt, _ in sets[:2]]
+    vs_all = vs + [vt.transpose(1, 2).contiguous() for _, _, vt, _ in sets[2:]]
     for causal, name in ((1, "causal"), (0, "noncausal")):
         r = {}
         for mname, mid in MODE_IDS.items():
@@ -474,6 +505,7 @@ def fused_attention(q, synth, a, heads=96, seq=512):
                 raise RuntimeError(q.status_str(rc))
             torch.bmm(probs, vs[i], out=og)
         ms_ex = graph_ms(explicit, 2, 100)
+        ms_sdpa = torch_sdpa_ms(sets, vs_all, causal, t, max(24, reps // 10))
         ms = r["quake2"]
         out[name] = {
             "fused_ms": {m: round(v, 6) for m, v in r.items()},
@@ -485,8 +517,10 @@ def fused_attention(q, synth, a, heads=96, seq=512):
             "quake2_frac_of_bf16_peak": round(flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
             "explicit_quake2_ms": round(ms_ex, 6),
             "fused_speedup_vs_explicit": round(ms_ex / ms, 3),
+            "torch_sdpa_ms": None if ms_sdpa is None else round(ms_sdpa, 6),
+            "fused_speedup_vs_torch_sdpa": None if ms_sdpa is None else round(ms_sdpa / ms, 3),
         }
-    del sets, scores, probs, kts, vs
+    del sets, scores, probs, kts, vs, vs_all
     return out
 
 
@@ -611,6 +645,7 @@ def main():
             torch.cuda.synchronize()
             del qg, kg, vg
         print(json.dumps({"attention_bf16_96x512x64": fused_attention(q, synth, a),
+                          "attention_bf16_64x1024x64": fused_attention(q, synth, a, 64, 1024),
                           "attention_bf16_32x2048x64": fused_attention(q, synth, a, 32, 2048)}),
               flush=True)
         return
@@ -697,6 +732,7 @@ def main():
         sec["exp_f16_2p28"] = native16(q, synth, a)
         sec["linear_gelu_bf16_4096x3072x768"] = linear_gelu(q, synth, a)
         sec["attention_bf16_96x512x64"] = fused_attention(q, synth, a)
+        sec["attention_bf16_64x1024x64"] = fused_attention(q, synth, a, 64, 1024)
         sec["attention_bf16_32x2048x64"] = fused_attention(q, synth, a, 32, 2048)
         imp = implicit_causal(q, synth, a)
         imp["no_masked_writes"]["speedup_vs_explicit_mask_input"] = round(

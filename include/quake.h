@@ -257,10 +257,11 @@ quake_status quake_linear_gelu(const void* x, const void* w, void* y, int64_t m,
  *          16-byte vectors, else element by element.
  *   o    : device, [heads, seq, dim] 16-bit, contiguous, 8-byte aligned; it
  *          must not overlap q, k or vt (other workgroups still read them).
- *   dim == 64 and seq <= 131072. Up to 512 keys a query's scores stay in
- *   registers (one pass); longer sequences take two passes over the keys
+ *   dim == 64 and seq <= 131072. Up to 1024 keys a query's scores stay in
+ *   registers (one pass: 32 queries per workgroup of four waves up to 512
+ *   keys, eight waves beyond); longer sequences take two passes over the keys
  *   (the scores once for the row max, then again for the exponentials and the
- *   second product), with results identical to what one pass would give;
+ *   second product), with the same arithmetic as one pass of four waves;
  *   t > 0 finite (1/sqrt(dim) for the usual scaling); causal != 0 lets query
  *   i use keys j <= i only (masked keys are neither loaded nor multiplied).
  *   dtype : QUAKE_BF16 or QUAKE_F16, the format of q, k, vt and o (else

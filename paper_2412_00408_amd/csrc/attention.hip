@@ -4,12 +4,12 @@
 // Every exponential of a query waits for the max of its whole row, so there is
 // no online rescaling: QuAKE is not multiplicative (Q(a) Q(b) != Q(a + b)), and
 // a flash-style running max would change the results Algorithm 2 defines. Up
-// to 512 keys the scores of a query stay in registers (attn_kernel); longer
-// sequences compute them twice, once for the max and once for the
-// exponentials (attn_long_kernel).
+// to 1024 keys the scores of a query stay in registers (attn_kernel, four
+// waves up to 512 keys, eight beyond); longer sequences compute them twice,
+// once for the max and once for the exponentials (attn_long_kernel).
 //
-// One workgroup = 32 queries of one head, four waves; wave w takes the 32-key
-// blocks w, w + 4, w + 8, ... (interleaved, so causal work stays balanced).
+// One workgroup = 32 queries of one head, W waves; wave w takes the 32-key
+// blocks w, w + W, w + 2 W, ... (interleaved, so causal work stays balanced).
 // The scores are computed transposed, S^T = K Q^T, on the matrix cores
 // (v_mfma_f32_32x32x16_bf16 / _f16; A = 32 keys x 16 dims of K, staged through
 // LDS as described below, B = the 32 queries' dims read straight from Q's
@@ -23,8 +23,8 @@
 //     without a trip through LDS. V is passed transposed ([head, dim, key]), so
 //     the A operand (32 dims x 16 keys) is 16 contiguous bytes of a row of V^T.
 // Causal key blocks above a query block's diagonal are neither loaded nor
-// multiplied. The four partial O^T meet in LDS; wave w adds up, normalises by
-// 1 / sum and stores one quarter of the 32 x 64 output tile.
+// multiplied. The W partial O^T meet in LDS; each wave adds up, normalises by
+// 1 / sum and stores 1 / W of the 32 x 64 output tile.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -41,12 +41,13 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kAttnD = 64;              // head dimension
-constexpr int kAttnMaxS = 512;          // longest sequence of the one-pass kernel: 16 key blocks
+constexpr int kAttnBlk = 4;             // key blocks of 32 per wave, one pass
+constexpr int kAttnMaxWaves = 8;        // waves of the largest one-pass workgroup
+constexpr int kAttnMaxS = 32 * kAttnBlk * kAttnMaxWaves;   // longest one-pass sequence: 1024
 constexpr int kAttnLongMaxS = 131072;   // longest sequence (two-pass kernel)
 constexpr int kAttnQ = 32;              // queries per workgroup
-constexpr int kAttnWaves = 4;
+constexpr int kAttnWaves = 4;           // waves of the two-pass workgroup
 constexpr int kAttnThreads = 64 * kAttnWaves;
-constexpr int kAttnBlk = kAttnMaxS / 32 / kAttnWaves;   // key blocks per wave, one pass
 
 struct AttnArgs {
   const uint16_t* q;
@@ -104,14 +105,26 @@ __device__ __forceinline__ float xor32(float v) {
 // K block: 32 keys x 128 B. Slot of (row r, chunk c): 8 r + (c ^ fk(r)) with
 // fk(r) = (r mod 8) ^ ((r / 8) mod 2).
 // Load j of 4 covers rows 8 j .. 8 j + 7; lane l takes row 8 j + l / 8,
-// chunk l mod 8. Rows past s are clamped to row s - 1 (their scores are
-// masked afterwards).
+// chunk l mod 8, at byte koff = 128 (l / 8) + 16 (l mod 8) + 1024 j from the
+// block's first row (a uniform base, so only koff lives in a vector register).
+// In a block that reaches past s, rows past s are clamped to row s - 1 (their
+// scores are masked afterwards).
+__device__ __forceinline__ uint32_t kblock_lane_offset(int lane) {
+  return (uint32_t)(128 * (lane >> 3) + 16 * (lane & 7));
+}
 __device__ __forceinline__ void kblock_load(const uint16_t* k, int kbase, int s, int lane,
-                                            u32x4_t (&g)[4]) {
+                                            uint32_t koff, u32x4_t (&g)[4]) {
+  if (kbase + 32 <= s) {
+    const char* base = reinterpret_cast<const char*>(k + (int64_t)kbase * kAttnD);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int row = min(kbase + 8 * j + (lane >> 3), s - 1);
-    g[j] = ld16(k + (int64_t)row * kAttnD + 8 * (lane & 7));
+    for (int j = 0; j < 4; ++j)
+      g[j] = *reinterpret_cast<const u32x4_t*>(base + koff + 1024 * j);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int row = min(kbase + 8 * j + (lane >> 3), s - 1);
+      g[j] = ld16(k + (int64_t)row * kAttnD + 8 * (lane & 7));
+    }
   }
 }
 __device__ __forceinline__ int kswz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
@@ -135,23 +148,34 @@ __device__ __forceinline__ void kblock_read(const u32x4_t* buf, int fr, int h, u
 enum VtKind { kVtFull = 0, kVtRagged = 1, kVtScalar = 2 };
 
 // V^T block: 64 dims x 32 keys (64 B). Slot of (row d, chunk c):
-// 4 d + (c ^ fv(d)) with fv(d) = ((d / 2) ^ (d / 4)) mod 4. Load j of 4 covers rows 16 j .. 16 j + 15; lane l
-// takes row 16 j + l / 4, keys kbase + 8 (l mod 4) .. + 7. In a block that
-// reaches past s (`tail`, uniform) keys at or past s read as zero without
-// leaving the row: their probabilities are zero, and the padding of the row
-// may hold anything.
+// 4 d + (c ^ fv(d)) with fv(d) = ((d / 2) ^ (d / 4)) mod 4. Load j of 4 covers
+// rows 16 j .. 16 j + 15; lane l takes row 16 j + l / 4, keys kbase + 8 (l mod 4)
+// .. + 7, at byte voff[j] = 2 ((16 j + l / 4) ldv + 8 (l mod 4)) from key
+// kbase of row 0 (a uniform base). In a block that reaches past s (`tail`,
+// uniform) keys at or past s read as zero without leaving the row: their
+// probabilities are zero, and the padding of the row may hold anything.
+__device__ __forceinline__ void vblock_lane_offsets(int lane, int ldv, uint32_t (&voff)[4]) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    voff[j] = 2u * ((uint32_t)(16 * j + (lane >> 2)) * (uint32_t)ldv + 8u * (uint32_t)(lane & 3));
+}
 template <int VK>
 __device__ __forceinline__ void vblock_load(const uint16_t* vt, int ldv, int kbase, int s,
-                                            bool tail, int lane, u32x4_t (&g)[4]) {
+                                            bool tail, int lane, const uint32_t (&voff)[4],
+                                            u32x4_t (&g)[4]) {
+  if (VK != kVtScalar && !tail) {
+    const char* base = reinterpret_cast<const char*>(vt + kbase);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) g[j] = *reinterpret_cast<const u32x4_t*>(base + voff[j]);
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const uint16_t* row = vt + (int64_t)(16 * j + (lane >> 2)) * ldv;
     const int key0 = kbase + 8 * (lane & 3);
     u32x4_t v;
-    if constexpr (VK == kVtFull) {
-      v = ld16(row + key0);
-    } else if constexpr (VK == kVtRagged) {
-      const int nv = tail ? s - key0 : 8;
+    if constexpr (VK != kVtScalar) {
+      const int nv = s - key0;
       v = ld16(row + (nv > 0 ? key0 : 0));
 #pragma unroll
       for (int i = 0; i < 4; ++i)
@@ -189,12 +213,77 @@ __device__ __forceinline__ void vblock_read(const u32x4_t* buf, int fr, int h,
     }
 }
 
-template <int DT, int MODE, int VK>
-__global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
-  __shared__ float s_max[kAttnWaves][kAttnQ];
-  __shared__ float s_sum[kAttnWaves][kAttnQ];
+// Sum of the N values v[LO .. LO + N) in a fixed pairwise order:
+// ((v0 + v1) + (v2 + v3)) + ...
+template <int LO, int N, int TOTAL>
+__device__ __forceinline__ float tree_sum(const float (&v)[TOTAL]) {
+  if constexpr (N == 1)
+    return v[LO];
+  else
+    return tree_sum<LO, N / 2, TOTAL>(v) + tree_sum<LO + N / 2, N / 2, TOTAL>(v);
+}
+
+// End of a tile of W waves: the row sum over the waves, the W partial O^T
+// through LDS (each wave's own 8 KB region, its staging reads done), and the
+// output. Accumulator register r of oacc[db] in lane l holds dim
+// 32 db + 8 (r / 4) + 4 (l / 32) + r mod 4 of query l mod 32; call j = 16 db + r
+// its row. Wave w adds rows R w .. R w + R - 1 (R = 32 / W) over the waves in
+// a fixed order, normalises them by 1 / sum and stores them, four consecutive
+// dims (8 bytes) at a time.
+template <int DT, int W>
+__device__ __forceinline__ void attn_finish(u32x4_t (*s_buf)[512], float (*s_sum)[kAttnQ],
+                                            const f32x16_t (&oacc)[2], float part, float m,
+                                            int wave, int lane, int query, int S,
+                                            uint16_t* orow) {
+  constexpr int R = 32 / W;
+  static_assert(W == 4 || W == 8, "four or eight waves");
+  part += xor32(part);
+  if (lane < 32) s_sum[wave][lane] = part;
+  __builtin_amdgcn_wave_barrier();
+  float* po = reinterpret_cast<float*>(s_buf[wave]);
+#pragma unroll
+  for (int db = 0; db < 2; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) po[(db * 16 + r) * 64 + lane] = oacc[db][r];
+  __syncthreads();
+  if (query >= S) return;
+  const int fr = lane & 31;
+  float sums[W];
+#pragma unroll
+  for (int w = 0; w < W; ++w) sums[w] = s_sum[w][fr];
+  const float total = tree_sum<0, W, W>(sums);
+  const float inv = (m == -INFINITY || !(total > 0.0f)) ? 0.0f : 1.0f / total;
+  float v[R];
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const int idx = (R * wave + i) * 64 + lane;
+    float parts[W];
+#pragma unroll
+    for (int w = 0; w < W; ++w) parts[w] = reinterpret_cast<const float*>(s_buf[w])[idx];
+    v[i] = tree_sum<0, W, W>(parts) * inv;
+  }
+  // row R wave + i: db = that / 16, r = that mod 16; four dims per store
+#pragma unroll
+  for (int i = 0; i < R; i += 4) {
+    const int j = R * wave + i, db = j >> 4, r = j & 15;
+    uint2 w2;
+    w2.x = pack16<DT>(v[i], v[i + 1]);
+    w2.y = pack16<DT>(v[i + 2], v[i + 3]);
+    *reinterpret_cast<uint2*>(orow + 32 * db + 8 * (r >> 2) + 4 * (lane >> 5)) = w2;
+  }
+}
+
+// One pass, up to 128 W keys (W = 4 or 8 waves): every score of the tile
+// stays in registers, four key blocks per wave at most. With 8 waves (513 to
+// 1024 keys) two workgroups share a CU (66 KB of LDS each); a 16-wave
+// workgroup (one per CU) for 2048 keys was measured slower than two passes
+// with the mask and no faster without it.
+template <int DT, int MODE, int VK, int W>
+__global__ __launch_bounds__(64 * W, W == 4 ? 4 : 1) void attn_kernel(AttnArgs g) {
+  __shared__ float s_max[W][kAttnQ];
+  __shared__ float s_sum[W][kAttnQ];
   // per wave: operand staging (4 KB), then its partial O^T (8 KB)
-  __shared__ u32x4_t s_buf[kAttnWaves][512];
+  __shared__ u32x4_t s_buf[W][512];
 
   const int lane = threadIdx.x & 63;
   // uniform across the wave: every condition below that depends on it is a
@@ -219,8 +308,8 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
   const int q0 = qb * kAttnQ;
   const int kblocks = (S + 31) >> 5;
   const int nkb = g.causal ? min(kblocks, qb + 1) : kblocks;   // live key blocks of the tile
-  // this wave's blocks are w, w + 4, ...: the first nlive of them are live
-  const int nlive = max(0, (nkb - wave + kAttnWaves - 1) / kAttnWaves);
+  // this wave's blocks are w, w + W, ...: the first nlive of them are live
+  const int nlive = max(0, (nkb - wave + W - 1) / W);
   const int fr = lane & 31, fk = 8 * (lane >> 5);
   const int query = q0 + fr;
   const uint16_t* Q = g.q + (int64_t)bh * S * kAttnD;
@@ -236,16 +325,19 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
   }
   u32x4_t* stage = s_buf[wave];
   const int h = lane >> 5;
+  const uint32_t koff = kblock_lane_offset(lane);
+  uint32_t voff[4];
+  vblock_lane_offsets(lane, g.ldv, voff);
   u32x4_t gk[4];
-  if (nlive > 0) kblock_load(K, 32 * wave, S, lane, gk);
+  if (nlive > 0) kblock_load(K, 32 * wave, S, lane, koff, gk);
   f32x16_t sacc[kAttnBlk];
   float m = -INFINITY;
 #pragma unroll
   for (int i = 0; i < kAttnBlk; ++i) {
     if (i < nlive) {
-      const int kbg = kAttnWaves * i + wave;
+      const int kbg = W * i + wave;
       kblock_store(stage, lane, gk);
-      if (i + 1 < nlive) kblock_load(K, 32 * (kbg + kAttnWaves), S, lane, gk);
+      if (i + 1 < nlive) kblock_load(K, 32 * (kbg + W), S, lane, koff, gk);
       __builtin_amdgcn_wave_barrier();   // lanes read what other lanes wrote
       u32x4_t ka[4];
       kblock_read(stage, fr, h, ka);
@@ -270,29 +362,27 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
   // the first block of V^T in flight across the reductions
   u32x4_t gv[4];
   if (nlive > 0)
-    vblock_load<VK>(Vt, g.ldv, 32 * wave, S, VK != kVtFull && 32 * wave + 32 > S, lane, gv);
+    vblock_load<VK>(Vt, g.ldv, 32 * wave, S, VK != kVtFull && 32 * wave + 32 > S, lane, voff, gv);
 
   // row (query) max: the lane's own values, lane l xor 32, the other waves
   m = fmaxf(m, xor32(m));
   if (lane < 32) s_max[wave][lane] = m;
   __syncthreads();
-  m = fmaxf(fmaxf(s_max[0][fr], s_max[1][fr]), fmaxf(s_max[2][fr], s_max[3][fr]));
+  m = s_max[0][fr];
+#pragma unroll
+  for (int w = 1; w < W; ++w) m = fmaxf(m, s_max[w][fr]);
 
-  // Algorithm 2: exponentials against the row max (c1 folds it in), their
-  // sum; the probabilities rounded to bfloat16 pairs (keys 8 gi + 4 (lane / 32)
-  // + 0..3 of each block) are consumed by the second product of the same
-  // block right away, so one block's exponentials (VALU) overlap the previous
-  // block's matrix-core work
+  // Algorithm 2: exponentials against the row max (c1 folds it in) and their
+  // sum, every block's before the second product, so that the binary32
+  // scores are dead before its accumulators and operands are live; the
+  // probabilities rounded to 16-bit pairs (keys 8 gi + 4 (lane / 32) + 0..3 of
+  // each block)
   const float c1 = (m == -INFINITY) ? 0.0f : __builtin_fmaf(-g.c0, m, MODE == EXACT ? 0.0f : kK127);
   float part = 0.0f;
-
-  // O^T = V^T P over this wave's live keys, the next block's V in flight
-  f32x16_t oacc[2] = {};
+  uint32_t pk[kAttnBlk][4][2];
 #pragma unroll
   for (int i = 0; i < kAttnBlk; ++i) {
     if (i < nlive) {
-      const int kbg = kAttnWaves * i + wave;
-      uint32_t pk[4][2];
 #pragma unroll
       for (int gi = 0; gi < 4; ++gi) {
         float e[4];
@@ -301,13 +391,22 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
           e[j] = qexp<MODE>(sacc[i][4 * gi + j], g.c0, c1);
           part += e[j];
         }
-        pk[gi][0] = pack16<DT>(e[0], e[1]);
-        pk[gi][1] = pack16<DT>(e[2], e[3]);
+        pk[i][gi][0] = pack16<DT>(e[0], e[1]);
+        pk[i][gi][1] = pack16<DT>(e[2], e[3]);
       }
+    }
+  }
+
+  // O^T = V^T P over this wave's live keys, the next block's V in flight
+  f32x16_t oacc[2] = {};
+#pragma unroll
+  for (int i = 0; i < kAttnBlk; ++i) {
+    if (i < nlive) {
+      const int kbg = W * i + wave;
       vblock_store(stage, lane, gv);
       if (i + 1 < nlive) {
-        const int nb = 32 * (kbg + kAttnWaves);
-        vblock_load<VK>(Vt, g.ldv, nb, S, VK != kVtFull && nb + 32 > S, lane, gv);
+        const int nb = 32 * (kbg + W);
+        vblock_load<VK>(Vt, g.ldv, nb, S, VK != kVtFull && nb + 32 > S, lane, voff, gv);
       }
       __builtin_amdgcn_wave_barrier();
       u32x4_t va[2][2];
@@ -316,10 +415,11 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         // lanes < 32 end with keys 16 ks + 0..7, lanes >= 32 with 16 ks + 8..15
-        const auto s0 = __builtin_amdgcn_permlane32_swap(pk[2 * ks][0], pk[2 * ks + 1][0], false, false);
-        const auto s1 = __builtin_amdgcn_permlane32_swap(pk[2 * ks][1], pk[2 * ks + 1][1], false, false);
+        const auto s0 = __builtin_amdgcn_permlane32_swap(pk[i][2 * ks][0], pk[i][2 * ks + 1][0],
+                                                         false, false);
+        const auto s1 = __builtin_amdgcn_permlane32_swap(pk[i][2 * ks][1], pk[i][2 * ks + 1][1],
+                                                         false, false);
         const u32x4_t bv = {s0[0], s1[0], s0[1], s1[1]};
-        
 #pragma unroll
         for (int db = 0; db < 2; ++db)
           oacc[db] = mma<DT>(va[ks][db], bv, oacc[db]);
@@ -327,44 +427,11 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_kernel(AttnArgs g) {
     }
   }
 
-  part += xor32(part);
-  if (lane < 32) s_sum[wave][lane] = part;
-
-  // the four partial O^T through LDS (each wave's own region, its staging
-  // reads done); wave w finishes dims 8 w + 4 (lane / 32) + 0..3 of both
-  // 32-dim halves
-  __builtin_amdgcn_wave_barrier();
-  float* po = reinterpret_cast<float*>(stage);
-#pragma unroll
-  for (int db = 0; db < 2; ++db)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) po[(db * 16 + r) * 64 + lane] = oacc[db][r];
-  __syncthreads();
-  if (query < S) {
-    const float total = (s_sum[0][fr] + s_sum[1][fr]) + (s_sum[2][fr] + s_sum[3][fr]);
-    const float inv = (m == -INFINITY || !(total > 0.0f)) ? 0.0f : 1.0f / total;
-    uint16_t* orow = g.o + ((int64_t)bh * S + query) * kAttnD;
-    const float* p0 = reinterpret_cast<const float*>(s_buf[0]);
-    const float* p1 = reinterpret_cast<const float*>(s_buf[1]);
-    const float* p2 = reinterpret_cast<const float*>(s_buf[2]);
-    const float* p3 = reinterpret_cast<const float*>(s_buf[3]);
-#pragma unroll
-    for (int db = 0; db < 2; ++db) {
-      float v[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int idx = (db * 16 + 4 * wave + j) * 64 + lane;
-        v[j] = ((p0[idx] + p1[idx]) + (p2[idx] + p3[idx])) * inv;
-      }
-      uint2 w;
-      w.x = pack16<DT>(v[0], v[1]);
-      w.y = pack16<DT>(v[2], v[3]);
-      *reinterpret_cast<uint2*>(orow + 32 * db + 8 * wave + 4 * (lane >> 5)) = w;
-    }
-  }
+  attn_finish<DT, W>(s_buf, s_sum, oacc, part, m, wave, lane, query, S,
+                     g.o + ((int64_t)bh * S + query) * kAttnD);
 }
 
-// Sequences longer than 512 keys: the same tiles, waves and staging, but the
+// Sequences longer than 1024 keys: the same tiles, four waves and staging, but the
 // scores are not kept. Pass 1 computes them to find each query's row max;
 // pass 2 computes them again, block by block, and takes the exponentials
 // against that max (Algorithm 2 needs the final max before any exponential),
@@ -399,6 +466,9 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_long_kernel(AttnArgs g) 
   const uint16_t* K = g.k + (int64_t)bh * S * kAttnD;
   const uint16_t* Vt = g.vt + (int64_t)bh * kAttnD * g.ldv;
   u32x4_t* stage = s_buf[wave];
+  const uint32_t koff = kblock_lane_offset(lane);
+  uint32_t voff[4];
+  vblock_lane_offsets(lane, g.ldv, voff);
 
   u32x4_t qf[4];
   {
@@ -406,10 +476,13 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_long_kernel(AttnArgs g) 
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) qf[ks] = ld16(qr + 16 * ks);
   }
-  // one block of S^T = K Q^T from the staged K block gk (masked past s and,
-  // on the diagonal, above it)
-  auto scores = [&](const u32x4_t (&gk)[4], int kbg) {
+  // One block of S^T = K Q^T (masked past s and, on the diagonal, above it):
+  // gk is written to the staging slots and then refilled with the block
+  // `next` (if any) while the scores are computed.
+  u32x4_t gk[4], gv[4];
+  auto scores = [&](int kbg, int next) {
     kblock_store(stage, lane, gk);
+    if (next >= 0) kblock_load(K, 32 * next, S, lane, koff, gk);
     __builtin_amdgcn_wave_barrier();   // lanes read what other lanes wrote
     u32x4_t ka[4];
     kblock_read(stage, fr, h, ka);
@@ -431,22 +504,17 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_long_kernel(AttnArgs g) 
   };
 
   // pass 1: the row max
-  u32x4_t gk[4], gv[4];
-  if (nlive > 0) kblock_load(K, 32 * wave, S, lane, gk);
+  if (nlive > 0) kblock_load(K, 32 * wave, S, lane, koff, gk);
   float m = -INFINITY;
   for (int i = 0; i < nlive; ++i) {
     const int kbg = kAttnWaves * i + wave;
-    u32x4_t cur[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) cur[j] = gk[j];
-    if (i + 1 < nlive) kblock_load(K, 32 * (kbg + kAttnWaves), S, lane, gk);
-    const f32x16_t sacc = scores(cur, kbg);
+    const f32x16_t sacc = scores(kbg, i + 1 < nlive ? kbg + kAttnWaves : -1);
 #pragma unroll
     for (int r = 0; r < 16; ++r) m = fmaxf(m, sacc[r]);
   }
   if (nlive > 0) {
-    kblock_load(K, 32 * wave, S, lane, gk);
-    vblock_load<VK>(Vt, g.ldv, 32 * wave, S, VK != kVtFull && 32 * wave + 32 > S, lane, gv);
+    kblock_load(K, 32 * wave, S, lane, koff, gk);
+    vblock_load<VK>(Vt, g.ldv, 32 * wave, S, VK != kVtFull && 32 * wave + 32 > S, lane, voff, gv);
   }
   m = fmaxf(m, xor32(m));
   if (lane < 32) s_max[wave][lane] = m;
@@ -459,18 +527,8 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_long_kernel(AttnArgs g) 
   f32x16_t oacc[2] = {};
   for (int i = 0; i < nlive; ++i) {
     const int kbg = kAttnWaves * i + wave;
-    const int nb = 32 * (kbg + kAttnWaves);
-    u32x4_t curk[4], curv[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      curk[j] = gk[j];
-      curv[j] = gv[j];
-    }
-    if (i + 1 < nlive) {
-      kblock_load(K, nb, S, lane, gk);
-      vblock_load<VK>(Vt, g.ldv, nb, S, VK != kVtFull && nb + 32 > S, lane, gv);
-    }
-    const f32x16_t sacc = scores(curk, kbg);
+    const int nb = kbg + kAttnWaves;
+    const f32x16_t sacc = scores(kbg, i + 1 < nlive ? nb : -1);
     uint32_t pk[4][2];
 #pragma unroll
     for (int gi = 0; gi < 4; ++gi) {
@@ -483,7 +541,9 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_long_kernel(AttnArgs g) 
       pk[gi][0] = pack16<DT>(e[0], e[1]);
       pk[gi][1] = pack16<DT>(e[2], e[3]);
     }
-    vblock_store(stage, lane, curv);
+    vblock_store(stage, lane, gv);
+    if (i + 1 < nlive)
+      vblock_load<VK>(Vt, g.ldv, 32 * nb, S, VK != kVtFull && 32 * nb + 32 > S, lane, voff, gv);
     __builtin_amdgcn_wave_barrier();
     u32x4_t va[2][2];
     vblock_read(stage, fr, h, va);
@@ -493,71 +553,44 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_long_kernel(AttnArgs g) 
       const auto s0 = __builtin_amdgcn_permlane32_swap(pk[2 * ks][0], pk[2 * ks + 1][0], false, false);
       const auto s1 = __builtin_amdgcn_permlane32_swap(pk[2 * ks][1], pk[2 * ks + 1][1], false, false);
       const u32x4_t bv = {s0[0], s1[0], s0[1], s1[1]};
-      
 #pragma unroll
       for (int db = 0; db < 2; ++db)
         oacc[db] = mma<DT>(va[ks][db], bv, oacc[db]);
     }
   }
-  part += xor32(part);
-  if (lane < 32) s_sum[wave][lane] = part;
 
-  __builtin_amdgcn_wave_barrier();
-  float* po = reinterpret_cast<float*>(stage);
-#pragma unroll
-  for (int db = 0; db < 2; ++db)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) po[(db * 16 + r) * 64 + lane] = oacc[db][r];
-  __syncthreads();
-  if (query < S) {
-    const float total = (s_sum[0][fr] + s_sum[1][fr]) + (s_sum[2][fr] + s_sum[3][fr]);
-    const float inv = (m == -INFINITY || !(total > 0.0f)) ? 0.0f : 1.0f / total;
-    uint16_t* orow = g.o + ((int64_t)bh * S + query) * kAttnD;
-    const float* p0 = reinterpret_cast<const float*>(s_buf[0]);
-    const float* p1 = reinterpret_cast<const float*>(s_buf[1]);
-    const float* p2 = reinterpret_cast<const float*>(s_buf[2]);
-    const float* p3 = reinterpret_cast<const float*>(s_buf[3]);
-#pragma unroll
-    for (int db = 0; db < 2; ++db) {
-      float v[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int idx = (db * 16 + 4 * wave + j) * 64 + lane;
-        v[j] = ((p0[idx] + p1[idx]) + (p2[idx] + p3[idx])) * inv;
-      }
-      uint2 w;
-      w.x = pack16<DT>(v[0], v[1]);
-      w.y = pack16<DT>(v[2], v[3]);
-      *reinterpret_cast<uint2*>(orow + 32 * db + 8 * wave + 4 * (lane >> 5)) = w;
-    }
-  }
+  attn_finish<DT, kAttnWaves>(s_buf, s_sum, oacc, part, m, wave, lane, query, S,
+                              g.o + ((int64_t)bh * S + query) * kAttnD);
 }
 
+// waves = 4, 8: the one-pass kernel with that many waves; 0: two passes
 template <int DT, int MODE, int VK>
-void launch_attn_vk(bool one_pass, dim3 grid, hipStream_t s, const AttnArgs& g) {
-  if (one_pass)
-    hipLaunchKernelGGL((attn_kernel<DT, MODE, VK>), grid, dim3(kAttnThreads), 0, s, g);
+void launch_attn_vk(int waves, dim3 grid, hipStream_t s, const AttnArgs& g) {
+  if (waves == 4)
+    hipLaunchKernelGGL((attn_kernel<DT, MODE, VK, 4>), grid, dim3(64 * 4), 0, s, g);
+  else if (waves == 8)
+    hipLaunchKernelGGL((attn_kernel<DT, MODE, VK, 8>), grid, dim3(64 * 8), 0, s, g);
   else
     hipLaunchKernelGGL((attn_long_kernel<DT, MODE, VK>), grid, dim3(kAttnThreads), 0, s, g);
 }
 
 template <int DT, int MODE>
-void launch_attn_mode(int vk, bool one_pass, dim3 grid, hipStream_t s, const AttnArgs& g) {
+void launch_attn_mode(int vk, int waves, dim3 grid, hipStream_t s, const AttnArgs& g) {
   if (vk == kVtFull)
-    launch_attn_vk<DT, MODE, kVtFull>(one_pass, grid, s, g);
+    launch_attn_vk<DT, MODE, kVtFull>(waves, grid, s, g);
   else if (vk == kVtRagged)
-    launch_attn_vk<DT, MODE, kVtRagged>(one_pass, grid, s, g);
+    launch_attn_vk<DT, MODE, kVtRagged>(waves, grid, s, g);
   else
-    launch_attn_vk<DT, MODE, kVtScalar>(one_pass, grid, s, g);
+    launch_attn_vk<DT, MODE, kVtScalar>(waves, grid, s, g);
 }
 
 template <int DT>
-void launch_attn(int mode, int vk, bool one_pass, dim3 grid, hipStream_t s, const AttnArgs& g) {
+void launch_attn(int mode, int vk, int waves, dim3 grid, hipStream_t s, const AttnArgs& g) {
   switch (mode) {
-    case QUAKE_EXACT: launch_attn_mode<DT, EXACT>(vk, one_pass, grid, s, g); break;
-    case QUAKE_1: launch_attn_mode<DT, Q1>(vk, one_pass, grid, s, g); break;
-    case QUAKE_2: launch_attn_mode<DT, Q2>(vk, one_pass, grid, s, g); break;
-    default: launch_attn_mode<DT, Q2M>(vk, one_pass, grid, s, g); break;
+    case QUAKE_EXACT: launch_attn_mode<DT, EXACT>(vk, waves, grid, s, g); break;
+    case QUAKE_1: launch_attn_mode<DT, Q1>(vk, waves, grid, s, g); break;
+    case QUAKE_2: launch_attn_mode<DT, Q2>(vk, waves, grid, s, g); break;
+    default: launch_attn_mode<DT, Q2M>(vk, waves, grid, s, g); break;
   }
 }
 
@@ -588,12 +621,14 @@ extern "C" quake_status quake_attention(const void* q, const void* k, const void
                    (uint32_t)(heads % 8 == 0 ? heads / 8 : 0)};
   const dim3 grid((uint32_t)(heads * qblocks));
   const hipStream_t s = static_cast<hipStream_t>(stream);
-  const bool vec = aligned16(vt) && ldv % 8 == 0;
+  // 16-byte rows, and byte offsets within a 64-row block of V^T that fit 32 bits
+  const bool vec = aligned16(vt) && ldv % 8 == 0 && ldv <= (1 << 24);
   const int vk = !vec ? kVtScalar : (seq % 32 == 0 ? kVtFull : kVtRagged);
-  const bool one_pass = seq <= kAttnMaxS;
+  // one pass with 4 key blocks per wave (128 keys), else two passes
+  const int waves = seq <= 512 ? 4 : seq <= kAttnMaxS ? 8 : 0;
   if (dtype == QUAKE_BF16)
-    launch_attn<BF16>(mode, vk, one_pass, grid, s, g);
+    launch_attn<BF16>(mode, vk, waves, grid, s, g);
   else
-    launch_attn<F16>(mode, vk, one_pass, grid, s, g);
+    launch_attn<F16>(mode, vk, waves, grid, s, g);
   return launch_status();
 }

@@ -4,8 +4,9 @@ every slot read back is the slot written for the same (row, chunk), and no
 16-byte access of the writes or the operand reads has a bank conflict, whether
 the LDS serves 8 lanes per clock over 32 four-byte banks or 16 lanes over 64;
 the probabilities reach the second product's B operand in the key order its A
-operand (V^T) uses; the tile order is a bijection onto (head, query tile); and
-the live-block count per wave matches the blocks the wave owns."""
+operand (V^T) uses; the tile order is a bijection onto (head, query tile); the
+live-block count per wave matches the blocks the wave owns (4 or 8 waves);
+and the waves' share of the output tile covers it once."""
 import itertools
 
 import pytest
@@ -112,16 +113,47 @@ def test_tile_order_is_a_bijection(heads, qblocks):
     assert len(seen) == heads * qblocks
 
 
-@pytest.mark.parametrize("seq,causal", itertools.product([1, 31, 32, 33, 200, 511, 512],
-                                                         [True, False]))
+def _waves(seq):
+    """Waves of the one-pass workgroup (four key blocks of 32 per wave), 0 for two passes."""
+    return 4 if seq <= 512 else 8 if seq <= 1024 else 0
+
+
+@pytest.mark.parametrize("seq,causal", itertools.product(
+    [1, 31, 32, 33, 200, 511, 512, 513, 1000, 1024, 1025, 2047, 2048, 2049, 3000], [True, False]))
 def test_live_blocks_per_wave(seq, causal):
     kblocks = (seq + 31) // 32
+    w_count = _waves(seq) or 4
     for qb in range((seq + 31) // 32):
         nkb = min(kblocks, qb + 1) if causal else kblocks
         owned = 0
-        for wave in range(4):
-            nlive = max(0, int((nkb - wave + 3) / 4))      # C++ division truncates toward 0
-            blocks = [4 * i + wave for i in range(4) if 4 * i + wave < nkb]
-            assert nlive == len(blocks) and blocks == [4 * i + wave for i in range(nlive)]
+        for wave in range(w_count):
+            nlive = max(0, int((nkb - wave + w_count - 1) / w_count))   # C++ division truncates
+            blocks = [w_count * i + wave for i in range(nkb) if w_count * i + wave < nkb]
+            assert nlive == len(blocks) and blocks == [w_count * i + wave for i in range(nlive)]
+            if _waves(seq):
+                assert nlive <= 4                  # the one-pass kernel holds four blocks per wave
             owned += nlive
         assert owned == nkb
+
+
+@pytest.mark.parametrize("waves", [4, 8])
+def test_output_rows_cover_the_tile_once(waves):
+    """attn_finish: wave w sums accumulator rows R w .. R w + R - 1 (R = 32 / W);
+    row j = 16 db + r of lane l is dim 32 db + 8 (r / 4) + 4 (l / 32) + r mod 4 of
+    query l mod 32; stores are runs of 4 consecutive dims, 8-byte aligned."""
+    rr = 32 // waves
+    run = 4
+    seen = set()
+    for w in range(waves):
+        for lane in range(64):
+            for i0 in range(0, rr, run):
+                dims = []
+                for i in range(i0, i0 + run):
+                    j = rr * w + i
+                    db, r = j >> 4, j & 15
+                    dims.append(32 * db + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3))
+                assert dims == list(range(dims[0], dims[0] + run))
+                assert (2 * dims[0]) % (2 * run) == 0          # byte offset in the row
+                for d in dims:
+                    seen.add((lane & 31, d))
+    assert len(seen) == 32 * 64 and seen == {(qq, d) for qq in range(32) for d in range(64)}

@@ -17,8 +17,9 @@ with pv = sum_k p_k |v_k| / sum_k p_k (textbook probabilities, times 1.1 to
 cover QuAKE's <= 3 % error). Further, at least 99 % of the elements must be
 within one bfloat16 ulp of the oracle (probability roundings rarely flip).
 Cases: every mode, causal and not, one to several 32-query tiles, a ragged
-last tile, ragged key blocks, the longest one-pass sequence (512) and longer
-ones (513 to 2048 keys, the two-pass kernel), a single key, padded v^T rows
+last tile, ragged key blocks, each one-pass workgroup size (4 waves up to 512
+keys, 8 up to 1024) with its longest sequence, longer ones (the two-pass
+kernel, from 1025 keys), a single key, padded v^T rows
 whose padding is NaN, and the full 96-head x 512 workload in the launch
 configuration the benchmark times, compared element by element."""
 import numpy as np
@@ -116,8 +117,10 @@ def _check(g_bits, r_bits, ins, seq, causal, name, dt="bf16"):
 
 
 SHAPES = [(2, 64), (3, 40), (2, 96), (1, 512), (2, 33), (5, 8)]
-# past 512 keys the two-pass kernel (scores computed twice, never stored)
-LONG_SHAPES = [(2, 513), (1, 1024), (1, 1000), (2, 2048)]
+# one pass with 8 waves (513 to 1024 keys)
+LONG_SHAPES = [(2, 513), (1, 777), (1, 1000), (2, 1024)]
+# past 1024 keys the two-pass kernel (scores computed twice, never stored)
+TWO_PASS_SHAPES = [(1, 1025), (1, 1500), (2, 2048), (1, 2049), (1, 4096)]
 
 
 @pytest.mark.parametrize("mode", [0, 1, 2, 3])
@@ -136,15 +139,26 @@ def test_long_sequences_match_oracle(q, mode, causal, heads, seq):
     _check(g, r, ins, seq, causal, "long h%d s%d m%d c%d" % (heads, seq, mode, causal))
 
 
+@pytest.mark.parametrize("mode", [0, 1, 2, 3])
 @pytest.mark.parametrize("causal", [True, False])
-def test_long_sequence_padded_vt_element_rows(q, causal):
-    g, r, ins = _run(q, 1, 777, 2, causal, 71, ldv=781, pad=float("nan"))
-    _check(g, r, ins, 777, causal, "long padded")
+@pytest.mark.parametrize("heads,seq", TWO_PASS_SHAPES)
+def test_two_pass_sequences_match_oracle(q, mode, causal, heads, seq):
+    g, r, ins = _run(q, heads, seq, mode, causal, 75 + seq)
+    _check(g, r, ins, seq, causal, "two-pass h%d s%d m%d c%d" % (heads, seq, mode, causal))
+
+
+@pytest.mark.parametrize("seq,ldv", [(777, 781), (777, 784), (1111, 1115), (2100, 2103),
+                                     (2100, 2104)])
+@pytest.mark.parametrize("causal", [True, False])
+def test_long_sequence_padded_vt_rows(q, causal, seq, ldv):
+    g, r, ins = _run(q, 1, seq, 2, causal, 71, ldv=ldv, pad=float("nan"))
+    _check(g, r, ins, seq, causal, "long padded s%d ldv%d" % (seq, ldv))
 
 
 @pytest.mark.parametrize("mode", [0, 1, 2, 3])
 @pytest.mark.parametrize("causal", [True, False])
-@pytest.mark.parametrize("heads,seq", [(2, 64), (3, 40), (1, 512), (2, 1000)])
+@pytest.mark.parametrize("heads,seq", [(2, 64), (3, 40), (1, 512), (2, 1000), (1, 1024),
+                                       (1, 2049)])
 def test_binary16_matches_oracle(q, mode, causal, heads, seq):
     g, r, ins = _run(q, heads, seq, mode, causal, 80 + seq, dt="f16")
     _check(g, r, ins, seq, causal, "f16 h%d s%d m%d c%d" % (heads, seq, mode, causal), "f16")
