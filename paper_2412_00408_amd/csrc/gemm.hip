@@ -167,15 +167,42 @@ __global__ __launch_bounds__(kGemmThreads, OCC) void gemm_kernel(GemmArgs g) {
     }
   }
 
-  // Epilogue: GELU on the binary32 accumulators, round to the 16-bit format, store.
+  // Epilogue: GELU on the binary32 accumulators, round to the 16-bit format,
+  // store. Accumulator r of block (i, j) in lane l is row
+  // 32 i + 8 (r / 4) + 4 (l / 32) + r mod 4 of the wave's rows and column
+  // 32 j + l mod 32 of its columns: for each (i, r) a half-wave stores 64
+  // contiguous bytes of one row. In a tile inside m and n (uniform) the row
+  // base of each (i, r) is uniform and the lane adds a 32-bit offset, so the
+  // stores need no per-element address arithmetic or bounds checks.
+  // the wave index made uniform here keeps the row bases of the stores in
+  // scalar registers (the main loop above is faster with its LDS fragment
+  // addresses formed per lane)
+  const int wu = __builtin_amdgcn_readfirstlane(wave);
+  const int wrow = row0 + (wu >> 1) * 64, wcol = col0 + (wu & 1) * 32 * TN;
+  if (row0 + kBM <= g.m && col0 + BN <= g.n && (int64_t)4 * g.ldy < INT32_MAX) {
+    const uint32_t lo = (uint32_t)(4 * (lane >> 5)) * (uint32_t)g.ldy + (uint32_t)fr;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        uint16_t* yr = g.y + (int64_t)(wrow + 32 * i + 8 * (r >> 2) + (r & 3)) * g.ldy + wcol;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          float v = acc[i][j][r];
+          if constexpr (GELU) v = gelu_q<MODE>(v, g.c0, g.c1, g.a);
+          yr[lo + 32 * j] = narrow16<DT>(v);
+        }
+      }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-      const int col = col0 + wn * 32 * TN + 32 * j + fr;
+      const int col = wcol + 32 * j + fr;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int row = row0 + wm * 64 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const int row = wrow + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
         float v = acc[i][j][r];
         if constexpr (GELU) v = gelu_q<MODE>(v, g.c0, g.c1, g.a);
         if (row < g.m && col < g.n)

@@ -182,6 +182,25 @@ def test_padded_vt_rows_with_nan_padding(q, causal, ldv):
     _check(g, r, ins, 200, causal, "padded")
 
 
+@pytest.mark.parametrize("seq", [64, 40])                  # whole key blocks; a ragged last one
+@pytest.mark.parametrize("ldv", [1 << 24, (1 << 24) + 8])   # rows read as 16-byte vectors with
+def test_vt_row_stride_at_the_lane_offset_limit(q, ldv, seq):  # the largest 32-bit lane offsets; past it
+    """v^T rows 2^24 elements apart (2 GiB per head), NaN in the padding: the
+    widest stride whose byte offsets within a 64-row block fit 32 bits, and the
+    next one, which takes the element-wise path."""
+    qc, kc, vtc = synth.attention_inputs(1, seq, 67 + seq)
+    say("attention bf16 heads=1 seq=%d ldv=%d (2 GiB v^T)" % (seq, ldv))
+    big = torch.full((1, 64, ldv), float("nan"), dtype=torch.bfloat16, device="cuda:0")
+    big[:, :, :seq] = vtc.to("cuda:0")
+    o = q.quake_attention(qc.to("cuda:0"), kc.to("cuda:0"), big[:, :, :seq], mode=2, t=T,
+                          causal=True)
+    torch.cuda.synchronize()
+    del big
+    ins = (host_bits(qc), host_bits(kc), host_bits(vtc))
+    ref = oracle.attention(*ins, 2, T, True, threads=THREADS)
+    _check(host_bits(o.cpu()), ref, ins, seq, True, "ldv %d seq %d" % (ldv, seq))
+
+
 def test_full_workload_causal_quake2(q):
     """96 heads x 512 keys, the configuration the benchmark times."""
     g, r, ins = _run(q, 96, 512, 2, True, 63)

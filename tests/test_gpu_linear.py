@@ -84,6 +84,29 @@ def test_strided_rows(q):
     _check(g, r, xb, wb, 768, 2.0, "strided")
 
 
+# output views of a wider buffer: (column offset, row stride) with 8-byte
+# aligned rows (vector stores) and without (element stores)
+@pytest.mark.parametrize("off,ldy", [(0, 200), (4, 196), (1, 200), (2, 194)])
+@pytest.mark.parametrize("n", [192, 130])
+def test_output_views_keep_their_padding(q, off, ldy, n):
+    m, k = 130, 72
+    say("linear gelu into a view: n %d offset %d ldy %d" % (n, off, ldy))
+    x = synth.normal((m, k), 1.0, "bf16", 1750)
+    w = synth.normal((n, k), 0.05, "bf16", 1751)
+    big = torch.full((m, ldy), 0x7FC1, dtype=torch.int16, device="cuda:0")   # a NaN pattern
+    y = big.view(torch.bfloat16)[:, off:off + n]
+    q.quake_linear_gelu(x.to("cuda:0"), w.to("cuda:0"), y=y, mode=2)
+    torch.cuda.synchronize()
+    got = big.cpu().numpy().view(np.uint16)
+    keep = np.ones(ldy, bool)
+    keep[off:off + n] = False
+    assert (got[:, keep] == 0x7FC1).all(), "writes outside the view"
+    xb, wb = host_bits(x), host_bits(w)
+    ref = oracle.linear_gelu(xb, wb, 2, gelu=True, dt="bf16", threads=THREADS)
+    _check(np.ascontiguousarray(got[:, off:off + n]), ref, xb, wb, k, 2.0,
+           "view n %d off %d ldy %d" % (n, off, ldy))
+
+
 @pytest.mark.parametrize("mode,dt", [(0, "bf16"), (2, "bf16"), (2, "f16")])
 def test_bert_mlp_shape(q, mode, dt):
     """The up-projection of a BERT-base MLP over 4096 tokens, [4096, 768] x [3072, 768]^T,
