@@ -32,6 +32,10 @@ def _ops(q, bufs):
     q.quake_linear_gelu(bufs["lin_x"], bufs["lin_w"], bufs["lin_y"], mode=2)   # matrix cores
     q.quake_attention(bufs["att_q"], bufs["att_k"], bufs["att_vt"], bufs["att_y"], mode=2,
                       t=0.125, causal=True)                                    # fused attention
+    q.quake_attention(bufs["att8_q"], bufs["att8_k"], bufs["att8_vt"], bufs["att8_y"], mode=2,
+                      t=0.125, causal=False)                                   # eight waves
+    q.quake_attention(bufs["att2p_q"], bufs["att2p_k"], bufs["att2p_vt"], bufs["att2p_y"],
+                      mode=2, t=0.125, causal=True)                            # two passes
 
 
 def _bufs():
@@ -45,13 +49,16 @@ def _bufs():
     b["e16_x"] = synth.WORKLOADS["sigmoid_f16_2p28"].make(n=1 << 20).to("cuda:0")
     b["lin_x"] = synth.normal((256, 768), 1.0, "bf16", 1201).to("cuda:0")
     b["lin_w"] = synth.normal((512, 768), 0.05, "bf16", 1202).to("cuda:0")
-    qa, ka, va = synth.attention_inputs(4, 512, 1203)
-    b["att_q"], b["att_k"], b["att_vt"] = qa.to("cuda:0"), ka.to("cuda:0"), va.to("cuda:0")
+    for name, heads, seq, seed in (("att", 4, 512, 1203), ("att8", 2, 700, 1204),
+                                   ("att2p", 1, 1100, 1205)):
+        qa, ka, va = synth.attention_inputs(heads, seq, seed)
+        b[name + "_q"], b[name + "_k"], b[name + "_vt"] = (qa.to("cuda:0"), ka.to("cuda:0"),
+                                                           va.to("cuda:0"))
+        b[name + "_y"] = torch.empty_like(b[name + "_q"])
     for k in ("gelu", "sig", "attn", "lm", "gen", "e16"):
         b[k + "_y"] = torch.empty_like(b[k + "_x"])
     b["causal_y"] = torch.empty_like(b["attn_x"])
     b["lin_y"] = torch.empty((256, 512), dtype=torch.bfloat16, device="cuda:0")
-    b["att_y"] = torch.empty_like(b["att_q"])
     return b
 
 
