@@ -676,8 +676,10 @@ def main():
     hnow = source_hash()
     tb = traffic_for(w.name + ":" + a.mode, hnow)
     line = {
-        "metric": "GB/s of algorithmic HBM traffic (input read once + output written once) and "
-                  "fraction of MI355X peak HBM bandwidth; speedup vs the exact-exp kernel",
+        # value: GB/s of algorithmic HBM traffic (input read once + output
+        # written once); roofline.frac: the fraction of the HBM peak;
+        # speedup_vs_exact: against the same kernel with the exact exponential
+        "metric": "softmax/GELU GB/s and % of HBM roofline on 1 MI355X; speedup vs exact-exp kernel",
         "value": round(head["gbps"], 2),
         "unit": "GB/s",
         "n_gpus": 1,
