@@ -286,26 +286,53 @@ def attention(q: np.ndarray, k: np.ndarray, vt: np.ndarray, mode: int, t: float,
 
 
 def _attention_heads(q, k, vt, mode, t, causal, threads, dt="bf16"):
-    """Scores: float64 products of the 16-bit inputs rounded once to
-    binary32, causal entries (key > query) set to -inf; numerators and sums as
-    softmax_numerators; the numerators rounded to the input format for the
-    second product (its operands are in that format), that product in float64,
-    divided by the float64 sum, rounded to the input format."""
+    """Every query of a few heads (see _attention_core)."""
     h, s_len, d = q.shape
-    qd = decode(np.ascontiguousarray(q).reshape(-1), dt).astype(np.float64).reshape(h, s_len, d)
+    return _attention_core(q, k, vt, np.arange(s_len), mode, t, causal, threads, dt)
+
+
+def _attention_core(q, k, vt, rows, mode, t, causal, threads, dt):
+    """Queries `rows` (their indices in the sequence; q holds those queries
+    only) against all keys. Scores: float64 products of the 16-bit inputs
+    rounded once to binary32, causal entries (key > query) set to -inf;
+    numerators and sums as softmax_numerators; the numerators rounded to the
+    input format for the second product (its operands are in that format),
+    that product in float64, divided by the float64 sum, rounded to the input
+    format."""
+    h, nr, d = q.shape
+    s_len = k.shape[1]
+    qd = decode(np.ascontiguousarray(q).reshape(-1), dt).astype(np.float64).reshape(h, nr, d)
     kd = decode(np.ascontiguousarray(k).reshape(-1), dt).astype(np.float64).reshape(h, s_len, d)
     vd = decode(np.ascontiguousarray(vt[:, :, :s_len]).reshape(-1), dt).astype(
         np.float64).reshape(h, d, s_len)
     scores = np.matmul(qd, np.transpose(kd, (0, 2, 1))).astype(np.float32)
     if causal:
-        mask = np.arange(s_len)[None, :] > np.arange(s_len)[:, None]
+        mask = np.arange(s_len)[None, :] > np.asarray(rows)[:, None]
         scores[:, mask] = -np.inf
-    p, sums = softmax_numerators(scores.reshape(h * s_len, s_len), mode, t, threads)
+    p, sums = softmax_numerators(scores.reshape(h * nr, s_len), mode, t, threads)
     pb = decode(round_to(p.astype(np.float64).reshape(-1), dt), dt).astype(np.float64)
-    o = np.matmul(pb.reshape(h, s_len, s_len), np.transpose(vd, (0, 2, 1)))
+    o = np.matmul(pb.reshape(h, nr, s_len), np.transpose(vd, (0, 2, 1)))
     with np.errstate(invalid="ignore", divide="ignore"):
-        o = np.where(sums.reshape(h, s_len, 1) > 0, o / sums.reshape(h, s_len, 1), 0.0)
-    return round_to(o.reshape(-1), dt).reshape(h, s_len, d)
+        o = np.where(sums.reshape(h, nr, 1) > 0, o / sums.reshape(h, nr, 1), 0.0)
+    return round_to(o.reshape(-1), dt).reshape(h, nr, d)
+
+
+def attention_rows(q: np.ndarray, k: np.ndarray, vt: np.ndarray, rows, mode: int, t: float,
+                   causal: bool = True, threads: int = 1, dt: str = "bf16") -> np.ndarray:
+    """The outputs of `attention` for the queries `rows` only ([h, len(rows),
+    d]): each query against all keys of its head (the causal mask at its own
+    index), so sequences too long for the whole score matrix can be checked
+    on sampled queries."""
+    rows = np.asarray(rows, np.int64)
+    h, s_len, d = q.shape
+    if rows.size and (rows.min() < 0 or rows.max() >= s_len):
+        raise ValueError("query index out of range")
+    out = np.empty((h, rows.size, d), np.uint16)
+    for h0 in range(0, h, 4):
+        sl = slice(h0, h0 + 4)
+        out[sl] = _attention_core(q[sl][:, rows], k[sl], vt[sl], rows, mode, t, causal, threads,
+                                  dt)
+    return out
 
 
 def linear_gelu(x: np.ndarray, w: np.ndarray, mode: int, gelu: bool = True, dt: str = "bf16",

@@ -85,6 +85,43 @@ def _bound_heads(qb, kb, vtb, seq, causal, ref, dt):
             + 2.0 ** -24 * sv)
 
 
+def _bound_rows(qb, kb, vtb, rows, causal, ref, dt="bf16"):
+    """_bound_heads for the queries `rows` only (one head at a time is enough
+    for the long sequences this serves)."""
+    seq = kb.shape[1]
+    rows = np.asarray(rows)
+    qd, kd = _dec(np.ascontiguousarray(qb[:, rows]), dt), _dec(kb, dt)
+    vd = _dec(vtb, dt)[:, :, :seq]
+    sc = np.matmul(qd, np.transpose(kd, (0, 2, 1)))
+    sa = np.matmul(np.abs(qd), np.transpose(np.abs(kd), (0, 2, 1)))
+    allowed = np.ones((rows.size, seq), bool)
+    if causal:
+        allowed = np.arange(seq)[None, :] <= rows[:, None]
+        sc[:, ~allowed] = -np.inf
+        sa[:, ~allowed] = 0.0
+    ds_max = 65 * 2.0 ** -24 * sa.max(axis=2, keepdims=True)
+    rp = 3 * T * ds_max + 2.0 ** -22
+    p = np.exp(T * (sc - sc.max(axis=2, keepdims=True)))
+    pv = 1.1 * np.matmul(p, np.transpose(np.abs(vd), (0, 2, 1))) / p.sum(axis=2, keepdims=True)
+    if dt == "bf16":
+        return _ulp(ref, dt) + (2.0 ** -7 + 2.2 * rp + (seq + 4) * 2.0 ** -24) * pv
+    sv = np.matmul(allowed[None].astype(np.float64), np.transpose(np.abs(vd), (0, 2, 1))) / \
+        p.sum(axis=2, keepdims=True)
+    return (_ulp(ref, dt) + (2.0 ** -10 + 2.2 * rp + (seq + 4) * 2.0 ** -24) * pv
+            + 2.0 ** -24 * sv)
+
+
+def _check_against(g_bits, r_bits, bound, name, dt="bf16"):
+    g, r = _dec(g_bits, dt), _dec(r_bits, dt)
+    assert not np.isnan(g).any(), "%s: unwritten or NaN outputs" % name
+    err = np.abs(g - r)
+    bad = ~(err <= bound)
+    i = int(np.argmax((err - bound).reshape(-1)))
+    assert not bad.any(), "%s: %d of %d outside the bound, worst at %d: gpu %r ref %r bound %r" % (
+        name, int(bad.sum()), bad.size, i, g.reshape(-1)[i], r.reshape(-1)[i], bound.reshape(-1)[i])
+    assert np.mean(err <= _ulp(r, dt)) >= 0.99, "%s: fewer than 99 %% within one ulp" % name
+
+
 def _run(q, heads, seq, mode, causal, seed, ldv=None, pad=0.0, dt="bf16"):
     say("attention %s heads=%d seq=%d ldv=%s mode=%d causal=%d seed=%d" % (
         dt, heads, seq, ldv, mode, causal, seed))
@@ -199,6 +236,25 @@ def test_vt_row_stride_at_the_lane_offset_limit(q, ldv, seq):  # the largest 32-
     ins = (host_bits(qc), host_bits(kc), host_bits(vtc))
     ref = oracle.attention(*ins, 2, T, True, threads=THREADS)
     _check(host_bits(o.cpu()), ref, ins, seq, True, "ldv %d seq %d" % (ldv, seq))
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_longest_sequence_on_sampled_queries(q, causal):
+    """131072 keys, the longest sequence accepted (one head, QuAKE2, two
+    passes): queries across the sequence (both ends, query-tile and key-block
+    edges, the middle) against the oracle's outputs for those queries."""
+    seq = 131072
+    say("attention bf16 heads=1 seq=%d causal=%d (sampled queries)" % (seq, causal))
+    qc, kc, vtc = synth.attention_inputs(1, seq, 77)
+    o = q.quake_attention(qc.to("cuda:0"), kc.to("cuda:0"), vtc.to("cuda:0"), mode=2, t=T,
+                          causal=causal)
+    torch.cuda.synchronize()
+    rows = np.array([0, 1, 31, 32, 1023, 1024, 65535, 65536, 99999, 131039, 131040, 131071])
+    ins = (host_bits(qc), host_bits(kc), host_bits(vtc))
+    got = np.ascontiguousarray(host_bits(o.cpu())[:, rows])
+    ref = oracle.attention_rows(*ins, rows, 2, T, causal, threads=THREADS)
+    _check_against(got, ref, _bound_rows(*ins, rows, causal, _dec(ref)),
+                   "longest causal %d" % causal)
 
 
 def test_full_workload_causal_quake2(q):

@@ -141,21 +141,21 @@ MUTANTS = {
     "probabilities_always_bfloat16": (
         'pb = decode(round_to(p.astype(np.float64).reshape(-1), dt), dt).astype(np.float64)',
         'pb = decode(round_to(p.astype(np.float64).reshape(-1), "bf16"), "bf16").astype(np.float64)'),
-    "causal_mask_includes_diagonal": ("np.arange(s_len)[None, :] > np.arange(s_len)[:, None]",
-                                      "np.arange(s_len)[None, :] >= np.arange(s_len)[:, None]"),
-    "v_not_transposed": ("o = np.matmul(pb.reshape(h, s_len, s_len), np.transpose(vd, (0, 2, 1)))",
-                         "o = np.matmul(pb.reshape(h, s_len, s_len), vd.reshape(h, s_len, d))"),
+    "causal_mask_includes_diagonal": ("np.arange(s_len)[None, :] > np.asarray(rows)[:, None]",
+                                      "np.arange(s_len)[None, :] >= np.asarray(rows)[:, None]"),
+    "v_not_transposed": ("o = np.matmul(pb.reshape(h, nr, s_len), np.transpose(vd, (0, 2, 1)))",
+                         "o = np.matmul(pb.reshape(h, nr, s_len), vd.reshape(h, s_len, d))"),
     "keys_transposed_as_queries": ("scores = np.matmul(qd, np.transpose(kd, (0, 2, 1)))",
                                    "scores = np.matmul(kd, np.transpose(qd, (0, 2, 1)))"),
-    "no_normalisation": ("o = np.where(sums.reshape(h, s_len, 1) > 0, o / sums.reshape(h, s_len, 1), 0.0)",
-                         "o = np.where(sums.reshape(h, s_len, 1) > 0, o, 0.0)"),
+    "no_normalisation": ("o = np.where(sums.reshape(h, nr, 1) > 0, o / sums.reshape(h, nr, 1), 0.0)",
+                         "o = np.where(sums.reshape(h, nr, 1) > 0, o, 0.0)"),
 }
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
 def test_pins_catch_attention_mutant(oracle, name):
-    src = textwrap.dedent(inspect.getsource(oracle.attention)) + "\n" + textwrap.dedent(
-        inspect.getsource(oracle._attention_heads))
+    src = "\n".join(textwrap.dedent(inspect.getsource(f)) for f in (
+        oracle.attention, oracle._attention_heads, oracle._attention_core))
     old, new = MUTANTS[name]
     assert old in src, name
     ns = dict(vars(oracle))
@@ -172,3 +172,23 @@ def test_pins_catch_attention_mutant(oracle, name):
         ref, pv, sv = _textbook(q, k, vt, 0.125, causal, dt)
         caught.append(not np.all(np.abs(o - ref) <= _bound(ref, pv, sv, dt, 0.0)))
     assert any(caught), name
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+@pytest.mark.parametrize("causal", [True, False])
+def test_sampled_rows_are_the_rows_of_the_full_result(oracle, causal, dt):
+    """attention_rows (queries taken one by one against all keys, the causal
+    mask at each query's own index) gives the rows of attention itself; the
+    float64 products may sum in another order, which moves a rounded output
+    by one ulp at most, and rarely."""
+    q, k, vt = _inputs(3, 200, 48, ldv=205, pad=float("nan"), dt=dt)
+    full = oracle.attention(q, k, vt, 2, 0.125, causal, dt=dt)
+    rows = [0, 1, 31, 32, 33, 100, 198, 199]
+    part = oracle.attention_rows(q, k, vt, rows, 2, 0.125, causal, dt=dt)
+    a, b = _f64(part, dt), _f64(full[:, rows], dt)
+    ulp = np.ldexp(1.0, (np.floor(np.log2(np.maximum(np.abs(b), 2.0 ** -126))) -
+                         (7 if dt == "bf16" else 10)).astype(int))
+    assert np.all(np.abs(a - b) <= ulp)
+    assert np.mean(a == b) >= 0.99
+    with pytest.raises(ValueError):
+        oracle.attention_rows(q, k, vt, [200], 2, 0.125, causal, dt=dt)
