@@ -377,8 +377,18 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
 
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
-  const uint32_t rr = blockIdx.x / G;
-  const uint32_t g = blockIdx.x - rr * G;
+  // Chunk g of row rr. blockIdx round-robins over the 8 XCDs; with the rows a
+  // multiple of 8, XCD x takes rows x, x + 8, ... with all their chunks, so a
+  // row's exchange stays among the workgroups of one XCD.
+  uint32_t rr, g;
+  if ((gridDim.x / G) % 8u == 0) {
+    const uint32_t sl = blockIdx.x >> 3;
+    rr = (blockIdx.x & 7u) + 8u * (sl / G);
+    g = sl % G;
+  } else {
+    rr = blockIdx.x / G;
+    g = blockIdx.x - rr * G;
+  }
   uint32_t* pm = ws.pmax + rr * G;
   uint64_t* ps = ws.psum + rr * G;
 
