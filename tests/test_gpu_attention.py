@@ -263,6 +263,18 @@ def test_full_workload_causal_quake2(q):
     _check(g, r, ins, 512, True, "full")
 
 
+def test_bench_config_1024_keys_causal_quake2(q):
+    """64 heads x 1024 keys, the eight-wave one-pass configuration the benchmark times."""
+    g, r, ins = _run(q, 64, 1024, 2, True, 92)
+    _check(g, r, ins, 1024, True, "64x1024 causal")
+
+
+def test_bench_config_2048_keys_noncausal_quake2(q):
+    """32 heads x 2048 keys without the mask, the two-pass configuration the benchmark times."""
+    g, r, ins = _run(q, 32, 2048, 2, False, 93)
+    _check(g, r, ins, 2048, False, "32x2048 non-causal")
+
+
 def test_full_workload_noncausal_exact(q):
     g, r, ins = _run(q, 96, 512, 0, False, 64)
     _check(g, r, ins, 512, False, "full exact")
