@@ -123,16 +123,23 @@ def prewarm(q, w, x_host, seconds, launch_kind):
     time_workload(q, w, MODE_IDS["quake2"], x_host, steps, 0, launch_kind)
 
 
-def time_workload(q, w, mode, x_host, steps, warmup, launch_kind, fused=True):
+def time_workload(q, w, mode, x_host, steps, warmup, launch_kind, fused=True, pairs=None):
+    """ms per launch over `steps` launches, nbuf per graph replay, rotating
+    over `pairs` input/output buffer pairs (default nbuf: enough for >= 1 GiB,
+    beyond the 256 MB Infinity Cache)."""
     import torch
     nbuf = min(64, max(2, math.ceil((1 << 30) / w.algo_bytes)))
+    pairs = nbuf if pairs is None else pairs
     xs, ys = [], []
     x0 = x_host.to("cuda:0")
-    for _ in range(nbuf):
+    for _ in range(pairs):
         xs.append(x0.clone())
         ys.append(torch.empty_like(x0))
     del x0
-    f = make_launcher(q, w, mode, xs, ys, fused)
+    f0 = make_launcher(q, w, mode, xs, ys, fused)
+
+    def f(i):
+        return f0(i % pairs)
     for i in range(max(warmup, nbuf)):
         rc = f(i % nbuf)
         if rc != 0:
@@ -188,9 +195,9 @@ def time_workload(q, w, mode, x_host, steps, warmup, launch_kind, fused=True):
         end.record(stream)
     torch.cuda.synchronize()
     ms = start.elapsed_time(end) / launches
-    out = ys[(launches - 1) % nbuf]
+    out = ys[(launches - 1) % pairs]
     del xs
-    return ms, launches, nbuf, kind, out
+    return ms, launches, pairs, kind, out
 
 
 # ---------------------------------------------------------------------------
@@ -743,6 +750,16 @@ def main():
         line["secondary"] = sec
     if not a.no_table4 and not a.only:
         line["table4"] = table4(q, synth, w, x_host, a)
+    if not a.only:
+        # the same kernel on one input/output pair reused launch after launch, so
+        # that the Infinity Cache (256 MB) serves much of it: context, not the metric
+        ms_w, _, _, kind_w, _ = time_workload(q, w, MODE_IDS[a.mode], x_host, a.steps, a.warmup,
+                                              a.launch, pairs=1)
+        line["mall_resident"] = {"ms_per_launch": ms_w,
+                                 "gbps": round(w.algo_bytes / (ms_w * 1e-3) / 1e9, 2),
+                                 "rotating_buffer_pairs": 1, "launch": kind_w,
+                                 "note": "one buffer pair reused (warm, MALL-resident); "
+                                         "not the metric"}
     line["kernel_source_hash"] = hnow
     print(json.dumps(line), flush=True)
 
