@@ -65,9 +65,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-table4", action="store_true",
+                    help="skip the fused-vs-unfused study (the paper's Table IV, on this GPU)")
     ap.add_argument("--mall-resident", action="store_true",
                     help="also time the headline kernel on one reused buffer pair (warm)")
-                    help="skip the fused-vs-unfused study (the paper's Table IV, on this GPU)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="also run torch copies of MIB MiB (reference kernel for counters)")
     ap.add_argument("--prewarm", type=float, default=1.0, metavar="SECONDS",
