@@ -1,7 +1,9 @@
 /*
  * Plain-C client of libquake: allocates device memory with the HIP runtime,
  * calls the C ABI declared in include/quake.h, and checks properties that hold
- * exactly or within a known bound (no Python, no torch involved).
+ * exactly or within a known bound (no Python, no torch involved): softmax rows,
+ * exact powers of two, attention of equal scores, the product with an identity
+ * matrix, and argument validation.
  *
  * Built by paper_2412_00408_amd/build.py (build_c_client) with gcc against
  * include/quake.h and the HIP runtime only; run by tests/test_gpu_c_client.py.
@@ -129,6 +131,55 @@ int main(void) {
     free(hq);
     free(hv);
     free(ho);
+  }
+
+  /* x w^T with x the identity and no GELU: each output is one product with
+     1.0 plus products with zero, so y = w^T bit for bit (128 x 192 x 128, one
+     full tile of the matrix-core kernel); with the GELU, zero weights give 0. */
+  {
+    const int64_t m = 128, k = 128, n = 192;
+    uint16_t* hx2 = (uint16_t*)calloc((size_t)(m * k), 2);
+    uint16_t* hw2 = (uint16_t*)malloc((size_t)(n * k) * 2);
+    uint16_t* hy2 = (uint16_t*)malloc((size_t)(m * n) * 2);
+    for (int64_t i = 0; i < m; ++i) hx2[i * k + i] = 0x3F80; /* bfloat16 1.0 */
+    for (int64_t r = 0; r < n; ++r)
+      for (int64_t c = 0; c < k; ++c) {
+        float f = (float)((r * 131 + c * 71) % 200 - 100) / 16.0f; /* exact in bfloat16 */
+        uint32_t b;
+        memcpy(&b, &f, 4);
+        hw2[r * k + c] = (uint16_t)(b >> 16);
+      }
+    void *dx2 = NULL, *dw2 = NULL, *dy2 = NULL;
+    HIPCHECK(hipMalloc(&dx2, (size_t)(m * k) * 2));
+    HIPCHECK(hipMalloc(&dw2, (size_t)(n * k) * 2));
+    HIPCHECK(hipMalloc(&dy2, (size_t)(m * n) * 2));
+    HIPCHECK(hipMemcpy(dx2, hx2, (size_t)(m * k) * 2, hipMemcpyHostToDevice));
+    HIPCHECK(hipMemcpy(dw2, hw2, (size_t)(n * k) * 2, hipMemcpyHostToDevice));
+    st = quake_linear_gelu(dx2, dw2, dy2, m, n, k, k, k, n, QUAKE_BF16, QUAKE_2, 0, NULL);
+    check(st == QUAKE_OK, "quake_linear_gelu returns QUAKE_OK");
+    HIPCHECK(hipDeviceSynchronize());
+    HIPCHECK(hipMemcpy(hy2, dy2, (size_t)(m * n) * 2, hipMemcpyDeviceToHost));
+    int id_ok = 1;
+    for (int64_t i = 0; i < m; ++i)
+      for (int64_t j = 0; j < n; ++j)
+        if (hy2[i * n + j] != hw2[j * k + i]) id_ok = 0;
+    check(id_ok, "identity x gives y = w^T exactly");
+    st = quake_linear_gelu(dx2, dw2, dy2, m, n, k, k, k, n, QUAKE_BF16, QUAKE_2, 1, NULL);
+    HIPCHECK(hipDeviceSynchronize());
+    HIPCHECK(hipMemcpy(hy2, dy2, (size_t)(m * n) * 2, hipMemcpyDeviceToHost));
+    int zero_ok = st == QUAKE_OK;
+    for (int64_t i = 0; i < m; ++i)
+      for (int64_t j = 0; j < n; ++j)
+        if (hw2[j * k + i] == 0 && hy2[i * n + j] != 0) zero_ok = 0;
+    check(zero_ok, "GELU of a zero product is 0");
+    check(quake_linear_gelu(dx2, dw2, dy2, m, n, 12, k, k, n, QUAKE_BF16, QUAKE_2, 1, NULL) ==
+              QUAKE_EINVAL, "linear k not a multiple of 8 rejected");
+    HIPCHECK(hipFree(dx2));
+    HIPCHECK(hipFree(dw2));
+    HIPCHECK(hipFree(dy2));
+    free(hx2);
+    free(hw2);
+    free(hy2);
   }
 
   /* argument validation happens before any HIP call */
