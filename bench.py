@@ -630,7 +630,7 @@ def traffic_for(name, hash_now):
 def main():
     a = parse()
     if a.gpus != 1:
-        print("bench.py measures one GPU only: this build's hot path runs on a single MI355X and "
+        print("bench.py measures one GPU only: libquake's hot path runs on a single MI355X and "
               "has no multi-GPU mode (asked for --gpus %d)" % a.gpus, file=sys.stderr)
         sys.exit(2)
     import torch

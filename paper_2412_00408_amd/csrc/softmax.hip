@@ -417,7 +417,7 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
     }
   }
 
-  // round 1: chunk maxima
+  // first exchange: the chunk maxima
   float m = wave_max(lmax);
   if (lane == 0) s_max[wave] = m;
   __syncthreads();
@@ -433,7 +433,7 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
   m = -INFINITY;
   for (uint32_t q = 0; q < G; ++q) m = fmaxf(m, s_pmax[q]);
 
-  // round 2: chunk sums with the row's final max
+  // second exchange: the chunk sums against the row's final max
   const RowExp<MODE, FUSE> ex = row_exp<MODE, FUSE>(kc, m);
   double acc = 0.0;
 #pragma unroll
