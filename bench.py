@@ -210,7 +210,7 @@ def copy_ceiling(w, reps):
     """A plain copy of the workload's input bytes (read numel elements, write
     numel elements: the same algorithmic bytes as the operator) with torch's
     copy kernel, over >= 1 GiB of rotating buffer pairs, graph-captured: the
-    bandwidth a kernel moving these bytes reaches on this box."""
+    bandwidth a kernel moving these bytes reaches on this machine."""
     import torch
     from paper_2412_00408_amd import synth
     nb = min(64, max(2, math.ceil((1 << 30) / w.algo_bytes)))
