@@ -22,6 +22,13 @@ MUTANTS = {
     "coefficient_a2": ("ym = fmaf(am, am, 2.0f) * third();", "ym = fmaf(am, am, 1.98f) * third();"),
     "no_schraudolph_bias": ("(mode == QO_Q1) ? 0.0436 : 0.0", "(mode == QO_Q1) ? 0.0 : 0.0"),
     "softmax_c1_sign": ("float c1 = fmaf(-c0, m, k127());", "float c1 = fmaf(c0, m, k127());"),
+    "softmax_c1_two_roundings": ("fmaf(-c0, m, k127())", "(k127() - c0 * m)"),
+    "softmax_c1_two_roundings_rows": ("float c1 = fmaf(-c0, m, k127());          /* 127*2^23 - c0*m */",
+                                      "float c1 = k127() - c0 * m;"),
+    "softmax_c1_two_roundings_causal": ("(mode == QO_EXACT) ? fmaf(-c0, m, 0.0f) : fmaf(-c0, m, k127());",
+                                        "(mode == QO_EXACT) ? fmaf(-c0, m, 0.0f) : k127() - c0 * m;"),
+    "softmax_c1_two_roundings_numerators": ("      float c1 = fmaf(-c0, m, k127());\n      for (int64_t j = 0; j < cols; ++j) {\n        pr[j]",
+                                            "      float c1 = k127() - c0 * m;\n      for (int64_t j = 0; j < cols; ++j) {\n        pr[j]"),
     "softmax_drop_last_term": ("tmp[j] = (double)quake_one(load_el(x, bx + j, dt), c0, c1, mode);\n        sum += tmp[j];",
                                "tmp[j] = (double)quake_one(load_el(x, bx + j, dt), c0, c1, mode);\n        if (j + 1 < cols) sum += tmp[j];"),
     "softmax_min_not_max": ("if (v > m) m = v;", "if (v > m || m == -INFINITY) m = (m == -INFINITY) ? v : fminf(m, v);"),

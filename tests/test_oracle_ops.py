@@ -7,10 +7,13 @@ error lies in [-0.18748 %, +0.34185 %], first order's in [-2.9777 %, +2.9881 %],
 QuAKE2 with the minimax coefficients of Eq. 6 (mode 3) in [-0.17248 %, +0.17248 %].
 """
 import math
+from fractions import Fraction
 
 import numpy as np
 import pytest
 from scipy.special import expit, softmax as sp_softmax
+
+from fp32ref import add32, bits32, f32, fma32, from_bits32, mul32, rne32
 
 LN2 = math.log(2.0)
 # max |rel err| of e, + l spacing; mode 3 is QuAKE2 with the minimax coefficients (+-0.17248 %)
@@ -108,6 +111,102 @@ def test_softmax_row_strides(oracle, dt):
     b = oracle.softmax(xs, dt, 2)
     assert np.array_equal(a[:, :40], b)
     assert np.all(a[:, 40:] == 0)
+
+
+# Reading R8: Algorithm 2 computes the row constant c1 = 127*2^23 - c0*m in
+# binary32. The oracle evaluates it as one fused multiply-add (one rounding).
+# Rows are built whose max m makes that value differ from a separate product
+# and subtraction (two roundings); the expected first-order results are then
+# evaluated exactly with IEEE-754 arithmetic written in the test.
+
+K127 = float(127 * 2 ** 23)
+
+
+def _split_c1_maxima(c0, n, seed):
+    """Binary32 row maxima in [-60, 60] for which fl(K127 - fl(c0 m)) differs
+    from the singly rounded fl(K127 - c0 m)."""
+    r = np.random.default_rng(seed)
+    out = []
+    for m in r.uniform(-60, 60, 4000).astype(np.float32):
+        m = float(m)
+        if fma32(-c0, m, K127) != add32(K127, -mul32(c0, m)):
+            out.append(m)
+        if len(out) == n:
+            break
+    assert len(out) == n
+    return out
+
+
+def _r8_rows(c0, seed, cols=24, rows=12):
+    """Rows whose first entry is the row max m (from _split_c1_maxima) and whose
+    other entries lie up to 12 below it."""
+    ms = _split_c1_maxima(c0, rows, seed)
+    r = np.random.default_rng(seed + 1)
+    x = np.empty((rows, cols), np.float32)
+    for i, m in enumerate(ms):
+        x[i, 0] = m
+        x[i, 1:] = (np.float32(m) - r.uniform(0.0, 12.0, cols - 1).astype(np.float32)).astype(np.float32)
+        assert x[i].max() == np.float32(m)
+    return x
+
+
+def _first_order_bits(row, c0):
+    """z of every entry: l = fl(x c0 + c1) with c1 = fl(K127 - c0 m), clamped to
+    [0, 255 * 2^23] and truncated (Eq. 3, recipe step a5)."""
+    m = float(row.max())
+    c1 = fma32(-c0, m, K127)
+    z = []
+    for v in row:
+        l = min(max(fma32(float(v), c0, c1), 0.0), float(255 * 2 ** 23))
+        z.append(int(l))
+    return z
+
+
+def _softmax_of_bits(z):
+    """Exact Fraction quotient z_j-as-float / sum, rounded once to binary32."""
+    y = [Fraction(from_bits32(b)) for b in z]
+    s = sum(y)
+    return [rne32(v / s) for v in y]
+
+
+@pytest.mark.parametrize("t", [1.0, 0.125])
+def test_softmax_row_c1_is_one_fused_multiply_add(oracle, t):
+    c0 = f32(2.0 ** 23 * t / LN2)
+    x = _r8_rows(c0, seed=81 + int(t * 8))
+    # numerators of Algorithm 2 (first order): the bits are z itself
+    p, _ = oracle.softmax_numerators(x, 1, t=t)
+    for i in range(x.shape[0]):
+        assert [bits32(float(v)) for v in p[i]] == _first_order_bits(x[i], c0), i
+    # the normalised rows: within one binary32 ulp of the exact quotient
+    # (the oracle sums and divides in double, then rounds once)
+    y = oracle.softmax(x, "f32", 1, t=t)
+    far = 0
+    for i in range(x.shape[0]):
+        z = _first_order_bits(x[i], c0)
+        want = _softmax_of_bits(z)
+        got = [float(v) for v in y[i]]
+        assert all(abs(bits32(g) - bits32(w)) <= 1 for g, w in zip(got, want)), i
+        # the two-rounding c1 would move this row by more than one ulp somewhere
+        m = float(x[i].max())
+        c1_two = add32(K127, -mul32(c0, m))
+        z2 = [int(min(max(fma32(float(v), c0, c1_two), 0.0), float(255 * 2 ** 23))) for v in x[i]]
+        alt = _softmax_of_bits(z2)
+        far += any(abs(bits32(a) - bits32(w)) > 1 for a, w in zip(alt, want))
+    assert far >= x.shape[0] // 2
+
+
+def test_causal_softmax_row_c1_is_one_fused_multiply_add(oracle):
+    # the implicit-mask softmax folds the max of each live prefix the same way;
+    # entry 0 holds the row max, so every prefix has it
+    c0 = f32(2.0 ** 23 / LN2)
+    x = _r8_rows(c0, seed=97, cols=12, rows=12)
+    y = oracle.softmax_causal(x, 12, 0, "f32", 1, t=1.0)
+    for i in range(12):
+        z = _first_order_bits(x[i, :i + 1], c0)
+        want = _softmax_of_bits(z)
+        got = [float(v) for v in y[i, :i + 1]]
+        assert all(abs(bits32(g) - bits32(w)) <= 1 for g, w in zip(got, want)), i
+        assert np.all(y[i, i + 1:] == 0)
 
 
 # ------------------------------ GELU ----------------------------------------
