@@ -7,15 +7,26 @@ A step is one launch of the operator over the whole workload (every step of
 the fused path: load + widen, (row max), affine map, clamp, convert, QuAKE2
 refinement, consumer, narrow + store). The default workload is the GELU of a
 BERT-base MLP activation, bf16 [4096, 3072]. Inputs are seeded synthetic data
-resident in HBM before the timed region; the timed launches rotate over
-enough input/output buffer pairs (>= 1 GiB) that the 256 MB Infinity Cache
-cannot serve them. Launch sequences are captured in a HIP graph (eager
-launches if capture is not possible) and timed with HIP events on the
-launching stream. Before the first measurement the kernel runs untimed for
---prewarm seconds (an idle MI355X takes a few hundred milliseconds to reach
-its steady clocks). The same kernel with the hardware exp2 (EXACT), with
-first-order QuAKE and with the minimax-coefficient QuAKE2 is timed in the same
-process for the speedup.
+resident in HBM before anything is timed; launch i works on buffer pair
+i mod P, with P pairs holding at least 1 GiB (more than twice the 256 MB
+Infinity Cache) where the step count allows.
+
+Timing protocol. After W untimed launches, the K launches of one timed
+region are captured in HIP graphs (a graph of min(K, 512) launches replayed
+whole, plus one graph of the remainder), so no Python or launch cost sits
+between them. One window is: synchronize; replay the K launches once untimed
+(the GPU is then busy while the host submits the timed replay); a HIP event on
+the launching stream; the K launches; an event; synchronize. ms_per_step is
+the event time over K. Several windows are timed per mode, the modes
+interleaved window by window, and each figure is the median over the windows.
+Before the first window the kernel runs untimed for --prewarm seconds (an idle
+MI355X takes a few hundred milliseconds to reach its steady clocks). The same
+kernel with the hardware exp2 (EXACT), with first-order QuAKE and with the
+minimax-coefficient QuAKE2 is timed the same way for speedup_vs_exact. With
+--trace-windows FILE the host clock readings around every window are written
+to FILE, and --summarize-trace CSV --trace-windows FILE turns a rocprofv3
+kernel trace of the same run into per-kernel medians over the timed
+dispatches only.
 
 Prints ONE JSON line. The oracle (CPU, plain C) is timed on the host cores on
 the same workload as `cpu_baseline`.
@@ -23,10 +34,12 @@ the same workload as `cpu_baseline`.
 from __future__ import annotations
 
 import argparse
+import csv
 import hashlib
 import json
 import math
 import os
+import statistics
 import sys
 import time
 
@@ -34,16 +47,24 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0       # MI355X HBM3E, AMD published peak
+PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 matrix-core peak
 MODE_IDS = {"exact": 0, "quake1": 1, "quake2": 2, "quake2m": 3}
-KERNEL_SOURCES = ["paper_2412_00408_amd/csrc/elementwise.hip",
-                  "paper_2412_00408_amd/csrc/softmax.hip",
-                  "paper_2412_00408_amd/csrc/quake_device.hpp"]
+GRAPH_MAX = 512              # launches per captured graph
+CSRC = "paper_2412_00408_amd/csrc/"
+# sources each operator's kernels are built from (a counter record is valid
+# only while they are unchanged)
+KERNEL_SOURCES = {
+    "gelu": [CSRC + "elementwise.hip", CSRC + "quake_device.hpp", CSRC + "quake_host.hpp"],
+    "sigmoid": [CSRC + "elementwise.hip", CSRC + "quake_device.hpp", CSRC + "quake_host.hpp"],
+    "silu": [CSRC + "elementwise.hip", CSRC + "quake_device.hpp", CSRC + "quake_host.hpp"],
+    "softmax": [CSRC + "softmax.hip", CSRC + "quake_device.hpp", CSRC + "quake_host.hpp"],
+}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.md")
 
 
-def source_hash() -> str:
+def source_hash(op: str) -> str:
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in KERNEL_SOURCES[op]:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -52,11 +73,12 @@ def source_hash() -> str:
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20000)
-    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=20, help="launches per timed window (K)")
+    ap.add_argument("--warmup", type=int, default=5, help="untimed launches before capture (W)")
+    ap.add_argument("--windows", type=int, default=25,
+                    help="timed windows of K launches per mode (median reported)")
     ap.add_argument("--workload", default="gelu_bf16_4096x3072")
     ap.add_argument("--mode", default="quake2", choices=sorted(MODE_IDS))
-    ap.add_argument("--launch", default="graph", choices=["graph", "eager"])
     ap.add_argument("--only", action="store_true",
                     help="time only --workload in --mode (for profiler passes)")
     ap.add_argument("--section", choices=["attention", "linear_gelu"],
@@ -74,171 +96,298 @@ def parse():
                     help="untimed back-to-back launches before the first measurement")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="CPU work (thread-seconds) spent timing the oracle")
+    ap.add_argument("--cpu-threads", type=int, default=0,
+                    help="oracle threads (default: the cores this process may run on, capped "
+                         "by OMP_NUM_THREADS when that is set)")
+    ap.add_argument("--trace-windows", metavar="FILE",
+                    help="write the host clock readings around every timed window to FILE")
+    ap.add_argument("--summarize-trace", metavar="CSV",
+                    help="print per-kernel medians over the timed dispatches of a rocprofv3 "
+                         "kernel trace (needs --trace-windows of the same run) and exit")
     return ap.parse_args()
 
 
 # ---------------------------------------------------------------------------
-# GPU side
+# Graph-timed windows
 # ---------------------------------------------------------------------------
 
-def make_launcher(q, w, mode, xs, ys, fused=True):
-    """Returns f(i) that launches the operator on buffer pair i (raw C ABI)."""
-    import torch
+def host_clocks():
+    return [time.clock_gettime_ns(time.CLOCK_BOOTTIME), time.monotonic_ns()]
+
+
+def graph_plan(steps):
+    """(launches per graph, replays of that graph, launches in the tail graph)
+    for exactly `steps` launches, every one of them inside a graph replay."""
+    ga = min(steps, GRAPH_MAX)
+    reps, rem = divmod(steps, ga)
+    return ga, reps, rem
+
+
+class GraphSeq:
+    """Exactly `steps` launches fn(0), ..., fn(steps - 1) as whole replays of
+    captured HIP graphs: a graph of min(steps, GRAPH_MAX) launches replayed
+    steps // that many times, then a graph of the remainder. fn(i, stream)
+    enqueues launch i on the raw stream handle and returns a status (0 or
+    None when fine)."""
+
+    def __init__(self, fn, steps, warmup=0):
+        import torch
+        self.steps = steps
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            for i in range(warmup):          # untimed, eager: also checks every status
+                rc = fn(i, s.cuda_stream)
+                if rc not in (0, None):
+                    raise RuntimeError("launch failed: status %s" % rc)
+        s.synchronize()
+        ga, self.reps, rem = graph_plan(steps)
+        self.graphs = [self._capture(fn, range(ga), s)]
+        self.tail = self._capture(fn, range(self.reps * ga, steps), s) if rem else None
+        torch.cuda.synchronize()
+        self.launch = ("graph: %d launches per window = %d replay(s) of a %d-launch graph%s"
+                       % (steps, self.reps, ga, " + one %d-launch graph" % rem if rem else ""))
+
+    @staticmethod
+    def _capture(fn, idx, s):
+        import torch
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            for i in idx:
+                rc = fn(i, s.cuda_stream)
+                if rc not in (0, None):
+                    raise RuntimeError("launch failed under capture: status %s" % rc)
+        return g
+
+    def replay(self):
+        for _ in range(self.reps):
+            self.graphs[0].replay()
+        if self.tail is not None:
+            self.tail.replay()
+
+
+class Timer:
+    """Windows of graph-timed launches, interleaved over several sequences;
+    keeps the host clock readings around each window for the trace summary."""
+
+    def __init__(self, windows):
+        self.windows = max(1, windows)
+        self.trace = {}
+
+    def run(self, seqs: dict, algo_bytes: dict | None = None) -> dict:
+        """seqs: label -> GraphSeq. Returns label -> list of ms per launch, one
+        per window."""
+        import torch
+        out = {k: [] for k in seqs}
+        st = torch.cuda.current_stream()
+        for _ in range(self.windows):
+            for label, sq in seqs.items():
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                torch.cuda.synchronize()
+                h0 = host_clocks()
+                sq.replay()                    # untimed: the GPU works while the timed replay is queued
+                e0.record(st)
+                sq.replay()
+                e1.record(st)
+                torch.cuda.synchronize()
+                h1 = host_clocks()
+                out[label].append(e0.elapsed_time(e1) / sq.steps)
+                rec = self.trace.setdefault(label, {"steps": sq.steps, "windows": []})
+                if algo_bytes and label in algo_bytes:
+                    rec["algo_bytes"] = algo_bytes[label]
+                rec["windows"].append(h0 + h1)
+        return out
+
+
+def med(v):
+    return statistics.median(v)
+
+
+def operand_pairs(w, steps=None):
+    """Buffer pairs: enough for >= 1 GiB of algorithmic traffic, at most 64,
+    and never more than the launches of one window use."""
+    nb = min(64, max(2, math.ceil((1 << 30) / w.algo_bytes)))
+    return nb if steps is None else max(1, min(nb, steps))
+
+
+def make_launcher(q, w, mode, xs, ys, fused=True, ws=None):
+    """f(i, stream) launching the operator on buffer pair i mod len(xs) through
+    the raw C ABI."""
     L = q.lib
     dt = q.DTYPES[xs[0].dtype]
     n = xs[0].numel()
-    stream = lambda: int(torch.cuda.current_stream().cuda_stream)  # noqa: E731
     xp = [x.data_ptr() for x in xs]
     yp = [y.data_ptr() for y in ys]
+    P = len(xs)
     if w.op == "gelu":
         g = L.quake_gelu if fused else L.quake_gelu_unfused
 
-        def f(i):
-            return g(xp[i], yp[i], n, dt, mode, stream())
+        def f(i, s):
+            return g(xp[i % P], yp[i % P], n, dt, mode, s)
     elif w.op in ("sigmoid", "silu"):
         silu = int(w.op == "silu")
 
-        def f(i):
-            return L.quake_sigmoid(xp[i], yp[i], n, dt, mode, silu, stream())
+        def f(i, s):
+            return L.quake_sigmoid(xp[i % P], yp[i % P], n, dt, mode, silu, s)
     elif w.op in ("exp", "exp16"):
         e = L.quake_exp16 if w.op == "exp16" else L.quake_exp
 
-        def f(i):
-            return e(xp[i], yp[i], n, dt, mode, 1.0, 0.0, stream())
+        def f(i, s):
+            return e(xp[i % P], yp[i % P], n, dt, mode, 1.0, 0.0, s)
     elif w.op == "softmax":
         rows, cols = w.rows, w.cols
-        sm = L.quake_softmax if fused else L.quake_softmax_unfused
+        if fused and ws is not None:
+            wp, wn = ws.data_ptr(), ws.numel()
 
-        def f(i):
-            return sm(xp[i], yp[i], rows, cols, cols, cols, dt, mode, w.t, stream())
+            def f(i, s):
+                return L.quake_softmax_ws(xp[i % P], yp[i % P], rows, cols, cols, cols, dt, mode,
+                                          w.t, wp, wn, s)
+        else:
+            sm = L.quake_softmax if fused else L.quake_softmax_unfused
+
+            def f(i, s):
+                return sm(xp[i % P], yp[i % P], rows, cols, cols, cols, dt, mode, w.t, s)
     else:
         raise KeyError(w.op)
     return f
 
 
-def prewarm(q, w, x_host, seconds, launch_kind):
-    """Untimed: run the workload's kernel back to back for about `seconds`, in
-    the same way as a measurement (rotating buffers, same launch kind), so the
-    GPU leaves its idle clock state before anything is measured (the first few
-    hundred milliseconds of work on an idle MI355X run several percent slower)."""
-    steps = max(1, int(seconds * 5e12 / w.algo_bytes))     # at about 5 TB/s
-    time_workload(q, w, MODE_IDS["quake2"], x_host, steps, 0, launch_kind)
+class Operands:
+    """P input/output buffer pairs of one workload on cuda:0 (and the split-row
+    softmax workspace where the rows need one)."""
+
+    def __init__(self, q, w, x_host, pairs, use_ws=True):
+        import torch
+        x0 = x_host.to("cuda:0")
+        self.xs = [x0.clone() for _ in range(pairs)]
+        self.ys = [torch.empty_like(x0) for _ in range(pairs)]
+        del x0
+        self.ws = q.softmax_workspace(w.rows, w.cols, self.xs[0].dtype) \
+            if (w.op == "softmax" and use_ws) else None
 
 
-def time_workload(q, w, mode, x_host, steps, warmup, launch_kind, fused=True, pairs=None):
-    """ms per launch over `steps` launches, nbuf per graph replay, rotating
-    over `pairs` input/output buffer pairs (default nbuf: enough for >= 1 GiB,
-    beyond the 256 MB Infinity Cache)."""
+def time_modes(q, timer, w, x_host, modes, steps, warmup, fused=True, pairs=None, prefix=None,
+               use_ws=True):
+    """Median ms per launch of the workload in each mode (same operands, modes
+    interleaved window by window). Returns (dict mode -> ms, launch text,
+    pairs, dict mode -> window list)."""
+    P = pairs or operand_pairs(w, steps)
+    ops = Operands(q, w, x_host, P, use_ws)
+    seqs = {}
+    for m in modes:
+        f = make_launcher(q, w, MODE_IDS[m], ops.xs, ops.ys, fused, ops.ws)
+        seqs["%s:%s" % (prefix or w.name, m)] = GraphSeq(f, steps, warmup)
+    label_bytes = {k: w.algo_bytes for k in seqs}
+    res = timer.run(seqs, label_bytes)
+    launch = next(iter(seqs.values())).launch
+    per = {k.split(":")[-1]: v for k, v in res.items()}
+    del seqs, ops
+    return {m: med(v) for m, v in per.items()}, launch, P, per
+
+
+def prewarm(q, w, x_host, seconds):
+    """Untimed: the workload's kernel back to back for about `seconds`, so the
+    GPU leaves its idle clock state before anything is measured."""
     import torch
-    nbuf = min(64, max(2, math.ceil((1 << 30) / w.algo_bytes)))
-    pairs = nbuf if pairs is None else pairs
-    xs, ys = [], []
-    x0 = x_host.to("cuda:0")
-    for _ in range(pairs):
-        xs.append(x0.clone())
-        ys.append(torch.empty_like(x0))
-    del x0
-    f0 = make_launcher(q, w, mode, xs, ys, fused)
-
-    def f(i):
-        return f0(i % pairs)
-    for i in range(max(warmup, nbuf)):
-        rc = f(i % nbuf)
-        if rc != 0:
-            raise RuntimeError("launch failed: %s" % q.status_str(rc))
+    P = operand_pairs(w)
+    ops = Operands(q, w, x_host, P)
+    f = make_launcher(q, w, MODE_IDS["quake2"], ops.xs, ops.ys, True, ops.ws)
+    sq = GraphSeq(f, P, 1)
+    reps = max(1, int(seconds * 5e12 / (w.algo_bytes * P)))    # at about 5 TB/s
+    for _ in range(reps):
+        sq.replay()
     torch.cuda.synchronize()
+    del sq, ops
 
-    kind = launch_kind
-    graph = None
-    if kind == "graph":
-        try:
-            s = torch.cuda.Stream()
-            s.wait_stream(torch.cuda.current_stream())
-            with torch.cuda.stream(s):        # per-stream workspaces exist before capture
-                for i in range(nbuf):
-                    f(i)
-            s.synchronize()
-            graph = torch.cuda.CUDAGraph()
-            with torch.cuda.stream(s):
-                with torch.cuda.graph(graph, stream=s):
-                    for i in range(nbuf):
-                        rc = f(i)
-                        if rc != 0:
-                            raise RuntimeError(q.status_str(rc))
-            torch.cuda.synchronize()
-            graph.replay()
-            torch.cuda.synchronize()
-        except Exception as e:  # cooperative launches may not be capturable
-            graph = None
-            kind = "eager (graph capture failed: %s)" % str(e).splitlines()[0][:80]
-            torch.cuda.synchronize()
 
-    stream = torch.cuda.current_stream()
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    if graph is not None:
-        # exactly `steps` launches: whole replays of the nbuf-launch graph, then
-        # the remainder launched directly on the same stream
-        reps, rem = divmod(steps, nbuf)
-        launches = steps
-        graph.replay()
-        torch.cuda.synchronize()
-        start.record(stream)
-        for _ in range(reps):
-            graph.replay()
-        for i in range(rem):
-            f(i)
-        end.record(stream)
-    else:
-        launches = steps
-        start.record(stream)
-        for i in range(steps):
-            f(i % nbuf)
-        end.record(stream)
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(end) / launches
-    out = ys[(launches - 1) % pairs]
-    del xs
-    return ms, launches, pairs, kind, out
+# ---------------------------------------------------------------------------
+# Copy ceiling: the library's own streaming copy, same bytes, same protocol
+# ---------------------------------------------------------------------------
+
+COPY_SHAPES = {0: "resident grid, 8 workgroups/CU, 2 vectors/lane/step",
+               1: "one vector per lane",
+               2: "resident grid, 4 workgroups/CU, 4 vectors/lane/step"}
+
+
+def copy_ceiling(q, timer, w, steps, warmup, name=None):
+    """quake_stream_copy moving the workload's bytes (numel elements read, numel
+    written: the operator's algorithmic bytes) in each copy shape, plus the
+    read-only and write-only halves, over the same number of rotating pairs and
+    the same graph-timed windows as the operator. The best copy shape is the
+    ceiling a kernel moving these bytes reaches on this machine."""
+    import torch
+    from paper_2412_00408_amd import synth
+    half = w.numel * synth.ELEM_BYTES[w.dt]
+    P = operand_pairs(w, steps)
+    srcs = [torch.full((half // 4,), 1.5, dtype=torch.float32, device="cuda:0") for _ in range(P)]
+    dsts = [torch.empty_like(srcs[0]) for _ in range(P)]
+    L = q.lib
+
+    def shape_fn(shape):
+        def f(i, s):
+            return L.quake_stream_copy(srcs[i % P].data_ptr(), dsts[i % P].data_ptr(), half, shape, s)
+        return f
+    label = name or w.name
+    seqs = {"copy:%s:shape%d" % (label, sh): GraphSeq(shape_fn(sh), steps, warmup)
+            for sh in (0, 1, 2, 3, 4)}
+    bytes_of = {k: (half if k.endswith(("shape3", "shape4")) else 2 * half) for k in seqs}
+    res = timer.run(seqs, bytes_of)
+    out = {"bytes": 2 * half, "rotating_buffer_pairs": P, "shapes": {}}
+    best = None
+    for k, v in res.items():
+        sh = int(k.rsplit("shape", 1)[1])
+        ms = med(v)
+        gbps = bytes_of[k] / (ms * 1e-3) / 1e9
+        key = {3: "read_only", 4: "write_only"}.get(sh, "copy_shape%d" % sh)
+        out["shapes"][key] = {"ms": round(ms, 6), "gbps": round(gbps, 2),
+                              "what": COPY_SHAPES.get(sh, key.replace("_", " ") + " (half the bytes)")}
+        if sh in COPY_SHAPES and (best is None or ms < best[1]):
+            best = (sh, ms, gbps)
+    out.update({"best_shape": best[0], "ms": round(best[1], 6), "gbps": round(best[2], 2),
+                "frac_of_peak": round(best[2] / PEAK_HBM_GBPS, 4)})
+    del seqs, srcs, dsts
+    return out
 
 
 # ---------------------------------------------------------------------------
 # CPU baseline: the oracle as it stands, on the host cores
 # ---------------------------------------------------------------------------
 
-def copy_ceiling(w, reps):
-    """A plain copy of the workload's input bytes (read numel elements, write
-    numel elements: the same algorithmic bytes as the operator) with torch's
-    copy kernel, over >= 1 GiB of rotating buffer pairs, graph-captured: the
-    bandwidth a kernel moving these bytes reaches on this machine."""
-    import torch
-    from paper_2412_00408_amd import synth
-    nb = min(64, max(2, math.ceil((1 << 30) / w.algo_bytes)))
-    n = w.numel * synth.ELEM_BYTES[w.dt] // 4
-    srcs = [torch.ones(n, dtype=torch.float32, device="cuda:0") for _ in range(nb)]
-    dsts = [torch.empty_like(srcs[0]) for _ in range(nb)]
-
-    def f(i, stream):
-        dsts[i].copy_(srcs[i])
-    ms = graph_ms(f, nb, max(10, reps // nb))
-    del srcs, dsts
-    return {"ms": ms, "gbps": round(w.algo_bytes / (ms * 1e-3) / 1e9, 2),
-            "kernel": "torch copy_ of %d bytes" % (n * 4)}
+def cpu_threads(requested: int):
+    try:
+        aff = len(os.sched_getaffinity(0))
+    except AttributeError:
+        aff = os.cpu_count() or 1
+    if requested > 0:
+        return requested, aff, "--cpu-threads %d" % requested
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    if env.isdigit() and 0 < int(env) < aff:
+        return int(env), aff, ("OMP_NUM_THREADS=%s: the CPU share this machine gives one GPU's "
+                               "jobs" % env)
+    return aff, aff, "every core in the affinity mask"
 
 
-def cpu_baseline(w, x_host, cpu_seconds):
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w, x_host, cpu_seconds, requested_threads):
     import oracle
     from paper_2412_00408_amd import synth
-    try:
-        threads = len(os.sched_getaffinity(0))
-    except AttributeError:
-        threads = os.cpu_count() or 1
-    threads = max(1, min(threads, 16))
+    threads, aff, why = cpu_threads(requested_threads)
     xb = synth.bits(x_host)
     mode = oracle.Q2
 
     def run(th, sample):
-        xs = xb[:sample] if w.op != "softmax" else xb[:sample]
+        xs = xb[:sample]
         if w.op == "gelu":
             oracle.gelu(xs, w.dt, mode, threads=th)
         elif w.op in ("sigmoid", "silu"):
@@ -246,7 +395,7 @@ def cpu_baseline(w, x_host, cpu_seconds):
         else:
             oracle.softmax(xs.reshape(-1, w.cols), w.dt, mode, t=w.t, threads=th)
 
-    # size the sample so one pass is ~0.5 s of CPU work on one thread
+    # size the sample so one pass is ~0.5 s of CPU work over all threads
     unit = w.cols if w.op == "softmax" else 1
     total_units = w.numel // unit
     probe = max(1, min(total_units, (1 << 20) // unit))
@@ -267,18 +416,9 @@ def cpu_baseline(w, x_host, cpu_seconds):
     t0 = time.perf_counter()
     run(1, sample)
     one = (2 * synth.ELEM_BYTES[w.dt] * elems) / (time.perf_counter() - t0) / 1e9
-    cpu = "unknown"
-    try:
-        with open("/proc/cpuinfo") as f:
-            for ln in f:
-                if ln.startswith("model name"):
-                    cpu = ln.split(":", 1)[1].strip()
-                    break
-    except OSError:
-        pass
     return {
         "value": round(gbps, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
-        "cpu_model": cpu,
+        "affinity_cores": aff, "threads_reason": why, "cpu_model": cpu_model(),
         "sample": "%d of %d elements of %s, quake2, %d passes over %.1f s wall" % (
             elems, w.numel, w.name, reps, wall),
         "single_thread_value": round(one, 3),
@@ -306,7 +446,7 @@ def cpu_mode_ratios(w, xb):
             (oracle.softmax if fused else oracle.softmax_unfused)(
                 xs.reshape(-1, w.cols), w.dt, mode, t=w.t, threads=1)
 
-    def med(fn):
+    def med3(fn):
         ts = []
         for _ in range(3):
             t0 = time.perf_counter()
@@ -314,18 +454,22 @@ def cpu_mode_ratios(w, xb):
             ts.append(time.perf_counter() - t0)
         return sorted(ts)[1]
 
-    t = {m: med(lambda m=m: op(MODE_IDS[m])) for m in ("exact", "quake1", "quake2", "quake2m")}
+    t = {m: med3(lambda m=m: op(MODE_IDS[m])) for m in ("exact", "quake1", "quake2", "quake2m")}
     out = {"elements": int(xs.size), "ns_per_element": {m: round(v / xs.size * 1e9, 2)
                                                        for m, v in t.items()},
            "speedup_vs_exact": {m: round(t["exact"] / v, 3) for m, v in t.items() if m != "exact"}}
     if w.op in ("gelu", "softmax"):
-        van = med(lambda: op(0, fused=False))
+        van = med3(lambda: op(0, fused=False))
         out["speedup_vs_unfused_exact"] = {m: round(van / t[m], 3)
                                            for m in ("quake1", "quake2", "quake2m")}
     return out
 
 
-def native16(q, synth, a):
+# ---------------------------------------------------------------------------
+# Secondary measurements
+# ---------------------------------------------------------------------------
+
+def native16(q, timer, synth, a):
     """e^x over 2^28 binary16 elements: the binary32 path (quake_exp: binary32
     arithmetic, result narrowed) against the construction in binary16's own
     layout (quake_exp16), QuAKE and QuAKE2; both read and write 2 bytes per
@@ -333,61 +477,35 @@ def native16(q, synth, a):
     import dataclasses
     w = synth.EXTRA_WORKLOADS["exp_f16_2p28"]
     xh = w.make()
-    steps = max(100, min(a.steps, int(1e12 / w.algo_bytes)))
+    steps = max(a.steps, operand_pairs(w))
     out = {"algo_bytes": w.algo_bytes}
     for path, wop in (("binary32_path", w), ("native16", dataclasses.replace(w, op="exp16"))):
+        ms, launch, _, _ = time_modes(q, timer, wop, xh, ("quake1", "quake2"), steps, 1,
+                                      prefix="%s_%s" % (w.name, path))
         for m in ("quake1", "quake2"):
-            ms = time_workload(q, wop, MODE_IDS[m], xh, steps, a.warmup, a.launch)[0]
-            out["%s_%s_ms" % (path, m)] = ms
-            out["%s_%s_gbps" % (path, m)] = round(w.algo_bytes / (ms * 1e-3) / 1e9, 2)
+            out["%s_%s_ms" % (path, m)] = ms[m]
+            out["%s_%s_gbps" % (path, m)] = round(w.algo_bytes / (ms[m] * 1e-3) / 1e9, 2)
+        out["launch"] = launch
     out["native16_speedup"] = {m: round(out["binary32_path_%s_ms" % m] / out["native16_%s_ms" % m], 4)
                                for m in ("quake1", "quake2")}
     return out
 
 
-PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix-core peak
+def graph_ms(timer, fns: dict, nb):
+    """Median ms per launch of each f(i, stream) in fns (i = operand set 0 ..
+    nb - 1), graph-timed windows as everywhere else."""
+    seqs = {k: GraphSeq(f, nb, 1) for k, f in fns.items()}
+    res = timer.run(seqs)
+    del seqs
+    return {k: med(v) for k, v in res.items()}
 
 
-def graph_ms(f, nb, reps):
-    """Average ms per launch of f(i, stream) for i = 0 .. nb-1 (one launch on
-    operand set i, enqueued on `stream`), captured once in a HIP graph and
-    replayed `reps` times: the Python cost of a launch stays out of the timed
-    region."""
-    import torch
-    s = torch.cuda.Stream()
-    s.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(s):
-        for i in range(nb):
-            f(i, s.cuda_stream)
-    s.synchronize()
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.stream(s):
-        with torch.cuda.graph(g, stream=s):
-            for i in range(nb):
-                rc = f(i, s.cuda_stream)
-                if rc not in (0, None):
-                    raise RuntimeError("launch failed: %d" % rc)
-    torch.cuda.synchronize()
-    g.replay()
-    torch.cuda.synchronize()
-    st = torch.cuda.current_stream()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(st)
-    for _ in range(reps):
-        g.replay()
-    e1.record(st)
-    torch.cuda.synchronize()
-    del g
-    return e0.elapsed_time(e1) / (reps * nb)
-
-
-def linear_gelu(q, synth, a):
+def linear_gelu(q, timer, synth, a):
     """GELU(x w^T) for the up-projection of a BERT-base MLP over 4096 tokens
     (x [4096, 768], w [3072, 768], bf16): the fused kernel in every mode, the
     same product without the GELU, the product followed by quake_gelu, and
     torch.matmul (the vendor BLAS) for context. Eight rotating operand sets
-    (about 290 MB) keep the timed launches out of the 256 MB Infinity Cache;
-    each variant is captured in a HIP graph over the eight sets and replayed."""
+    (about 290 MB) keep the timed launches out of the 256 MB Infinity Cache."""
     import torch
     m, n, k = 4096, 3072, 768
     nb = 8
@@ -396,7 +514,6 @@ def linear_gelu(q, synth, a):
     ys = [torch.empty((m, n), dtype=torch.bfloat16, device="cuda:0") for _ in range(nb)]
     wts = [w.t().contiguous() for w in ws]
     flop = 2.0 * m * n * k
-    reps = max(10, min(a.steps, 2000) // nb)
     L = q.lib
 
     def lin(mode, gelu):
@@ -411,66 +528,41 @@ def linear_gelu(q, synth, a):
     def vendor(i, stream):
         torch.matmul(xs[i], wts[i], out=ys[i])
 
+    fns = {"linear_gelu:fused_%s" % mn: lin(MODE_IDS[mn], 1) for mn in MODE_IDS}
+    fns.update({"linear_gelu:product_only": lin(2, 0), "linear_gelu:quake_gelu": gelu_only,
+                "linear_gelu:torch_matmul": vendor})
+    r = graph_ms(timer, fns, nb)
     out = {"shape_mnk": [m, n, k], "flop": flop, "peak_tflops": PEAK_BF16_TFLOPS,
-           "launch": "graph (%d launches per replay)" % nb}
-    for mname in ("exact", "quake1", "quake2", "quake2m"):
-        out["fused_%s_ms" % mname] = graph_ms(lin(MODE_IDS[mname], 1), nb, reps)
-    ms0 = graph_ms(lin(2, 0), nb, reps)
-    msg = graph_ms(gelu_only, nb, reps)
-    mst = graph_ms(vendor, nb, reps)
+           "launch": "graph: %d launches per window, %d windows, median" % (nb, timer.windows)}
+    for mn in MODE_IDS:
+        out["fused_%s_ms" % mn] = r["linear_gelu:fused_%s" % mn]
+    ms0, msg, mst = (r["linear_gelu:product_only"], r["linear_gelu:quake_gelu"],
+                     r["linear_gelu:torch_matmul"])
     out.update({"product_only_ms": ms0, "quake_gelu_ms": msg, "torch_matmul_ms": mst})
     out["fused_quake2_tflops"] = round(flop / (out["fused_quake2_ms"] * 1e-3) / 1e12, 1)
+    out["fused_quake2_frac_of_peak"] = round(out["fused_quake2_tflops"] / PEAK_BF16_TFLOPS, 4)
     out["product_only_tflops"] = round(flop / (ms0 * 1e-3) / 1e12, 1)
     out["product_only_frac_of_peak"] = round(out["product_only_tflops"] / PEAK_BF16_TFLOPS, 4)
     out["fused_vs_product_then_gelu"] = round((ms0 + msg) / out["fused_quake2_ms"], 4)
-    out["epilogue_ms_over_product"] = {mm: round(out["fused_%s_ms" % mm] - ms0, 5)
-                                       for mm in ("exact", "quake1", "quake2", "quake2m")}
+    out["epilogue_ms_over_product"] = {mm: round(out["fused_%s_ms" % mm] - ms0, 5) for mm in MODE_IDS}
     del xs, ws, ys, wts
     return out
 
 
-def torch_sdpa_ms(sets, vs, causal, t, n):
-    """ms per call of torch.nn.functional.scaled_dot_product_attention on the
-    given (q, k, v^T, o) sets (v passed as vs, [heads, seq, d]) with only the
-    flash and memory-efficient backends allowed (no fallback to the math
-    path), launched eagerly back to back; None where neither is available."""
-    import torch
-    from torch.nn.attention import SDPBackend, sdpa_kernel
-    try:
-        with sdpa_kernel([SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION]):
-            def f(i):
-                qg, kg, _, _ = sets[i % len(sets)]
-                return torch.nn.functional.scaled_dot_product_attention(
-                    qg[None], kg[None], vs[i % len(vs)][None], is_causal=bool(causal), scale=t)
-            for i in range(10):
-                f(i)
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            for i in range(n):
-                f(i)
-            e1.record()
-            torch.cuda.synchronize()
-            return e0.elapsed_time(e1) / n
-    except RuntimeError:
-        return None
-
-
-def fused_attention(q, synth, a, heads=96, seq=512):
+def fused_attention(q, timer, synth, a, heads=96, seq=512):
     """softmax(t q k^T) v over the attention workload's heads (8 x 12 heads,
     512 tokens, head dimension 64, bf16, t = 1/8; or another heads x seq) in one kernel
     (quake_attention), causal and not, in every mode, against the explicit
     path on the same inputs: the score product (torch.bmm, the vendor BLAS),
     quake_softmax_causal / quake_softmax over the bf16 scores, and the second
     product (torch.bmm). Algorithmic bytes: q, k and v read once, o written
-    once; useful flops: 4 d per (query, live key) pair. The fused launches are
-    captured in a HIP graph over 12 rotating operand sets (about 300 MB, more
-    than the Infinity Cache holds) and replayed; the explicit path is captured
-    the same way over two sets. For context, torch's own fused attention
-    (scaled_dot_product_attention restricted to its flash / memory-efficient
-    kernels, exact exponential, so other numbers) is timed over the same 12
-    rotating sets with eager launches."""
+    once; useful flops: 4 d per (query, live key) pair. 12 rotating operand
+    sets (about 300 MB, more than the Infinity Cache holds). For context,
+    torch's own fused attention (scaled_dot_product_attention restricted to
+    its flash / memory-efficient kernels, exact exponential, so other
+    numbers) is timed over the same sets, graph-captured like the rest."""
     import torch
+    from torch.nn.attention import SDPBackend, sdpa_kernel
     d, t, nb = 64, 0.125, 12
     sets = []
     for i in range(nb):
@@ -480,30 +572,30 @@ def fused_attention(q, synth, a, heads=96, seq=512):
     L = q.lib
     algo = 4 * heads * seq * d * 2
     pairs = {1: heads * seq * (seq + 1) // 2, 0: heads * seq * seq}
-    # about the same GPU time per configuration at every length
-    reps = max(10, min(a.steps, 20000) // nb * 512 * 512 // (seq * seq))
-
+    tag = "attention_%dx%d" % (heads, seq)
     out = {"heads": heads, "seq": seq, "head_dim": d, "t": t, "algo_bytes": algo,
-           "launch": "graph (%d launches per replay)" % nb}
+           "launch": "graph: %d launches per window, %d windows, median" % (nb, timer.windows)}
     scores = torch.empty((heads, seq, seq), dtype=torch.bfloat16, device="cuda:0")
     probs = torch.empty_like(scores)
     kts = [kk.transpose(1, 2).contiguous() for _, kk, _, _ in sets[:2]]
     vs = [vt.transpose(1, 2).contiguous() for _, _, vt, _ in sets[:2]]
     vs_all = vs + [vt.transpose(1, 2).contiguous() for _, _, vt, _ in sets[2:]]
     for causal, name in ((1, "causal"), (0, "noncausal")):
-        r = {}
+        fns = {}
         for mname, mid in MODE_IDS.items():
             def f(i, stream, mid=mid, causal=causal):
                 qg, kg, vg, og = sets[i]
                 return L.quake_attention(qg.data_ptr(), kg.data_ptr(), vg.data_ptr(),
                                          og.data_ptr(), heads, seq, d, seq, 2, mid, t, causal,
                                          stream)
-            r[mname] = graph_ms(f, nb, reps)
+            fns["%s:%s:%s" % (tag, name, mname)] = f
+        r = graph_ms(timer, fns, nb)
+        r = {k.rsplit(":", 1)[1]: v for k, v in r.items()}
         flop = 4.0 * d * pairs[causal]
 
-        def explicit(i, stream):
+        def explicit(i, stream, causal=causal):
             qg, _, _, og = sets[i]
-            torch.bmm(qg, kts[i], out=scores)
+            torch.bmm(qg, kts[i % 2], out=scores)
             if causal:
                 rc = L.quake_softmax_causal(scores.data_ptr(), probs.data_ptr(), heads * seq, seq,
                                             seq, seq, seq, 0, 1, 2, 2, t, stream)
@@ -512,9 +604,20 @@ def fused_attention(q, synth, a, heads=96, seq=512):
                                      seq, 2, 2, t, stream)
             if rc != 0:
                 raise RuntimeError(q.status_str(rc))
-            torch.bmm(probs, vs[i], out=og)
-        ms_ex = graph_ms(explicit, 2, 100)
-        ms_sdpa = torch_sdpa_ms(sets, vs_all, causal, t, max(24, reps // 10))
+            torch.bmm(probs, vs[i % 2], out=og)
+
+        def sdpa(i, stream, causal=causal):
+            qg, kg, _, _ = sets[i]
+            with sdpa_kernel([SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION]):
+                torch.nn.functional.scaled_dot_product_attention(
+                    qg[None], kg[None], vs_all[i][None], is_causal=bool(causal), scale=t)
+        ms_ex = graph_ms(timer, {"%s:%s:explicit" % (tag, name): explicit}, 2)
+        ms_ex = next(iter(ms_ex.values()))
+        try:
+            ms_sdpa = next(iter(graph_ms(timer, {"%s:%s:torch_sdpa" % (tag, name): sdpa},
+                                         nb).values()))
+        except RuntimeError:
+            ms_sdpa = None
         ms = r["quake2"]
         out[name] = {
             "fused_ms": {m: round(v, 6) for m, v in r.items()},
@@ -533,35 +636,25 @@ def fused_attention(q, synth, a, heads=96, seq=512):
     return out
 
 
-def implicit_causal(q, synth, a):
+def implicit_causal(q, timer, synth, a):
     """The attention workload with the causal mask implied (quake_softmax_causal):
     only live entries are read, so its algorithmic bytes are the live inputs
-    plus every output."""
+    plus every output (or, without masked writes, the stored vectors)."""
     import torch
     w = synth.WORKLOADS["attn_softmax_bf16_causal"]
     xh = w.make()
-    nbuf = 12
+    nbuf = operand_pairs(w)
     xs = [xh.to("cuda:0") for _ in range(nbuf)]
     ys = [torch.empty_like(xs[0]) for _ in range(nbuf)]
     L = q.lib
-    res = {}
+    fns = {}
     for mode, wm in ((0, 1), (2, 1), (2, 0)):
-        def f(i, mode=mode, wm=wm):
-            return L.quake_softmax_causal(xs[i].data_ptr(), ys[i].data_ptr(), w.rows, w.cols, w.cols,
-                                          w.cols, w.cols, 0, wm, 2, mode, w.t,
-                                          int(torch.cuda.current_stream().cuda_stream))
-        for i in range(nbuf):
-            f(i)
-        torch.cuda.synchronize()
-        st = torch.cuda.current_stream()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        steps = 960
-        e0.record(st)
-        for i in range(steps):
-            f(i % nbuf)
-        e1.record(st)
-        torch.cuda.synchronize()
-        res[(mode, wm)] = e0.elapsed_time(e1) / steps
+        def f(i, s, mode=mode, wm=wm):
+            return L.quake_softmax_causal(xs[i % nbuf].data_ptr(), ys[i % nbuf].data_ptr(), w.rows,
+                                          w.cols, w.cols, w.cols, w.cols, 0, wm, 2, mode, w.t, s)
+        fns["attn_softmax_implicit:mode%d:wm%d" % (mode, wm)] = f
+    r = graph_ms(timer, fns, max(a.steps, nbuf))
+    res = {(int(k.split(":")[1][4:]), int(k.split(":")[2][2:])): v for k, v in r.items()}
     heads = w.shape[0] * w.shape[1]
     live = heads * (w.cols * (w.cols + 1) // 2)
     algo = 2 * live + 2 * w.numel
@@ -576,26 +669,32 @@ def implicit_causal(q, synth, a):
             "no_masked_writes": {"quake2_ms": ms_nw, "algo_bytes": algo_nw,
                                  "quake2_gbps": round(algo_nw / (ms_nw * 1e-3) / 1e9, 2),
                                  "speedup_vs_explicit_mask_input": None},
-            "launch": "eager"}
+            "launch": "graph: %d launches per window, %d windows, median"
+                      % (max(a.steps, nbuf), timer.windows)}
 
 
-def table4(q, synth, w_head, x_head, a):
+def table4(q, timer, synth, a):
     """The paper's fusion study (Sec. V-A, Table IV) on this GPU: the vanilla
     operator (unfused, exact exp), QuAKE plugged in without folding, and the
     fused QuAKE operators, on the paper's op-level shapes and on two workloads
     above. Ratios are time(vanilla)/time(unfused QuAKE) ("without fusion") and
     time(unfused)/time(fused) ("additional from fusion")."""
+    import torch
     out = {}
     cases = list(synth.TABLE4_WORKLOADS.values()) + [synth.WORKLOADS["gelu_bf16_4096x3072"],
                                                      synth.WORKLOADS["attn_softmax_bf16_causal"]]
+    variants = (("vanilla", 0, False), ("unfused_quake1", 1, False), ("unfused_quake2", 2, False),
+                ("fused_exact", 0, True), ("fused_quake1", 1, True), ("fused_quake2", 2, True))
     for w in cases:
-        xh = x_head if w.name == w_head.name else w.make()
-        steps = max(50, min(a.steps, int(1e12 / w.algo_bytes)))    # about 0.2 s per variant
-        t = {}
-        for key, mode, fused in (("vanilla", 0, False), ("unfused_quake1", 1, False),
-                                 ("unfused_quake2", 2, False), ("fused_exact", 0, True),
-                                 ("fused_quake1", 1, True), ("fused_quake2", 2, True)):
-            t[key] = time_workload(q, w, mode, xh, steps, 10, a.launch, fused)[0]
+        xh = w.make()
+        steps = max(a.steps, operand_pairs(w))
+        P = operand_pairs(w, steps)
+        ops = Operands(q, w, xh, P)
+        seqs = {"table4:%s:%s" % (w.name, key): GraphSeq(
+            make_launcher(q, w, mode, ops.xs, ops.ys, fused, ops.ws), steps, 1)
+            for key, mode, fused in variants}
+        r = timer.run(seqs, {k: w.algo_bytes for k in seqs})
+        t = {k.rsplit(":", 1)[1]: med(v) for k, v in r.items()}
         out[w.name] = {
             "ms": {k: round(v, 6) for k, v in t.items()},
             "speedup_without_fusion": {"quake1": round(t["vanilla"] / t["unfused_quake1"], 4),
@@ -604,8 +703,10 @@ def table4(q, synth, w_head, x_head, a):
                 "quake1": round(t["unfused_quake1"] / t["fused_quake1"], 4),
                 "quake2": round(t["unfused_quake2"] / t["fused_quake2"], 4)},
             "fused_quake2_gbps": round(w.algo_bytes / (t["fused_quake2"] * 1e-3) / 1e9, 2),
+            "launch": next(iter(seqs.values())).launch,
         }
-        del xh
+        del seqs, ops, xh
+        torch.cuda.empty_cache()
     return out
 
 
@@ -617,26 +718,107 @@ def traffic_for(name, hash_now):
             text = f.read()
     except OSError:
         return None
-    hashes = [ln.split(":", 1)[1].strip() for ln in text.splitlines() if ln.startswith("source_hash:")]
-    if not hashes or hashes[-1] != hash_now:
-        return None
+    cur = None
     for ln in text.splitlines():
+        if ln.startswith("source_hash"):
+            cur = ln.split(":", 1)[1].strip()
+            continue
         cells = [c.strip() for c in ln.strip().strip("|").split("|")]
-        if len(cells) == 8 and cells[0] == name:
-            return int(cells[5])
+        if len(cells) >= 6 and cells[0] == name and cur == hash_now:
+            try:
+                return int(cells[5])
+            except ValueError:
+                return None
     return None
 
 
+# ---------------------------------------------------------------------------
+# Trace summary: medians over the timed dispatches of a rocprofv3 kernel trace
+# ---------------------------------------------------------------------------
+
+def summarize_trace(csv_path, windows_path):
+    """For every timed label of a run made with --trace-windows, the kernels
+    dispatched inside its windows (host clock readings taken after the
+    synchronisations that bracket each window), of which the second half in
+    each window is the timed replay (the first half is the untimed replay that
+    precedes it). Prints a Markdown table of the median, mean, minimum and
+    maximum duration over those timed dispatches."""
+    with open(windows_path) as f:
+        wins = json.load(f)
+    rows = []
+    with open(csv_path, newline="") as f:
+        for r in csv.DictReader(f):
+            name = r.get("Kernel_Name") or r.get("KernelName") or r.get("kernel_name")
+            t0 = int(r.get("Start_Timestamp") or r.get("start_timestamp") or r.get("BeginNs"))
+            t1 = int(r.get("End_Timestamp") or r.get("end_timestamp") or r.get("EndNs"))
+            rows.append((t0, t1, name))
+    rows.sort()
+    starts = [r[0] for r in rows]
+
+    def inside(a, b):
+        import bisect
+        i = bisect.bisect_left(starts, a)
+        out = []
+        while i < len(rows) and rows[i][0] <= b:
+            if rows[i][1] <= b:
+                out.append(rows[i])
+            i += 1
+        return out
+    # which host clock the trace's timestamps follow: the one that puts the
+    # most dispatches inside the windows
+    best_clock, best_n = 0, -1
+    for c in (0, 1):
+        n = sum(len(inside(w[c], w[2 + c])) for lab in wins.values() for w in lab["windows"][:3])
+        if n > best_n:
+            best_clock, best_n = c, n
+    print("| label | kernel | timed dispatches | median ns | mean ns | min ns | max ns | "
+          "GB/s at median | fraction of 8 TB/s |")
+    print("|---|---|---|---|---|---|---|---|---|")
+    all_by_name = {}
+    for r in rows:
+        all_by_name.setdefault(r[2], []).append(r[1] - r[0])
+    for label, rec in wins.items():
+        per = {}
+        for w in rec["windows"]:
+            got = inside(w[best_clock], w[2 + best_clock])
+            by = {}
+            for r in got:
+                by.setdefault(r[2], []).append(r[1] - r[0])
+            for name, d in by.items():
+                per.setdefault(name, []).extend(d[len(d) // 2:])
+        for name, d in per.items():
+            mdn = statistics.median(d)
+            ab = rec.get("algo_bytes")
+            gb = "%.1f" % (ab / mdn) if ab else "—"
+            fr = "%.4f" % (ab / mdn / PEAK_HBM_GBPS) if ab else "—"
+            print("| %s | `%s` | %d | %.1f | %.1f | %d | %d | %s | %s |" % (
+                label, name[:90], len(d), mdn, statistics.mean(d), min(d), max(d), gb, fr))
+    print()
+    print("clock: %s; all dispatches of each kernel in the trace (prewarm and warm-up "
+          "included) are not in this table." % ("CLOCK_BOOTTIME" if best_clock == 0 else
+                                                  "CLOCK_MONOTONIC"))
+
+
+# ---------------------------------------------------------------------------
+
 def main():
     a = parse()
+    if a.summarize_trace:
+        if not a.trace_windows:
+            sys.exit("--summarize-trace needs --trace-windows FILE of the same run")
+        summarize_trace(a.summarize_trace, a.trace_windows)
+        return
     if a.gpus != 1:
         print("bench.py measures one GPU only: libquake's hot path runs on a single MI355X and "
               "has no multi-GPU mode (asked for --gpus %d)" % a.gpus, file=sys.stderr)
         sys.exit(2)
+    if a.steps < 1 or a.warmup < 0:
+        sys.exit("--steps must be >= 1 and --warmup >= 0")
     import torch
     from paper_2412_00408_amd import quake as q, synth
 
     assert torch.cuda.is_available(), "bench.py needs cuda:0"
+    timer = Timer(a.windows)
     if a.calibrate_copy:
         nb = a.calibrate_copy << 20
         src = torch.empty(nb // 4, dtype=torch.float32, device="cuda:0").fill_(1.0)
@@ -653,10 +835,11 @@ def main():
                 q.quake_attention(qg, kg, vg, mode=MODE_IDS[a.mode], t=0.125)
             torch.cuda.synchronize()
             del qg, kg, vg
-        print(json.dumps({"attention_bf16_96x512x64": fused_attention(q, synth, a),
-                          "attention_bf16_64x1024x64": fused_attention(q, synth, a, 64, 1024),
-                          "attention_bf16_32x2048x64": fused_attention(q, synth, a, 32, 2048)}),
+        print(json.dumps({"attention_bf16_96x512x64": fused_attention(q, timer, synth, a),
+                          "attention_bf16_64x1024x64": fused_attention(q, timer, synth, a, 64, 1024),
+                          "attention_bf16_32x2048x64": fused_attention(q, timer, synth, a, 32, 2048)}),
               flush=True)
+        write_windows(a, timer)
         return
     if a.section == "linear_gelu":
         if a.prewarm > 0:
@@ -667,34 +850,32 @@ def main():
                 q.quake_linear_gelu(xg, wg, mode=MODE_IDS[a.mode])
             torch.cuda.synchronize()
             del xg, wg
-        print(json.dumps({"linear_gelu_bf16_4096x3072x768": linear_gelu(q, synth, a)}), flush=True)
+        print(json.dumps({"linear_gelu_bf16_4096x3072x768": linear_gelu(q, timer, synth, a)}),
+              flush=True)
+        write_windows(a, timer)
         return
     w = synth.WORKLOADS[a.workload]
     x_host = w.make()
 
     if a.prewarm > 0:
-        prewarm(q, w, x_host, a.prewarm, a.launch)
+        prewarm(q, w, x_host, a.prewarm)
     modes = [a.mode] if a.only else ["exact", "quake1", "quake2", "quake2m"]
-    res = {}
-    for m in modes:
-        ms, launches, nbuf, kind, _ = time_workload(q, w, MODE_IDS[m], x_host, a.steps, a.warmup,
-                                                    a.launch)
-        res[m] = dict(ms=ms, gbps=w.algo_bytes / (ms * 1e-3) / 1e9, launches=launches, nbuf=nbuf,
-                      launch=kind)
-    head = res[a.mode]
-    hnow = source_hash()
+    ms, launch, pairs, per = time_modes(q, timer, w, x_host, modes, a.steps, a.warmup)
+    head_ms = ms[a.mode]
+    gbps = w.algo_bytes / (head_ms * 1e-3) / 1e9
+    hnow = source_hash(w.op)
     tb = traffic_for(w.name + ":" + a.mode, hnow)
     line = {
         # value: GB/s of algorithmic HBM traffic (input read once + output
         # written once); roofline.frac: the fraction of the HBM peak;
         # speedup_vs_exact: against the same kernel with the exact exponential
         "metric": "softmax/GELU GB/s and % of HBM roofline on 1 MI355X; speedup vs exact-exp kernel",
-        "value": round(head["gbps"], 2),
+        "value": round(gbps, 2),
         "unit": "GB/s",
         "n_gpus": 1,
-        "steps": head["launches"],
+        "steps": a.steps,
         "warmup": a.warmup,
-        "ms_per_step": head["ms"],
+        "ms_per_step": head_ms,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -702,70 +883,87 @@ def main():
         "data": "synthetic (seeded, %s)" % w.name,
         "config": {"workload": w.name, "op": w.op, "io_dtype": w.dt, "shape": list(w.shape),
                    "mode": a.mode, "elements": w.numel, "algo_bytes": w.algo_bytes,
-                   "launch": head["launch"], "rotating_buffer_pairs": head["nbuf"]},
-        "roofline": {"bound": "hbm", "achieved": round(head["gbps"], 2), "peak": PEAK_HBM_GBPS,
-                     "unit": "GB/s", "frac": round(head["gbps"] / PEAK_HBM_GBPS, 4),
+                   "launch": launch, "rotating_buffer_pairs": pairs},
+        "timing": {"windows": timer.windows, "steps_per_window": a.steps, "statistic": "median",
+                   "window_ms_per_step": {m: [round(v, 6) for v in per[m]] for m in per}},
+        "roofline": {"bound": "hbm", "achieved": round(gbps, 2), "peak": PEAK_HBM_GBPS,
+                     "unit": "GB/s", "frac": round(gbps / PEAK_HBM_GBPS, 4),
                      "traffic": tb},
-        "modes": {m: {"ms_per_launch": r["ms"], "gbps": round(r["gbps"], 2),
-                      "elements_per_s": w.numel / (r["ms"] * 1e-3)} for m, r in res.items()},
+        "modes": {m: {"ms_per_launch": v, "gbps": round(w.algo_bytes / (v * 1e-3) / 1e9, 2),
+                      "elements_per_s": w.numel / (v * 1e-3)} for m, v in ms.items()},
     }
+    if "exact" in ms:
+        line["speedup_vs_exact"] = {m: round(ms["exact"] / v, 4) for m, v in ms.items()
+                                    if m != "exact"}
     if not a.only:
-        cc = copy_ceiling(w, a.steps)
-        line["copy_ceiling"] = dict(cc, frac=round(cc["gbps"] / PEAK_HBM_GBPS, 4),
-                                    value_over_copy=round(head["gbps"] / cc["gbps"], 4))
-    if "exact" in res:
-        line["speedup_vs_exact"] = {m: round(res["exact"]["ms"] / r["ms"], 4)
-                                    for m, r in res.items() if m != "exact"}
+        cc = copy_ceiling(q, timer, w, a.steps, a.warmup)
+        cc["value_over_best_copy"] = round(gbps / cc["gbps"], 4)
+        line["copy_ceiling"] = cc
     if not a.no_cpu_baseline and not a.only:
-        line["cpu_baseline"] = cpu_baseline(w, x_host, a.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(w, x_host, a.cpu_seconds, a.cpu_threads)
     if not a.no_secondary and not a.only:
         sec = {}
         for name, w2 in synth.WORKLOADS.items():
             if name == w.name:
                 continue
             xh = w2.make()
-            r2 = {}
-            # about 0.2 s of GPU time per mode at ~5 TB/s, at most --steps launches
-            sec_steps = max(100, min(a.steps, int(1e12 / w2.algo_bytes)))
-            for m in ("exact", "quake1", "quake2", "quake2m"):
-                ms, launches, nbuf, kind, _ = time_workload(q, w2, MODE_IDS[m], xh,
-                                                            sec_steps, a.warmup, a.launch)
-                r2[m] = (ms, kind)
-            ms2 = r2["quake2"][0]
-            gb = w2.algo_bytes / (ms2 * 1e-3) / 1e9
-            sec[name] = {"quake2_ms": ms2, "quake2_gbps": round(gb, 2),
-                         "frac_of_peak": round(gb / PEAK_HBM_GBPS, 4),
-                         "speedup_vs_exact": round(r2["exact"][0] / ms2, 4),
-                         "quake1_speedup_vs_exact": round(r2["exact"][0] / r2["quake1"][0], 4),
-                         "quake2m_speedup_vs_exact": round(r2["exact"][0] / r2["quake2m"][0], 4),
-                         "launch": r2["quake2"][1]}
+            steps2 = max(a.steps, operand_pairs(w2))
+            ms2, launch2, _, _ = time_modes(q, timer, w2, xh, list(MODE_IDS), steps2, 1)
+            q2 = ms2["quake2"]
+            gb = w2.algo_bytes / (q2 * 1e-3) / 1e9
+            entry = {"quake2_ms": q2, "quake2_gbps": round(gb, 2),
+                     "frac_of_peak": round(gb / PEAK_HBM_GBPS, 4),
+                     "speedup_vs_exact": round(ms2["exact"] / q2, 4),
+                     "quake1_speedup_vs_exact": round(ms2["exact"] / ms2["quake1"], 4),
+                     "quake2m_speedup_vs_exact": round(ms2["exact"] / ms2["quake2m"], 4),
+                     "launch": launch2,
+                     "traffic": traffic_for(name + ":quake2", source_hash(w2.op))}
+            if w2.algo_bytes >= (16 << 20):
+                cc2 = copy_ceiling(q, timer, w2, steps2, 1)
+                entry["copy_ceiling_gbps"] = cc2["gbps"]
+                entry["value_over_best_copy"] = round(gb / cc2["gbps"], 4)
+            if name == "lmhead_softmax_f32_64x128256":
+                ms3, _, _, _ = time_modes(q, timer, w2, xh, ["quake2"], steps2, 1,
+                                          prefix="lmhead_no_workspace", use_ws=False)
+                entry["no_workspace_quake2_ms"] = ms3["quake2"]
+                entry["note"] = ("with a workspace (quake_softmax_ws): rows split over exchanging "
+                                 "workgroups; no_workspace: quake_softmax, a workgroup per row")
+            sec[name] = entry
             del xh
-        sec["exp_f16_2p28"] = native16(q, synth, a)
-        sec["linear_gelu_bf16_4096x3072x768"] = linear_gelu(q, synth, a)
-        sec["attention_bf16_96x512x64"] = fused_attention(q, synth, a)
-        sec["attention_bf16_64x1024x64"] = fused_attention(q, synth, a, 64, 1024)
-        sec["attention_bf16_32x2048x64"] = fused_attention(q, synth, a, 32, 2048)
-        imp = implicit_causal(q, synth, a)
+            torch.cuda.empty_cache()
+        sec["exp_f16_2p28"] = native16(q, timer, synth, a)
+        sec["linear_gelu_bf16_4096x3072x768"] = linear_gelu(q, timer, synth, a)
+        sec["attention_bf16_96x512x64"] = fused_attention(q, timer, synth, a)
+        sec["attention_bf16_64x1024x64"] = fused_attention(q, timer, synth, a, 64, 1024)
+        sec["attention_bf16_32x2048x64"] = fused_attention(q, timer, synth, a, 32, 2048)
+        imp = implicit_causal(q, timer, synth, a)
         imp["no_masked_writes"]["speedup_vs_explicit_mask_input"] = round(
             sec["attn_softmax_bf16_causal"]["quake2_ms"] / imp["no_masked_writes"]["quake2_ms"], 4)
         sec["attn_softmax_bf16_causal_implicit"] = imp
         line["secondary"] = sec
     if not a.no_table4 and not a.only:
-        line["table4"] = table4(q, synth, w, x_host, a)
+        line["table4"] = table4(q, timer, synth, a)
     if a.mall_resident and not a.only:
         # the same kernel on one input/output pair reused launch after launch, so
         # that the Infinity Cache (256 MB) serves much of it: context, not the
-        # metric (opt-in, so that a kernel trace of the default command averages
+        # metric (opt-in, so that a kernel trace of the default command holds
         # cold launches only)
-        ms_w, _, _, kind_w, _ = time_workload(q, w, MODE_IDS[a.mode], x_host, a.steps, a.warmup,
-                                              a.launch, pairs=1)
-        line["mall_resident"] = {"ms_per_launch": ms_w,
-                                 "gbps": round(w.algo_bytes / (ms_w * 1e-3) / 1e9, 2),
-                                 "rotating_buffer_pairs": 1, "launch": kind_w,
+        msw, launchw, _, _ = time_modes(q, timer, w, x_host, [a.mode], a.steps, a.warmup, pairs=1,
+                                        prefix="mall_resident")
+        line["mall_resident"] = {"ms_per_launch": msw[a.mode],
+                                 "gbps": round(w.algo_bytes / (msw[a.mode] * 1e-3) / 1e9, 2),
+                                 "rotating_buffer_pairs": 1, "launch": launchw,
                                  "note": "one buffer pair reused (warm, MALL-resident); "
                                          "not the metric"}
     line["kernel_source_hash"] = hnow
     print(json.dumps(line), flush=True)
+    write_windows(a, timer)
+
+
+def write_windows(a, timer):
+    if a.trace_windows:
+        with open(a.trace_windows, "w") as f:
+            json.dump(timer.trace, f)
 
 
 if __name__ == "__main__":

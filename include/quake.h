@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define QUAKE_ABI_VERSION 3
+#define QUAKE_ABI_VERSION 4
 
 typedef enum {
   QUAKE_F32 = 0,  /* IEEE binary32 */
@@ -122,13 +122,58 @@ quake_status quake_exp(const void* x, void* y, int64_t n, quake_dtype dtype,
  * Folding m into c1 (one binary32 rounding of c0*m) shifts every exponent's
  * argument by up to |t*m| * 2^-24 (natural-log units); rows with |t*m| above
  * about 1e9 are outside the folded form's range and may give NaN.
- * Rows longer than one workgroup's registers are split over several
- * workgroups that exchange (max, sum) through a small per-stream device
- * workspace the library allocates on first use and keeps until exit.
+ * Rows of more than 16384 elements are longer than one workgroup's registers;
+ * without a workspace each such row is reduced by one workgroup that reads it
+ * three times (max, sum, normalise; the re-reads are served by the caches).
+ * quake_softmax_ws computes the same operator for those rows (the partial sums
+ * in another order) with every element read from HBM once. The library
+ * allocates nothing and keeps no state.
  */
 quake_status quake_softmax(const void* x, void* y, int64_t rows, int64_t cols,
                            int64_t ldx, int64_t ldy, quake_dtype dtype,
                            quake_mode mode, float t, void* stream);
+
+/*
+ * quake_softmax_workspace_size — bytes of device workspace quake_softmax_ws
+ * uses for rows x cols (any dtype): 0 when rows fit one workgroup's registers
+ * (cols <= 16384) or when cols > 2^22 (such rows take the workspace-free
+ * kernel), else 256 + 12 * G * R + 4 * R rounded up to 256, with
+ * G = ceil(cols / 16384) chunks per row and R = min(rows, 1024) rows per
+ * launch (6656 bytes for 64 x 128256). bytes: host pointer, non-NULL.
+ */
+quake_status quake_softmax_workspace_size(int64_t rows, int64_t cols, quake_dtype dtype,
+                                          int64_t* bytes);
+
+/*
+ * quake_softmax_ws — quake_softmax (Algorithm 2, same arguments, same results
+ * up to the summation order of the partial sums) where rows longer than one
+ * workgroup's registers (16384 < cols <= 2^22, vectorisable layout) are split
+ * into G chunks of 16384 elements held by G workgroups. Every exponent of a
+ * row needs the row's final max (Algorithm 2; QuAKE is not multiplicative, so
+ * partial sums cannot be rescaled), so the chunks exchange their maxima, then
+ * their sums, through `workspace`; x is read once from HBM.
+ *   workspace       : device memory owned by the caller, 16-byte aligned, of
+ *                     at least quake_softmax_workspace_size(rows, cols) bytes
+ *                     (else QUAKE_EINVAL), zero-filled before its first use
+ *                     (e.g. hipMemset or torch.zeros). Every call returns the
+ *                     slots to zero when it completes, so one workspace serves
+ *                     any number of stream-ordered calls (and graph replays).
+ *                     Calls that may run concurrently (different streams)
+ *                     need different workspaces. NULL (with workspace_bytes
+ *                     0) gives exactly quake_softmax.
+ *   Word 0 of the workspace (uint32) is the exchange's wait limit in ticks of
+ *   the GPU's 100 MHz constant clock, 0 meaning the default of 10000 (100 us):
+ *   a workgroup that has waited that long for a peer's value computes it from
+ *   x itself, with the peer's loads and summation order, so the result is the
+ *   same bits; progress never depends on the peers being resident (other
+ *   streams may hold any number of CUs). Word 1 (uint32) counts the
+ *   workgroups that did so (a diagnostic; the library only increments it).
+ *   Bytes 8 .. 255 are reserved and must stay zero.
+ * Other arguments, layout, errors and input contract as quake_softmax.
+ */
+quake_status quake_softmax_ws(const void* x, void* y, int64_t rows, int64_t cols, int64_t ldx,
+                              int64_t ldy, quake_dtype dtype, quake_mode mode, float t,
+                              void* workspace, int64_t workspace_bytes, void* stream);
 
 /*
  * quake_gelu — tanh-form GELU (Sec. II-C, Eq. 4) rewritten as
@@ -275,24 +320,20 @@ quake_status quake_attention(const void* q, const void* k, const void* vt, void*
                              quake_mode mode, float t, int causal, void* stream);
 
 /*
- * quake_softmax_split_timeouts — number of exchange waits of the split-row
- * softmax path (rows longer than one workgroup holds) that gave up at their
- * spin limit on `stream` since the previous call, which then resets it. Every
- * such wait is bounded so the kernel always finishes; a nonzero count means
- * the affected rows' outputs are not valid. With every workgroup of a launch
- * resident at once (the library sizes launches so), the count stays 0.
- * Synchronises `stream`. count: host pointer, non-NULL (else QUAKE_EINVAL).
+ * quake_stream_copy — a measurement aid, not part of the method: copies
+ * `bytes` (a multiple of 16, below 2^35) from x to y with plain non-temporal
+ * 16-byte loads and stores, in one of the launch shapes the operators use, so
+ * that an operator's time can be set against the time this device takes to
+ * move the same bytes. shape: 0 resident grid of 8 workgroups per CU, two
+ * vectors per lane per step, software-pipelined (the mid-size elementwise
+ * kernels' shape); 1 one vector per lane (the large elementwise kernels'
+ * shape); 2 resident grid of 4 workgroups per CU, four vectors per lane per
+ * step; 3 read only (x is read, y is written only if a 16-byte vector's four
+ * words XOR to 0x9E3779B9, which the caller's data should avoid); 4 write
+ * only (zeros to y; x unused). x, y: device, 16-byte aligned, not overlapping.
+ * Other shapes, sizes or alignments return QUAKE_EINVAL.
  */
-quake_status quake_softmax_split_timeouts(void* stream, int64_t* count);
-
-/*
- * quake_test_split_fault — test hook for the bounded waits above: while on,
- * split-row launches withhold chunk 0's exchange in every row, so every wait
- * of those rows runs to a short spin limit and is counted by
- * quake_softmax_split_timeouts; their outputs are invalid. Returns the
- * previous setting. Not for production use.
- */
-int quake_test_split_fault(int on);
+quake_status quake_stream_copy(const void* x, void* y, int64_t bytes, int shape, void* stream);
 
 /* Static, human-readable name of a status code (never NULL). */
 const char* quake_status_str(quake_status s);

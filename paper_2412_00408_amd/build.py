@@ -23,7 +23,8 @@ C_CLIENT_SRC = os.path.join(ROOT, "tests", "c", "abi_smoke.c")
 C_CLIENT = os.path.join(ROOT, "tests", "c", "abi_smoke")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 
-SOURCES = ["elementwise.hip", "softmax.hip", "native16.hip", "gemm.hip", "attention.hip", "abi.cpp"]
+SOURCES = ["elementwise.hip", "softmax.hip", "native16.hip", "gemm.hip", "attention.hip",
+           "ceiling.hip", "abi.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = [

@@ -139,17 +139,14 @@ constexpr int kEwPipeBlocksPerCu = 8;
 // At or above this many vectors per CU the one-shot kernel is used.
 constexpr int64_t kEwOneShotVecPerCu = 64 * kEwBlock;
 
+// Compute units of the current device (the runtime answers from its cached
+// device properties; nothing is kept here).
 static int device_cus() {
-  static int cached[64] = {0};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cached[dev] == 0) {
-    int cus = 0;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-      cus = 256;
-    cached[dev] = cus;
-  }
-  return cached[dev];
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    return 256;
+  return cus;
 }
 
 template <int DT, int OP, int MODE>

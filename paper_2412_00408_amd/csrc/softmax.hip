@@ -12,13 +12,17 @@
 //                         4 rows per 256-thread workgroup, no LDS, no barrier.
 //   sm_rows<NV, WAVES=4>  one workgroup per row (rows up to 256*NV vectors, i.e.
 //                         16384 elements), cross-wave max/sum through LDS.
-//   sm_split<NV>          rows longer than a workgroup's registers: G
-//                         workgroups per row each hold one chunk in VGPRs and
-//                         exchange their chunk max, then their chunk sum,
-//                         through sentinel slots of a small device workspace
-//                         (relaxed atomics, no fences). A launch never has more
-//                         workgroups than fit on the device at once, so every
-//                         wait ends; each wait is also bounded by a spin limit.
+//   sm_split<NV>          rows longer than a workgroup's registers, with a
+//                         workspace from the caller: G workgroups per row each
+//                         hold one chunk in VGPRs and exchange their chunk max,
+//                         then their chunk sum, through the workspace's slots
+//                         (relaxed atomics, no fences). A workgroup that waits
+//                         too long for a peer computes the peer's value from x
+//                         itself (same bits), so no wait depends on the peers
+//                         being resident.
+//   sm_long               the same rows without a workspace: one 1024-thread
+//                         workgroup per row, three passes (max, sum,
+//                         normalise), the re-reads served by the caches.
 //   sm_generic            any alignment / stride / length: one workgroup per
 //                         row, three passes (max, sum, normalise) with scalar
 //                         accesses; the re-reads are served by the caches.
@@ -28,10 +32,6 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
-#include <atomic>
-#include <map>
-#include <mutex>
-#include <utility>
 
 #include "quake_device.hpp"
 #include "quake_host.hpp"
@@ -320,46 +320,107 @@ __global__ __launch_bounds__(kSmBlock) void sm_causal_pair_kernel(const char* __
 // ---------------------------------------------------------------------------
 // Split rows: G workgroups per row, exchanging chunk max and chunk sum.
 //
-// Exchange without fences: every chunk owns one 32-bit slot for its max and
-// one 64-bit slot for its sum, both holding a sentinel between launches. A
-// workgroup publishes its value with a relaxed agent-scope atomic store and
-// polls the G slots of its row with relaxed agent-scope atomic loads until no
-// sentinel is left. The value is itself the atomic object, so no release /
-// acquire fence (and no L2 write-back or invalidate) is needed. After reading
+// Every exponent of a row needs the row's final max (Algorithm 2), so a row
+// longer than one workgroup's registers is held by G workgroups that exchange
+// their chunk maxima, then their chunk sums against the final max, through a
+// workspace the caller owns. Each chunk has a 32-bit max slot and a 64-bit sum
+// slot; a value is published as the complement of its bits with a relaxed
+// agent-scope atomic store, so 0 means "not published yet" and a zero-filled
+// workspace is the initial state. The value is itself the atomic object: no
+// release / acquire fence (no L2 write-back or invalidate) is needed. After
 // both rounds each workgroup counts itself done; the last one of the row puts
-// the sentinels back, so the workspace is ready for the next launch (also on
-// graph replay). Launches use at most as many workgroups as can be resident
-// at once, so every polled value is eventually written; every wait is also
-// bounded by a spin limit and then flags an error instead of hanging.
+// the slots back to 0, so the workspace is ready for the next launch (also on
+// graph replay).
+//
+// No wait depends on co-residency: a workgroup that has polled a slot for the
+// wait limit (s_memrealtime ticks) without seeing it published computes that
+// chunk's value itself from x, with the same loads, lane layout and summation
+// order as the chunk's owner, so the bits are the same either way. A launch
+// may therefore be larger than the device, and other streams may hold any
+// number of CUs; only the speed changes.
 // ---------------------------------------------------------------------------
 struct SplitWs {
-  uint32_t* pmax;        // [kWsSlots]  chunk maxima (binary32 bits), index rr * G + g
-  uint64_t* psum;        // [kWsSlots]  chunk sums (binary64 bits)
-  uint32_t* done;        // [kWsSlots]  per-row count of finished workgroups
-  uint32_t* err;         // [1]         number of waits that hit their spin limit
-  uint32_t spin_limit;   // polls before a wait gives up
-  uint32_t withhold;     // test hook: chunk 0 of every row never publishes
+  uint32_t* hdr;    // [0] wait limit in s_memrealtime ticks (0: the default)
+                    // [1] count of chunk values recomputed after a wait gave up
+  uint64_t* psum;   // [R*G] ~bits of chunk sums (binary64), 0 = not published
+  uint32_t* pmax;   // [R*G] ~bits of chunk maxima (binary32), 0 = not published
+  uint32_t* done;   // [R]   workgroups of the row past both exchanges
 };
 
-constexpr uint32_t kWsSlots = 8192;                 // max rows * G per launch
-constexpr uint32_t kSpinLimit = 1u << 20;           // about a second of polling
-constexpr uint32_t kTestSpinLimit = 1u << 12;       // short limit while a fault is injected
-constexpr int kMaxG = kSmBlock;                     // one polling lane per chunk
-constexpr uint32_t kSent32 = 0xFFFFFFFFu;           // a NaN never published
-constexpr uint64_t kSent64 = 0xFFFFFFFFFFFFFFFFull; // a NaN never published
+constexpr int kMaxG = kSmBlock;                    // one polling lane per chunk
+constexpr uint64_t kDefaultWaitTicks = 10000;      // 100 us at the 100 MHz constant clock
+constexpr size_t kWsHeader = 256;                  // bytes before the slot arrays
 
 template <typename T>
-__device__ __forceinline__ T poll_slot(T* slot, T sentinel, T fallback, const SplitWs& ws) {
+__device__ __forceinline__ bool poll_slot(T* slot, uint64_t limit, T* out) {
+  const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
   T v;
-  uint32_t spins = 0;
-  while ((v = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) == sentinel) {
+  while ((v = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) == 0) {
+    if (__builtin_amdgcn_s_memrealtime() - t0 > limit) return false;
     __builtin_amdgcn_s_sleep(1);
-    if (++spins >= ws.spin_limit) {
-      __hip_atomic_fetch_add(ws.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      return fallback;
-    }
   }
-  return v;
+  *out = ~v;
+  return true;
+}
+
+// One 16-byte vector of a row widened to binary32, masked as the register-
+// resident kernels mask it: vectors past the row end are -inf, and with the
+// causal mask entries at or past the live length L are -inf.
+template <int DT, bool CAUSAL>
+__device__ __forceinline__ void widen_masked(u32x4 raw, uint32_t vi, uint32_t nvr, uint32_t L,
+                                             float* f) {
+  constexpr int V = kV<DT>;
+  if (!CAUSAL && vi >= nvr) raw = neg_inf_vec<DT>();
+  unpack<DT>(raw, f);
+  if constexpr (CAUSAL) {
+#pragma unroll
+    for (int j = 0; j < V; ++j) f[j] = (vi * V + j < L) ? f[j] : -INFINITY;
+  }
+}
+
+// Chunk q's max and sum computed from x by the whole workgroup, for a chunk
+// whose owner has not published in time: thread t takes vectors
+// q*CHV + k*256 + t, k = 0 .. NV-1, as the owner's thread t holds them, so the
+// per-vector partial sums, the per-lane double accumulation, the wave trees
+// and the cross-wave pairing are the owner's, bit for bit.
+template <int DT, bool CAUSAL, int NV>
+__device__ float chunk_max_from_x(const u32x4* xr, uint32_t q, uint32_t nvr, uint32_t vlast,
+                                  uint32_t L, float* s4) {
+  constexpr int V = kV<DT>;
+  float lmax = -INFINITY;
+  for (int k = 0; k < NV; ++k) {
+    const uint32_t vi = q * (kSmBlock * NV) + k * kSmBlock + threadIdx.x;
+    float f[V];
+    widen_masked<DT, CAUSAL>(__builtin_nontemporal_load(xr + umin32(vi, vlast)), vi, nvr, L, f);
+#pragma unroll
+    for (int j = 0; j < V; ++j) lmax = fmaxf(lmax, f[j]);
+  }
+  const float m = wave_max(lmax);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) s4[threadIdx.x >> 6] = m;
+  __syncthreads();
+  return fmaxf(fmaxf(s4[0], s4[1]), fmaxf(s4[2], s4[3]));
+}
+
+template <int DT, int MODE, bool FUSE, bool CAUSAL, int NV>
+__device__ double chunk_sum_from_x(const u32x4* xr, uint32_t q, uint32_t nvr, uint32_t vlast,
+                                   uint32_t L, const RowExp<MODE, FUSE>& ex, double* s4) {
+  constexpr int V = kV<DT>;
+  double acc = 0.0;
+  for (int k = 0; k < NV; ++k) {
+    const uint32_t vi = q * (kSmBlock * NV) + k * kSmBlock + threadIdx.x;
+    float f[V];
+    widen_masked<DT, CAUSAL>(__builtin_nontemporal_load(xr + umin32(vi, vlast)), vi, nvr, L, f);
+    float part = 0.0f;
+#pragma unroll
+    for (int j = 0; j < V; ++j) part += ex(f[j]);
+    acc += (double)part;
+  }
+  const double s = wave_sum(acc);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) s4[threadIdx.x >> 6] = s;
+  __syncthreads();
+  return (s4[0] + s4[1]) + (s4[2] + s4[3]);
 }
 
 template <int DT, int MODE, bool FUSE, bool CAUSAL, int NV>
@@ -367,21 +428,24 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
                                                            char* __restrict__ y, uint32_t nvr,
                                                            int64_t ldx_b, int64_t ldy_b,
                                                            SmConst kc, CausalArg ca, uint32_t G,
-                                                           SplitWs ws) {
+                                                           uint32_t xcd_map, SplitWs ws) {
   constexpr int V = kV<DT>;
   constexpr int CHV = kSmBlock * NV;   // vectors per chunk
   __shared__ float s_max[4];
   __shared__ double s_sum[4];
+  __shared__ float s_fmax[4];
+  __shared__ double s_fsum[4];
   __shared__ float s_pmax[kMaxG];
   __shared__ double s_psum[kMaxG];
+  __shared__ uint32_t s_missing;
 
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
-  // Chunk g of row rr. blockIdx round-robins over the 8 XCDs; with the rows a
-  // multiple of 8, XCD x takes rows x, x + 8, ... with all their chunks, so a
-  // row's exchange stays among the workgroups of one XCD.
+  // Chunk g of row rr. blockIdx round-robins over the 8 XCDs; with xcd_map
+  // (rows a multiple of 8, few chunks per row) XCD x takes rows x, x + 8, ...
+  // with all their chunks, so a row's exchange stays within one XCD's L2.
   uint32_t rr, g;
-  if ((gridDim.x / G) % 8u == 0) {
+  if (xcd_map) {
     const uint32_t sl = blockIdx.x >> 3;
     rr = (blockIdx.x & 7u) + 8u * (sl / G);
     g = sl % G;
@@ -391,6 +455,8 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
   }
   uint32_t* pm = ws.pmax + rr * G;
   uint64_t* ps = ws.psum + rr * G;
+  const uint32_t lim_in = ws.hdr[0];
+  const uint64_t limit = lim_in ? (uint64_t)lim_in : kDefaultWaitTicks;
 
   const u32x4* xr = reinterpret_cast<const u32x4*>(x + (int64_t)rr * ldx_b);
   u32x4* yr = reinterpret_cast<u32x4*>(y + (int64_t)rr * ldy_b);
@@ -407,31 +473,37 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
   float lmax = -INFINITY;
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
-    const uint32_t vi = v0 + k * kSmBlock + threadIdx.x;
-    if (!CAUSAL && vi >= nvr) raw[k] = neg_inf_vec<DT>();
-    unpack<DT>(raw[k], f[k]);
+    widen_masked<DT, CAUSAL>(raw[k], v0 + k * kSmBlock + threadIdx.x, nvr, L, f[k]);
 #pragma unroll
-    for (int j = 0; j < V; ++j) {
-      if constexpr (CAUSAL) f[k][j] = (vi * V + j < L) ? f[k][j] : -INFINITY;
-      lmax = fmaxf(lmax, f[k][j]);
-    }
+    for (int j = 0; j < V; ++j) lmax = fmaxf(lmax, f[k][j]);
   }
 
   // first exchange: the chunk maxima
   float m = wave_max(lmax);
   if (lane == 0) s_max[wave] = m;
+  if (threadIdx.x == 0) s_missing = 0;
   __syncthreads();
-  const bool publish = !(ws.withhold && g == 0);
-  if (threadIdx.x == 0 && publish) {
+  if (threadIdx.x == 0) {
     m = fmaxf(fmaxf(s_max[0], s_max[1]), fmaxf(s_max[2], s_max[3]));
     const uint32_t mb = (m != m) ? as_u(-INFINITY) : as_u(m);
-    __hip_atomic_store(pm + g, mb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(pm + g, ~mb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  if (threadIdx.x < G)
-    s_pmax[threadIdx.x] = as_f(poll_slot<uint32_t>(pm + threadIdx.x, kSent32, as_u(-INFINITY), ws));
+  if (threadIdx.x < G) {
+    uint32_t v;
+    const bool ok = poll_slot<uint32_t>(pm + threadIdx.x, limit, &v);
+    s_pmax[threadIdx.x] = ok ? as_f(v) : __builtin_nanf("");   // NaN: not published in time
+    if (!ok) s_missing = 1;
+  }
   __syncthreads();
+  const bool missing_max = s_missing != 0;
   m = -INFINITY;
-  for (uint32_t q = 0; q < G; ++q) m = fmaxf(m, s_pmax[q]);
+  for (uint32_t q = 0; q < G; ++q) m = fmaxf(m, s_pmax[q]);   // fmaxf skips the NaN marks
+  if (missing_max) {   // uniform: every thread reads the same LDS words
+    for (uint32_t q = 0; q < G; ++q) {
+      if (s_pmax[q] != s_pmax[q])
+        m = fmaxf(m, chunk_max_from_x<DT, CAUSAL, NV>(xr, q, nvr, vlast, L, s_fmax));
+    }
+  }
 
   // second exchange: the chunk sums against the row's final max
   const RowExp<MODE, FUSE> ex = row_exp<MODE, FUSE>(kc, m);
@@ -449,22 +521,44 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
   double total = wave_sum(acc);
   if (lane == 0) s_sum[wave] = total;
   __syncthreads();
-  if (threadIdx.x == 0 && publish) {
+  if (threadIdx.x == 0) {
+    s_missing = 0;
     total = (s_sum[0] + s_sum[1]) + (s_sum[2] + s_sum[3]);
     const uint64_t tb = (total != total) ? 0x7FF8000000000000ull : __builtin_bit_cast(uint64_t, total);
-    __hip_atomic_store(ps + g, tb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(ps + g, ~tb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  if (threadIdx.x < G)
-    s_psum[threadIdx.x] = __builtin_bit_cast(double, poll_slot<uint64_t>(ps + threadIdx.x, kSent64, 0, ws));
   __syncthreads();
+  if (threadIdx.x < G) {
+    uint64_t v;
+    const bool ok = poll_slot<uint64_t>(ps + threadIdx.x, limit, &v);
+    s_psum[threadIdx.x] = ok ? __builtin_bit_cast(double, v) : __builtin_nan("");
+    if (!ok) s_missing = 1;
+  }
+  __syncthreads();
+  const bool missing_sum = s_missing != 0;
+  if (missing_sum) {
+    for (uint32_t q = 0; q < G; ++q) {
+      const double sq = s_psum[q];
+      __syncthreads();   // every thread has read s_psum[q] before thread 0 may rewrite it
+      if (sq != sq) {
+        const double v = chunk_sum_from_x<DT, MODE, FUSE, CAUSAL, NV>(xr, q, nvr, vlast, L, ex, s_fsum);
+        if (threadIdx.x == 0) s_psum[q] = v;
+      }
+    }
+    __syncthreads();
+  }
   if (threadIdx.x == 0) {
-    // This workgroup has read both rounds (the values are in LDS); the last
-    // workgroup of the row restores the sentinels for the next launch.
+    if (missing_max || missing_sum)
+      __hip_atomic_fetch_add(ws.hdr + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // This workgroup's two publishing stores are complete before it counts
+    // itself done, so no publish can land after the row's slots are cleared;
+    // the last workgroup of the row clears them for the next launch.
+    __builtin_amdgcn_s_waitcnt(0);
     const uint32_t old = __hip_atomic_fetch_add(ws.done + rr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (old == G - 1) {
       for (uint32_t q = 0; q < G; ++q) {
-        __hip_atomic_store(pm + q, kSent32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(ps + q, kSent64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(pm + q, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(ps + q, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       __hip_atomic_store(ws.done + rr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
@@ -484,13 +578,95 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
   }
 }
 
-__global__ void split_ws_init_kernel(SplitWs w, uint32_t n) {
-  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
-    w.pmax[i] = kSent32;
-    w.psum[i] = kSent64;
-    w.done[i] = 0;
+// ---------------------------------------------------------------------------
+// Long rows without a workspace: one 1024-thread workgroup per row, three
+// passes over the row (max; sum of the exponentials against it; normalise and
+// store). The second and third reads are mostly served by the caches. No
+// exchange between workgroups, so nothing but x and y is touched.
+// ---------------------------------------------------------------------------
+constexpr int kLongBlock = 1024;
+constexpr int kLongUnroll = 4;
+
+template <int DT, int MODE, bool FUSE, bool CAUSAL>
+__global__ __launch_bounds__(kLongBlock) void sm_long_kernel(const char* __restrict__ x,
+                                                            char* __restrict__ y, uint32_t nvr,
+                                                            int64_t ldx_b, int64_t ldy_b,
+                                                            SmConst kc, CausalArg ca) {
+  constexpr int V = kV<DT>;
+  constexpr int W = kLongBlock / 64;
+  constexpr uint32_t STEP = kLongBlock * kLongUnroll;
+  __shared__ float s_max[W];
+  __shared__ double s_sum[W];
+  const uint32_t rr = blockIdx.x;
+  const u32x4* xr = reinterpret_cast<const u32x4*>(x + (int64_t)rr * ldx_b);
+  u32x4* yr = reinterpret_cast<u32x4*>(y + (int64_t)rr * ldy_b);
+  const uint32_t L = (uint32_t)live_len<CAUSAL>(ca, rr, (int64_t)nvr * V);
+  const uint32_t nvl = CAUSAL ? (L + V - 1) / V : nvr;
+  const uint32_t vlast = (nvl > 0 ? nvl : 1) - 1;
+
+  float lmax = -INFINITY;
+  for (uint32_t b = threadIdx.x; b < nvl; b += STEP) {
+    u32x4 raw[kLongUnroll];
+#pragma unroll
+    for (int u = 0; u < kLongUnroll; ++u)
+      raw[u] = __builtin_nontemporal_load(xr + umin32(b + u * kLongBlock, vlast));
+#pragma unroll
+    for (int u = 0; u < kLongUnroll; ++u) {
+      float f[V];
+      widen_masked<DT, CAUSAL>(raw[u], b + u * kLongBlock, nvr, L, f);
+#pragma unroll
+      for (int j = 0; j < V; ++j) lmax = fmaxf(lmax, f[j]);
+    }
   }
-  if (blockIdx.x == 0 && threadIdx.x == 0) *w.err = 0;
+  float m = wave_max(lmax);
+  if ((threadIdx.x & 63) == 0) s_max[threadIdx.x >> 6] = m;
+  __syncthreads();
+  m = s_max[0];
+  for (int w = 1; w < W; ++w) m = fmaxf(m, s_max[w]);
+
+  const RowExp<MODE, FUSE> ex = row_exp<MODE, FUSE>(kc, m);
+  double acc = 0.0;
+  for (uint32_t b = threadIdx.x; b < nvl; b += STEP) {
+    u32x4 raw[kLongUnroll];
+#pragma unroll
+    for (int u = 0; u < kLongUnroll; ++u)
+      raw[u] = __builtin_nontemporal_load(xr + umin32(b + u * kLongBlock, vlast));
+#pragma unroll
+    for (int u = 0; u < kLongUnroll; ++u) {
+      const uint32_t vi = b + u * kLongBlock;
+      float f[V];
+      widen_masked<DT, CAUSAL>(raw[u], vi, nvr, L, f);
+      float part = 0.0f;
+#pragma unroll
+      for (int j = 0; j < V; ++j) part += ex(f[j]);
+      if (vi < nvl) acc += (double)part;
+    }
+  }
+  double total = wave_sum(acc);
+  if ((threadIdx.x & 63) == 0) s_sum[threadIdx.x >> 6] = total;
+  __syncthreads();
+  total = s_sum[0];
+  for (int w = 1; w < W; ++w) total += s_sum[w];
+  const float r = (m == -INFINITY) ? 0.0f : (float)(1.0 / total);
+
+  const uint32_t nst = (!CAUSAL || ca.write_masked) ? nvr : nvl;
+  for (uint32_t b = threadIdx.x; b < nst; b += STEP) {
+    u32x4 raw[kLongUnroll];
+#pragma unroll
+    for (int u = 0; u < kLongUnroll; ++u)
+      raw[u] = __builtin_nontemporal_load(xr + umin32(b + u * kLongBlock, vlast));
+#pragma unroll
+    for (int u = 0; u < kLongUnroll; ++u) {
+      const uint32_t vi = b + u * kLongBlock;
+      if (vi < nst) {
+        float f[V];
+        widen_masked<DT, CAUSAL>(raw[u], vi, nvr, L, f);
+#pragma unroll
+        for (int j = 0; j < V; ++j) f[j] = ex(f[j]) * r;
+        __builtin_nontemporal_store(pack<DT>(f), yr + vi);
+      }
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -539,86 +715,6 @@ __global__ __launch_bounds__(kSmBlock) void sm_generic_kernel(const void* __rest
 // ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
-struct WsKey {
-  int dev;
-  hipStream_t stream;
-  bool operator<(const WsKey& o) const {
-    return dev != o.dev ? dev < o.dev : (uintptr_t)stream < (uintptr_t)o.stream;
-  }
-};
-
-static std::mutex g_ws_mu;
-static std::map<WsKey, SplitWs> g_ws;
-static std::atomic<int> g_test_fault{0};
-
-// Workspace of the split kernel for (current device, stream): allocated and
-// filled with sentinels on first use (on that stream), kept until the process
-// ends. Launches on one stream are ordered, so they may share it; different
-// streams get their own.
-static quake_status split_workspace(hipStream_t s, SplitWs* out) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return QUAKE_EHIP;
-  std::lock_guard<std::mutex> lk(g_ws_mu);
-  const bool fault = g_test_fault.load(std::memory_order_relaxed) != 0;
-  auto it = g_ws.find(WsKey{dev, s});
-  if (it != g_ws.end()) {
-    *out = it->second;
-    out->withhold = fault ? 1u : 0u;
-    out->spin_limit = fault ? kTestSpinLimit : kSpinLimit;
-    return QUAKE_OK;
-  }
-  const size_t n_psum = kWsSlots * sizeof(uint64_t), n_pmax = kWsSlots * sizeof(uint32_t);
-  const size_t n_done = kWsSlots * sizeof(uint32_t), n_err = 256;
-  char* base = nullptr;
-  if (hipMalloc(&base, n_psum + n_pmax + n_done + n_err) != hipSuccess) return QUAKE_EHIP;
-  SplitWs w;
-  w.psum = reinterpret_cast<uint64_t*>(base);
-  w.pmax = reinterpret_cast<uint32_t*>(base + n_psum);
-  w.done = reinterpret_cast<uint32_t*>(base + n_psum + n_pmax);
-  w.err = reinterpret_cast<uint32_t*>(base + n_psum + n_pmax + n_done);
-  w.spin_limit = kSpinLimit;
-  w.withhold = 0;
-  hipLaunchKernelGGL(split_ws_init_kernel, dim3(8), dim3(256), 0, s, w, kWsSlots);
-  if (hipGetLastError() != hipSuccess) return QUAKE_EHIP;
-  g_ws.emplace(WsKey{dev, s}, w);
-  *out = w;
-  out->withhold = fault ? 1u : 0u;
-  out->spin_limit = fault ? kTestSpinLimit : kSpinLimit;
-  return QUAKE_OK;
-}
-
-static quake_status split_timeouts(hipStream_t s, int64_t* count) {
-  *count = 0;
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return QUAKE_EHIP;
-  uint32_t* err = nullptr;
-  {
-    std::lock_guard<std::mutex> lk(g_ws_mu);
-    auto it = g_ws.find(WsKey{dev, s});
-    if (it == g_ws.end()) return QUAKE_OK;   // no split-row launch on this stream yet
-    err = it->second.err;
-  }
-  uint32_t v = 0;
-  if (hipStreamSynchronize(s) != hipSuccess) return QUAKE_EHIP;
-  if (hipMemcpy(&v, err, sizeof(v), hipMemcpyDeviceToHost) != hipSuccess) return QUAKE_EHIP;
-  if (v != 0) {
-    const uint32_t zero = 0;
-    if (hipMemcpy(err, &zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess) return QUAKE_EHIP;
-  }
-  *count = v;
-  return QUAKE_OK;
-}
-
-// Co-resident workgroups of one kernel on the current device.
-template <typename K>
-static int coresident_blocks(K kernel) {
-  int dev = 0, nb = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kernel, kSmBlock, 0) != hipSuccess) return 0;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-  return nb * cus;
-}
-
 struct SmArgs {
   const char* x;
   char* y;
@@ -707,42 +803,76 @@ static quake_status launch_generic(const void* x, void* y, const SmArgs& a, int6
   return QUAKE_OK;
 }
 
-// Returns QUAKE_OK on success, or 1 + status on failure; -1 if the split path
-// cannot be used (too many chunks per row) and the caller should fall back.
-template <int DT, int MODE, bool FUSE, bool CAUSAL, int NV>
-static int launch_split(const SmArgs& a) {
+template <int DT, int MODE, bool FUSE, bool CAUSAL>
+static quake_status launch_long(const SmArgs& a) {
   constexpr int V = kV<DT>;
-  constexpr int CHV = kSmBlock * NV;
+  constexpr int64_t kLongRows = int64_t(1) << 30;      // rows per launch (one workgroup each)
   const uint32_t nvr = (uint32_t)(a.cols / V);
-  const uint32_t G = (nvr + CHV - 1) / CHV;
-  auto kern = sm_split_kernel<DT, MODE, FUSE, CAUSAL, NV>;
-  static int cached[64] = {0};   // per device; a benign race only recomputes it
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 1 + QUAKE_EHIP;
-  int cap = (dev >= 0 && dev < 64) ? cached[dev] : 0;
-  if (cap == 0) {
-    cap = std::min<int>(coresident_blocks(kern), (int)kWsSlots);
-    if (dev >= 0 && dev < 64) cached[dev] = cap;
+  for (int64_t r0 = 0; r0 < a.rows; r0 += kLongRows) {
+    const int64_t nr = std::min(kLongRows, a.rows - r0);
+    hipLaunchKernelGGL((sm_long_kernel<DT, MODE, FUSE, CAUSAL>), dim3((uint32_t)nr),
+                       dim3(kLongBlock), 0, a.s, a.x + r0 * a.ldx_b, a.y + r0 * a.ldy_b, nvr,
+                       a.ldx_b, a.ldy_b, a.kc, causal_at(a, r0));
+    const quake_status st = launch_status();
+    if (st != QUAKE_OK) return st;
   }
-  if (G > (uint32_t)kMaxG || cap < (int)G) return -1;
-  SplitWs ws;
-  quake_status st = split_workspace(a.s, &ws);
-  if (st != QUAKE_OK) return 1 + st;
-  // every workgroup of one launch fits on the device at once
-  const int64_t rows_per_launch = cap / G;
-  for (int64_t r0 = 0; r0 < a.rows; r0 += rows_per_launch) {
-    const int64_t nr = std::min(rows_per_launch, a.rows - r0);
+  return QUAKE_OK;
+}
+
+// Split-row geometry: 64 elements per lane per chunk (16 vectors of binary32,
+// 8 of 16-bit), 256 lanes per workgroup, so a chunk is 16384 elements; rows of
+// more than one chunk and at most kMaxG chunks exchange through a workspace.
+constexpr int64_t kChunkElems = 16384;
+constexpr int64_t kSplitRows = 1024;   // rows per launch: the workspace holds their slots
+
+static bool split_chunks(int64_t cols, uint32_t* G) {
+  if (cols <= kChunkElems || cols > kChunkElems * kMaxG) return false;
+  *G = (uint32_t)((cols + kChunkElems - 1) / kChunkElems);
+  return true;
+}
+
+static int64_t split_ws_bytes(int64_t rows, int64_t cols) {
+  uint32_t G = 0;
+  if (rows <= 0 || !split_chunks(cols, &G)) return 0;
+  const int64_t R = std::min(rows, kSplitRows);
+  const int64_t b = (int64_t)kWsHeader + R * G * 12 + R * 4;
+  return (b + 255) / 256 * 256;
+}
+
+static SplitWs split_ws_view(char* base, int64_t rows, uint32_t G) {
+  const int64_t S = std::min(rows, kSplitRows) * G;
+  SplitWs w;
+  w.hdr = reinterpret_cast<uint32_t*>(base);
+  w.psum = reinterpret_cast<uint64_t*>(base + kWsHeader);
+  w.pmax = reinterpret_cast<uint32_t*>(base + kWsHeader + 8 * S);
+  w.done = reinterpret_cast<uint32_t*>(base + kWsHeader + 12 * S);
+  return w;
+}
+
+template <int DT, int MODE, bool FUSE, bool CAUSAL>
+static quake_status launch_split(const SmArgs& a, char* ws) {
+  constexpr int V = kV<DT>;
+  constexpr int NV = (DT == F32) ? 16 : 8;
+  static_assert(kSmBlock * NV * V == kChunkElems, "chunk geometry");
+  uint32_t G = 0;
+  if (!split_chunks(a.cols, &G)) return QUAKE_EINVAL;
+  const uint32_t nvr = (uint32_t)(a.cols / V);
+  const SplitWs w = split_ws_view(ws, a.rows, G);
+  for (int64_t r0 = 0; r0 < a.rows; r0 += kSplitRows) {
+    const int64_t nr = std::min(kSplitRows, a.rows - r0);
+    const uint32_t xcd = (nr % 8 == 0 && G <= 32) ? 1u : 0u;
     hipLaunchKernelGGL((sm_split_kernel<DT, MODE, FUSE, CAUSAL, NV>), dim3((uint32_t)(nr * G)),
                        dim3(kSmBlock), 0, a.s, a.x + r0 * a.ldx_b, a.y + r0 * a.ldy_b, nvr, a.ldx_b,
-                       a.ldy_b, a.kc, causal_at(a, r0), G, ws);
-    st = launch_status();
-    if (st != QUAKE_OK) return 1 + st;
+                       a.ldy_b, a.kc, causal_at(a, r0), G, xcd, w);
+    const quake_status st = launch_status();
+    if (st != QUAKE_OK) return st;
   }
   return QUAKE_OK;
 }
 
 template <int DT, int MODE, bool FUSE, bool CAUSAL>
-static quake_status sm_dispatch(const void* x, void* y, int64_t ldx, int64_t ldy, const SmArgs& ain) {
+static quake_status sm_dispatch(const void* x, void* y, int64_t ldx, int64_t ldy, const SmArgs& ain,
+                                char* ws) {
   constexpr int V = kV<DT>;
   constexpr int64_t esz = kEsz<DT>;
   const int64_t cols = ain.cols;
@@ -777,21 +907,27 @@ static quake_status sm_dispatch(const void* x, void* y, int64_t ldx, int64_t ldy
   if constexpr (DT == F32) {
     if (nvr <= 4096) return launch_rows<DT, MODE, FUSE, CAUSAL, 16, 4>(a);
   }
-  // 64 elements per lane per chunk: 16 vectors of binary32 or 8 of 16-bit
-  const int rc = launch_split<DT, MODE, FUSE, CAUSAL, (DT == F32 ? 16 : 8)>(a);
-  if (rc >= 0) return rc == 0 ? QUAKE_OK : (quake_status)(rc - 1);
-  return launch_generic<DT, MODE, FUSE, CAUSAL>(x, y, ain, ldx, ldy);
+  // Longer rows: chunks exchanged between workgroups through the caller's
+  // workspace, or, without one, a workgroup per row reading it three times.
+  if constexpr (FUSE && !CAUSAL) {
+    uint32_t G = 0;
+    if (ws != nullptr && split_chunks(cols, &G)) return launch_split<DT, MODE, FUSE, CAUSAL>(a, ws);
+  }
+  return launch_long<DT, MODE, FUSE, CAUSAL>(a);
 }
 
 template <bool FUSE, bool CAUSAL>
 static quake_status softmax_entry(const void* x, void* y, int64_t rows, int64_t cols, int64_t ldx,
                                   int64_t ldy, int dtype, int mode, float t, int64_t period,
-                                  int64_t shift, int write_masked, void* stream) {
+                                  int64_t shift, int write_masked, void* ws, int64_t ws_bytes,
+                                  void* stream) {
   if (!valid_dtype(dtype)) return QUAKE_EDTYPE;
   if (!valid_mode(mode)) return QUAKE_EMODE;
-  if (rows < 0 || cols < 0 || ldx < 0 || ldy < 0) return QUAKE_EINVAL;
+  if (rows < 0 || cols < 0 || ldx < 0 || ldy < 0 || ws_bytes < 0) return QUAKE_EINVAL;
   if (CAUSAL && (period <= 0 || period > INT32_MAX || shift < -(int64_t(1) << 40) ||
                  shift > (int64_t(1) << 40)))
+    return QUAKE_EINVAL;
+  if (ws != nullptr && (((uintptr_t)ws & 15u) != 0 || ws_bytes < split_ws_bytes(rows, cols)))
     return QUAKE_EINVAL;
   if (rows == 0) return QUAKE_OK;
   if (cols == 0 || ldx < cols || ldy < cols || x == nullptr || y == nullptr) return QUAKE_EINVAL;
@@ -807,8 +943,9 @@ static quake_status softmax_entry(const void* x, void* y, int64_t rows, int64_t 
   const SmArgs a{static_cast<const char*>(x), static_cast<char*>(y), rows, cols, 0, 0, kc,
                  CAUSAL ? period : 0, shift, (uint32_t)(write_masked != 0),
                  static_cast<hipStream_t>(stream)};
+  char* w = static_cast<char*>(ws);
 #define QK_SM_CASE(D, M) \
-  if (dtype == D && mode == M) return sm_dispatch<D, M, FUSE, CAUSAL>(x, y, ldx, ldy, a);
+  if (dtype == D && mode == M) return sm_dispatch<D, M, FUSE, CAUSAL>(x, y, ldx, ldy, a, w);
   QK_SM_CASE(F32, EXACT) QK_SM_CASE(F32, Q1) QK_SM_CASE(F32, Q2) QK_SM_CASE(F32, Q2M)
   QK_SM_CASE(F16, EXACT) QK_SM_CASE(F16, Q1) QK_SM_CASE(F16, Q2) QK_SM_CASE(F16, Q2M)
   QK_SM_CASE(BF16, EXACT) QK_SM_CASE(BF16, Q1) QK_SM_CASE(BF16, Q2) QK_SM_CASE(BF16, Q2M)
@@ -823,13 +960,33 @@ using namespace qk;
 extern "C" quake_status quake_softmax(const void* x, void* y, int64_t rows, int64_t cols,
                                       int64_t ldx, int64_t ldy, quake_dtype dtype,
                                       quake_mode mode, float t, void* stream) {
-  return softmax_entry<true, false>(x, y, rows, cols, ldx, ldy, dtype, mode, t, 0, 0, 1, stream);
+  return softmax_entry<true, false>(x, y, rows, cols, ldx, ldy, dtype, mode, t, 0, 0, 1, nullptr,
+                                    0, stream);
+}
+
+extern "C" quake_status quake_softmax_workspace_size(int64_t rows, int64_t cols,
+                                                     quake_dtype dtype, int64_t* bytes) {
+  if (bytes == nullptr) return QUAKE_EINVAL;
+  *bytes = 0;
+  if (!valid_dtype(dtype)) return QUAKE_EDTYPE;
+  if (rows < 0 || cols < 0) return QUAKE_EINVAL;
+  *bytes = split_ws_bytes(rows, cols);
+  return QUAKE_OK;
+}
+
+extern "C" quake_status quake_softmax_ws(const void* x, void* y, int64_t rows, int64_t cols,
+                                         int64_t ldx, int64_t ldy, quake_dtype dtype,
+                                         quake_mode mode, float t, void* workspace,
+                                         int64_t workspace_bytes, void* stream) {
+  return softmax_entry<true, false>(x, y, rows, cols, ldx, ldy, dtype, mode, t, 0, 0, 1,
+                                    workspace, workspace_bytes, stream);
 }
 
 extern "C" quake_status quake_softmax_unfused(const void* x, void* y, int64_t rows, int64_t cols,
                                               int64_t ldx, int64_t ldy, quake_dtype dtype,
                                               quake_mode mode, float t, void* stream) {
-  return softmax_entry<false, false>(x, y, rows, cols, ldx, ldy, dtype, mode, t, 0, 0, 1, stream);
+  return softmax_entry<false, false>(x, y, rows, cols, ldx, ldy, dtype, mode, t, 0, 0, 1, nullptr,
+                                     0, stream);
 }
 
 extern "C" quake_status quake_softmax_causal(const void* x, void* y, int64_t rows, int64_t cols,
@@ -837,14 +994,5 @@ extern "C" quake_status quake_softmax_causal(const void* x, void* y, int64_t row
                                              int64_t shift, int write_masked, quake_dtype dtype,
                                              quake_mode mode, float t, void* stream) {
   return softmax_entry<true, true>(x, y, rows, cols, ldx, ldy, dtype, mode, t, period, shift,
-                                   write_masked, stream);
-}
-
-extern "C" quake_status quake_softmax_split_timeouts(void* stream, int64_t* count) {
-  if (count == nullptr) return QUAKE_EINVAL;
-  return split_timeouts(static_cast<hipStream_t>(stream), count);
-}
-
-extern "C" int quake_test_split_fault(int on) {
-  return g_test_fault.exchange(on ? 1 : 0);
+                                   write_masked, nullptr, 0, stream);
 }

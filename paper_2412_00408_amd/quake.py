@@ -39,20 +39,20 @@ def _load() -> ctypes.CDLL:
     L.quake_exp16.argtypes = [vp, vp, i64, ci, ci, cf, cf, vp]
     L.quake_linear_gelu.argtypes = [vp, vp, vp, i64, i64, i64, i64, i64, i64, ci, ci, ci, vp]
     L.quake_softmax.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp]
+    L.quake_softmax_ws.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp, i64, vp]
+    L.quake_softmax_workspace_size.argtypes = [i64, i64, ci, ctypes.POINTER(i64)]
     L.quake_gelu.argtypes = [vp, vp, i64, ci, ci, vp]
     L.quake_softmax_unfused.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp]
     L.quake_gelu_unfused.argtypes = [vp, vp, i64, ci, ci, vp]
     L.quake_softmax_causal.argtypes = [vp, vp, i64, i64, i64, i64, i64, i64, ci, ci, ci, cf, vp]
     L.quake_sigmoid.argtypes = [vp, vp, i64, ci, ci, ci, vp]
     L.quake_attention.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, ci, ci, cf, ci, vp]
+    L.quake_stream_copy.argtypes = [vp, vp, i64, ci, vp]
     for f in (L.quake_exp, L.quake_exp16, L.quake_linear_gelu, L.quake_softmax, L.quake_gelu,
-              L.quake_sigmoid, L.quake_attention,
+              L.quake_softmax_ws, L.quake_softmax_workspace_size,
+              L.quake_sigmoid, L.quake_attention, L.quake_stream_copy,
               L.quake_softmax_unfused, L.quake_gelu_unfused, L.quake_softmax_causal):
         f.restype = ci
-    L.quake_softmax_split_timeouts.argtypes = [vp, ctypes.POINTER(i64)]
-    L.quake_softmax_split_timeouts.restype = ci
-    L.quake_test_split_fault.argtypes = [ci]
-    L.quake_test_split_fault.restype = ci
     L.quake_status_str.argtypes = [ci]
     L.quake_status_str.restype = ctypes.c_char_p
     L.quake_abi_version.argtypes = []
@@ -71,14 +71,19 @@ def abi_version() -> int:
     return lib.quake_abi_version()
 
 
-def softmax_split_timeouts(stream=None) -> int:
-    """Waits of the split-row softmax that hit their spin limit on the stream
-    since the last query (0 in normal operation); synchronises the stream."""
+def softmax_workspace_size(rows: int, cols: int, dtype=torch.float32) -> int:
+    """Bytes of workspace quake_softmax_ws uses for rows x cols (0: none)."""
     c = ctypes.c_int64(0)
-    s = int(torch.cuda.current_stream().cuda_stream) if stream is None else int(
-        getattr(stream, "cuda_stream", stream))
-    _raise("quake_softmax_split_timeouts", lib.quake_softmax_split_timeouts(s, ctypes.byref(c)))
+    _raise("quake_softmax_workspace_size",
+           lib.quake_softmax_workspace_size(rows, cols, DTYPES[dtype], ctypes.byref(c)))
     return c.value
+
+
+def softmax_workspace(rows: int, cols: int, dtype=torch.float32, device="cuda:0"):
+    """A zero-filled device workspace for quake_softmax_ws over rows x cols, or
+    None when that shape needs none."""
+    n = softmax_workspace_size(rows, cols, dtype)
+    return torch.zeros(n, dtype=torch.uint8, device=device) if n else None
 
 
 def _stream(t: torch.Tensor, stream) -> int:
@@ -252,8 +257,12 @@ def quake_softmax_unfused(x, y=None, mode=QUAKE_2, t=1.0, stream=None):
     return quake_softmax(x, y, mode, t, stream, _fn="quake_softmax_unfused")
 
 
-def quake_softmax(x, y=None, mode=QUAKE_2, t=1.0, stream=None, _fn="quake_softmax"):
-    """Softmax of t*x over the last dimension (Algorithm 2)."""
+def quake_softmax(x, y=None, mode=QUAKE_2, t=1.0, stream=None, workspace=None,
+                  _fn="quake_softmax"):
+    """Softmax of t*x over the last dimension (Algorithm 2). With `workspace`
+    (a zero-filled uint8 device tensor of softmax_workspace_size bytes, e.g.
+    from softmax_workspace) rows longer than 16384 elements are split over
+    workgroups that exchange their maxima and sums (quake_softmax_ws)."""
     if x.dim() == 0:
         raise ValueError("softmax needs at least one dimension")
     _check_io(x, None, contiguous=False)
@@ -263,8 +272,17 @@ def quake_softmax(x, y=None, mode=QUAKE_2, t=1.0, stream=None, _fn="quake_softma
         raise ValueError("output must match the input's dtype, device and shape")
     rows, cols, ldx = _rows_view(x, "input")
     _, _, ldy = _rows_view(y, "output")
-    _raise(_fn, getattr(lib, _fn)(x.data_ptr(), y.data_ptr(), rows, cols, ldx, ldy,
-                                  DTYPES[x.dtype], MODES[mode], t, _stream(x, stream)))
+    args = (x.data_ptr(), y.data_ptr(), rows, cols, ldx, ldy, DTYPES[x.dtype], MODES[mode], t)
+    if workspace is not None:
+        if _fn != "quake_softmax":
+            raise ValueError("%s takes no workspace" % _fn)
+        if not workspace.is_cuda or workspace.device != x.device or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous tensor on x's device")
+        nbytes = workspace.numel() * workspace.element_size()
+        _raise("quake_softmax_ws", lib.quake_softmax_ws(*args, workspace.data_ptr(), nbytes,
+                                                        _stream(x, stream)))
+    else:
+        _raise(_fn, getattr(lib, _fn)(*args, _stream(x, stream)))
     return y
 
 

@@ -1,8 +1,9 @@
 /*
  * Plain-C client of libquake: allocates device memory with the HIP runtime,
  * calls the C ABI declared in include/quake.h, and checks properties that hold
- * exactly or within a known bound (no Python, no torch involved): softmax rows,
- * exact powers of two, attention of equal scores, the product with an identity
+ * exactly or within a known bound (no Python, no torch involved): softmax rows
+ * (also split over workgroups that exchange through a caller-owned
+ * workspace), exact powers of two, attention of equal scores, the product with an identity
  * matrix, and argument validation.
  *
  * Built by paper_2412_00408_amd/build.py (build_c_client) with gcc against
@@ -68,6 +69,65 @@ int main(void) {
     if (fabs(sum - 1.0) > cols * 6e-8) sums_ok = 0;
   }
   check(sums_ok, "every softmax row sums to 1 within n * 2^-24");
+
+  /* rows of 40000 binary32 values with a workspace the caller allocates and
+   * zero-fills: the split-row path, whose chunks exchange their maxima and
+   * sums through it. Rows sum to 1, agree with the workspace-free kernel
+   * within the softmax tolerance, and the slots are zero again afterwards. */
+  {
+    const int R = 4, C = 40000;
+    float* lx = (float*)malloc(sizeof(float) * R * C);
+    float* la = (float*)malloc(sizeof(float) * R * C);
+    float* lb = (float*)malloc(sizeof(float) * R * C);
+    for (int i = 0; i < R * C; ++i) {
+      s = s * 1664525u + 1013904223u;
+      lx[i] = ((float)(s >> 8) / 16777216.0f - 0.5f) * 12.0f;
+    }
+    int64_t nb = 0;
+    check(quake_softmax_workspace_size(R, C, QUAKE_F32, &nb) == QUAKE_OK && nb > 256,
+          "workspace size query");
+    void *lxd = NULL, *lad = NULL, *lbd = NULL, *wsd = NULL;
+    HIPCHECK(hipMalloc(&lxd, sizeof(float) * R * C));
+    HIPCHECK(hipMalloc(&lad, sizeof(float) * R * C));
+    HIPCHECK(hipMalloc(&lbd, sizeof(float) * R * C));
+    HIPCHECK(hipMalloc(&wsd, (size_t)nb));
+    HIPCHECK(hipMemset(wsd, 0, (size_t)nb));
+    HIPCHECK(hipMemcpy(lxd, lx, sizeof(float) * R * C, hipMemcpyHostToDevice));
+    check(quake_softmax_ws(lxd, lad, R, C, C, C, QUAKE_F32, QUAKE_2, 1.0f, wsd, nb - 1, NULL) ==
+              QUAKE_EINVAL, "a workspace smaller than the query is rejected");
+    st = quake_softmax_ws(lxd, lad, R, C, C, C, QUAKE_F32, QUAKE_2, 1.0f, wsd, nb, NULL);
+    check(st == QUAKE_OK, "quake_softmax_ws with a caller workspace returns QUAKE_OK");
+    st = quake_softmax(lxd, lbd, R, C, C, C, QUAKE_F32, QUAKE_2, 1.0f, NULL);
+    check(st == QUAKE_OK, "quake_softmax on the same long rows returns QUAKE_OK");
+    HIPCHECK(hipDeviceSynchronize());
+    HIPCHECK(hipMemcpy(la, lad, sizeof(float) * R * C, hipMemcpyDeviceToHost));
+    HIPCHECK(hipMemcpy(lb, lbd, sizeof(float) * R * C, hipMemcpyDeviceToHost));
+    int lsum_ok = 1, agree = 1;
+    for (int r = 0; r < R; ++r) {
+      double sum = 0.0;
+      for (int j = 0; j < C; ++j) {
+        const double a = la[r * C + j], b = lb[r * C + j];
+        sum += a;
+        if (fabs(a - b) > 1e-6 * fabs(b) + 1.2e-38) agree = 0;
+      }
+      if (fabs(sum - 1.0) > C * 6e-8) lsum_ok = 0;
+    }
+    check(lsum_ok, "split rows sum to 1 within n * 2^-24");
+    check(agree, "split and workspace-free rows agree within 1e-6 relative");
+    unsigned char* hws = (unsigned char*)malloc((size_t)nb);
+    HIPCHECK(hipMemcpy(hws, wsd, (size_t)nb, hipMemcpyDeviceToHost));
+    int zero = 1;
+    for (int64_t i = 256; i < nb; ++i) zero &= hws[i] == 0;
+    check(zero, "the workspace slots are zero again after the call");
+    free(hws);
+    free(lx);
+    free(la);
+    free(lb);
+    HIPCHECK(hipFree(lxd));
+    HIPCHECK(hipFree(lad));
+    HIPCHECK(hipFree(lbd));
+    HIPCHECK(hipFree(wsd));
+  }
 
   /* QuAKE2 is exact at integer powers of two (Sec. III-B): with a = fl32(ln2),
    * c0 = fl32(2^23 * a / ln2) = 2^23 and c1 = 127 * 2^23, so l = (k + 127) * 2^23

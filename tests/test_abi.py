@@ -39,6 +39,19 @@ def test_library_exports_every_declared_symbol(q):
         assert hasattr(lib, name), name
 
 
+def test_binding_declares_every_argument_list(q):
+    # ctypes passes an undeclared argument as a C int: a 64-bit device pointer
+    # or stream handle would be cut to 32 bits. Every entry point the header
+    # declares must have its argument types (and return type) set.
+    src = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    for name in declared_functions():
+        decl = re.search(r"\b%s\s*\(([^)]*)\)" % name, src).group(1).strip()
+        nargs = 0 if decl in ("", "void") else decl.count(",") + 1
+        fn = getattr(q.lib, name)
+        assert fn.argtypes is not None and len(fn.argtypes) == nargs, name
+        assert fn.restype is not None, name
+
+
 def test_version_and_status_strings(q):
     src = open(HEADER).read()
     ver = int(re.search(r"#define QUAKE_ABI_VERSION (\d+)", src).group(1))
@@ -101,6 +114,37 @@ def test_softmax_validation(q):
     assert call(t=1e38) == q.EINVAL            # c0 = 2^23 t / ln2 overflows
     assert call(dt=5) == q.EDTYPE
     assert call(mode=9) == q.EMODE
+
+
+def test_softmax_workspace_size_and_validation(q):
+    import ctypes
+    L = q.lib
+
+    def size(rows, cols, dt=0):
+        c = ctypes.c_int64(-1)
+        rc = L.quake_softmax_workspace_size(rows, cols, dt, ctypes.byref(c))
+        return rc, c.value
+    # rows that fit one workgroup (<= 16384 elements) or need more than 256
+    # chunks take no workspace
+    assert size(64, 16384) == (q.OK, 0)
+    assert size(0, 128256) == (q.OK, 0)
+    assert size(64, (1 << 22) + 1) == (q.OK, 0)
+    # 64 x 128256: 8 chunks per row, 256 + 12 * 512 + 4 * 64 bytes
+    assert size(64, 128256) == (q.OK, 6656)
+    assert size(64, 128256, 2) == (q.OK, 6656)             # independent of the format
+    assert size(5000, 20000)[1] == ((256 + 12 * 2 * 1024 + 4 * 1024 + 255) // 256) * 256
+    assert size(-1, 10)[0] == q.EINVAL and size(1, -1)[0] == q.EINVAL
+    assert size(1, 10, 7)[0] == q.EDTYPE
+    assert L.quake_softmax_workspace_size(1, 10, 0, None) == q.EINVAL
+
+    A = 0x10000   # 16-byte aligned, never dereferenced
+
+    def call(ws=A, nbytes=6656, rows=64, cols=128256):
+        return L.quake_softmax_ws(A, A, rows, cols, cols, cols, 0, 2, 1.0, ws, nbytes, None)
+    assert call(nbytes=6655) == q.EINVAL                   # smaller than the size query
+    assert call(ws=A + 8) == q.EINVAL                      # not 16-byte aligned
+    assert call(nbytes=-1) == q.EINVAL
+    assert call(rows=0) == q.OK                            # empty: nothing launched
 
 
 def test_binding_rejects_host_tensors(q):

@@ -1,6 +1,8 @@
 """GPU robustness: HIP-graph replay of every kernel family (elementwise,
-softmax, the 16-bit construction, linear+GELU, fused attention), and the bounded
-waits of the split-row softmax forced to time out from the host."""
+softmax, the 16-bit construction, linear+GELU, fused attention), a first-ever
+split-row softmax call made under graph capture, and the split-row exchange
+made to give up its waits (a wait limit of one tick set in the caller's
+workspace), which must give the same bits."""
 import numpy as np
 import pytest
 import torch
@@ -25,7 +27,8 @@ def _ops(q, bufs):
     q.quake_gelu(bufs["gelu_x"], bufs["gelu_y"], mode=2)                       # pipelined stride
     q.quake_sigmoid(bufs["sig_x"], bufs["sig_y"], mode=2, silu=True)           # one-shot
     q.quake_softmax(bufs["attn_x"], bufs["attn_y"], mode=2, t=0.125)           # wave per row
-    q.quake_softmax(bufs["lm_x"], bufs["lm_y"], mode=2)                        # split rows
+    q.quake_softmax(bufs["lm_x"], bufs["lm_y"], mode=2, workspace=bufs["lm_ws"])  # split rows
+    q.quake_softmax(bufs["lm_x"], bufs["lm2_y"], mode=2)                       # long rows
     q.quake_softmax_causal(bufs["attn_x"], bufs["causal_y"], period=512, mode=2, t=0.125)
     q.quake_softmax(bufs["gen_x"], bufs["gen_y"], mode=1)                      # generic
     q.quake_exp16(bufs["e16_x"], bufs["e16_y"], mode=2)                        # 16-bit layout
@@ -36,6 +39,11 @@ def _ops(q, bufs):
                       t=0.125, causal=False)                                   # eight waves
     q.quake_attention(bufs["att2p_q"], bufs["att2p_k"], bufs["att2p_vt"], bufs["att2p_y"],
                       mode=2, t=0.125, causal=True)                            # two passes
+
+
+def quake_ws(rows, cols):
+    from paper_2412_00408_amd import quake
+    return quake.softmax_workspace(rows, cols)
 
 
 def _bufs():
@@ -58,6 +66,8 @@ def _bufs():
     for k in ("gelu", "sig", "attn", "lm", "gen", "e16"):
         b[k + "_y"] = torch.empty_like(b[k + "_x"])
     b["causal_y"] = torch.empty_like(b["attn_x"])
+    b["lm2_y"] = torch.empty_like(b["lm_x"])
+    b["lm_ws"] = quake_ws(16, 128256)
     b["lin_y"] = torch.empty((256, 512), dtype=torch.bfloat16, device="cuda:0")
     return b
 
@@ -66,7 +76,7 @@ def test_graph_replay_matches_eager(q):
     bufs = _bufs()
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(s):          # eager reference, and per-stream workspaces before capture
+    with torch.cuda.stream(s):          # eager reference
         _ops(q, bufs)
     s.synchronize()
     ref = {k: v.clone() for k, v in bufs.items() if k.endswith("_y")}
@@ -90,28 +100,65 @@ def test_graph_replay_matches_eager(q):
         for k, v in ref.items():
             msg = check_bits(host_bits(bufs[k]), host_bits(v), name="replay %d %s" % (rep, k))
             assert msg is None, msg
-    assert q.softmax_split_timeouts(s) == 0
+    assert int(bufs["lm_ws"][256:].count_nonzero()) == 0
 
 
-def test_split_waits_forced_to_time_out_then_recover(q):
+def test_first_split_call_inside_graph_capture(q):
+    # the workspace is the caller's and starts zero-filled, so the very first
+    # split-row call may be captured: nothing is allocated or initialised
     w = synth.WORKLOADS["lmhead_softmax_f32_64x128256"]
-    x = w.make(rows=8)
-    xg = x.to("cuda:0")
-    ref = oracle.softmax(host_bits(x), "f32", 2, threads=THREADS)
-    y = q.quake_softmax(xg, mode=2)
-    assert q.softmax_split_timeouts() == 0
-    assert_parity(host_bits(y), ref, "f32", "op", "split before fault")
-    say("forced split timeouts")
-    prev = q.lib.quake_test_split_fault(1)
-    try:
-        assert prev == 0
-        q.quake_softmax(xg, y, mode=2)          # every wait of every row gives up, kernel ends
-        n = q.softmax_split_timeouts()
-    finally:
-        q.lib.quake_test_split_fault(0)
-    assert n > 0
-    # the workspace is back in its initial state: the next call is exact again
-    y2 = q.quake_softmax(xg, mode=2)
+    x = w.make(rows=24).to("cuda:0")
+    ws = q.softmax_workspace(24, 128256)
+    y = torch.empty_like(x)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
     torch.cuda.synchronize()
-    assert q.softmax_split_timeouts() == 0
-    assert_parity(host_bits(y2), ref, "f32", "op", "split after fault")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        q.quake_softmax(x, y, mode=2, workspace=ws)
+    torch.cuda.synchronize()
+    ws_ref = q.softmax_workspace(24, 128256)
+    ref = q.quake_softmax(x, mode=2, workspace=ws_ref)
+    torch.cuda.synchronize()
+    oref = oracle.softmax(host_bits(x), "f32", 2, threads=THREADS)
+    assert_parity(host_bits(ref), oref, "f32", "op", "eager split")
+    for rep in range(4):
+        say("first split call captured, replay", rep)
+        y.fill_(3.0)
+        _ = q.quake_softmax(x, mode=1, workspace=ws_ref)     # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        msg = check_bits(host_bits(y), host_bits(ref), name="captured split replay %d" % rep)
+        assert msg is None, msg
+        assert int(ws[256:].count_nonzero()) == 0
+
+
+def test_split_waits_given_up_give_the_same_bits(q):
+    # word 0 of the workspace is the wait limit: one tick (10 ns) makes nearly
+    # every workgroup stop waiting for its peers and compute their chunk
+    # maxima and sums from x itself, with the peers' loads and summation order
+    w = synth.WORKLOADS["lmhead_softmax_f32_64x128256"]
+    for rows, cols, seed in ((8, 128256, 0), (40, 50000, 1)):
+        x = w.make(rows=rows).to("cuda:0") if cols == 128256 else \
+            synth.normal((rows, cols), 3.0, "f32", 1300 + seed).to("cuda:0")
+        ref_ws = q.softmax_workspace(rows, cols)
+        ref = q.quake_softmax(x, mode=2, workspace=ref_ws)
+        ws = q.softmax_workspace(rows, cols)
+        ws[0:4].view(torch.int32).fill_(1)
+        say("split waits given up", rows, cols)
+        y = q.quake_softmax(x, mode=2, workspace=ws)
+        torch.cuda.synchronize()
+        recomputed = int(ws[4:8].view(torch.int32)[0])
+        assert recomputed > 0, "no workgroup gave up a wait"
+        assert int(ws[256:].count_nonzero()) == 0
+        msg = check_bits(host_bits(y), host_bits(ref), name="given-up waits %dx%d" % (rows, cols))
+        assert msg is None, msg
+        # the same workspace with the default limit: the same bits again
+        ws[0:4].view(torch.int32).fill_(0)
+        y2 = q.quake_softmax(x, mode=2, workspace=ws)
+        torch.cuda.synchronize()
+        assert check_bits(host_bits(y2), host_bits(ref)) is None
+        assert int(ref_ws[4:8].view(torch.int32)[0]) == 0
+    oref = oracle.softmax(host_bits(x), "f32", 2, threads=THREADS)
+    assert_parity(host_bits(y), oref, "f32", "op", "given-up waits vs the oracle")

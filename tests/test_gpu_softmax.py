@@ -23,15 +23,19 @@ def q():
     return quake
 
 
-def _run(q, x_cpu, mode, t, ld_pad=0, offset=0, fused=True):
+def _run(q, x_cpu, mode, t, ld_pad=0, offset=0, fused=True, ws=False):
     """Softmax of a [rows, cols] CPU tensor on the GPU and in the oracle.
 
     ld_pad > 0 stores rows with stride cols + ld_pad (input and output);
-    offset > 0 shifts both base pointers by that many elements."""
+    offset > 0 shifts both base pointers by that many elements; ws passes a
+    fresh zero-filled workspace (quake_softmax_ws), whose slots must be zero
+    again afterwards."""
     dt = {torch.float32: "f32", torch.float16: "f16", torch.bfloat16: "bf16"}[x_cpu.dtype]
     rows, cols = x_cpu.shape
     ld = cols + ld_pad
     xb = host_bits(x_cpu)
+    wsb = q.softmax_workspace(rows, cols, x_cpu.dtype) if ws else None
+    kw = {"workspace": wsb} if wsb is not None else {}
     if ld_pad or offset:
         big = torch.zeros(rows * ld + offset + 8, dtype=x_cpu.dtype)
         view = big[offset:offset + rows * ld].view(rows, ld)[:, :cols]
@@ -40,7 +44,7 @@ def _run(q, x_cpu, mode, t, ld_pad=0, offset=0, fused=True):
         xg = gx[offset:offset + rows * ld].view(rows, ld)[:, :cols]
         gy = torch.full_like(gx, 7.0)
         yg = gy[offset:offset + rows * ld].view(rows, ld)[:, :cols]
-        (q.quake_softmax if fused else q.quake_softmax_unfused)(xg, yg, mode=mode, t=t)
+        (q.quake_softmax if fused else q.quake_softmax_unfused)(xg, yg, mode=mode, t=t, **kw)
         torch.cuda.synchronize()
         out = gy.cpu()
         # padding around the rows must be untouched
@@ -50,12 +54,21 @@ def _run(q, x_cpu, mode, t, ld_pad=0, offset=0, fused=True):
         g = host_bits(out[offset:offset + rows * ld].view(rows, ld)[:, :cols].contiguous())
     else:
         xg = x_cpu.to("cuda:0")
-        yg = (q.quake_softmax if fused else q.quake_softmax_unfused)(xg, mode=mode, t=t)
+        yg = (q.quake_softmax if fused else q.quake_softmax_unfused)(xg, mode=mode, t=t, **kw)
         torch.cuda.synchronize()
         g = host_bits(yg)
+    if wsb is not None:
+        assert int(wsb[256:].count_nonzero()) == 0, "workspace slots not returned to zero"
+        assert int(wsb[4:8].view(torch.int32)[0]) == 0, "an exchange wait gave up on an idle GPU"
     fn = oracle.softmax if fused else oracle.softmax_unfused
     ref = fn(xb.reshape(rows, cols), dt, mode, t=t, threads=THREADS)
     return g, ref, dt
+
+
+def _paths(cols):
+    """Rows longer than one workgroup's registers run twice: without a
+    workspace (one workgroup per row) and split over exchanging workgroups."""
+    return (False, True) if cols > 16384 else (False,)
 
 
 COLS_F32 = [1, 2, 3, 4, 100, 128, 252, 256, 260, 512, 1000, 1024, 2048, 4096, 8188, 8192, 8196,
@@ -68,9 +81,10 @@ COLS_16 = [1, 8, 24, 512, 1000, 1024, 2048, 4096, 8192, 16384, 16392, 32768, 128
 def test_lengths_f32(q, cols, mode):
     rows = 5 if cols >= 65536 else 37
     x = synth.normal((rows, cols), 3.0, "f32", 200 + cols % 97)
-    say("softmax f32", rows, cols, mode)
-    g, r, dt = _run(q, x, mode, 1.0)
-    assert_parity(g, r, dt, "op", "softmax f32 %dx%d mode %d" % (rows, cols, mode))
+    for ws in _paths(cols):
+        say("softmax f32", rows, cols, mode, "workspace" if ws else "")
+        g, r, dt = _run(q, x, mode, 1.0, ws=ws)
+        assert_parity(g, r, dt, "op", "softmax f32 %dx%d mode %d ws %d" % (rows, cols, mode, ws))
 
 
 @pytest.mark.parametrize("cols", COLS_16)
@@ -79,9 +93,10 @@ def test_lengths_f32(q, cols, mode):
 def test_lengths_16bit(q, cols, dt, mode):
     rows = 5 if cols >= 32768 else 29
     x = synth.normal((rows, cols), 2.0, dt, 300 + cols % 89)
-    say("softmax", dt, rows, cols, mode)
-    g, r, d = _run(q, x, mode, 0.7)
-    assert_parity(g, r, d, "op", "softmax %s %dx%d mode %d" % (dt, rows, cols, mode))
+    for ws in _paths(cols):
+        say("softmax", dt, rows, cols, mode, "workspace" if ws else "")
+        g, r, d = _run(q, x, mode, 0.7, ws=ws)
+        assert_parity(g, r, d, "op", "softmax %s %dx%d mode %d ws %d" % (dt, rows, cols, mode, ws))
 
 
 @pytest.mark.parametrize("cols", [128, 512, 3000, 8192, 50000])
@@ -89,9 +104,11 @@ def test_lengths_16bit(q, cols, dt, mode):
 def test_strides_and_misalignment(q, cols, dt):
     x = synth.normal((9, cols), 2.0, dt, 400)
     for pad, off in [(8, 0), (3, 0), (0, 1), (5, 3)]:
-        say("softmax strided", dt, cols, pad, off)
-        g, r, d = _run(q, x, 2, 1.0, ld_pad=pad, offset=off)
-        assert_parity(g, r, d, "op", "softmax %s cols %d pad %d off %d" % (dt, cols, pad, off))
+        for ws in _paths(cols):
+            say("softmax strided", dt, cols, pad, off, "workspace" if ws else "")
+            g, r, d = _run(q, x, 2, 1.0, ld_pad=pad, offset=off, ws=ws)
+            assert_parity(g, r, d, "op", "softmax %s cols %d pad %d off %d ws %d"
+                          % (dt, cols, pad, off, ws))
 
 
 @pytest.mark.parametrize("cols", [64, 512, 4096, 128256])
@@ -105,12 +122,13 @@ def test_masked_rows(q, cols, mode):
     v[5, cols - 1] = 1.5                 # only the last entry is live -> one-hot
     for dt in ("f32", "bf16"):
         x = synth.to_format(v, dt)
-        say("softmax masked", dt, cols, mode)
-        g, ref, d = _run(q, x, mode, 1.0)
-        assert_parity(g, ref, d, "op", "masked %s cols %d mode %d" % (dt, cols, mode))
-        gv = oracle.decode(g.reshape(-1), d).reshape(12, cols)
-        assert np.all(gv[3] == 0.0)
-        assert abs(float(gv[5, cols - 1]) - 1.0) <= 2.0 ** -23 and np.all(gv[5, :-1] == 0.0)
+        for ws in _paths(cols):
+            say("softmax masked", dt, cols, mode, "workspace" if ws else "")
+            g, ref, d = _run(q, x, mode, 1.0, ws=ws)
+            assert_parity(g, ref, d, "op", "masked %s cols %d mode %d ws %d" % (dt, cols, mode, ws))
+            gv = oracle.decode(g.reshape(-1), d).reshape(12, cols)
+            assert np.all(gv[3] == 0.0)
+            assert abs(float(gv[5, cols - 1]) - 1.0) <= 2.0 ** -23 and np.all(gv[5, :-1] == 0.0)
 
 
 @pytest.mark.parametrize("t", [0.125, 0.5, 1.0, 3.0, 20.0])
@@ -118,46 +136,57 @@ def test_masked_rows(q, cols, mode):
 def test_temperatures(q, t, cols):
     x = synth.normal((6, cols), 2.0, "f32", 500)
     for mode in MODES:
-        say("softmax t", t, cols, mode)
-        g, r, d = _run(q, x, mode, t)
-        assert_parity(g, r, d, "op", "t %g cols %d mode %d" % (t, cols, mode))
+        for ws in _paths(cols):
+            say("softmax t", t, cols, mode, "workspace" if ws else "")
+            g, r, d = _run(q, x, mode, t, ws=ws)
+            assert_parity(g, r, d, "op", "t %g cols %d mode %d ws %d" % (t, cols, mode, ws))
 
 
 def test_many_rows_split_path_multiple_launches(q):
-    # 600 rows of 100000 fp32: more row chunks than fit co-resident at once
-    x = synth.normal((600, 100000), 3.0, "f32", 600)
-    say("softmax split 600x100000")
-    g, r, d = _run(q, x, 2, 1.0)
-    assert_parity(g, r, d, "op", "split 600x100000")
+    # 1100 rows of 100000 fp32 with a workspace: two launches (1024 rows each
+    # at most) of 7 chunks per row, each launch many times the workgroups the
+    # device holds at once
+    x = synth.normal((1100, 100000), 3.0, "f32", 600)
+    say("softmax split 1100x100000")
+    g, r, d = _run(q, x, 2, 1.0, ws=True)
+    assert_parity(g, r, d, "op", "split 1100x100000")
 
 
 def test_inplace_and_determinism(q):
     for cols in (512, 4096, 128256, 1001):
         x = synth.normal((7, cols), 3.0, "bf16", 700).to("cuda:0")
-        a = q.quake_softmax(x, mode=2)
-        b = q.quake_softmax(x, mode=2)
-        z = x.clone()
-        q.quake_softmax(z, z, mode=2)
-        torch.cuda.synchronize()
-        say("softmax inplace/determinism", cols)
-        assert check_bits(host_bits(a), host_bits(b)) is None
-        assert check_bits(host_bits(a), host_bits(z)) is None
+        for ws in _paths(cols):
+            w = q.softmax_workspace(7, cols, x.dtype) if ws else None
+            a = q.quake_softmax(x, mode=2, workspace=w)
+            b = q.quake_softmax(x, mode=2, workspace=w)
+            z = x.clone()
+            q.quake_softmax(z, z, mode=2, workspace=w)
+            torch.cuda.synchronize()
+            say("softmax inplace/determinism", cols, "workspace" if ws else "")
+            assert check_bits(host_bits(a), host_bits(b)) is None
+            assert check_bits(host_bits(a), host_bits(z)) is None
 
 
 def test_split_path_on_two_streams(q):
+    # two split launches at once, one workspace per stream: together they ask
+    # for more workgroups than the device holds, which only changes the speed
     x = synth.normal((64, 128256), 3.0, "f32", 800).to("cuda:0")
-    ref = q.quake_softmax(x, mode=2)
+    w0 = q.softmax_workspace(64, 128256)
+    ref = q.quake_softmax(x, mode=2, workspace=w0)
     torch.cuda.synchronize()
     s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    ws = {s1: q.softmax_workspace(64, 128256), s2: q.softmax_workspace(64, 128256)}
     s1.wait_stream(torch.cuda.current_stream())
     s2.wait_stream(torch.cuda.current_stream())
     outs = []
     for s in (s1, s2, s1, s2):
         with torch.cuda.stream(s):
-            outs.append(q.quake_softmax(x, mode=2))
+            outs.append(q.quake_softmax(x, mode=2, workspace=ws[s]))
     torch.cuda.synchronize()
     for o in outs:
         assert check_bits(host_bits(o), host_bits(ref)) is None
+    for w in ws.values():
+        assert int(w[256:].count_nonzero()) == 0
 
 
 # ---------------------------------------------------------------- workloads
@@ -189,9 +218,11 @@ def test_workload_attn_softmax_bf16_causal(q, mode):
 @pytest.mark.parametrize("mode", MODES)
 def test_workload_lmhead_softmax_f32_64x128256(q, mode):
     w = synth.WORKLOADS["lmhead_softmax_f32_64x128256"]
-    say(w.name, mode)
-    g, r, d = _run(q, w.make(), mode, w.t)
-    assert_parity(g, r, d, "op", "%s mode %d" % (w.name, mode))
+    x = w.make()
+    for ws in (False, True):
+        say(w.name, mode, "workspace" if ws else "")
+        g, r, d = _run(q, x, mode, w.t, ws=ws)
+        assert_parity(g, r, d, "op", "%s mode %d ws %d" % (w.name, mode, ws))
 
 
 # ------------------------------------------- unfused form (Table IV study)
