@@ -14,11 +14,16 @@ Infinity Cache) where the step count allows.
 Timing protocol. After W untimed launches, the K launches of one timed
 region are captured in HIP graphs (a graph of min(K, 512) launches replayed
 whole, plus one graph of the remainder), so no Python or launch cost sits
-between them. One window is: synchronize; replay the K launches once untimed
-(the GPU is then busy while the host submits the timed replay); a HIP event on
-the launching stream; the K launches; an event; synchronize. ms_per_step is
-the event time over K. Several windows are timed per mode, the modes
-interleaved window by window, and each figure is the median over the windows.
+between them; so are 2K launches. One window is: synchronize; the K launches
+once, untimed (the GPU is then busy while the host queues the rest); HIP
+events on the launching stream around the K launches, then around the 2K
+launches; synchronize. Starting a graph after an event costs a fixed ~13 us
+on this runtime, which a window of 20 launches would spread over the
+launches; the difference of the two event times holds exactly K launches
+without it, and ms_per_step is that difference over K (the plain K-launch
+event time is reported beside it). Several windows are timed per mode, the
+modes interleaved window by window, and each figure is the median over the
+windows.
 Before the first window the kernel runs untimed for --prewarm seconds (an idle
 MI355X takes a few hundred milliseconds to reach its steady clocks). The same
 kernel with the hardware exp2 (EXACT), with first-order QuAKE and with the
@@ -125,10 +130,9 @@ def graph_plan(steps):
 
 class GraphSeq:
     """Exactly `steps` launches fn(0), ..., fn(steps - 1) as whole replays of
-    captured HIP graphs: a graph of min(steps, GRAPH_MAX) launches replayed
-    steps // that many times, then a graph of the remainder. fn(i, stream)
-    enqueues launch i on the raw stream handle and returns a status (0 or
-    None when fine)."""
+    captured HIP graphs (graph_plan), and the same for 2 * steps launches.
+    fn(i, stream) enqueues launch i on the raw stream handle and returns a
+    status (0 or None when fine)."""
 
     def __init__(self, fn, steps, warmup=0):
         import torch
@@ -141,12 +145,19 @@ class GraphSeq:
                 if rc not in (0, None):
                     raise RuntimeError("launch failed: status %s" % rc)
         s.synchronize()
-        ga, self.reps, rem = graph_plan(steps)
-        self.graphs = [self._capture(fn, range(ga), s)]
-        self.tail = self._capture(fn, range(self.reps * ga, steps), s) if rem else None
+        self.seq = {n: self._build(fn, n, s) for n in (steps, 2 * steps)}
         torch.cuda.synchronize()
-        self.launch = ("graph: %d launches per window = %d replay(s) of a %d-launch graph%s"
-                       % (steps, self.reps, ga, " + one %d-launch graph" % rem if rem else ""))
+        ga, reps, rem = graph_plan(steps)
+        self.launch = ("graph: %d launches per timed region = %d replay(s) of a %d-launch graph%s"
+                       % (steps, reps, ga, " + one %d-launch graph" % rem if rem else ""))
+
+    @staticmethod
+    def _build(fn, n, s):
+        ga, reps, rem = graph_plan(n)
+        graphs = [GraphSeq._capture(fn, range(ga), s)] * reps
+        if rem:
+            graphs.append(GraphSeq._capture(fn, range(reps * ga, n), s))
+        return graphs
 
     @staticmethod
     def _capture(fn, idx, s):
@@ -159,40 +170,53 @@ class GraphSeq:
                     raise RuntimeError("launch failed under capture: status %s" % rc)
         return g
 
-    def replay(self):
-        for _ in range(self.reps):
-            self.graphs[0].replay()
-        if self.tail is not None:
-            self.tail.replay()
+    def replay(self, twice=False):
+        for g in self.seq[2 * self.steps if twice else self.steps]:
+            g.replay()
 
 
 class Timer:
     """Windows of graph-timed launches, interleaved over several sequences;
-    keeps the host clock readings around each window for the trace summary."""
+    keeps the host clock readings around each window for the trace summary.
+
+    One window of a sequence of K launches: synchronize; the K launches once,
+    untimed (the GPU is then busy while the host queues the rest); event A; the
+    K launches; event B; event C; 2K launches; event D; synchronize. Event
+    time over K launches (B - A) also holds the fixed cost of starting a graph
+    after an event, about 13 us on this runtime (measured: 9.71 us per GELU
+    launch over windows of 20 against 9.2 us kernel time); the difference
+    (D - C) - (B - A) holds exactly K launches and none of that cost, and is
+    what is reported per launch."""
 
     def __init__(self, windows):
         self.windows = max(1, windows)
         self.trace = {}
+        self.plain = {}
 
     def run(self, seqs: dict, algo_bytes: dict | None = None) -> dict:
         """seqs: label -> GraphSeq. Returns label -> list of ms per launch, one
-        per window."""
+        per window (differential); self.plain[label] keeps B - A over K."""
         import torch
         out = {k: [] for k in seqs}
         st = torch.cuda.current_stream()
         for _ in range(self.windows):
             for label, sq in seqs.items():
-                e0 = torch.cuda.Event(enable_timing=True)
-                e1 = torch.cuda.Event(enable_timing=True)
+                ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
                 torch.cuda.synchronize()
                 h0 = host_clocks()
-                sq.replay()                    # untimed: the GPU works while the timed replay is queued
-                e0.record(st)
+                sq.replay()                    # untimed: the GPU works while the timed replays are queued
+                ev[0].record(st)
                 sq.replay()
-                e1.record(st)
+                ev[1].record(st)
+                ev[2].record(st)
+                sq.replay(twice=True)
+                ev[3].record(st)
                 torch.cuda.synchronize()
                 h1 = host_clocks()
-                out[label].append(e0.elapsed_time(e1) / sq.steps)
+                t1 = ev[0].elapsed_time(ev[1])
+                t2 = ev[2].elapsed_time(ev[3])
+                out[label].append((t2 - t1) / sq.steps)
+                self.plain.setdefault(label, []).append(t1 / sq.steps)
                 rec = self.trace.setdefault(label, {"steps": sq.steps, "windows": []})
                 if algo_bytes and label in algo_bytes:
                     rec["algo_bytes"] = algo_bytes[label]
@@ -518,14 +542,17 @@ def linear_gelu(q, timer, synth, a):
 
     def lin(mode, gelu):
         def f(i, stream):
+            i %= nb
             return L.quake_linear_gelu(xs[i].data_ptr(), ws[i].data_ptr(), ys[i].data_ptr(), m, n, k,
                                        k, k, n, 2, mode, gelu, stream)
         return f
 
     def gelu_only(i, stream):
+        i %= nb
         return L.quake_gelu(ys[i].data_ptr(), ys[i].data_ptr(), m * n, 2, 2, stream)
 
     def vendor(i, stream):
+        i %= nb
         torch.matmul(xs[i], wts[i], out=ys[i])
 
     fns = {"linear_gelu:fused_%s" % mn: lin(MODE_IDS[mn], 1) for mn in MODE_IDS}
@@ -584,7 +611,7 @@ def fused_attention(q, timer, synth, a, heads=96, seq=512):
         fns = {}
         for mname, mid in MODE_IDS.items():
             def f(i, stream, mid=mid, causal=causal):
-                qg, kg, vg, og = sets[i]
+                qg, kg, vg, og = sets[i % nb]
                 return L.quake_attention(qg.data_ptr(), kg.data_ptr(), vg.data_ptr(),
                                          og.data_ptr(), heads, seq, d, seq, 2, mid, t, causal,
                                          stream)
@@ -594,6 +621,7 @@ def fused_attention(q, timer, synth, a, heads=96, seq=512):
         flop = 4.0 * d * pairs[causal]
 
         def explicit(i, stream, causal=causal):
+            i %= 2
             qg, _, _, og = sets[i]
             torch.bmm(qg, kts[i % 2], out=scores)
             if causal:
@@ -607,6 +635,7 @@ def fused_attention(q, timer, synth, a, heads=96, seq=512):
             torch.bmm(probs, vs[i % 2], out=og)
 
         def sdpa(i, stream, causal=causal):
+            i %= nb
             qg, kg, _, _ = sets[i]
             with sdpa_kernel([SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION]):
                 torch.nn.functional.scaled_dot_product_attention(
@@ -739,10 +768,9 @@ def traffic_for(name, hash_now):
 def summarize_trace(csv_path, windows_path):
     """For every timed label of a run made with --trace-windows, the kernels
     dispatched inside its windows (host clock readings taken after the
-    synchronisations that bracket each window), of which the second half in
-    each window is the timed replay (the first half is the untimed replay that
-    precedes it). Prints a Markdown table of the median, mean, minimum and
-    maximum duration over those timed dispatches."""
+    synchronisations that bracket each window): K untimed launches, then the
+    3K timed ones (K, then 2K). Prints a Markdown table of the median, mean,
+    minimum and maximum duration over the timed dispatches."""
     with open(windows_path) as f:
         wins = json.load(f)
     rows = []
@@ -785,7 +813,7 @@ def summarize_trace(csv_path, windows_path):
             for r in got:
                 by.setdefault(r[2], []).append(r[1] - r[0])
             for name, d in by.items():
-                per.setdefault(name, []).extend(d[len(d) // 2:])
+                per.setdefault(name, []).extend(d[len(d) // 4:])
         for name, d in per.items():
             mdn = statistics.median(d)
             ab = rec.get("algo_bytes")
@@ -885,7 +913,10 @@ def main():
                    "mode": a.mode, "elements": w.numel, "algo_bytes": w.algo_bytes,
                    "launch": launch, "rotating_buffer_pairs": pairs},
         "timing": {"windows": timer.windows, "steps_per_window": a.steps, "statistic": "median",
-                   "window_ms_per_step": {m: [round(v, 6) for v in per[m]] for m in per}},
+                   "per_launch": "(2K-launch event time - K-launch event time) / K",
+                   "window_ms_per_step": {m: [round(v, 6) for v in per[m]] for m in per},
+                   "plain_k_window_ms_per_step": {
+                       m: round(med(timer.plain["%s:%s" % (w.name, m)]), 6) for m in per}},
         "roofline": {"bound": "hbm", "achieved": round(gbps, 2), "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": round(gbps / PEAK_HBM_GBPS, 4),
                      "traffic": tb},

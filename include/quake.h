@@ -166,7 +166,9 @@ quake_status quake_softmax_workspace_size(int64_t rows, int64_t cols, quake_dtyp
  *   a workgroup that has waited that long for a peer's value computes it from
  *   x itself, with the peer's loads and summation order, so the result is the
  *   same bits; progress never depends on the peers being resident (other
- *   streams may hold any number of CUs). Word 1 (uint32) counts the
+ *   streams may hold any number of CUs); 0xFFFFFFFF means no waiting at all
+ *   (every workgroup computes every chunk value of its row from x: the same
+ *   bits, about G times the reads). Word 1 (uint32) counts the
  *   workgroups that did so (a diagnostic; the library only increments it).
  *   Bytes 8 .. 255 are reserved and must stay zero.
  * Other arguments, layout, errors and input contract as quake_softmax.

@@ -337,7 +337,8 @@ __global__ __launch_bounds__(kSmBlock) void sm_causal_pair_kernel(const char* __
 // chunk's value itself from x, with the same loads, lane layout and summation
 // order as the chunk's owner, so the bits are the same either way. A launch
 // may therefore be larger than the device, and other streams may hold any
-// number of CUs; only the speed changes.
+// number of CUs; only the speed changes. The limit 0xFFFFFFFF means no wait
+// at all: every workgroup computes every chunk value of its row itself.
 // ---------------------------------------------------------------------------
 struct SplitWs {
   uint32_t* hdr;    // [0] wait limit in s_memrealtime ticks (0: the default)
@@ -351,8 +352,11 @@ constexpr int kMaxG = kSmBlock;                    // one polling lane per chunk
 constexpr uint64_t kDefaultWaitTicks = 10000;      // 100 us at the 100 MHz constant clock
 constexpr size_t kWsHeader = 256;                  // bytes before the slot arrays
 
+constexpr uint32_t kNoWait = 0xFFFFFFFFu;          // wait limit word: never wait
+
 template <typename T>
 __device__ __forceinline__ bool poll_slot(T* slot, uint64_t limit, T* out) {
+  if (limit == kNoWait) return false;   // every peer value is computed from x
   const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
   T v;
   while ((v = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) == 0) {

@@ -37,13 +37,13 @@ def test_operand_pairs():
 
 
 def test_trace_summary_takes_the_timed_half(tmp_path):
-    # two windows; in each, 3 untimed dispatches of 100 ns then 3 timed of 40 ns
-    # (and one dispatch outside every window that must be ignored)
+    # two windows; in each, 3 untimed dispatches of 100 ns then 3 + 6 timed of
+    # 40 ns (and one dispatch outside every window that must be ignored)
     rows, wins, t = [], [], 1_000_000
     rows.append(("k", t - 500_000, t - 499_000))
     for _ in range(2):
         w0 = t
-        for d in (100, 100, 100, 40, 40, 40):
+        for d in (100, 100, 100) + (40,) * 9:
             rows.append(("k", t, t + d))
             t += 1000
         wins.append([w0 - 10, 0, t + 10, 0])   # [boot start, mono start, boot end, mono end]
@@ -60,5 +60,5 @@ def test_trace_summary_takes_the_timed_half(tmp_path):
                          check=True).stdout
     line = [ln for ln in out.splitlines() if ln.startswith("| lab:quake2")][0]
     cells = [c.strip() for c in line.strip("|").split("|")]
-    assert cells[2] == "6" and float(cells[3]) == 40.0 and cells[5] == "40" and cells[6] == "40"
+    assert cells[2] == "18" and float(cells[3]) == 40.0 and cells[5] == "40" and cells[6] == "40"
     assert float(cells[7]) == 10.0                       # 400 bytes / 40 ns
