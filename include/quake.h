@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define QUAKE_ABI_VERSION 4
+#define QUAKE_ABI_VERSION 5
 
 typedef enum {
   QUAKE_F32 = 0,  /* IEEE binary32 */
@@ -83,7 +83,8 @@ typedef enum {
   QUAKE_EINVAL = 1,  /* bad pointer / size / stride / scalar argument */
   QUAKE_EDTYPE = 2,  /* unknown quake_dtype */
   QUAKE_EMODE = 3,   /* unknown quake_mode */
-  QUAKE_EHIP = 4     /* a HIP runtime call or kernel launch failed */
+  QUAKE_EHIP = 4,    /* a HIP runtime call or kernel launch failed */
+  QUAKE_ENOSCRATCH = 5  /* quake_softmax_noalloc: the shape needs more than its fixed scratch */
 } quake_status;
 
 /*
@@ -176,6 +177,26 @@ quake_status quake_softmax_workspace_size(int64_t rows, int64_t cols, quake_dtyp
 quake_status quake_softmax_ws(const void* x, void* y, int64_t rows, int64_t cols, int64_t ldx,
                               int64_t ldy, quake_dtype dtype, quake_mode mode, float t,
                               void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * quake_softmax_noalloc — quake_softmax_ws without a workspace argument, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): the exchange uses a
+ * fixed 262144-byte device array of the library instead, one per GPU, held
+ * until the process ends. No allocation or free happens in this call; the
+ * first call on a device looks the array up and clears it with a kernel on
+ * `stream`. Same arguments (minus the workspace), same kernels and the same
+ * bits as quake_softmax_ws. Shapes whose workspace
+ * (quake_softmax_workspace_size) exceeds 262144 bytes return
+ * QUAKE_ENOSCRATCH before any HIP call (rows <= 1024 with cols <= 327680, or
+ * 64 rows of up to 2^22, fit); shapes needing no workspace run as
+ * quake_softmax. Every call on one GPU shares that GPU's array, which every
+ * call leaves zeroed: calls that may overlap on one GPU (different streams,
+ * host threads) race and must not be issued.
+ */
+quake_status quake_softmax_noalloc(const void* x, void* y, int64_t rows, int64_t cols, int64_t ldx,
+                                   int64_t ldy, quake_dtype dtype, quake_mode mode, float t,
+                                   void* stream);
 
 /*
  * quake_gelu — tanh-form GELU (Sec. II-C, Eq. 4) rewritten as

@@ -8,6 +8,8 @@ extern "C" const char* quake_status_str(quake_status s) {
     case QUAKE_EDTYPE: return "QUAKE_EDTYPE: unknown quake_dtype";
     case QUAKE_EMODE: return "QUAKE_EMODE: unknown quake_mode";
     case QUAKE_EHIP: return "QUAKE_EHIP: HIP runtime call or kernel launch failed";
+    case QUAKE_ENOSCRATCH:
+      return "QUAKE_ENOSCRATCH: the shape needs more than the library's fixed split-row scratch";
   }
   return "QUAKE_?: unknown status";
 }

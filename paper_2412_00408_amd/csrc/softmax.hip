@@ -32,6 +32,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "quake_device.hpp"
 #include "quake_host.hpp"
@@ -924,7 +925,7 @@ template <bool FUSE, bool CAUSAL>
 static quake_status softmax_entry(const void* x, void* y, int64_t rows, int64_t cols, int64_t ldx,
                                   int64_t ldy, int dtype, int mode, float t, int64_t period,
                                   int64_t shift, int write_masked, void* ws, int64_t ws_bytes,
-                                  void* stream) {
+                                  void* stream, bool check_only = false) {
   if (!valid_dtype(dtype)) return QUAKE_EDTYPE;
   if (!valid_mode(mode)) return QUAKE_EMODE;
   if (rows < 0 || cols < 0 || ldx < 0 || ldy < 0 || ws_bytes < 0) return QUAKE_EINVAL;
@@ -944,6 +945,7 @@ static quake_status softmax_entry(const void* x, void* y, int64_t rows, int64_t 
     const Affine af = exp_affine(1.0, 0.0, mode);   // the standard e^s
     kc = SmConst{af.c0, af.c1, t};
   }
+  if (check_only) return QUAKE_OK;
   const SmArgs a{static_cast<const char*>(x), static_cast<char*>(y), rows, cols, 0, 0, kc,
                  CAUSAL ? period : 0, shift, (uint32_t)(write_masked != 0),
                  static_cast<hipStream_t>(stream)};
@@ -957,9 +959,64 @@ static quake_status softmax_entry(const void* x, void* y, int64_t rows, int64_t 
   return QUAKE_EMODE;
 }
 
+// ---------------------------------------------------------------------------
+// Fixed scratch for callers that cannot allocate (quake_softmax_noalloc): the
+// split-row exchange's workspace as a device array of the library, one copy
+// per device, zero at load and zeroed once more at set-up on each device.
+// ---------------------------------------------------------------------------
+constexpr int64_t kScratchBytes = 256 * 1024;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+constexpr int kMaxScratchDevices = 64;
+static std::mutex g_scratch_mu;
+static char* g_scratch_ptr[kMaxScratchDevices];   // device address of `scratch`, per device
+
+__global__ void scratch_zero_kernel(uint32_t* p, uint32_t n) {
+  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0u;
+}
+
+// Device address of the current device's scratch. The first call on a device
+// looks the array up (its name is only a host-side stand-in) and clears it
+// with a kernel on `s`, ahead of the caller's own kernels on that stream.
+static quake_status scratch_on_current_device(hipStream_t s, char** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return QUAKE_EHIP;
+  if (dev < 0 || dev >= kMaxScratchDevices) return QUAKE_EHIP;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return QUAKE_EHIP;
+    hipLaunchKernelGGL(scratch_zero_kernel, dim3(64), dim3(256), 0, s, static_cast<uint32_t*>(p),
+                       (uint32_t)(kScratchBytes / 4));
+    if (hipGetLastError() != hipSuccess) return QUAKE_EHIP;
+    g_scratch_ptr[dev] = static_cast<char*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return QUAKE_OK;
+}
+
 }  // namespace qk
 
 using namespace qk;
+
+extern "C" quake_status quake_softmax_noalloc(const void* x, void* y, int64_t rows, int64_t cols,
+                                              int64_t ldx, int64_t ldy, quake_dtype dtype,
+                                              quake_mode mode, float t, void* stream) {
+  quake_status st = softmax_entry<true, false>(x, y, rows, cols, ldx, ldy, dtype, mode, t, 0, 0, 1,
+                                               nullptr, 0, stream, true);
+  if (st != QUAKE_OK || rows == 0) return st;
+  const int64_t need = split_ws_bytes(rows, cols);
+  if (need == 0)   // no exchange for this shape: exactly quake_softmax
+    return softmax_entry<true, false>(x, y, rows, cols, ldx, ldy, dtype, mode, t, 0, 0, 1,
+                                      nullptr, 0, stream);
+  if (need > kScratchBytes) return QUAKE_ENOSCRATCH;
+  char* ws = nullptr;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  st = scratch_on_current_device(s, &ws);
+  if (st != QUAKE_OK) return st;
+  return softmax_entry<true, false>(x, y, rows, cols, ldx, ldy, dtype, mode, t, 0, 0, 1, ws,
+                                    kScratchBytes, stream);
+}
 
 extern "C" quake_status quake_softmax(const void* x, void* y, int64_t rows, int64_t cols,
                                       int64_t ldx, int64_t ldy, quake_dtype dtype,

@@ -20,7 +20,7 @@ EXACT, QUAKE_1, QUAKE_2, QUAKE_2M = 0, 1, 2, 3
 MODES = {"exact": EXACT, "quake1": QUAKE_1, "quake2": QUAKE_2, "quake2m": QUAKE_2M, EXACT: EXACT,
          QUAKE_1: QUAKE_1, QUAKE_2: QUAKE_2, QUAKE_2M: QUAKE_2M}
 DTYPES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
-OK, EINVAL, EDTYPE, EMODE, EHIP = 0, 1, 2, 3, 4
+OK, EINVAL, EDTYPE, EMODE, EHIP, ENOSCRATCH = 0, 1, 2, 3, 4, 5
 
 
 class QuakeError(RuntimeError):
@@ -40,6 +40,7 @@ def _load() -> ctypes.CDLL:
     L.quake_linear_gelu.argtypes = [vp, vp, vp, i64, i64, i64, i64, i64, i64, ci, ci, ci, vp]
     L.quake_softmax.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp]
     L.quake_softmax_ws.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp, i64, vp]
+    L.quake_softmax_noalloc.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp]
     L.quake_softmax_workspace_size.argtypes = [i64, i64, ci, ctypes.POINTER(i64)]
     L.quake_gelu.argtypes = [vp, vp, i64, ci, ci, vp]
     L.quake_softmax_unfused.argtypes = [vp, vp, i64, i64, i64, i64, ci, ci, cf, vp]
@@ -49,7 +50,7 @@ def _load() -> ctypes.CDLL:
     L.quake_attention.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, ci, ci, cf, ci, vp]
     L.quake_stream_copy.argtypes = [vp, vp, i64, ci, vp]
     for f in (L.quake_exp, L.quake_exp16, L.quake_linear_gelu, L.quake_softmax, L.quake_gelu,
-              L.quake_softmax_ws, L.quake_softmax_workspace_size,
+              L.quake_softmax_ws, L.quake_softmax_workspace_size, L.quake_softmax_noalloc,
               L.quake_sigmoid, L.quake_attention, L.quake_stream_copy,
               L.quake_softmax_unfused, L.quake_gelu_unfused, L.quake_softmax_causal):
         f.restype = ci
@@ -284,6 +285,12 @@ def quake_softmax(x, y=None, mode=QUAKE_2, t=1.0, stream=None, workspace=None,
     else:
         _raise(_fn, getattr(lib, _fn)(*args, _stream(x, stream)))
     return y
+
+
+def quake_softmax_noalloc(x, y=None, mode=QUAKE_2, t=1.0, stream=None):
+    """quake_softmax_ws with the library's fixed device scratch instead of a
+    workspace (no allocation; calls must not overlap on one GPU)."""
+    return quake_softmax(x, y, mode, t, stream, _fn="quake_softmax_noalloc")
 
 
 def quake_softmax_causal(x, y=None, period=None, shift=0, mode=QUAKE_2, t=1.0, write_masked=True,

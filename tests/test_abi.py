@@ -57,7 +57,7 @@ def test_version_and_status_strings(q):
     ver = int(re.search(r"#define QUAKE_ABI_VERSION (\d+)", src).group(1))
     assert q.abi_version() == ver
     for code, tag in [(0, "QUAKE_OK"), (1, "QUAKE_EINVAL"), (2, "QUAKE_EDTYPE"), (3, "QUAKE_EMODE"),
-                      (4, "QUAKE_EHIP")]:
+                      (4, "QUAKE_EHIP"), (5, "QUAKE_ENOSCRATCH")]:
         assert q.status_str(code).startswith(tag)
     assert q.status_str(99).startswith("QUAKE_?")
 
