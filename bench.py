@@ -106,6 +106,9 @@ def parse():
                          "by OMP_NUM_THREADS when that is set)")
     ap.add_argument("--trace-windows", metavar="FILE",
                     help="write the host clock readings around every timed window to FILE")
+    ap.add_argument("--summarize-counters", nargs="+", metavar="CSV",
+                    help="print per-kernel medians of the counters in rocprofv3 --pmc CSV files "
+                         "and exit")
     ap.add_argument("--summarize-trace", metavar="CSV",
                     help="print per-kernel medians over the timed dispatches of a rocprofv3 "
                          "kernel trace (needs --trace-windows of the same run) and exit")
@@ -827,10 +830,36 @@ def summarize_trace(csv_path, windows_path):
                                                   "CLOCK_MONOTONIC"))
 
 
+def summarize_counters(paths):
+    """Per kernel and counter, the median over dispatches of the value a
+    rocprofv3 --pmc CSV records (rows of one dispatch summed first). Prints a
+    Markdown table."""
+    per = {}
+    for p in paths:
+        with open(p, newline="") as f:
+            for r in csv.DictReader(f):
+                name = r.get("Kernel_Name") or r.get("kernel_name")
+                ctr = r.get("Counter_Name") or r.get("counter_name")
+                val = float(r.get("Counter_Value") or r.get("counter_value") or 0.0)
+                disp = r.get("Dispatch_Id") or r.get("dispatch_id") or r.get("Correlation_Id")
+                key = (name, ctr)
+                per.setdefault(key, {}).setdefault(disp, 0.0)
+                per[key][disp] += val
+    print("| kernel | counter | dispatches | median | min | max |")
+    print("|---|---|---|---|---|---|")
+    for (name, ctr), d in sorted(per.items()):
+        v = sorted(d.values())
+        print("| `%s` | %s | %d | %.1f | %.1f | %.1f |" % (name[:100], ctr, len(v),
+                                                         statistics.median(v), v[0], v[-1]))
+
+
 # ---------------------------------------------------------------------------
 
 def main():
     a = parse()
+    if a.summarize_counters:
+        summarize_counters(a.summarize_counters)
+        return
     if a.summarize_trace:
         if not a.trace_windows:
             sys.exit("--summarize-trace needs --trace-windows FILE of the same run")

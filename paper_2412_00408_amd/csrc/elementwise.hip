@@ -5,8 +5,7 @@
 // stores (the data is touched once); a wave reads 1 KiB contiguous per load
 // instruction. Two launch shapes, chosen by size: a one-shot grid with one
 // vector per lane for large inputs, and a resident, software-pipelined
-// grid-stride loop (four vectors per lane per step) for mid-size ones, where
-// launch ramp and tail dominate.
+// grid-stride loop for mid-size ones (where launch ramp and tail dominate).
 // Elements past the last whole vector are handled by one workgroup's first
 // lanes with scalar accesses. Buffers that are not 16-byte aligned take a
 // scalar grid-stride kernel with the same per-element arithmetic.
@@ -79,19 +78,15 @@ __global__ __launch_bounds__(kEwBlock) void ew_oneshot_kernel(const u32x4* __res
   }
 }
 
-// Mid-size inputs: a resident grid (four workgroups per CU) strides over the
-// vectors, four per lane per step, and issues the next step's loads before the
-// current step's arithmetic so every lane always has loads in flight. (Of the
-// copy shapes measured at the 25 MB of a 4096 x 3072 bf16 activation, four
-// vectors per lane and four workgroups per CU moved the bytes fastest: 8.4 us
-// against 9.4 us for two vectors and eight workgroups.)
-constexpr int kEwPipeU = 4;
+// Mid-size inputs: a resident grid (a few workgroups per CU) strides over the
+// vectors, two per lane per step, and issues the next step's loads before the
+// current step's arithmetic so every lane always has loads in flight.
 template <int DT, int OP, int MODE>
 __global__ __launch_bounds__(kEwBlock) void ew_pipe_kernel(const u32x4* __restrict__ x,
                                                           u32x4* __restrict__ y, uint32_t nvec,
                                                           uint32_t tail, EwParams p) {
   constexpr int V = kV<DT>;
-  constexpr int U = kEwPipeU;
+  constexpr int U = 2;
   const uint32_t step = gridDim.x * (kEwBlock * U);
   uint32_t base = blockIdx.x * (kEwBlock * U) + threadIdx.x;
   u32x4 cur[U];
@@ -140,7 +135,7 @@ __global__ __launch_bounds__(kEwBlock) void ew_scalar_kernel(const void* __restr
 // Elements per launch: a multiple of every vector width, below 2^31.
 constexpr int64_t kEwChunk = int64_t(1) << 30;
 // Resident workgroups per CU for the strided kernel.
-constexpr int kEwPipeBlocksPerCu = 4;
+constexpr int kEwPipeBlocksPerCu = 8;
 // At or above this many vectors per CU the one-shot kernel is used.
 constexpr int64_t kEwOneShotVecPerCu = 64 * kEwBlock;
 
@@ -174,7 +169,7 @@ quake_status ew_launch(const void* x, void* y, int64_t n, const EwParams& p, hip
         hipLaunchKernelGGL((ew_oneshot_kernel<DT, OP, MODE>), dim3(grid), dim3(kEwBlock), 0, s, xv,
                            yv, nvec, tail, p);
       } else {
-        const int64_t want = ((int64_t)nvec + kEwPipeU * kEwBlock - 1) / (kEwPipeU * kEwBlock);
+        const int64_t want = ((int64_t)nvec + 2 * kEwBlock - 1) / (2 * kEwBlock);
         const uint32_t grid =
             (uint32_t)std::max<int64_t>(1, std::min<int64_t>(want, (int64_t)kEwPipeBlocksPerCu * cus));
         hipLaunchKernelGGL((ew_pipe_kernel<DT, OP, MODE>), dim3(grid), dim3(kEwBlock), 0, s, xv, yv,
