@@ -190,25 +190,36 @@ __device__ __forceinline__ void store1(void* p, int64_t i, float v) {
 // ---------------------------------------------------------------------------
 // 64-lane reductions. Four DPP steps make every lane of a 16-lane row hold the
 // row's result (xor 1, xor 2 via quad_perm; xor 4 via row_half_mirror; xor 8
-// via row_mirror), then the four rows are combined from lanes 0, 16, 32, 48
-// with v_readlane. Every lane returns the same value; the combination order is
-// fixed, so the result is deterministic. All 64 lanes must be active.
+// via row_mirror); then row_bcast:15 combines rows 0 and 1 into row 1 and rows
+// 2 and 3 into row 3, and row_bcast:31 row 1 into row 3, so lane 63 holds
+// op(op(r0, r1), op(r2, r3)), the same tree (and, addition being commutative,
+// the same bits) as combining the four row results pairwise; one v_readlane
+// hands it to every lane. All 64 lanes must be active.
 // ---------------------------------------------------------------------------
 constexpr int kDppXor1 = 0xB1;          // quad_perm [1,0,3,2]
 constexpr int kDppXor2 = 0x4E;          // quad_perm [2,3,0,1]
 constexpr int kDppHalfMirror = 0x141;   // row_half_mirror
 constexpr int kDppMirror = 0x140;       // row_mirror
+constexpr int kDppRowBcast15 = 0x142;   // lane 15 of each row to the next row
+constexpr int kDppRowBcast31 = 0x143;   // lane 31 to rows 2 and 3
 
-template <int CTRL>
-__device__ __forceinline__ float dpp_f32(float v) {
-  return as_f((uint32_t)__builtin_amdgcn_update_dpp(0, (int)as_u(v), CTRL, 0xF, 0xF, false));
+// v of the lane CTRL names; lanes of rows not in ROWS (or whose source is
+// invalid) get `old`
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t old, uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, CTRL, ROWS, 0xF, false);
 }
 
-template <int CTRL>
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return as_f(dpp_u32<CTRL, ROWS>(0u, as_u(v)));
+}
+
+template <int CTRL, int ROWS = 0xF>
 __device__ __forceinline__ double dpp_f64(double v) {
   const uint64_t u = __builtin_bit_cast(uint64_t, v);
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, CTRL, 0xF, 0xF, false);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), CTRL, 0xF, 0xF, false);
+  const uint32_t lo = dpp_u32<CTRL, ROWS>(0u, (uint32_t)u);
+  const uint32_t hi = dpp_u32<CTRL, ROWS>(0u, (uint32_t)(u >> 32));
   return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
 }
 
@@ -226,8 +237,8 @@ __device__ __forceinline__ double readlane_f64(double v, int lane) {
 // The wave maximum runs on order-preserving integer images of the values: a
 // binary32 pattern with its magnitude bits flipped when negative compares as a
 // signed int32 exactly as the floats compare (NaN aside), so each step is one
-// v_max_i32 with a DPP operand and the last combination runs on the scalar
-// unit. A float max would need the DPP value quieted (IEEE mode) first.
+// v_max_i32 with a DPP operand. A float max would need the DPP value quieted
+// (IEEE mode) first.
 __device__ __forceinline__ int32_t ord_key(float v) {
   const int32_t u = (int32_t)as_u(v);
   return u ^ (int32_t)((uint32_t)(u >> 31) >> 1);
@@ -235,9 +246,9 @@ __device__ __forceinline__ int32_t ord_key(float v) {
 __device__ __forceinline__ float ord_val(int32_t k) {
   return as_f((uint32_t)(k ^ (int32_t)((uint32_t)(k >> 31) >> 1)));
 }
-template <int CTRL>
+template <int CTRL, int ROWS = 0xF>
 __device__ __forceinline__ int32_t dpp_max_i32(int32_t k) {
-  const int32_t o = __builtin_amdgcn_update_dpp(INT32_MIN, k, CTRL, 0xF, 0xF, false);
+  const int32_t o = (int32_t)dpp_u32<CTRL, ROWS>((uint32_t)INT32_MIN, (uint32_t)k);
   return k > o ? k : o;
 }
 
@@ -247,10 +258,9 @@ __device__ __forceinline__ float wave_max(float v) {
   k = dpp_max_i32<kDppXor2>(k);
   k = dpp_max_i32<kDppHalfMirror>(k);
   k = dpp_max_i32<kDppMirror>(k);
-  const int32_t a = __builtin_amdgcn_readlane(k, 0), b = __builtin_amdgcn_readlane(k, 16);
-  const int32_t c = __builtin_amdgcn_readlane(k, 32), d = __builtin_amdgcn_readlane(k, 48);
-  const int32_t ab = a > b ? a : b, cd = c > d ? c : d;
-  return ord_val(ab > cd ? ab : cd);
+  k = dpp_max_i32<kDppRowBcast15, 0xA>(k);
+  k = dpp_max_i32<kDppRowBcast31, 0xC>(k);
+  return ord_val(__builtin_amdgcn_readlane(k, 63));
 }
 
 __device__ __forceinline__ float wave_sum_f32(float v) {
@@ -258,7 +268,9 @@ __device__ __forceinline__ float wave_sum_f32(float v) {
   v += dpp_f32<kDppXor2>(v);
   v += dpp_f32<kDppHalfMirror>(v);
   v += dpp_f32<kDppMirror>(v);
-  return (readlane_f32(v, 0) + readlane_f32(v, 16)) + (readlane_f32(v, 32) + readlane_f32(v, 48));
+  v += dpp_f32<kDppRowBcast15, 0xA>(v);   // rows 0 and 2 add the 0 `old`
+  v += dpp_f32<kDppRowBcast31, 0xC>(v);
+  return readlane_f32(v, 63);
 }
 
 __device__ __forceinline__ double wave_sum(double v) {
@@ -266,7 +278,9 @@ __device__ __forceinline__ double wave_sum(double v) {
   v += dpp_f64<kDppXor2>(v);
   v += dpp_f64<kDppHalfMirror>(v);
   v += dpp_f64<kDppMirror>(v);
-  return (readlane_f64(v, 0) + readlane_f64(v, 16)) + (readlane_f64(v, 32) + readlane_f64(v, 48));
+  v += dpp_f64<kDppRowBcast15, 0xA>(v);
+  v += dpp_f64<kDppRowBcast31, 0xC>(v);
+  return readlane_f64(v, 63);
 }
 
 }  // namespace qk

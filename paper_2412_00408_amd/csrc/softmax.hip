@@ -119,7 +119,7 @@ __device__ __forceinline__ int64_t live_len(const CausalArg& ca, uint32_t local_
 // ---------------------------------------------------------------------------
 // Register-resident rows: one wave (WAVES = 1) or one workgroup (WAVES = 4).
 // ---------------------------------------------------------------------------
-template <int DT, int MODE, bool FUSE, bool CAUSAL, int NV, int WAVES>
+template <int DT, int MODE, bool FUSE, bool CAUSAL, int NV, int WAVES, bool FULL = false>
 __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restrict__ x,
                                                           char* __restrict__ y, uint32_t rows,
                                                           uint32_t nvr, int64_t ldx_b,
@@ -144,13 +144,15 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
   // Every lane loads (vectors past the row end re-read the row's last vector,
   // which stays in one cache line) and padding lanes select -inf: no branch
   // around the loads, so the whole row stays in registers without merges.
-  // With the causal mask only vectors holding live entries are read.
+  // With the causal mask only vectors holding live entries are read. FULL:
+  // the row is exactly NV vectors per lane, so there is nothing to pad.
   const uint32_t L = (uint32_t)live_len<CAUSAL>(ca, row, (int64_t)nvr * V);
   const uint32_t nvl = CAUSAL ? (L + V - 1) / V : nvr;
   const uint32_t vlast = (nvl > 0 ? nvl : 1) - 1;
   u32x4 raw[NV];
 #pragma unroll
-  for (int k = 0; k < NV; ++k) raw[k] = __builtin_nontemporal_load(xr + umin32(k * LANES + lid, vlast));
+  for (int k = 0; k < NV; ++k)
+    raw[k] = __builtin_nontemporal_load(xr + (FULL ? k * LANES + lid : umin32(k * LANES + lid, vlast)));
   float f[NV][V];
   float lmax = -INFINITY;
 #pragma unroll
@@ -158,7 +160,7 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
     const uint32_t vi = k * LANES + lid;
     // whole vectors past the row end become -inf before widening (one select
     // per word); only the causal boundary needs a per-element mask
-    if (!CAUSAL && vi >= nvr) raw[k] = neg_inf_vec<DT>();
+    if (!FULL && !CAUSAL && vi >= nvr) raw[k] = neg_inf_vec<DT>();
     unpack<DT>(raw[k], f[k]);
 #pragma unroll
     for (int j = 0; j < V; ++j) {
@@ -174,17 +176,20 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
     m = fmaxf(fmaxf(s_max[0], s_max[1]), fmaxf(s_max[2], s_max[3]));
   }
 
+  // Partial sums start from their first term: every exponential is >= +0,
+  // so 0 + e would be e exactly and the sums are the same bits.
   const RowExp<MODE, FUSE> ex = row_exp<MODE, FUSE>(kc, m);
   Acc acc = 0;
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
-    float part = 0.0f;
+    f[k][0] = ex(f[k][0]);
+    float part = f[k][0];
 #pragma unroll
-    for (int j = 0; j < V; ++j) {
+    for (int j = 1; j < V; ++j) {
       f[k][j] = ex(f[k][j]);
       part += f[k][j];
     }
-    acc += (Acc)part;
+    acc = (k == 0) ? (Acc)part : acc + (Acc)part;
   }
   Acc total = wave_sum_acc(acc);
   if constexpr (WAVES > 1) {
@@ -197,7 +202,7 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
     const uint32_t vi = k * LANES + lid;
-    if (vi < nvr && (!CAUSAL || ca.write_masked || vi < nvl)) {
+    if ((FULL || vi < nvr) && (!CAUSAL || ca.write_masked || vi < nvl)) {
 #pragma unroll
       for (int j = 0; j < V; ++j) f[k][j] *= r;
       __builtin_nontemporal_store(pack<DT>(f[k]), yr + vi);
@@ -742,12 +747,18 @@ static quake_status launch_rows(const SmArgs& a) {
   constexpr int V = kV<DT>;
   constexpr int RPB = kSmBlock / (64 * WAVES);
   const uint32_t nvr = (uint32_t)(a.cols / V);
+  const bool full = !CAUSAL && nvr == (uint32_t)(64 * WAVES * NV);
   for (int64_t r0 = 0; r0 < a.rows; r0 += kRowChunk) {
     const int64_t nr = std::min(kRowChunk, a.rows - r0);
     const uint32_t grid = (uint32_t)((nr + RPB - 1) / RPB);
-    hipLaunchKernelGGL((sm_rows_kernel<DT, MODE, FUSE, CAUSAL, NV, WAVES>), dim3(grid),
-                       dim3(kSmBlock), 0, a.s, a.x + r0 * a.ldx_b, a.y + r0 * a.ldy_b,
-                       (uint32_t)nr, nvr, a.ldx_b, a.ldy_b, a.kc, causal_at(a, r0));
+    if (full)
+      hipLaunchKernelGGL((sm_rows_kernel<DT, MODE, FUSE, CAUSAL, NV, WAVES, true>), dim3(grid),
+                         dim3(kSmBlock), 0, a.s, a.x + r0 * a.ldx_b, a.y + r0 * a.ldy_b,
+                         (uint32_t)nr, nvr, a.ldx_b, a.ldy_b, a.kc, causal_at(a, r0));
+    else
+      hipLaunchKernelGGL((sm_rows_kernel<DT, MODE, FUSE, CAUSAL, NV, WAVES>), dim3(grid),
+                         dim3(kSmBlock), 0, a.s, a.x + r0 * a.ldx_b, a.y + r0 * a.ldy_b,
+                         (uint32_t)nr, nvr, a.ldx_b, a.ldy_b, a.kc, causal_at(a, r0));
     const quake_status st = launch_status();
     if (st != QUAKE_OK) return st;
   }
