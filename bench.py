@@ -773,7 +773,10 @@ def summarize_trace(csv_path, windows_path):
     dispatched inside its windows (host clock readings taken after the
     synchronisations that bracket each window): K untimed launches, then the
     3K timed ones (K, then 2K). Prints a Markdown table of the median, mean,
-    minimum and maximum duration over the timed dispatches."""
+    minimum and maximum duration over the timed dispatches, and the median
+    spacing of consecutive timed dispatches' starts (the per-launch period the
+    events measure; below the duration where short kernels overlap their
+    neighbours)."""
     with open(windows_path) as f:
         wins = json.load(f)
     rows = []
@@ -803,27 +806,31 @@ def summarize_trace(csv_path, windows_path):
         if n > best_n:
             best_clock, best_n = c, n
     print("| label | kernel | timed dispatches | median ns | mean ns | min ns | max ns | "
-          "GB/s at median | fraction of 8 TB/s |")
-    print("|---|---|---|---|---|---|---|---|---|")
+          "GB/s at median | fraction of 8 TB/s | median launch period ns |")
+    print("|---|---|---|---|---|---|---|---|---|---|")
     all_by_name = {}
     for r in rows:
         all_by_name.setdefault(r[2], []).append(r[1] - r[0])
     for label, rec in wins.items():
-        per = {}
+        per, period = {}, {}
         for w in rec["windows"]:
             got = inside(w[best_clock], w[2 + best_clock])
-            by = {}
+            by, wstarts = {}, {}
             for r in got:
                 by.setdefault(r[2], []).append(r[1] - r[0])
+                wstarts.setdefault(r[2], []).append(r[0])
             for name, d in by.items():
                 per.setdefault(name, []).extend(d[len(d) // 4:])
+                st = wstarts[name][len(d) // 4:]
+                period.setdefault(name, []).extend(b - a for a, b in zip(st, st[1:]))
         for name, d in per.items():
             mdn = statistics.median(d)
             ab = rec.get("algo_bytes")
             gb = "%.1f" % (ab / mdn) if ab else "—"
             fr = "%.4f" % (ab / mdn / PEAK_HBM_GBPS) if ab else "—"
-            print("| %s | `%s` | %d | %.1f | %.1f | %d | %d | %s | %s |" % (
-                label, name[:90], len(d), mdn, statistics.mean(d), min(d), max(d), gb, fr))
+            pr = "%.1f" % statistics.median(period[name]) if period.get(name) else "—"
+            print("| %s | `%s` | %d | %.1f | %.1f | %d | %d | %s | %s | %s |" % (
+                label, name[:90], len(d), mdn, statistics.mean(d), min(d), max(d), gb, fr, pr))
     print()
     print("clock: %s; all dispatches of each kernel in the trace (prewarm and warm-up "
           "included) are not in this table." % ("CLOCK_BOOTTIME" if best_clock == 0 else

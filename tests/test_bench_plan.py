@@ -62,3 +62,4 @@ def test_trace_summary_takes_the_timed_half(tmp_path):
     cells = [c.strip() for c in line.strip("|").split("|")]
     assert cells[2] == "18" and float(cells[3]) == 40.0 and cells[5] == "40" and cells[6] == "40"
     assert float(cells[7]) == 10.0                       # 400 bytes / 40 ns
+    assert float(cells[9]) == 1000.0                     # starts 1000 ns apart
