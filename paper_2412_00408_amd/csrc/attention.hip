@@ -48,6 +48,11 @@ constexpr int kAttnLongMaxS = 131072;   // longest sequence (two-pass kernel)
 constexpr int kAttnQ = 32;              // queries per workgroup
 constexpr int kAttnWaves = 4;           // waves of the two-pass workgroup
 constexpr int kAttnThreads = 64 * kAttnWaves;
+// Two-pass workgroups take two groups of 32 queries from this many such
+// tiles on (two workgroups per CU of 256 without the mask; with it four, as
+// the longest causal tiles then take twice as long and the launch's tail
+// grows), else one group.
+constexpr int kAttnLongQGMinTiles = 512, kAttnLongQGMinTilesCausal = 1024;
 
 struct AttnArgs {
   const uint16_t* q;
@@ -56,7 +61,7 @@ struct AttnArgs {
   uint16_t* o;
   int32_t s;         // sequence length, 1 .. 131072
   int32_t ldv;       // row stride of V^T in elements, >= s
-  int32_t qblocks;   // ceil(s / 32)
+  int32_t qtiles;    // query tiles of the launched kernel: ceil(s / 32), two-pass ceil(s / 64)
   float c0;          // Algorithm 2: 2^23 t / ln2 (EXACT: t / ln2)
   uint32_t causal;
   uint32_t xcd_heads;   // heads a multiple of 8: heads per XCD, else 0
@@ -223,53 +228,65 @@ __device__ __forceinline__ float tree_sum(const float (&v)[TOTAL]) {
     return tree_sum<LO, N / 2, TOTAL>(v) + tree_sum<LO + N / 2, N / 2, TOTAL>(v);
 }
 
-// End of a tile of W waves: the row sum over the waves, the W partial O^T
-// through LDS (each wave's own 8 KB region, its staging reads done), and the
-// output. Accumulator register r of oacc[db] in lane l holds dim
-// 32 db + 8 (r / 4) + 4 (l / 32) + r mod 4 of query l mod 32; call j = 16 db + r
-// its row. Wave w adds rows R w .. R w + R - 1 (R = 32 / W) over the waves in
-// a fixed order, normalises them by 1 / sum and stores them, four consecutive
-// dims (8 bytes) at a time.
-template <int DT, int W>
-__device__ __forceinline__ void attn_finish(u32x4_t (*s_buf)[512], float (*s_sum)[kAttnQ],
-                                            const f32x16_t (&oacc)[2], float part, float m,
-                                            int wave, int lane, int query, int S,
-                                            uint16_t* orow) {
+// End of a tile of W waves and QG groups of 32 queries: the row sums over the
+// waves, the W partial O^T through LDS (each wave's own 8 KB region, its
+// staging reads done; one group after the other), and the output. Accumulator
+// register r of oacc[c][db] in lane l holds dim 32 db + 8 (r / 4) + 4 (l / 32) +
+// r mod 4 of query 32 c + l mod 32 of the tile; call j = 16 db + r its row.
+// Wave w adds rows R w .. R w + R - 1 (R = 32 / W) over the waves in a fixed
+// order, normalises them by 1 / sum and stores them, four consecutive dims
+// (8 bytes) at a time. Every wave reaches every barrier: lanes of queries past
+// s only skip their stores.
+template <int DT, int W, int QG>
+__device__ __forceinline__ void attn_finish(u32x4_t (*s_buf)[512], float* s_sum,
+                                            const f32x16_t (&oacc)[QG][2], const float (&part)[QG],
+                                            const float (&m)[QG], int wave, int lane, int q0,
+                                            int S, uint16_t* ohead) {
   constexpr int R = 32 / W;
   static_assert(W == 4 || W == 8, "four or eight waves");
-  part += xor32(part);
-  if (lane < 32) s_sum[wave][lane] = part;
-  __builtin_amdgcn_wave_barrier();
-  float* po = reinterpret_cast<float*>(s_buf[wave]);
-#pragma unroll
-  for (int db = 0; db < 2; ++db)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) po[(db * 16 + r) * 64 + lane] = oacc[db][r];
-  __syncthreads();
-  if (query >= S) return;
   const int fr = lane & 31;
-  float sums[W];
 #pragma unroll
-  for (int w = 0; w < W; ++w) sums[w] = s_sum[w][fr];
-  const float total = tree_sum<0, W, W>(sums);
-  const float inv = (m == -INFINITY || !(total > 0.0f)) ? 0.0f : 1.0f / total;
-  float v[R];
-#pragma unroll
-  for (int i = 0; i < R; ++i) {
-    const int idx = (R * wave + i) * 64 + lane;
-    float parts[W];
-#pragma unroll
-    for (int w = 0; w < W; ++w) parts[w] = reinterpret_cast<const float*>(s_buf[w])[idx];
-    v[i] = tree_sum<0, W, W>(parts) * inv;
+  for (int c = 0; c < QG; ++c) {
+    const float p = part[c] + xor32(part[c]);
+    if (lane < 32) s_sum[(wave * QG + c) * 32 + lane] = p;
   }
-  // row R wave + i: db = that / 16, r = that mod 16; four dims per store
 #pragma unroll
-  for (int i = 0; i < R; i += 4) {
-    const int j = R * wave + i, db = j >> 4, r = j & 15;
-    uint2 w2;
-    w2.x = pack16<DT>(v[i], v[i + 1]);
-    w2.y = pack16<DT>(v[i + 2], v[i + 3]);
-    *reinterpret_cast<uint2*>(orow + 32 * db + 8 * (r >> 2) + 4 * (lane >> 5)) = w2;
+  for (int c = 0; c < QG; ++c) {
+    if (c > 0) __syncthreads();   // every wave has read the previous group's partials
+    __builtin_amdgcn_wave_barrier();
+    float* po = reinterpret_cast<float*>(s_buf[wave]);
+#pragma unroll
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) po[(db * 16 + r) * 64 + lane] = oacc[c][db][r];
+    __syncthreads();
+    const int query = q0 + 32 * c + fr;
+    if (query < S) {
+      float sums[W];
+#pragma unroll
+      for (int w = 0; w < W; ++w) sums[w] = s_sum[(w * QG + c) * 32 + fr];
+      const float total = tree_sum<0, W, W>(sums);
+      const float inv = (m[c] == -INFINITY || !(total > 0.0f)) ? 0.0f : 1.0f / total;
+      float v[R];
+#pragma unroll
+      for (int i = 0; i < R; ++i) {
+        const int idx = (R * wave + i) * 64 + lane;
+        float parts[W];
+#pragma unroll
+        for (int w = 0; w < W; ++w) parts[w] = reinterpret_cast<const float*>(s_buf[w])[idx];
+        v[i] = tree_sum<0, W, W>(parts) * inv;
+      }
+      uint16_t* orow = ohead + (int64_t)query * kAttnD;
+      // row R wave + i: db = that / 16, r = that mod 16; four dims per store
+#pragma unroll
+      for (int i = 0; i < R; i += 4) {
+        const int j = R * wave + i, db = j >> 4, r = j & 15;
+        uint2 w2;
+        w2.x = pack16<DT>(v[i], v[i + 1]);
+        w2.y = pack16<DT>(v[i + 2], v[i + 3]);
+        *reinterpret_cast<uint2*>(orow + 32 * db + 8 * (r >> 2) + 4 * (lane >> 5)) = w2;
+      }
+    }
   }
 }
 
@@ -292,17 +309,17 @@ __global__ __launch_bounds__(64 * W, W == 4 ? 4 : 1) void attn_kernel(AttnArgs g
   // Tile order. blockIdx round-robins over the 8 XCDs; with the heads a
   // multiple of 8, XCD x takes heads x H8 .. x H8 + H8 - 1 (H8 = heads / 8), so
   // their K and V stay in that XCD's L2, and it starts its tiles longest causal
-  // rows first across all its heads (query tile qblocks - 1 of every head, then
-  // qblocks - 2, ...), which keeps the end of the launch from waiting on a few
+  // rows first across all its heads (query tile qtiles - 1 of every head, then
+  // qtiles - 2, ...), which keeps the end of the launch from waiting on a few
   // long tiles started late.
   int bh, qb;
   if (g.xcd_heads) {
     const uint32_t x = blockIdx.x & 7u, slot = blockIdx.x >> 3;
     bh = (int)(x * g.xcd_heads + slot % g.xcd_heads);
-    qb = g.qblocks - 1 - (int)(slot / g.xcd_heads);
+    qb = g.qtiles - 1 - (int)(slot / g.xcd_heads);
   } else {
-    bh = (int)(blockIdx.x / (uint32_t)g.qblocks);
-    qb = g.qblocks - 1 - (int)(blockIdx.x % (uint32_t)g.qblocks);
+    bh = (int)(blockIdx.x / (uint32_t)g.qtiles);
+    qb = g.qtiles - 1 - (int)(blockIdx.x % (uint32_t)g.qtiles);
   }
   const int S = g.s;
   const int q0 = qb * kAttnQ;
@@ -427,41 +444,52 @@ __global__ __launch_bounds__(64 * W, W == 4 ? 4 : 1) void attn_kernel(AttnArgs g
     }
   }
 
-  attn_finish<DT, W>(s_buf, s_sum, oacc, part, m, wave, lane, query, S,
-                     g.o + ((int64_t)bh * S + query) * kAttnD);
+  const f32x16_t oacc1[1][2] = {{oacc[0], oacc[1]}};
+  const float part1[1] = {part}, m1[1] = {m};
+  attn_finish<DT, W, 1>(s_buf, &s_sum[0][0], oacc1, part1, m1, wave, lane, q0, S,
+                        g.o + (int64_t)bh * S * kAttnD);
 }
 
-// Sequences longer than 1024 keys: the same tiles, four waves and staging, but the
+// Sequences longer than 1024 keys: four waves and the same staging, but the
 // scores are not kept. Pass 1 computes them to find each query's row max;
 // pass 2 computes them again, block by block, and takes the exponentials
 // against that max (Algorithm 2 needs the final max before any exponential),
-// their sum and the second product. The scores, the max, the exponentials,
-// the sums and the products are computed by the same instructions in the same
-// order as in the one-pass kernel, so both give identical results.
-template <int DT, int MODE, int VK>
-__global__ __launch_bounds__(kAttnThreads, 3) void attn_long_kernel(AttnArgs g) {
-  __shared__ float s_max[kAttnWaves][kAttnQ];
-  __shared__ float s_sum[kAttnWaves][kAttnQ];
+// their sum and the second product. A workgroup takes QG groups of 32
+// queries: every key and value block a wave stages serves all groups (one
+// load and one trip through LDS for 32 QG queries), and the groups' products
+// and exponentials are independent chains. Per query the scores, the max,
+// the exponentials, the sums and the products are computed by the same
+// instructions in the same order as in the one-pass kernel, so both give
+// identical results. With the mask, the key block past group 0's diagonal
+// (group 1's diagonal block) is skipped for group 0, as in the one-pass kernel.
+template <int DT, int MODE, int VK, int QG>
+__global__ __launch_bounds__(kAttnThreads, QG == 1 ? 3 : 2) void attn_long_kernel(AttnArgs g) {
+  __shared__ float s_max[kAttnWaves][QG * kAttnQ];
+  __shared__ float s_sum[kAttnWaves * QG * kAttnQ];
   __shared__ u32x4_t s_buf[kAttnWaves][512];
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  int bh, qb;
+  int bh, qt;
   if (g.xcd_heads) {
     const uint32_t x = blockIdx.x & 7u, slot = blockIdx.x >> 3;
     bh = (int)(x * g.xcd_heads + slot % g.xcd_heads);
-    qb = g.qblocks - 1 - (int)(slot / g.xcd_heads);
+    qt = g.qtiles - 1 - (int)(slot / g.xcd_heads);
   } else {
-    bh = (int)(blockIdx.x / (uint32_t)g.qblocks);
-    qb = g.qblocks - 1 - (int)(blockIdx.x % (uint32_t)g.qblocks);
+    bh = (int)(blockIdx.x / (uint32_t)g.qtiles);
+    qt = g.qtiles - 1 - (int)(blockIdx.x % (uint32_t)g.qtiles);
   }
   const int S = g.s;
-  const int q0 = qb * kAttnQ;
+  const int q0 = qt * QG * kAttnQ;
   const int kblocks = (S + 31) >> 5;
-  const int nkb = g.causal ? min(kblocks, qb + 1) : kblocks;
+  // group c (queries q0 + 32 c ..) has its diagonal in key block QG qt + c and
+  // needs the key blocks before nkbc[c]; the last group needs the most
+  int nkbc[QG];
+#pragma unroll
+  for (int c = 0; c < QG; ++c) nkbc[c] = g.causal ? min(kblocks, QG * qt + c + 1) : kblocks;
+  const int nkb = nkbc[QG - 1];
   const int nlive = max(0, (nkb - wave + kAttnWaves - 1) / kAttnWaves);
   const int fr = lane & 31, fk = 8 * (lane >> 5), h = lane >> 5;
-  const int query = q0 + fr;
   const uint16_t* Q = g.q + (int64_t)bh * S * kAttnD;
   const uint16_t* K = g.k + (int64_t)bh * S * kAttnD;
   const uint16_t* Vt = g.vt + (int64_t)bh * kAttnD * g.ldv;
@@ -470,30 +498,34 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_long_kernel(AttnArgs g) 
   uint32_t voff[4];
   vblock_lane_offsets(lane, g.ldv, voff);
 
-  u32x4_t qf[4];
-  {
-    const uint16_t* qr = Q + (int64_t)min(query, S - 1) * kAttnD + fk;
+  u32x4_t qf[QG][4];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) qf[ks] = ld16(qr + 16 * ks);
+  for (int c = 0; c < QG; ++c) {
+    const uint16_t* qr = Q + (int64_t)min(q0 + 32 * c + fr, S - 1) * kAttnD + fk;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) qf[c][ks] = ld16(qr + 16 * ks);
   }
-  // One block of S^T = K Q^T (masked past s and, on the diagonal, above it):
-  // gk is written to the staging slots and then refilled with the block
-  // `next` (if any) while the scores are computed.
+  // K block kbg: gk is written to the staging slots and then refilled with the
+  // block `next` (if any); the A operands are read back into ka
   u32x4_t gk[4], gv[4];
-  auto scores = [&](int kbg, int next) {
+  auto stage_k = [&](int next, u32x4_t (&ka)[4]) {
     kblock_store(stage, lane, gk);
     if (next >= 0) kblock_load(K, 32 * next, S, lane, koff, gk);
     __builtin_amdgcn_wave_barrier();   // lanes read what other lanes wrote
-    u32x4_t ka[4];
     kblock_read(stage, fr, h, ka);
     __builtin_amdgcn_wave_barrier();   // before the slots are written again
+  };
+  // group c's block of S^T = K Q^T; with `masked`, keys past s and, on the
+  // group's diagonal, keys above it are set to -inf
+  auto scores = [&](const u32x4_t (&ka)[4], int c, int kbg, bool masked) {
     const f32x16_t zero = {};
-    f32x16_t sacc = mma<DT>(ka[0], qf[0], zero);
+    f32x16_t sacc = mma<DT>(ka[0], qf[c][0], zero);
 #pragma unroll
     for (int ks = 1; ks < 4; ++ks)
-      sacc = mma<DT>(ka[ks], qf[ks], sacc);
-    const bool diag = g.causal && kbg == qb;
-    if (diag || (VK != kVtFull && 32 * kbg + 32 > S)) {
+      sacc = mma<DT>(ka[ks], qf[c][ks], sacc);
+    const bool diag = g.causal && kbg == QG * qt + c;
+    if (masked && (diag || (VK != kVtFull && 32 * kbg + 32 > S))) {
+      const int query = q0 + 32 * c + fr;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int key = 32 * kbg + 8 * (r >> 2) + 4 * h + (r & 3);
@@ -502,45 +534,92 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_long_kernel(AttnArgs g) 
     }
     return sacc;
   };
+  // A block is plain when every group needs it and none masks it: no key past
+  // s, no group's diagonal. Its groups then run as one branch-free stretch, so
+  // the scheduler can overlap one group's products with another's VALU work.
+  auto plain_block = [&](int kbg) {
+    return kbg < nkbc[0] && !(g.causal && kbg >= QG * qt) &&
+           !(VK != kVtFull && 32 * kbg + 32 > S);
+  };
 
   // pass 1: the row max
   if (nlive > 0) kblock_load(K, 32 * wave, S, lane, koff, gk);
-  float m = -INFINITY;
+  float m[QG];
+#pragma unroll
+  for (int c = 0; c < QG; ++c) m[c] = -INFINITY;
   for (int i = 0; i < nlive; ++i) {
     const int kbg = kAttnWaves * i + wave;
-    const f32x16_t sacc = scores(kbg, i + 1 < nlive ? kbg + kAttnWaves : -1);
+    u32x4_t ka[4];
+    stage_k(i + 1 < nlive ? kbg + kAttnWaves : -1, ka);
+    if (plain_block(kbg)) {
+      f32x16_t sacc[QG];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) m = fmaxf(m, sacc[r]);
+      for (int c = 0; c < QG; ++c) sacc[c] = scores(ka, c, kbg, false);
+#pragma unroll
+      for (int c = 0; c < QG; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) m[c] = fmaxf(m[c], sacc[c][r]);
+    } else {
+#pragma unroll
+      for (int c = 0; c < QG; ++c) {
+        if (kbg < nkbc[c]) {
+          const f32x16_t sacc = scores(ka, c, kbg, true);
+#pragma unroll
+          for (int r = 0; r < 16; ++r) m[c] = fmaxf(m[c], sacc[r]);
+        }
+      }
+    }
   }
   if (nlive > 0) {
     kblock_load(K, 32 * wave, S, lane, koff, gk);
     vblock_load<VK>(Vt, g.ldv, 32 * wave, S, VK != kVtFull && 32 * wave + 32 > S, lane, voff, gv);
   }
-  m = fmaxf(m, xor32(m));
-  if (lane < 32) s_max[wave][lane] = m;
+#pragma unroll
+  for (int c = 0; c < QG; ++c) {
+    m[c] = fmaxf(m[c], xor32(m[c]));
+    if (lane < 32) s_max[wave][32 * c + lane] = m[c];
+  }
   __syncthreads();
-  m = fmaxf(fmaxf(s_max[0][fr], s_max[1][fr]), fmaxf(s_max[2][fr], s_max[3][fr]));
-  const float c1 = (m == -INFINITY) ? 0.0f : __builtin_fmaf(-g.c0, m, MODE == EXACT ? 0.0f : kK127);
+  float c1[QG];
+#pragma unroll
+  for (int c = 0; c < QG; ++c) {
+    const int j = 32 * c + fr;
+    m[c] = fmaxf(fmaxf(s_max[0][j], s_max[1][j]), fmaxf(s_max[2][j], s_max[3][j]));
+    c1[c] = (m[c] == -INFINITY) ? 0.0f
+                                : __builtin_fmaf(-g.c0, m[c], MODE == EXACT ? 0.0f : kK127);
+  }
 
-  // pass 2: the scores again, their exponentials, the sum and O^T = V^T P
-  float part = 0.0f;
-  f32x16_t oacc[2] = {};
+  // pass 2: the scores again, their exponentials, the sums and O^T = V^T P
+  float part[QG];
+  f32x16_t oacc[QG][2];
+#pragma unroll
+  for (int c = 0; c < QG; ++c) {
+    part[c] = 0.0f;
+    oacc[c][0] = f32x16_t{};
+    oacc[c][1] = f32x16_t{};
+  }
   for (int i = 0; i < nlive; ++i) {
     const int kbg = kAttnWaves * i + wave;
     const int nb = kbg + kAttnWaves;
-    const f32x16_t sacc = scores(kbg, i + 1 < nlive ? nb : -1);
-    uint32_t pk[4][2];
+    u32x4_t ka[4];
+    stage_k(i + 1 < nlive ? nb : -1, ka);
+    uint32_t pk[QG][4][2];
+    auto exps = [&](const f32x16_t& sacc, int c) {
 #pragma unroll
-    for (int gi = 0; gi < 4; ++gi) {
-      float e[4];
+      for (int gi = 0; gi < 4; ++gi) {
+        float e[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        e[j] = qexp<MODE>(sacc[4 * gi + j], g.c0, c1);
-        part += e[j];
+        for (int j = 0; j < 4; ++j) {
+          e[j] = qexp<MODE>(sacc[4 * gi + j], g.c0, c1[c]);
+          part[c] += e[j];
+        }
+        pk[c][gi][0] = pack16<DT>(e[0], e[1]);
+        pk[c][gi][1] = pack16<DT>(e[2], e[3]);
       }
-      pk[gi][0] = pack16<DT>(e[0], e[1]);
-      pk[gi][1] = pack16<DT>(e[2], e[3]);
-    }
+    };
+#pragma unroll
+    for (int c = 0; c < QG; ++c)
+      if (kbg < nkbc[c]) exps(scores(ka, c, kbg, true), c);
     vblock_store(stage, lane, gv);
     if (i + 1 < nlive)
       vblock_load<VK>(Vt, g.ldv, 32 * nb, S, VK != kVtFull && 32 * nb + 32 > S, lane, voff, gv);
@@ -548,49 +627,60 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attn_long_kernel(AttnArgs g) 
     u32x4_t va[2][2];
     vblock_read(stage, fr, h, va);
     __builtin_amdgcn_wave_barrier();
+    auto pv = [&](int c) {
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const auto s0 = __builtin_amdgcn_permlane32_swap(pk[2 * ks][0], pk[2 * ks + 1][0], false, false);
-      const auto s1 = __builtin_amdgcn_permlane32_swap(pk[2 * ks][1], pk[2 * ks + 1][1], false, false);
-      const u32x4_t bv = {s0[0], s1[0], s0[1], s1[1]};
+      for (int ks = 0; ks < 2; ++ks) {
+        const auto s0 = __builtin_amdgcn_permlane32_swap(pk[c][2 * ks][0], pk[c][2 * ks + 1][0],
+                                                         false, false);
+        const auto s1 = __builtin_amdgcn_permlane32_swap(pk[c][2 * ks][1], pk[c][2 * ks + 1][1],
+                                                         false, false);
+        const u32x4_t bv = {s0[0], s1[0], s0[1], s1[1]};
 #pragma unroll
-      for (int db = 0; db < 2; ++db)
-        oacc[db] = mma<DT>(va[ks][db], bv, oacc[db]);
-    }
+        for (int db = 0; db < 2; ++db)
+          oacc[c][db] = mma<DT>(va[ks][db], bv, oacc[c][db]);
+      }
+    };
+#pragma unroll
+    for (int c = 0; c < QG; ++c)
+      if (kbg < nkbc[c]) pv(c);
   }
 
-  attn_finish<DT, kAttnWaves>(s_buf, s_sum, oacc, part, m, wave, lane, query, S,
-                              g.o + ((int64_t)bh * S + query) * kAttnD);
+  attn_finish<DT, kAttnWaves, QG>(s_buf, s_sum, oacc, part, m, wave, lane, q0, S,
+                                  g.o + (int64_t)bh * S * kAttnD);
 }
 
-// waves = 4, 8: the one-pass kernel with that many waves; 0: two passes
+// waves = 4, 8: the one-pass kernel with that many waves; 0: two passes with
+// qg groups of 32 queries per workgroup
 template <int DT, int MODE, int VK>
-void launch_attn_vk(int waves, dim3 grid, hipStream_t s, const AttnArgs& g) {
+void launch_attn_vk(int waves, int qg, dim3 grid, hipStream_t s, const AttnArgs& g) {
   if (waves == 4)
     hipLaunchKernelGGL((attn_kernel<DT, MODE, VK, 4>), grid, dim3(64 * 4), 0, s, g);
   else if (waves == 8)
     hipLaunchKernelGGL((attn_kernel<DT, MODE, VK, 8>), grid, dim3(64 * 8), 0, s, g);
+  else if (qg == 2)
+    hipLaunchKernelGGL((attn_long_kernel<DT, MODE, VK, 2>), grid, dim3(kAttnThreads), 0, s, g);
   else
-    hipLaunchKernelGGL((attn_long_kernel<DT, MODE, VK>), grid, dim3(kAttnThreads), 0, s, g);
+    hipLaunchKernelGGL((attn_long_kernel<DT, MODE, VK, 1>), grid, dim3(kAttnThreads), 0, s, g);
 }
 
 template <int DT, int MODE>
-void launch_attn_mode(int vk, int waves, dim3 grid, hipStream_t s, const AttnArgs& g) {
+void launch_attn_mode(int vk, int waves, int qg, dim3 grid, hipStream_t s, const AttnArgs& g) {
   if (vk == kVtFull)
-    launch_attn_vk<DT, MODE, kVtFull>(waves, grid, s, g);
+    launch_attn_vk<DT, MODE, kVtFull>(waves, qg, grid, s, g);
   else if (vk == kVtRagged)
-    launch_attn_vk<DT, MODE, kVtRagged>(waves, grid, s, g);
+    launch_attn_vk<DT, MODE, kVtRagged>(waves, qg, grid, s, g);
   else
-    launch_attn_vk<DT, MODE, kVtScalar>(waves, grid, s, g);
+    launch_attn_vk<DT, MODE, kVtScalar>(waves, qg, grid, s, g);
 }
 
 template <int DT>
-void launch_attn(int mode, int vk, int waves, dim3 grid, hipStream_t s, const AttnArgs& g) {
+void launch_attn(int mode, int vk, int waves, int qg, dim3 grid, hipStream_t s,
+                 const AttnArgs& g) {
   switch (mode) {
-    case QUAKE_EXACT: launch_attn_mode<DT, EXACT>(vk, waves, grid, s, g); break;
-    case QUAKE_1: launch_attn_mode<DT, Q1>(vk, waves, grid, s, g); break;
-    case QUAKE_2: launch_attn_mode<DT, Q2>(vk, waves, grid, s, g); break;
-    default: launch_attn_mode<DT, Q2M>(vk, waves, grid, s, g); break;
+    case QUAKE_EXACT: launch_attn_mode<DT, EXACT>(vk, waves, qg, grid, s, g); break;
+    case QUAKE_1: launch_attn_mode<DT, Q1>(vk, waves, qg, grid, s, g); break;
+    case QUAKE_2: launch_attn_mode<DT, Q2>(vk, waves, qg, grid, s, g); break;
+    default: launch_attn_mode<DT, Q2M>(vk, waves, qg, grid, s, g); break;
   }
 }
 
@@ -613,22 +703,26 @@ extern "C" quake_status quake_attention(const void* q, const void* k, const void
   if (q == nullptr || k == nullptr || vt == nullptr || o == nullptr) return QUAKE_EINVAL;
   if (!aligned16(q) || !aligned16(k) || ((uintptr_t)vt & 1u) != 0 || ((uintptr_t)o & 7u) != 0)
     return QUAKE_EINVAL;
-  const int64_t qblocks = (seq + kAttnQ - 1) / kAttnQ;
-  if (heads > INT32_MAX / qblocks || heads * ldv * kAttnD > INT64_MAX / 4) return QUAKE_EINVAL;
+  // one pass with 4 key blocks per wave (128 keys), else two passes
+  const int waves = seq <= 512 ? 4 : seq <= kAttnMaxS ? 8 : 0;
+  const int64_t tiles2 = (seq + 2 * kAttnQ - 1) / (2 * kAttnQ);   // per head, with two groups
+  const int64_t min_tiles = causal ? kAttnLongQGMinTilesCausal : kAttnLongQGMinTiles;
+  const int qg = (waves == 0 && heads >= (min_tiles + tiles2 - 1) / tiles2) ? 2 : 1;
+  const int64_t tile = kAttnQ * qg;   // queries per workgroup
+  const int64_t qtiles = (seq + tile - 1) / tile;
+  if (heads > INT32_MAX / qtiles || heads * ldv * kAttnD > INT64_MAX / 4) return QUAKE_EINVAL;
   const AttnArgs g{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                    static_cast<const uint16_t*>(vt), static_cast<uint16_t*>(o), (int32_t)seq,
-                   (int32_t)ldv, (int32_t)qblocks, c0, (uint32_t)(causal != 0),
+                   (int32_t)ldv, (int32_t)qtiles, c0, (uint32_t)(causal != 0),
                    (uint32_t)(heads % 8 == 0 ? heads / 8 : 0)};
-  const dim3 grid((uint32_t)(heads * qblocks));
+  const dim3 grid((uint32_t)(heads * qtiles));
   const hipStream_t s = static_cast<hipStream_t>(stream);
   // 16-byte rows, and byte offsets within a 64-row block of V^T that fit 32 bits
   const bool vec = aligned16(vt) && ldv % 8 == 0 && ldv <= (1 << 24);
   const int vk = !vec ? kVtScalar : (seq % 32 == 0 ? kVtFull : kVtRagged);
-  // one pass with 4 key blocks per wave (128 keys), else two passes
-  const int waves = seq <= 512 ? 4 : seq <= kAttnMaxS ? 8 : 0;
   if (dtype == QUAKE_BF16)
-    launch_attn<BF16>(mode, vk, waves, grid, s, g);
+    launch_attn<BF16>(mode, vk, waves, qg, grid, s, g);
   else
-    launch_attn<F16>(mode, vk, waves, grid, s, g);
+    launch_attn<F16>(mode, vk, waves, qg, grid, s, g);
   return launch_status();
 }

@@ -19,9 +19,11 @@ within one bfloat16 ulp of the oracle (probability roundings rarely flip).
 Cases: every mode, causal and not, one to several 32-query tiles, a ragged
 last tile, ragged key blocks, each one-pass workgroup size (4 waves up to 512
 keys, 8 up to 1024) with its longest sequence, longer ones (the two-pass
-kernel, from 1025 keys), a single key, padded v^T rows
-whose padding is NaN, and the full 96-head x 512 workload in the launch
-configuration the benchmark times, compared element by element."""
+kernel, from 1025 keys, with one or two 32-query groups per tile, including
+last tiles whose second group lies partly or wholly past the sequence), a
+single key, padded v^T rows whose padding is NaN, and the full 96-head x 512
+workload in the launch configuration the benchmark times, compared element by
+element."""
 import numpy as np
 import pytest
 import torch
@@ -182,6 +184,67 @@ def test_long_sequences_match_oracle(q, mode, causal, heads, seq):
 def test_two_pass_sequences_match_oracle(q, mode, causal, heads, seq):
     g, r, ins = _run(q, heads, seq, mode, causal, 75 + seq)
     _check(g, r, ins, seq, causal, "two-pass h%d s%d m%d c%d" % (heads, seq, mode, causal))
+
+
+def _two_group_heads(seq, causal):
+    """The fewest heads for which the two-pass kernel takes tiles of two
+    32-query groups: 512 such tiles of 64 queries without the mask, 1024 with
+    it (below that it takes one group per tile)."""
+    tiles = -(-seq // 64)
+    return -(-(1024 if causal else 512) // tiles)
+
+
+# ragged tails where the last tile's second group is partly (1130) or wholly
+# (1100, 1056) past s, and a key block past the last full one (2049)
+TWO_GROUP_SEQS = [1130, 1056, 2049]
+
+
+@pytest.mark.parametrize("mode", [0, 1, 2, 3])
+@pytest.mark.parametrize("causal", [True, False])
+def test_two_group_two_pass_matches_oracle(q, mode, causal):
+    heads = _two_group_heads(1100, causal)
+    g, r, ins = _run(q, heads, 1100, mode, causal, 85)
+    _check(g, r, ins, 1100, causal, "two-group h%d s1100 m%d c%d" % (heads, mode, causal))
+
+
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("seq", TWO_GROUP_SEQS)
+def test_two_group_ragged_tails_match_oracle(q, causal, seq):
+    heads = _two_group_heads(seq, causal)
+    g, r, ins = _run(q, heads, seq, 2, causal, 86 + seq)
+    _check(g, r, ins, seq, causal, "two-group h%d s%d c%d" % (heads, seq, causal))
+
+
+@pytest.mark.parametrize("ldv", [1103, 1104])
+@pytest.mark.parametrize("causal", [True, False])
+def test_two_group_padded_vt_rows(q, causal, ldv):
+    heads = _two_group_heads(1100, causal)
+    g, r, ins = _run(q, heads, 1100, 2, causal, 87, ldv=ldv, pad=float("nan"))
+    _check(g, r, ins, 1100, causal, "two-group padded h%d ldv%d c%d" % (heads, ldv, causal))
+
+
+@pytest.mark.parametrize("mode", [0, 2])
+@pytest.mark.parametrize("causal", [True, False])
+def test_two_group_binary16_matches_oracle(q, mode, causal):
+    heads = _two_group_heads(1100, causal)
+    g, r, ins = _run(q, heads, 1100, mode, causal, 88, dt="f16")
+    _check(g, r, ins, 1100, causal, "two-group f16 h%d m%d c%d" % (heads, mode, causal), dt="f16")
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_two_group_and_one_group_give_the_same_bits(q, causal):
+    """Enough heads of 1100 keys for two-group tiles; each head alone (too few
+    tiles for two groups) runs as one-group tiles. Per query the arithmetic
+    is the same, so the outputs must agree bit for bit."""
+    heads = _two_group_heads(1100, causal)
+    say("attention two-group vs one-group heads=%d causal=%d" % (heads, causal))
+    qc, kc, vtc = synth.attention_inputs(heads, 1100, 89)
+    qg, kg, vtg = qc.to("cuda:0"), kc.to("cuda:0"), vtc.to("cuda:0")
+    whole = q.quake_attention(qg, kg, vtg, mode=2, t=T, causal=causal)
+    for hd in (0, heads // 2, heads - 1):
+        one = q.quake_attention(qg[hd:hd + 1].contiguous(), kg[hd:hd + 1].contiguous(),
+                                vtg[hd:hd + 1].contiguous(), mode=2, t=T, causal=causal)
+        assert torch.equal(one[0].view(torch.int16), whole[hd].view(torch.int16)), hd
 
 
 @pytest.mark.parametrize("seq,ldv", [(777, 781), (777, 784), (1111, 1115), (2100, 2103),
