@@ -29,6 +29,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <type_traits>
 
 #include "quake_device.hpp"
 #include "quake_host.hpp"
@@ -397,17 +398,24 @@ __global__ __launch_bounds__(64 * W, W == 4 ? 4 : 1) void attn_kernel(AttnArgs g
   const float c1 = (m == -INFINITY) ? 0.0f : __builtin_fmaf(-g.c0, m, MODE == EXACT ? 0.0f : kK127);
   float part = 0.0f;
   uint32_t pk[kAttnBlk][4][2];
+  // the folded clamp (qexp_row) where registers allow a second copy of the
+  // loop: with four waves the kernel is held to 128 VGPRs
+  const bool below = W == 8 && row_c1_below(c1);
 #pragma unroll
   for (int i = 0; i < kAttnBlk; ++i) {
     if (i < nlive) {
 #pragma unroll
       for (int gi = 0; gi < 4; ++gi) {
         float e[4];
+        if (W == 8 && below) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          e[j] = qexp<MODE>(sacc[i][4 * gi + j], g.c0, c1);
-          part += e[j];
+          for (int j = 0; j < 4; ++j) e[j] = qexp_row<MODE, true>(sacc[i][4 * gi + j], g.c0, c1);
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) e[j] = qexp<MODE>(sacc[i][4 * gi + j], g.c0, c1);
         }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) part += e[j];
         pk[i][gi][0] = pack16<DT>(e[0], e[1]);
         pk[i][gi][1] = pack16<DT>(e[2], e[3]);
       }
@@ -588,6 +596,9 @@ __global__ __launch_bounds__(kAttnThreads, QG == 1 ? 3 : 2) void attn_long_kerne
     c1[c] = (m[c] == -INFINITY) ? 0.0f
                                 : __builtin_fmaf(-g.c0, m[c], MODE == EXACT ? 0.0f : kK127);
   }
+  bool below = true;
+#pragma unroll
+  for (int c = 0; c < QG; ++c) below = below && row_c1_below(c1[c]);
 
   // pass 2: the scores again, their exponentials, the sums and O^T = V^T P
   float part[QG];
@@ -604,13 +615,13 @@ __global__ __launch_bounds__(kAttnThreads, QG == 1 ? 3 : 2) void attn_long_kerne
     u32x4_t ka[4];
     stage_k(i + 1 < nlive ? nb : -1, ka);
     uint32_t pk[QG][4][2];
-    auto exps = [&](const f32x16_t& sacc, int c) {
+    auto exps = [&](const f32x16_t& sacc, int c, auto below) {
 #pragma unroll
       for (int gi = 0; gi < 4; ++gi) {
         float e[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          e[j] = qexp<MODE>(sacc[4 * gi + j], g.c0, c1[c]);
+          e[j] = qexp_row<MODE, decltype(below)::value>(sacc[4 * gi + j], g.c0, c1[c]);
           part[c] += e[j];
         }
         pk[c][gi][0] = pack16<DT>(e[0], e[1]);
@@ -618,8 +629,15 @@ __global__ __launch_bounds__(kAttnThreads, QG == 1 ? 3 : 2) void attn_long_kerne
       }
     };
 #pragma unroll
-    for (int c = 0; c < QG; ++c)
-      if (kbg < nkbc[c]) exps(scores(ka, c, kbg, true), c);
+    for (int c = 0; c < QG; ++c) {
+      if (kbg < nkbc[c]) {
+        const f32x16_t sacc = scores(ka, c, kbg, true);
+        if (below)
+          exps(sacc, c, std::true_type{});
+        else
+          exps(sacc, c, std::false_type{});
+      }
+    }
     vblock_store(stage, lane, gv);
     if (i + 1 < nlive)
       vblock_load<VK>(Vt, g.ldv, 32 * nb, S, VK != kVtFull && 32 * nb + 32 > S, lane, voff, gv);

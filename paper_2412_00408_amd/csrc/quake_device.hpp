@@ -46,11 +46,10 @@ __device__ __forceinline__ uint32_t umin32(uint32_t a, uint32_t b) { return a < 
 __device__ __forceinline__ float as_f(uint32_t u) { return __builtin_bit_cast(float, u); }
 __device__ __forceinline__ uint32_t as_u(float f) { return __builtin_bit_cast(uint32_t, f); }
 
-// QuAKE / QuAKE2 of an already affine-mapped argument l (Eq. 5 applied).
+// QuAKE / QuAKE2 from z, the truncated integer of the clamped argument
+// (Eq. 3): Eq. 2 reads z as a binary32, Algorithm 1 refines its mantissa.
 template <int MODE>
-__device__ __forceinline__ float quake_of_l(float l) {
-  l = __builtin_amdgcn_fmed3f(l, 0.0f, kLHi);
-  const uint32_t z = (uint32_t)(int32_t)l;
+__device__ __forceinline__ float quake_of_z(uint32_t z) {
   if constexpr (MODE == Q1) {
     return as_f(z);
   } else if constexpr (MODE == Q2) {
@@ -69,6 +68,26 @@ __device__ __forceinline__ float quake_of_l(float l) {
   }
 }
 
+// QuAKE / QuAKE2 of an already affine-mapped argument l (Eq. 5 applied).
+template <int MODE>
+__device__ __forceinline__ float quake_of_l(float l) {
+  l = __builtin_amdgcn_fmed3f(l, 0.0f, kLHi);
+  return quake_of_z<MODE>((uint32_t)(int32_t)l);
+}
+
+// The same for an argument l known to stay below 255 * 2^23 (Algorithm 2
+// with a row constant |c1| < 2^54: for x <= m, l = fma(x, c0, c1) is at most
+// 127 * 2^23 plus half an ulp of c1, < 2^29). v_cvt_u32_f32 truncates and
+// saturates negative arguments to 0, which is the lower clamp, and the upper
+// clamp cannot act, so the bits are those of quake_of_l with one instruction
+// fewer.
+template <int MODE>
+__device__ __forceinline__ float quake_of_l_below(float l) {
+  uint32_t z;
+  asm("v_cvt_u32_f32 %0, %1" : "=v"(z) : "v"(l));
+  return quake_of_z<MODE>(z);
+}
+
 // e^(p x + q) with c0, c1 folded on the host (Eq. 5). EXACT: the same fused
 // binary32 argument in base 2, exponentiated by the hardware v_exp_f32.
 template <int MODE>
@@ -79,6 +98,22 @@ __device__ __forceinline__ float qexp(float x, float c0, float c1) {
   } else {
     return quake_of_l<MODE>(l);
   }
+}
+
+// qexp for Algorithm 2's exponentials, x <= the row max m: with BELOW (every
+// lane's |c1| < 2^54, see quake_of_l_below) the clamp is folded into the
+// conversion.
+template <int MODE, bool BELOW>
+__device__ __forceinline__ float qexp_row(float x, float c0, float c1) {
+  if constexpr (MODE == EXACT || !BELOW) {
+    return qexp<MODE>(x, c0, c1);
+  } else {
+    return quake_of_l_below<MODE>(__builtin_fmaf(x, c0, c1));
+  }
+}
+// whether every lane of the wave may take qexp_row<MODE, true> with its c1
+__device__ __forceinline__ bool row_c1_below(float c1) {
+  return __all(__builtin_fabsf(c1) < 0x1p54f) != 0;
 }
 
 // num / (1 + e) with one v_rcp_f32. Both operands are scaled by 1/4 (exact
