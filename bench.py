@@ -89,6 +89,9 @@ def parse():
     ap.add_argument("--section", choices=["attention", "linear_gelu"],
                     help="time only the fused attention (quake_attention) or the fused "
                          "linear+GELU (quake_linear_gelu) and print its JSON (for profiler passes)")
+    ap.add_argument("--attn-config", default=None,
+                    help="with --section attention: only this heads x seq, optionally with "
+                         ":causal or :noncausal, e.g. 32x2048:noncausal (for counter passes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-table4", action="store_true",
@@ -579,7 +582,7 @@ def linear_gelu(q, timer, synth, a):
     return out
 
 
-def fused_attention(q, timer, synth, a, heads=96, seq=512):
+def fused_attention(q, timer, synth, a, heads=96, seq=512, masks=(1, 0)):
     """softmax(t q k^T) v over the attention workload's heads (8 x 12 heads,
     512 tokens, head dimension 64, bf16, t = 1/8; or another heads x seq) in one kernel
     (quake_attention), causal and not, in every mode, against the explicit
@@ -611,6 +614,8 @@ def fused_attention(q, timer, synth, a, heads=96, seq=512):
     vs = [vt.transpose(1, 2).contiguous() for _, _, vt, _ in sets[:2]]
     vs_all = vs + [vt.transpose(1, 2).contiguous() for _, _, vt, _ in sets[2:]]
     for causal, name in ((1, "causal"), (0, "noncausal")):
+        if causal not in masks:
+            continue
         fns = {}
         for mname, mid in MODE_IDS.items():
             def f(i, stream, mid=mid, causal=causal):
@@ -899,10 +904,17 @@ def main():
                 q.quake_attention(qg, kg, vg, mode=MODE_IDS[a.mode], t=0.125)
             torch.cuda.synchronize()
             del qg, kg, vg
-        print(json.dumps({"attention_bf16_96x512x64": fused_attention(q, timer, synth, a),
-                          "attention_bf16_64x1024x64": fused_attention(q, timer, synth, a, 64, 1024),
-                          "attention_bf16_32x2048x64": fused_attention(q, timer, synth, a, 32, 2048)}),
-              flush=True)
+        if a.attn_config:
+            shape, _, mask = a.attn_config.partition(":")
+            heads, seq = (int(v) for v in shape.split("x"))
+            masks = {"causal": (1,), "noncausal": (0,), "": (1, 0)}[mask]
+            res = {"attention_bf16_%dx%dx64" % (heads, seq):
+                   fused_attention(q, timer, synth, a, heads, seq, masks)}
+        else:
+            res = {"attention_bf16_96x512x64": fused_attention(q, timer, synth, a),
+                   "attention_bf16_64x1024x64": fused_attention(q, timer, synth, a, 64, 1024),
+                   "attention_bf16_32x2048x64": fused_attention(q, timer, synth, a, 32, 2048)}
+        print(json.dumps(res), flush=True)
         write_windows(a, timer)
         return
     if a.section == "linear_gelu":

@@ -63,3 +63,14 @@ def test_trace_summary_takes_the_timed_half(tmp_path):
     assert cells[2] == "18" and float(cells[3]) == 40.0 and cells[5] == "40" and cells[6] == "40"
     assert float(cells[7]) == 10.0                       # 400 bytes / 40 ns
     assert float(cells[9]) == 1000.0                     # starts 1000 ns apart
+
+
+def test_attention_config_filter_parses(monkeypatch):
+    """--attn-config selects one heads x seq shape and optionally one mask of
+    the attention section (used for counter passes)."""
+    monkeypatch.setattr(sys, "argv", ["bench.py", "--section", "attention",
+                                      "--attn-config", "32x2048:noncausal"])
+    a = bench.parse()
+    assert a.section == "attention" and a.attn_config == "32x2048:noncausal"
+    shape, _, mask = a.attn_config.partition(":")
+    assert tuple(int(v) for v in shape.split("x")) == (32, 2048) and mask == "noncausal"
