@@ -78,6 +78,21 @@ def test_shapes_and_modes(q, m, n, k, mode, dt):
                "linear %s %dx%dx%d mode %d gelu %d" % (dt, m, n, k, mode, gelu), dt)
 
 
+# a grid of at most one tile per CU over k >= 1024 loads every slab two slabs
+# ahead into a second register set: odd and even slab counts, a k tail,
+# ragged m and n, both tile widths
+@pytest.mark.parametrize("m,n,k", [(128, 192, 1024), (200, 130, 1032), (1, 1, 2056),
+                                   (129, 576, 1096), (300, 384, 4096)])
+@pytest.mark.parametrize("mode", [0, 2])
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+def test_long_k_two_slabs_ahead(q, m, n, k, mode, dt):
+    for gelu in (True, False):
+        say("linear gelu long k", dt, m, n, k, mode, gelu)
+        g, r, xb, wb = _run(q, m, n, k, mode, gelu, 1650 + m % 7 + n % 5, dt=dt)
+        _check(g, r, xb, wb, k, 2.0 if gelu else 1.0,
+               "linear long k %s %dx%dx%d mode %d gelu %d" % (dt, m, n, k, mode, gelu), dt)
+
+
 def test_strided_rows(q):
     say("linear gelu strided")
     g, r, xb, wb = _run(q, 256, 256, 768, 2, True, 1700, pad=24)
@@ -117,3 +132,13 @@ def test_bert_mlp_shape(q, mode, dt):
     # most outputs are the oracle's 16-bit value itself (binary16 has 3 more
     # bits, so more of them differ by the accumulation order)
     assert np.count_nonzero(err == 0) > (0.95 if dt == "bf16" else 0.75) * err.size
+
+
+def test_bert_down_projection_shape(q):
+    """The down-projection of a BERT-base MLP over 4096 tokens, [4096, 3072] x
+    [768, 3072]^T, the product alone: 128 tiles over k = 3072, so the slabs go
+    two ahead."""
+    say("linear 4096x768x3072")
+    g, r, xb, wb = _run(q, 4096, 768, 3072, 2, False, 1850)
+    err = _check(g, r, xb, wb, 3072, 1.0, "bert down projection")
+    assert np.count_nonzero(err == 0) > 0.9 * err.size
