@@ -64,7 +64,8 @@ def _run(q, m, n, k, mode, gelu, seed, pad=0, dt="bf16"):
     return host_bits(y), ref, xb, wb
 
 
-# n a multiple of 192 takes the 128 x 192 tile, other n the 128 x 128 tile
+# grids below one 128 x 192 tile per CU (256 CUs) take the 128 x 128 tile,
+# whatever n; the wide tile is tested below
 @pytest.mark.parametrize("m,n,k", [(128, 128, 64), (256, 384, 768), (200, 130, 72), (1, 1, 8),
                                    (129, 257, 136), (64, 1000, 32), (200, 192, 72),
                                    (129, 576, 136), (1, 192, 8)])
@@ -91,6 +92,19 @@ def test_long_k_two_slabs_ahead(q, m, n, k, mode, dt):
         g, r, xb, wb = _run(q, m, n, k, mode, gelu, 1650 + m % 7 + n % 5, dt=dt)
         _check(g, r, xb, wb, k, 2.0 if gelu else 1.0,
                "linear long k %s %dx%dx%d mode %d gelu %d" % (dt, m, n, k, mode, gelu), dt)
+
+
+# n a multiple of 192 with at least one 128 x 192 tile per CU takes the wide
+# tile: a ragged last tile row and a k tail, and exactly 256 tiles over
+# k >= 1024 (the wide tile with slabs two ahead)
+@pytest.mark.parametrize("m,n,k,mode,dt", [(2043, 3072, 72, 2, "bf16"), (2043, 3072, 72, 0, "f16"),
+                                           (2048, 3072, 1032, 2, "bf16"), (2048, 3072, 1032, 3, "f16")])
+def test_wide_tile_grid(q, m, n, k, mode, dt):
+    for gelu in (True, False):
+        say("linear gelu wide tiles", dt, m, n, k, mode, gelu)
+        g, r, xb, wb = _run(q, m, n, k, mode, gelu, 1670 + m % 7, dt=dt)
+        _check(g, r, xb, wb, k, 2.0 if gelu else 1.0,
+               "linear wide %s %dx%dx%d mode %d gelu %d" % (dt, m, n, k, mode, gelu), dt)
 
 
 def test_strided_rows(q):
@@ -136,8 +150,8 @@ def test_bert_mlp_shape(q, mode, dt):
 
 def test_bert_down_projection_shape(q):
     """The down-projection of a BERT-base MLP over 4096 tokens, [4096, 3072] x
-    [768, 3072]^T, the product alone: 128 tiles over k = 3072, so the slabs go
-    two ahead."""
+    [768, 3072]^T, the product alone: 192 tiles of 128 x 128 (the wide tile
+    would leave half the CUs idle) over k = 3072, so the slabs go two ahead."""
     say("linear 4096x768x3072")
     g, r, xb, wb = _run(q, 4096, 768, 3072, 2, False, 1850)
     err = _check(g, r, xb, wb, 3072, 1.0, "bert down projection")

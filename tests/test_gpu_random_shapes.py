@@ -125,9 +125,10 @@ def test_random_elementwise(q, op, n, dt, mode, a, b, seed):
 
 
 def _linear_cases(n, seed):
-    """(m, n, k, mode, dt, gelu, pad, seed): output widths on both sides of
-    the 192- and 128-wide tiles, ragged m and n, k a multiple of 8 from one
-    slab to several with a tail, operand rows padded to a longer stride."""
+    """(m, n, k, mode, dt, gelu, pad, seed): output widths around multiples
+    of 128 and 192 (grids this small take the 128-wide tile), ragged m and n,
+    k a multiple of 8 from one slab to several with a tail, operand rows
+    padded to a longer stride."""
     rng = np.random.default_rng(seed)
     out = []
     while len(out) < n:
