@@ -297,7 +297,8 @@ quake_status quake_exp16(const void* x, void* y, int64_t n, quake_dtype dtype, q
  *   w : device, n x k 16-bit (a linear layer's weight), row r at w + r*ldw,
  *       16-byte aligned.
  *   y : device, m x n 16-bit, row r at y + r*ldy.
- *   k, ldx, ldw: multiples of 8; ldx, ldw >= k; ldy >= n.
+ *   k, ldx, ldw: multiples of 8; ldx, ldw >= k; ldy >= n; k <= 2^31 - 257,
+ *       m <= 2^31 - 129, n <= 2^31 - 193.
  *   dtype : QUAKE_BF16 or QUAKE_F16 (binary16), the format of x, w and y
  *       (else QUAKE_EDTYPE); mode: any quake_mode.
  * Products are accumulated in binary32 (order unspecified), then the GELU of

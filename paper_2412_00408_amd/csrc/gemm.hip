@@ -280,7 +280,9 @@ extern "C" quake_status quake_linear_gelu(const void* x, const void* w, void* y,
   if (k == 0 || k % 8 != 0 || x == nullptr || w == nullptr || y == nullptr) return QUAKE_EINVAL;
   if (ldx < k || ldw < k || ldy < n || ldx % 8 != 0 || ldw % 8 != 0) return QUAKE_EINVAL;
   if (!aligned16(x) || !aligned16(w)) return QUAKE_EINVAL;
-  if (m > INT32_MAX - kBM || n > INT32_MAX - kMaxBN || k > INT32_MAX - kBK) return QUAKE_EINVAL;
+  // 32-bit row, column and k arithmetic in the kernel: the last slab loaded
+  // (two slabs ahead) starts below k + 2 kBK
+  if (m > INT32_MAX - kBM || n > INT32_MAX - kMaxBN || k > INT32_MAX - 4 * kBK) return QUAKE_EINVAL;
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)

@@ -205,6 +205,8 @@ def test_linear_gelu_validation(q):
     assert call(w=A + 8) == q.EINVAL
     assert call(y=0) == q.EINVAL
     assert call(m=-1) == q.EINVAL
+    big = (1 << 31) - 128                                  # within two slabs of 2^31
+    assert call(k=big, ldx=big, ldw=big) == q.EINVAL
 
 
 def test_attention_validation(q):
