@@ -87,8 +87,9 @@ def parse():
     ap.add_argument("--only", action="store_true",
                     help="time only --workload in --mode (for profiler passes)")
     ap.add_argument("--section", choices=["attention", "linear_gelu"],
-                    help="time only the fused attention (quake_attention) or the fused "
-                         "linear+GELU (quake_linear_gelu) and print its JSON (for profiler passes)")
+                    help="time only the fused attention (quake_attention) or "
+                         "quake_linear_gelu (the BERT-base MLP's up-projection with its GELU, "
+                         "and its down-projection) and print its JSON (for profiler passes)")
     ap.add_argument("--attn-config", default=None,
                     help="with --section attention: only this heads x seq, optionally with "
                          ":causal or :noncausal, e.g. 32x2048:noncausal (for counter passes)")
@@ -582,6 +583,44 @@ def linear_gelu(q, timer, synth, a):
     return out
 
 
+def linear_down(q, timer, synth, a):
+    """The down-projection of the same BERT-base MLP, x [4096, 3072] times
+    w [768, 3072]^T in bf16, the product alone (no activation follows it in
+    the model): a grid too small for the 128 x 192 tile to cover the CUs, so
+    quake_linear_gelu takes 192 tiles of 128 x 128 and loads each slab two
+    ahead. torch.matmul (the vendor BLAS) on the same operands for context.
+    Eight rotating operand sets (about 290 MB)."""
+    import torch
+    m, n, k = 4096, 768, 3072
+    nb = 8
+    xs = [synth.normal((m, k), 1.0, "bf16", 1960 + i).to("cuda:0") for i in range(nb)]
+    ws = [synth.normal((n, k), 0.02, "bf16", 1980 + i).to("cuda:0") for i in range(nb)]
+    ys = [torch.empty((m, n), dtype=torch.bfloat16, device="cuda:0") for _ in range(nb)]
+    wts = [w.t().contiguous() for w in ws]
+    flop = 2.0 * m * n * k
+    L = q.lib
+
+    def product(i, stream):
+        i %= nb
+        return L.quake_linear_gelu(xs[i].data_ptr(), ws[i].data_ptr(), ys[i].data_ptr(), m, n, k,
+                                   k, k, n, 2, 2, 0, stream)
+
+    def vendor(i, stream):
+        i %= nb
+        torch.matmul(xs[i], wts[i], out=ys[i])
+
+    r = graph_ms(timer, {"linear_down:product": product, "linear_down:torch_matmul": vendor}, nb)
+    ms0, mst = r["linear_down:product"], r["linear_down:torch_matmul"]
+    out = {"shape_mnk": [m, n, k], "flop": flop, "peak_tflops": PEAK_BF16_TFLOPS,
+           "launch": "graph: %d launches per window, %d windows, median" % (nb, timer.windows),
+           "product_ms": ms0, "torch_matmul_ms": mst,
+           "product_tflops": round(flop / (ms0 * 1e-3) / 1e12, 1),
+           "product_frac_of_peak": round(flop / (ms0 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+           "product_vs_torch_matmul": round(mst / ms0, 4)}
+    del xs, ws, ys, wts
+    return out
+
+
 def fused_attention(q, timer, synth, a, heads=96, seq=512, masks=(1, 0)):
     """softmax(t q k^T) v over the attention workload's heads (8 x 12 heads,
     512 tokens, head dimension 64, bf16, t = 1/8; or another heads x seq) in one kernel
@@ -926,7 +965,8 @@ def main():
                 q.quake_linear_gelu(xg, wg, mode=MODE_IDS[a.mode])
             torch.cuda.synchronize()
             del xg, wg
-        print(json.dumps({"linear_gelu_bf16_4096x3072x768": linear_gelu(q, timer, synth, a)}),
+        print(json.dumps({"linear_gelu_bf16_4096x3072x768": linear_gelu(q, timer, synth, a),
+                          "linear_bf16_4096x768x3072": linear_down(q, timer, synth, a)}),
               flush=True)
         write_windows(a, timer)
         return
@@ -1012,6 +1052,7 @@ def main():
             torch.cuda.empty_cache()
         sec["exp_f16_2p28"] = native16(q, timer, synth, a)
         sec["linear_gelu_bf16_4096x3072x768"] = linear_gelu(q, timer, synth, a)
+        sec["linear_bf16_4096x768x3072"] = linear_down(q, timer, synth, a)
         sec["attention_bf16_96x512x64"] = fused_attention(q, timer, synth, a)
         sec["attention_bf16_64x1024x64"] = fused_attention(q, timer, synth, a, 64, 1024)
         sec["attention_bf16_32x2048x64"] = fused_attention(q, timer, synth, a, 32, 2048)
