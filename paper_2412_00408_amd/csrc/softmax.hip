@@ -33,6 +33,7 @@
 
 #include <algorithm>
 #include <mutex>
+#include <type_traits>
 
 #include "quake_device.hpp"
 #include "quake_host.hpp"
@@ -93,6 +94,21 @@ __device__ __forceinline__ RowExp<MODE, FUSE> row_exp(const SmConst& k, float m)
   } else {
     return RowExp<MODE, FUSE>{k.c0, k.c1s, m == -INFINITY ? 0.0f : m, k.t};
   }
+}
+
+// The exponential of one entry with the clamp folded into the conversion
+// (BELOW: every entry is at most the row max and |c1| < 2^54, so the upper
+// clamp cannot act): the bits of ex(v) with one instruction fewer.
+template <bool BELOW, int MODE, bool FUSE>
+__device__ __forceinline__ float row_exp_at(const RowExp<MODE, FUSE>& ex, float v) {
+  if constexpr (FUSE && BELOW) return qexp_row<MODE, true>(v, ex.c0, ex.c1);
+  else return ex(v);
+}
+// whether the wave may take row_exp_at<true>
+template <int MODE, bool FUSE>
+__device__ __forceinline__ bool row_exp_below(const RowExp<MODE, FUSE>& ex) {
+  if constexpr (FUSE && MODE != EXACT) return row_c1_below(ex.c1);
+  else return false;
 }
 
 // Implicit causal mask: row r (global index) uses only its first
@@ -516,18 +532,27 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
   }
 
   // second exchange: the chunk sums against the row's final max
+  // the exponentials sit between the two exchanges, on the critical path: the
+  // folded clamp where the row constant allows it (same bits)
   const RowExp<MODE, FUSE> ex = row_exp<MODE, FUSE>(kc, m);
   double acc = 0.0;
+  auto exps = [&](auto below) {
+    constexpr bool B = decltype(below)::value;
 #pragma unroll
-  for (int k = 0; k < NV; ++k) {
-    float part = 0.0f;
+    for (int k = 0; k < NV; ++k) {
+      float part = 0.0f;
 #pragma unroll
-    for (int j = 0; j < V; ++j) {
-      f[k][j] = ex(f[k][j]);
-      part += f[k][j];
+      for (int j = 0; j < V; ++j) {
+        f[k][j] = row_exp_at<B>(ex, f[k][j]);
+        part += f[k][j];
+      }
+      acc += (double)part;
     }
-    acc += (double)part;
-  }
+  };
+  if (row_exp_below(ex))
+    exps(std::true_type{});
+  else
+    exps(std::false_type{});
   double total = wave_sum(acc);
   if (lane == 0) s_sum[wave] = total;
   __syncthreads();
