@@ -20,15 +20,20 @@
 //                         too long for a peer computes the peer's value from x
 //                         itself (same bits), so no wait depends on the peers
 //                         being resident.
-//   sm_long               the same rows without a workspace: one 1024-thread
-//                         workgroup per row, three passes (max, sum,
-//                         normalise), the re-reads served by the caches.
+//   sm_res                the same rows without a workspace, up to 129024
+//                         (binary32) or 131072 (16-bit) elements: one
+//                         512-thread workgroup per row holds the row in VGPRs
+//                         and LDS (one read, each exponential taken once).
+//   sm_long               longer or causal rows without a workspace: one
+//                         1024-thread workgroup per row, three passes (max,
+//                         sum, normalise), the re-reads served by the caches.
 //   sm_generic            any alignment / stride / length: one workgroup per
 //                         row, three passes (max, sum, normalise) with scalar
 //                         accesses; the re-reads are served by the caches.
 // Sums: fp32 within one 16-byte vector (at most 8 terms), then, in a fixed
 // order, double across vectors, lanes, waves and workgroups for binary32
-// outputs and fp32 for 16-bit outputs (double across split workgroups).
+// outputs and fp32 for 16-bit outputs in the row kernels (double in the split,
+// resident and long kernels).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -705,6 +710,137 @@ __global__ __launch_bounds__(kLongBlock) void sm_long_kernel(const char* __restr
 }
 
 // ---------------------------------------------------------------------------
+// Rows without a workspace that fit one workgroup (up to 129024 binary32 or
+// 131072 16-bit elements): one 512-thread workgroup per row reads the row once
+// and keeps it, NK 16-byte vectors per thread in VGPRs and NL more per thread
+// in LDS as binary32, so every exponential is taken once and nothing is read
+// twice. Thread t holds vectors k * 512 + t. Whole blocks of 512 vectors past
+// the row's end are skipped (a workgroup-uniform branch); inside the last
+// block, lanes past the end load the last vector again, which leaves the max
+// unchanged, is left out of the sum and is never stored. REGFULL: every
+// register block lies inside the row, so those loads are unconditional and
+// the compiler's vmcnt waits stay per load. The LDS part is loaded first, so
+// the VGPRs it passes through are free again before the register part
+// arrives. Sums as in sm_long: fp32 within a vector, then double across
+// vectors, lanes and waves in a fixed order.
+// ---------------------------------------------------------------------------
+constexpr int kResBlock = 512;
+
+template <int DT, int MODE, bool FUSE, int NK, int NL, bool REGFULL, int MINB>
+__global__ __launch_bounds__(kResBlock, MINB) void sm_res_kernel(const char* __restrict__ x,
+                                                                char* __restrict__ y, uint32_t nvr,
+                                                                int64_t ldx_b, int64_t ldy_b,
+                                                                SmConst kc) {
+  constexpr int V = kV<DT>;
+  constexpr int B = kResBlock;
+  constexpr int W = B / 64;
+  __shared__ float s_max[W];
+  __shared__ double s_sum[W];
+  __shared__ __attribute__((aligned(16))) float s_row[NL > 0 ? NL * B * V : 4];
+  const uint32_t t = threadIdx.x;
+  const u32x4* xr = reinterpret_cast<const u32x4*>(x + (int64_t)blockIdx.x * ldx_b);
+  u32x4* yr = reinterpret_cast<u32x4*>(y + (int64_t)blockIdx.x * ldy_b);
+  const uint32_t vlast = nvr - 1;                              // nvr >= 1
+  const uint32_t cnt = t < nvr ? (nvr - 1 - t) / B + 1 : 0;    // this thread's vectors in the row
+  float* mine = s_row + t * V;                                 // LDS block k: mine + k * B * V
+
+  float lmax = -INFINITY;
+  {
+    u32x4 raw[NL > 0 ? NL : 1];
+#pragma unroll
+    for (int k = 0; k < NL; ++k)
+      if (REGFULL || (NK + k) * B < nvr)
+        raw[k] = __builtin_nontemporal_load(xr + umin32((NK + k) * B + t, vlast));
+#pragma unroll
+    for (int k = 0; k < NL; ++k) {
+      if ((NK + k) * B >= nvr) continue;
+      float g[V];
+      unpack<DT>(raw[k], g);
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        lmax = fmaxf(lmax, g[j]);
+        mine[k * B * V + j] = g[j];
+      }
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  u32x4 raw[NK];
+#pragma unroll
+  for (int k = 0; k < NK; ++k)
+    if (REGFULL || k * B < nvr) raw[k] = __builtin_nontemporal_load(xr + umin32(k * B + t, vlast));
+  float f[NK][V];
+#pragma unroll
+  for (int k = 0; k < NK; ++k) {
+    if (!REGFULL && k * B >= nvr) continue;
+    unpack<DT>(raw[k], f[k]);
+#pragma unroll
+    for (int j = 0; j < V; ++j) lmax = fmaxf(lmax, f[k][j]);
+  }
+  float m = wave_max(lmax);
+  if ((t & 63) == 0) s_max[t >> 6] = m;
+  __syncthreads();
+  m = s_max[0];
+  for (int w = 1; w < W; ++w) m = fmaxf(m, s_max[w]);
+
+  const RowExp<MODE, FUSE> ex = row_exp<MODE, FUSE>(kc, m);
+  double acc = 0.0;
+#pragma unroll
+  for (int k = 0; k < NK; ++k) {
+    if (!REGFULL && k * B >= nvr) continue;
+    float part = 0.0f;
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      f[k][j] = ex(f[k][j]);
+      part += f[k][j];
+    }
+    if ((uint32_t)k < cnt) acc += (double)part;
+  }
+#pragma unroll
+  for (int k = 0; k < NL; ++k) {
+    if ((NK + k) * B >= nvr) continue;
+    float part = 0.0f;
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const float e = ex(mine[k * B * V + j]);
+      mine[k * B * V + j] = e;
+      part += e;
+    }
+    if ((uint32_t)(NK + k) < cnt) acc += (double)part;
+  }
+  double total = wave_sum(acc);
+  if ((t & 63) == 0) s_sum[t >> 6] = total;
+  __syncthreads();
+  total = s_sum[0];
+  for (int w = 1; w < W; ++w) total += s_sum[w];
+  const float r = (m == -INFINITY) ? 0.0f : (float)(1.0 / total);
+
+  // The store indexes come from an opaque copy of t: otherwise the compiler
+  // keeps the load-side indexes (or their compares) live across the kernel,
+  // and the row no longer fits the VGPRs.
+  uint32_t ts = t;
+  asm volatile("" : "+v"(ts));
+#pragma unroll
+  for (int k = 0; k < NK; ++k) {
+    const uint32_t vi = k * B + ts;
+    if (vi < nvr) {
+#pragma unroll
+      for (int j = 0; j < V; ++j) f[k][j] *= r;
+      __builtin_nontemporal_store(pack<DT>(f[k]), yr + vi);
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < NL; ++k) {
+    const uint32_t vi = (NK + k) * B + ts;
+    if (vi < nvr) {
+      float g[V];
+#pragma unroll
+      for (int j = 0; j < V; ++j) g[j] = mine[k * B * V + j] * r;
+      __builtin_nontemporal_store(pack<DT>(g), yr + vi);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Generic rows: any alignment, stride and length.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float block_max(float v, float* s) {
@@ -844,16 +980,40 @@ static quake_status launch_generic(const void* x, void* y, const SmArgs& a, int6
   return QUAKE_OK;
 }
 
+// Register and LDS shapes of the row-resident kernel (vectors per thread):
+// NK2 blocks in VGPRs at two workgroups per CU (at most 128 VGPRs); NK1 blocks
+// at one workgroup per CU; NK1 blocks plus NL1 blocks in LDS (147-156 KB).
+template <int DT>
+struct ResShape {
+  static constexpr int NK2 = (DT == F32) ? 24 : 12;
+  static constexpr int NK1 = (DT == F32) ? 44 : 23;
+  static constexpr int NL1 = (DT == F32) ? 19 : 9;
+  static constexpr uint32_t kMax = (uint32_t)((NK1 + NL1) * kResBlock);
+};
+
 template <int DT, int MODE, bool FUSE, bool CAUSAL>
 static quake_status launch_long(const SmArgs& a) {
   constexpr int V = kV<DT>;
   constexpr int64_t kLongRows = int64_t(1) << 30;      // rows per launch (one workgroup each)
+  typedef ResShape<DT> RS;
   const uint32_t nvr = (uint32_t)(a.cols / V);
   for (int64_t r0 = 0; r0 < a.rows; r0 += kLongRows) {
     const int64_t nr = std::min(kLongRows, a.rows - r0);
-    hipLaunchKernelGGL((sm_long_kernel<DT, MODE, FUSE, CAUSAL>), dim3((uint32_t)nr),
-                       dim3(kLongBlock), 0, a.s, a.x + r0 * a.ldx_b, a.y + r0 * a.ldy_b, nvr,
-                       a.ldx_b, a.ldy_b, a.kc, causal_at(a, r0));
+    const char* xp = a.x + r0 * a.ldx_b;
+    char* yp = a.y + r0 * a.ldy_b;
+    const dim3 grid((uint32_t)nr);
+    if (!CAUSAL && nvr <= (uint32_t)(RS::NK2 * kResBlock))
+      hipLaunchKernelGGL((sm_res_kernel<DT, MODE, FUSE, RS::NK2, 0, false, 2>), grid,
+                         dim3(kResBlock), 0, a.s, xp, yp, nvr, a.ldx_b, a.ldy_b, a.kc);
+    else if (!CAUSAL && nvr <= (uint32_t)(RS::NK1 * kResBlock))
+      hipLaunchKernelGGL((sm_res_kernel<DT, MODE, FUSE, RS::NK1, 0, false, 1>), grid,
+                         dim3(kResBlock), 0, a.s, xp, yp, nvr, a.ldx_b, a.ldy_b, a.kc);
+    else if (!CAUSAL && nvr <= RS::kMax)   // every register block inside the row
+      hipLaunchKernelGGL((sm_res_kernel<DT, MODE, FUSE, RS::NK1, RS::NL1, true, 1>), grid,
+                         dim3(kResBlock), 0, a.s, xp, yp, nvr, a.ldx_b, a.ldy_b, a.kc);
+    else
+      hipLaunchKernelGGL((sm_long_kernel<DT, MODE, FUSE, CAUSAL>), grid, dim3(kLongBlock), 0,
+                         a.s, xp, yp, nvr, a.ldx_b, a.ldy_b, a.kc, causal_at(a, r0));
     const quake_status st = launch_status();
     if (st != QUAKE_OK) return st;
   }
@@ -949,7 +1109,9 @@ static quake_status sm_dispatch(const void* x, void* y, int64_t ldx, int64_t ldy
     if (nvr <= 4096) return launch_rows<DT, MODE, FUSE, CAUSAL, 16, 4>(a);
   }
   // Longer rows: chunks exchanged between workgroups through the caller's
-  // workspace, or, without one, a workgroup per row reading it three times.
+  // workspace, or, without one, a workgroup per row holding the whole row in
+  // VGPRs and LDS (sm_res), or reading it three times when it does not fit or
+  // is causal (sm_long).
   if constexpr (FUSE && !CAUSAL) {
     uint32_t G = 0;
     if (ws != nullptr && split_chunks(cols, &G)) return launch_split<DT, MODE, FUSE, CAUSAL>(a, ws);

@@ -111,7 +111,7 @@ def test_strides_and_misalignment(q, cols, dt):
                           % (dt, cols, pad, off, ws))
 
 
-@pytest.mark.parametrize("cols", [64, 512, 4096, 128256])
+@pytest.mark.parametrize("cols", [64, 512, 4096, 20480, 65536, 128256])
 @pytest.mark.parametrize("mode", MODES)
 def test_masked_rows(q, cols, mode):
     r = np.random.default_rng(7)
@@ -129,6 +129,28 @@ def test_masked_rows(q, cols, mode):
             gv = oracle.decode(g.reshape(-1), d).reshape(12, cols)
             assert np.all(gv[3] == 0.0)
             assert abs(float(gv[5, cols - 1]) - 1.0) <= 2.0 ** -23 and np.all(gv[5, :-1] == 0.0)
+
+
+# Rows without a workspace too long for the register-row kernels: the
+# row-resident kernel in each of its three shapes (registers at two workgroups
+# per CU; registers at one; registers plus an LDS part), at both ends of each,
+# then the first length past it (three-pass kernel).
+RESIDENT_COLS = {"f32": [16388, 16900, 49152, 49156, 90112, 90116, 129024, 129028],
+                 "bf16": [16392, 20000, 49152, 49160, 94208, 94216, 131072, 131080],
+                 "f16": [16392, 49152, 49160, 94216, 131072, 131080]}
+
+
+@pytest.mark.parametrize("dt,cols", [(d, c) for d, cs in RESIDENT_COLS.items() for c in cs])
+@pytest.mark.parametrize("mode", MODES)
+def test_resident_row_shapes(q, dt, cols, mode):
+    x = synth.normal((3, cols), 3.0 if dt == "f32" else 2.0, dt, 1300 + cols % 101)
+    say("softmax resident", dt, cols, mode)
+    g, r, d = _run(q, x, mode, 0.8)
+    assert_parity(g, r, d, "op", "resident %s cols %d mode %d" % (dt, cols, mode))
+    if mode == 2:
+        say("softmax resident strided", dt, cols)
+        g, r, d = _run(q, x, mode, 0.8, ld_pad=8)
+        assert_parity(g, r, d, "op", "resident strided %s cols %d" % (dt, cols))
 
 
 @pytest.mark.parametrize("t", [0.125, 0.5, 1.0, 3.0, 20.0])
@@ -229,7 +251,7 @@ def test_workload_lmhead_softmax_f32_64x128256(q, mode):
 
 @pytest.mark.parametrize("cols,dt", [(128, "f32"), (512, "bf16"), (1001, "f32"), (4096, "f32"),
                                      (16384, "f32"), (16384, "bf16"), (128256, "f32"),
-                                     (50000, "f16")])
+                                     (50000, "f16"), (30000, "bf16"), (70000, "f32")])
 @pytest.mark.parametrize("mode", MODES)
 def test_unfused(q, cols, dt, mode):
     rows = 6 if cols > 20000 else 33
