@@ -110,9 +110,10 @@ quake_status quake_exp(const void* x, void* y, int64_t n, quake_dtype dtype,
  * c1 = fmaf(-c0, m, 127 * 2^23); y[r, j] = QuAKEx(x[r, j]) / sum_j QuAKEx(x[r, j]).
  * Every exponent of a row is taken against the row's final maximum (QuAKE is
  * not multiplicative, so online rescaling of partial sums would change the
- * result). Sums are accumulated in fp32 within each 16-byte vector, then in
- * double (binary32 outputs) or fp32 (16-bit outputs) across vectors, lanes and
- * waves, and in double across the workgroups of a split row.
+ * result). Sums are accumulated in fp32 within each 16-byte vector, then
+ * across vectors, lanes and waves in fp32 for 16-bit rows of at most 16384
+ * elements in 16-byte-aligned rows and in double otherwise, and in double
+ * across the workgroups of a split row.
  *   x    : device, rows x cols elements, row r at x + r*ldx (elements).
  *   y    : device, row r at y + r*ldy (elements).
  *   ldx, ldy >= cols. cols >= 1 when rows >= 1.
@@ -123,12 +124,16 @@ quake_status quake_exp(const void* x, void* y, int64_t n, quake_dtype dtype,
  * Folding m into c1 (one binary32 rounding of c0*m) shifts every exponent's
  * argument by up to |t*m| * 2^-24 (natural-log units); rows with |t*m| above
  * about 1e9 are outside the folded form's range and may give NaN.
- * Rows of more than 16384 elements are longer than one workgroup's registers;
- * without a workspace each such row is reduced by one workgroup that reads it
- * three times (max, sum, normalise; the re-reads are served by the caches).
- * quake_softmax_ws computes the same operator for those rows (the partial sums
- * in another order) with every element read from HBM once. The library
- * allocates nothing and keeps no state.
+ * Rows of more than 16384 elements do not fit one wave's or one 256-thread
+ * workgroup's registers. Without a workspace, such a row of up to 129024
+ * (binary32) or 131072 (16-bit) elements in 16-byte-aligned rows is held by
+ * one 512-thread workgroup in its registers and LDS (each element read once);
+ * longer rows, and the other layouts, are reduced by one workgroup that reads
+ * the row three times (max, sum, normalise; the re-reads are served by the
+ * caches). quake_softmax_ws computes the same operator for those rows (the
+ * partial sums in another order) over several workgroups per row, every
+ * element read from HBM once. The library allocates nothing and keeps no
+ * state.
  */
 quake_status quake_softmax(const void* x, void* y, int64_t rows, int64_t cols,
                            int64_t ldx, int64_t ldy, quake_dtype dtype,
