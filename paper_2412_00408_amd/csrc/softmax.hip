@@ -27,9 +27,16 @@
 //   sm_long               longer or causal rows without a workspace: one
 //                         1024-thread workgroup per row, three passes (max,
 //                         sum, normalise), the re-reads served by the caches.
-//   sm_generic            any alignment / stride / length: one workgroup per
-//                         row, three passes (max, sum, normalise) with scalar
-//                         accesses; the re-reads are served by the caches.
+//   shifted rows          rows whose start is not 16-byte aligned (a length
+//                         that is not a multiple of the vector, an offset
+//                         base) at the same offset in x and y: sm_rows and
+//                         sm_res read the aligned vectors that cover each
+//                         row, mask the elements outside it and store the
+//                         row's first and last vectors element by element.
+//   sm_generic            any other alignment / stride / length: one
+//                         workgroup per row, three passes (max, sum,
+//                         normalise) with scalar accesses; the re-reads are
+//                         served by the caches.
 // Sums: fp32 within one 16-byte vector (at most 8 terms), then, in a fixed
 // order, double across vectors, lanes, waves and workgroups for binary32
 // outputs and fp32 for 16-bit outputs in the row kernels (double in the split,
@@ -138,9 +145,49 @@ __device__ __forceinline__ int64_t live_len(const CausalArg& ca, uint32_t local_
 }
 
 // ---------------------------------------------------------------------------
+// Rows whose start is not 16-byte aligned (a length that is not a multiple of
+// the vector, or a shifted base): the row is read as the aligned 16-byte
+// vectors that cover it, from the aligned address s elements before its start
+// (s = 0 .. V-1). An aligned 16-byte vector never crosses a page, so reading
+// the few elements around the row cannot fault; they are masked to -inf and
+// never written. Element e of that vector space is row element e - s.
+// ---------------------------------------------------------------------------
+// -inf for the elements of vector vi outside the row [s, s + cols).
+template <int V>
+__device__ __forceinline__ void mask_outside(float* f, uint32_t vi, uint32_t s, uint32_t cols) {
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    const uint32_t e = vi * V + j;
+    if (e < s || e - s >= cols) f[j] = -INFINITY;
+  }
+}
+
+// Stores the elements of vector vi that lie inside the row, one element at a
+// time, with the rounding of the whole-vector store.
+template <int DT>
+__device__ __forceinline__ void store_inside(char* ya, uint32_t vi, uint32_t s, uint32_t cols,
+                                             const float* f) {
+  constexpr int V = kV<DT>;
+  const u32x4 p = pack<DT>(f);
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    const uint32_t e = vi * V + j;
+    if (e >= s && e - s < cols) {
+      if constexpr (DT == F32) {
+        reinterpret_cast<uint32_t*>(ya)[e] = p[j];
+      } else {
+        const uint32_t w = p[j >> 1];
+        reinterpret_cast<uint16_t*>(ya)[e] = (uint16_t)((j & 1) ? (w >> 16) : (w & 0xffffu));
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Register-resident rows: one wave (WAVES = 1) or one workgroup (WAVES = 4).
 // ---------------------------------------------------------------------------
-template <int DT, int MODE, bool FUSE, bool CAUSAL, int NV, int WAVES, bool FULL = false>
+template <int DT, int MODE, bool FUSE, bool CAUSAL, int NV, int WAVES, bool FULL = false,
+          bool SHIFT = false>
 __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restrict__ x,
                                                           char* __restrict__ y, uint32_t rows,
                                                           uint32_t nvr, int64_t ldx_b,
@@ -159,8 +206,20 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
   const uint32_t row = blockIdx.x * ROWS_PER_BLOCK + threadIdx.x / LANES;
   if (WAVES == 1 && row >= rows) return;   // uniform per wave
 
-  const u32x4* xr = reinterpret_cast<const u32x4*>(x + (int64_t)row * ldx_b);
-  u32x4* yr = reinterpret_cast<u32x4*>(y + (int64_t)row * ldy_b);
+  // SHIFT: nvr carries the row length in elements; the row is read as the
+  // aligned vectors that cover it (x and y rows share their offset s).
+  const char* xrow = x + (int64_t)row * ldx_b;
+  char* yrow = y + (int64_t)row * ldy_b;
+  uint32_t s = 0, cols = 0;
+  if constexpr (SHIFT) {
+    s = (uint32_t)(((uintptr_t)xrow & 15u) / kEsz<DT>);
+    cols = nvr;
+    nvr = (s + cols + V - 1) / V;
+    xrow -= s * kEsz<DT>;
+    yrow -= s * kEsz<DT>;
+  }
+  const u32x4* xr = reinterpret_cast<const u32x4*>(xrow);
+  u32x4* yr = reinterpret_cast<u32x4*>(yrow);
 
   // Every lane loads (vectors past the row end re-read the row's last vector,
   // which stays in one cache line) and padding lanes select -inf: no branch
@@ -183,6 +242,9 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
     // per word); only the causal boundary needs a per-element mask
     if (!FULL && !CAUSAL && vi >= nvr) raw[k] = neg_inf_vec<DT>();
     unpack<DT>(raw[k], f[k]);
+    if constexpr (SHIFT) {
+      if (vi == 0 || vi + 1 == nvr) mask_outside<V>(f[k], vi, s, cols);
+    }
 #pragma unroll
     for (int j = 0; j < V; ++j) {
       if constexpr (CAUSAL) f[k][j] = (vi * V + j < L) ? f[k][j] : -INFINITY;
@@ -226,7 +288,10 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
     if ((FULL || vi < nvr) && (!CAUSAL || ca.write_masked || vi < nvl)) {
 #pragma unroll
       for (int j = 0; j < V; ++j) f[k][j] *= r;
-      __builtin_nontemporal_store(pack<DT>(f[k]), yr + vi);
+      if (SHIFT && (vi == 0 || vi + 1 == nvr))
+        store_inside<DT>(yrow, vi, s, cols, f[k]);
+      else
+        __builtin_nontemporal_store(pack<DT>(f[k]), yr + vi);
     }
   }
 }
@@ -726,7 +791,7 @@ __global__ __launch_bounds__(kLongBlock) void sm_long_kernel(const char* __restr
 // ---------------------------------------------------------------------------
 constexpr int kResBlock = 512;
 
-template <int DT, int MODE, bool FUSE, int NK, int NL, bool REGFULL, int MINB>
+template <int DT, int MODE, bool FUSE, int NK, int NL, bool REGFULL, int MINB, bool SHIFT = false>
 __global__ __launch_bounds__(kResBlock, MINB) void sm_res_kernel(const char* __restrict__ x,
                                                                 char* __restrict__ y, uint32_t nvr,
                                                                 int64_t ldx_b, int64_t ldy_b,
@@ -738,8 +803,20 @@ __global__ __launch_bounds__(kResBlock, MINB) void sm_res_kernel(const char* __r
   __shared__ double s_sum[W];
   __shared__ __attribute__((aligned(16))) float s_row[NL > 0 ? NL * B * V : 4];
   const uint32_t t = threadIdx.x;
-  const u32x4* xr = reinterpret_cast<const u32x4*>(x + (int64_t)blockIdx.x * ldx_b);
-  u32x4* yr = reinterpret_cast<u32x4*>(y + (int64_t)blockIdx.x * ldy_b);
+  // SHIFT: nvr carries the row length in elements; the row is read as the
+  // aligned vectors that cover it (x and y rows share their offset s).
+  const char* xrow = x + (int64_t)blockIdx.x * ldx_b;
+  char* yrow = y + (int64_t)blockIdx.x * ldy_b;
+  uint32_t s = 0, cols = 0;
+  if constexpr (SHIFT) {
+    s = (uint32_t)(((uintptr_t)xrow & 15u) / kEsz<DT>);
+    cols = nvr;
+    nvr = (s + cols + V - 1) / V;
+    xrow -= s * kEsz<DT>;
+    yrow -= s * kEsz<DT>;
+  }
+  const u32x4* xr = reinterpret_cast<const u32x4*>(xrow);
+  u32x4* yr = reinterpret_cast<u32x4*>(yrow);
   const uint32_t vlast = nvr - 1;                              // nvr >= 1
   const uint32_t cnt = t < nvr ? (nvr - 1 - t) / B + 1 : 0;    // this thread's vectors in the row
   float* mine = s_row + t * V;                                 // LDS block k: mine + k * B * V
@@ -756,6 +833,10 @@ __global__ __launch_bounds__(kResBlock, MINB) void sm_res_kernel(const char* __r
       if ((NK + k) * B >= nvr) continue;
       float g[V];
       unpack<DT>(raw[k], g);
+      if constexpr (SHIFT) {
+        const uint32_t vi = (NK + k) * B + t;
+        if (vi + 1 >= nvr) mask_outside<V>(g, vi, s, cols);   // the last vector, or past it
+      }
 #pragma unroll
       for (int j = 0; j < V; ++j) {
         lmax = fmaxf(lmax, g[j]);
@@ -773,6 +854,10 @@ __global__ __launch_bounds__(kResBlock, MINB) void sm_res_kernel(const char* __r
   for (int k = 0; k < NK; ++k) {
     if (!REGFULL && k * B >= nvr) continue;
     unpack<DT>(raw[k], f[k]);
+    if constexpr (SHIFT) {
+      const uint32_t vi = k * B + t;
+      if (vi == 0 || vi + 1 >= nvr) mask_outside<V>(f[k], vi, s, cols);
+    }
 #pragma unroll
     for (int j = 0; j < V; ++j) lmax = fmaxf(lmax, f[k][j]);
   }
@@ -825,7 +910,10 @@ __global__ __launch_bounds__(kResBlock, MINB) void sm_res_kernel(const char* __r
     if (vi < nvr) {
 #pragma unroll
       for (int j = 0; j < V; ++j) f[k][j] *= r;
-      __builtin_nontemporal_store(pack<DT>(f[k]), yr + vi);
+      if (SHIFT && (vi == 0 || vi + 1 == nvr))
+        store_inside<DT>(yrow, vi, s, cols, f[k]);
+      else
+        __builtin_nontemporal_store(pack<DT>(f[k]), yr + vi);
     }
   }
 #pragma unroll
@@ -835,7 +923,10 @@ __global__ __launch_bounds__(kResBlock, MINB) void sm_res_kernel(const char* __r
       float g[V];
 #pragma unroll
       for (int j = 0; j < V; ++j) g[j] = mine[k * B * V + j] * r;
-      __builtin_nontemporal_store(pack<DT>(g), yr + vi);
+      if (SHIFT && vi + 1 == nvr)
+        store_inside<DT>(yrow, vi, s, cols, g);
+      else
+        __builtin_nontemporal_store(pack<DT>(g), yr + vi);
     }
   }
 }
@@ -1071,6 +1162,80 @@ static quake_status launch_split(const SmArgs& a, char* ws) {
   return QUAKE_OK;
 }
 
+// Rows whose start is not 16-byte aligned, at the same offset in x and y:
+// the register-row kernels (up to 16384 elements) and the row-resident kernel
+// (up to its capacity) read the aligned vectors that cover each row. Classes
+// by the most vectors a row of this length can cover, (cols + 2V - 2) / V.
+template <int DT>
+static bool shifted_fits(const void* x, const void* y, int64_t rows, int64_t cols, int64_t ldx,
+                         int64_t ldy) {
+  constexpr int V = kV<DT>;
+  constexpr int64_t esz = kEsz<DT>;
+  const uintptr_t ux = (uintptr_t)x, uy = (uintptr_t)y;
+  return ux % esz == 0 && uy % esz == 0 && ((ux - uy) & 15u) == 0 &&
+         (rows <= 1 || (((ldx & 15) * esz) & 15) == (((ldy & 15) * esz) & 15)) &&
+         (cols + 2 * V - 2) / V <= (int64_t)ResShape<DT>::kMax;
+}
+
+template <int DT, int MODE, int NV, int WAVES>
+static quake_status launch_rows_shifted(const SmArgs& a) {
+  constexpr int RPB = kSmBlock / (64 * WAVES);
+  for (int64_t r0 = 0; r0 < a.rows; r0 += kRowChunk) {
+    const int64_t nr = std::min(kRowChunk, a.rows - r0);
+    const uint32_t grid = (uint32_t)((nr + RPB - 1) / RPB);
+    hipLaunchKernelGGL((sm_rows_kernel<DT, MODE, true, false, NV, WAVES, false, true>),
+                       dim3(grid), dim3(kSmBlock), 0, a.s, a.x + r0 * a.ldx_b,
+                       a.y + r0 * a.ldy_b, (uint32_t)nr, (uint32_t)a.cols, a.ldx_b, a.ldy_b,
+                       a.kc, causal_at(a, r0));
+    const quake_status st = launch_status();
+    if (st != QUAKE_OK) return st;
+  }
+  return QUAKE_OK;
+}
+
+template <int DT, int MODE>
+static quake_status launch_res_shifted(const SmArgs& a) {
+  constexpr int V = kV<DT>;
+  constexpr int64_t kResRows = int64_t(1) << 30;       // rows per launch (one workgroup each)
+  typedef ResShape<DT> RS;
+  const int64_t nvm = (a.cols + 2 * V - 2) / V;
+  const uint32_t cols = (uint32_t)a.cols;
+  for (int64_t r0 = 0; r0 < a.rows; r0 += kResRows) {
+    const int64_t nr = std::min(kResRows, a.rows - r0);
+    const char* xp = a.x + r0 * a.ldx_b;
+    char* yp = a.y + r0 * a.ldy_b;
+    const dim3 grid((uint32_t)nr);
+    if (nvm <= RS::NK2 * kResBlock)
+      hipLaunchKernelGGL((sm_res_kernel<DT, MODE, true, RS::NK2, 0, false, 2, true>), grid,
+                         dim3(kResBlock), 0, a.s, xp, yp, cols, a.ldx_b, a.ldy_b, a.kc);
+    else if (nvm <= RS::NK1 * kResBlock)
+      hipLaunchKernelGGL((sm_res_kernel<DT, MODE, true, RS::NK1, 0, false, 1, true>), grid,
+                         dim3(kResBlock), 0, a.s, xp, yp, cols, a.ldx_b, a.ldy_b, a.kc);
+    else
+      hipLaunchKernelGGL((sm_res_kernel<DT, MODE, true, RS::NK1, RS::NL1, true, 1, true>), grid,
+                         dim3(kResBlock), 0, a.s, xp, yp, cols, a.ldx_b, a.ldy_b, a.kc);
+    const quake_status st = launch_status();
+    if (st != QUAKE_OK) return st;
+  }
+  return QUAKE_OK;
+}
+
+template <int DT, int MODE>
+static quake_status launch_shifted(const SmArgs& a) {
+  constexpr int V = kV<DT>;
+  const int64_t nvm = (a.cols + 2 * V - 2) / V;
+  if (nvm <= 64) return launch_rows_shifted<DT, MODE, 1, 1>(a);
+  if (nvm <= 128) return launch_rows_shifted<DT, MODE, 2, 1>(a);
+  if (nvm <= 256) return launch_rows_shifted<DT, MODE, 4, 1>(a);
+  if (nvm <= 512) return launch_rows_shifted<DT, MODE, 8, 1>(a);
+  if (nvm <= 1024) return launch_rows_shifted<DT, MODE, 4, 4>(a);
+  if (nvm <= 2048) return launch_rows_shifted<DT, MODE, 8, 4>(a);
+  if constexpr (DT == F32) {
+    if (nvm <= 4096) return launch_rows_shifted<DT, MODE, 16, 4>(a);
+  }
+  return launch_res_shifted<DT, MODE>(a);
+}
+
 template <int DT, int MODE, bool FUSE, bool CAUSAL>
 static quake_status sm_dispatch(const void* x, void* y, int64_t ldx, int64_t ldy, const SmArgs& ain,
                                 char* ws) {
@@ -1079,12 +1244,17 @@ static quake_status sm_dispatch(const void* x, void* y, int64_t ldx, int64_t ldy
   const int64_t cols = ain.cols;
   const bool vec = aligned16(x) && aligned16(y) && (ldx * esz) % 16 == 0 && (ldy * esz) % 16 == 0 &&
                    cols % V == 0 && cols < (int64_t(1) << 31) - 16;
-  if (!vec) return launch_generic<DT, MODE, FUSE, CAUSAL>(x, y, ain, ldx, ldy);
   SmArgs a = ain;
   a.x = static_cast<const char*>(x);
   a.y = static_cast<char*>(y);
   a.ldx_b = ldx * esz;
   a.ldy_b = ldy * esz;
+  if (!vec) {
+    if constexpr (FUSE && !CAUSAL) {
+      if (shifted_fits<DT>(x, y, a.rows, cols, ldx, ldy)) return launch_shifted<DT, MODE>(a);
+    }
+    return launch_generic<DT, MODE, FUSE, CAUSAL>(x, y, ain, ldx, ldy);
+  }
   const int64_t nvr = cols / V;
   if constexpr (CAUSAL) {
     if (pair_applies<DT, MODE, FUSE>(a)) {

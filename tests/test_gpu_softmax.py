@@ -111,7 +111,7 @@ def test_strides_and_misalignment(q, cols, dt):
                           % (dt, cols, pad, off, ws))
 
 
-@pytest.mark.parametrize("cols", [64, 512, 4096, 20480, 65536, 128256])
+@pytest.mark.parametrize("cols", [64, 512, 1001, 4096, 20480, 50257, 65536, 128256])
 @pytest.mark.parametrize("mode", MODES)
 def test_masked_rows(q, cols, mode):
     r = np.random.default_rng(7)
@@ -151,6 +151,58 @@ def test_resident_row_shapes(q, dt, cols, mode):
         say("softmax resident strided", dt, cols)
         g, r, d = _run(q, x, mode, 0.8, ld_pad=8)
         assert_parity(g, r, d, "op", "resident strided %s cols %d" % (dt, cols))
+
+
+def _shifted_cols(dt):
+    """Ragged lengths at both ends of every class of the shifted-row path: a
+    row of cols elements covers at most (cols + 2V - 2) // V aligned vectors,
+    so a class of Nv vectors takes cols <= (Nv - 1) V + 1. The last length is
+    one past the row-resident kernel's capacity: the generic kernel."""
+    V = 4 if dt == "f32" else 8
+    limits = [64, 128, 256, 512, 1024, 2048] + ([4096] if dt == "f32" else [])
+    limits += [24 * 512, 44 * 512, 63 * 512] if dt == "f32" else [12 * 512, 23 * 512, 32 * 512]
+    out = [1, 2, 3, V + 1]
+    for n in limits:
+        out += [(n - 1) * V + 1, (n - 1) * V + 2]
+    return out
+
+
+SHIFTED = [(dt, c) for dt in ("f32", "bf16", "f16") for c in _shifted_cols(dt)]
+
+
+# Rows whose start is not 16-byte aligned: consecutive rows of a ragged length
+# start at every offset in turn; the shifted-row kernels read the aligned
+# vectors around each row (and the first length past them the generic kernel).
+@pytest.mark.parametrize("dt,cols", SHIFTED)
+@pytest.mark.parametrize("mode", MODES)
+def test_shifted_rows(q, dt, cols, mode):
+    rows = 9 if cols < 40000 else 5
+    x = synth.normal((rows, cols), 3.0 if dt == "f32" else 2.0, dt, 1500 + cols % 113)
+    for ws in _paths(cols):
+        say("softmax shifted", dt, rows, cols, mode, "workspace" if ws else "")
+        g, r, d = _run(q, x, mode, 0.9, ws=ws)
+        assert_parity(g, r, d, "op", "shifted %s %dx%d mode %d ws %d" % (dt, rows, cols, mode, ws))
+
+
+@pytest.mark.parametrize("cols", [7, 1001, 5000, 50257])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_shifted_offsets_and_strides(q, cols, dt):
+    """Aligned lengths behind an offset base, ragged strides, and x and y at
+    different offsets (the generic kernel)."""
+    x = synth.normal((6, cols), 2.0, dt, 1600 + cols)
+    for pad, off in [(0, 1), (0, 3), (1, 0), (5, 2), (3, 7)]:
+        say("softmax shifted offsets", dt, cols, pad, off)
+        g, r, d = _run(q, x, 2, 1.0, ld_pad=pad, offset=off)
+        assert_parity(g, r, d, "op", "shifted %s cols %d pad %d off %d" % (dt, cols, pad, off))
+    tdt = x.dtype
+    big = torch.zeros(6 * cols + 1, dtype=tdt)
+    big[1:].view(6, cols).copy_(x)
+    xg = big.to("cuda:0")[1:].view(6, cols)            # x one element past 16 bytes
+    yg = q.quake_softmax(xg, mode=2, t=1.0)            # y aligned: offsets differ
+    torch.cuda.synchronize()
+    g = host_bits(yg)
+    r = oracle.softmax(host_bits(x).reshape(6, cols), dt, 2, t=1.0, threads=THREADS)
+    assert_parity(g, r, dt, "op", "x and y at different offsets %s cols %d" % (dt, cols))
 
 
 @pytest.mark.parametrize("t", [0.125, 0.5, 1.0, 3.0, 20.0])
