@@ -1045,8 +1045,20 @@ def main():
                 ms3, _, _, _ = time_modes(q, timer, w2, xh, ["quake2"], steps2, 1,
                                           prefix="lmhead_no_workspace", use_ws=False)
                 entry["no_workspace_quake2_ms"] = ms3["quake2"]
+                # a vocabulary that is not a multiple of the 16-byte vector: every
+                # row starts at another offset from a 16-byte boundary
+                wr = synth.Workload("lmhead_softmax_f32_64x50257", "softmax", "f32",
+                                    (64, 50257), 64, 50257, 1.0, w2.seed)
+                xr = synth.spiked_logits(64, 50257, 3.0, 16, 20.0, "f32", w2.seed)
+                msr, _, _, _ = time_modes(q, timer, wr, xr, ["quake2"],
+                                          max(a.steps, operand_pairs(wr)), 1)
+                entry["ragged_vocab_64x50257_quake2_ms"] = msr["quake2"]
+                entry["ragged_vocab_64x50257_gbps"] = round(
+                    wr.algo_bytes / (msr["quake2"] * 1e-3) / 1e9, 2)
                 entry["note"] = ("with a workspace (quake_softmax_ws): rows split over exchanging "
-                                 "workgroups; no_workspace: quake_softmax, a workgroup per row")
+                                 "workgroups; no_workspace: quake_softmax, a workgroup per row "
+                                 "holding the row; ragged_vocab: 64 x 50257 rows, each read as "
+                                 "the aligned vectors that cover it, a workgroup per row")
             sec[name] = entry
             del xh
             torch.cuda.empty_cache()

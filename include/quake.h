@@ -111,9 +111,9 @@ quake_status quake_exp(const void* x, void* y, int64_t n, quake_dtype dtype,
  * Every exponent of a row is taken against the row's final maximum (QuAKE is
  * not multiplicative, so online rescaling of partial sums would change the
  * result). Sums are accumulated in fp32 within each 16-byte vector, then
- * across vectors, lanes and waves in fp32 for 16-bit rows of at most 16384
- * elements in 16-byte-aligned rows and in double otherwise, and in double
- * across the workgroups of a split row.
+ * across vectors, lanes and waves in fp32 (16-bit rows of up to 16384
+ * elements held by one wave or one 256-thread workgroup) or double (all
+ * other rows), and in double across the workgroups of a split row.
  *   x    : device, rows x cols elements, row r at x + r*ldx (elements).
  *   y    : device, row r at y + r*ldy (elements).
  *   ldx, ldy >= cols. cols >= 1 when rows >= 1.
@@ -124,16 +124,24 @@ quake_status quake_exp(const void* x, void* y, int64_t n, quake_dtype dtype,
  * Folding m into c1 (one binary32 rounding of c0*m) shifts every exponent's
  * argument by up to |t*m| * 2^-24 (natural-log units); rows with |t*m| above
  * about 1e9 are outside the folded form's range and may give NaN.
+ * Rows whose start is not 16-byte aligned (a length that is not a multiple
+ * of 16 bytes, an offset base) but lies at the same offset from a 16-byte
+ * boundary in x and y are read as the aligned 16-byte blocks that cover them:
+ * up to 15 bytes before and after each row are read (never written, and
+ * never outside the 16-byte blocks that hold the row's own first and last
+ * bytes); other layouts take a scalar kernel.
  * Rows of more than 16384 elements do not fit one wave's or one 256-thread
  * workgroup's registers. Without a workspace, such a row of up to 129024
- * (binary32) or 131072 (16-bit) elements in 16-byte-aligned rows is held by
- * one 512-thread workgroup in its registers and LDS (each element read once);
- * longer rows, and the other layouts, are reduced by one workgroup that reads
- * the row three times (max, sum, normalise; the re-reads are served by the
- * caches). quake_softmax_ws computes the same operator for those rows (the
- * partial sums in another order) over several workgroups per row, every
- * element read from HBM once. The library allocates nothing and keeps no
- * state.
+ * (binary32) or 131072 (16-bit) elements (a few fewer for a row whose start
+ * is not 16-byte aligned) is held by one 512-thread workgroup in its
+ * registers and LDS (each element read once); longer rows, and the layouts
+ * that take the scalar kernel, are reduced by one workgroup that reads the
+ * row three times (max, sum, normalise; the re-reads are served by the
+ * caches). quake_softmax_ws computes the same operator for 16-byte-aligned
+ * long rows (the partial sums in another order) over several workgroups per
+ * row, every element read from HBM once; rows that are not 16-byte aligned
+ * take the one-workgroup kernels there too. The library allocates nothing
+ * and keeps no state.
  */
 quake_status quake_softmax(const void* x, void* y, int64_t rows, int64_t cols,
                            int64_t ldx, int64_t ldy, quake_dtype dtype,
