@@ -153,6 +153,19 @@ template <int DT, int OP, int MODE>
 quake_status ew_launch(const void* x, void* y, int64_t n, const EwParams& p, hipStream_t s) {
   constexpr int V = kV<DT>;
   constexpr int64_t esz = kEsz<DT>;
+  // x and y at the same offset from a 16-byte boundary (an offset view of
+  // aligned buffers): the few elements before the first boundary take the
+  // scalar kernel, the rest the vector kernels.
+  const uintptr_t ux = (uintptr_t)x, uy = (uintptr_t)y;
+  if ((ux & 15u) != 0 && ((ux - uy) & 15u) == 0 && ux % esz == 0) {
+    const int64_t head = std::min<int64_t>(n, (int64_t)((16u - (ux & 15u)) & 15u) / esz);
+    hipLaunchKernelGGL((ew_scalar_kernel<DT, OP, MODE>), dim3(1), dim3(kEwBlock), 0, s, x, y,
+                       (uint32_t)head, p);
+    const quake_status st = launch_status();
+    if (st != QUAKE_OK || head == n) return st;
+    return ew_launch<DT, OP, MODE>(static_cast<const char*>(x) + head * esz,
+                                   static_cast<char*>(y) + head * esz, n - head, p, s);
+  }
   const bool vec = aligned16(x) && aligned16(y);
   const int cus = device_cus();
   for (int64_t off = 0; off < n; off += kEwChunk) {

@@ -128,6 +128,19 @@ constexpr int64_t kN16Chunk = int64_t(1) << 30;   // elements per launch, a mult
 template <int DT, int MODE>
 static quake_status exp16_launch(const void* x, void* y, int64_t n, const N16Const& k,
                                  hipStream_t s) {
+  // x and y at the same offset from a 16-byte boundary: the elements before
+  // the first boundary take the scalar kernel, the rest the vector kernel.
+  const uintptr_t ux = (uintptr_t)x, uy = (uintptr_t)y;
+  if ((ux & 15u) != 0 && ((ux - uy) & 15u) == 0 && ux % 2 == 0) {
+    const int64_t head = std::min<int64_t>(n, (int64_t)((16u - (ux & 15u)) & 15u) / 2);
+    hipLaunchKernelGGL((exp16_scalar_kernel<DT, MODE>), dim3(1), dim3(kN16Block), 0, s,
+                       static_cast<const uint16_t*>(x), static_cast<uint16_t*>(y),
+                       (uint32_t)head, k);
+    const quake_status st = launch_status();
+    if (st != QUAKE_OK || head == n) return st;
+    return exp16_launch<DT, MODE>(static_cast<const uint16_t*>(x) + head,
+                                  static_cast<uint16_t*>(y) + head, n - head, k, s);
+  }
   const bool vec = aligned16(x) && aligned16(y);
   for (int64_t o = 0; o < n; o += kN16Chunk) {
     const int64_t m = std::min(kN16Chunk, n - o);

@@ -104,6 +104,43 @@ def test_ragged_lengths(q, n, dt):
         assert_parity(g, r, d, kind_of(op, 2), "ragged %s %s %d" % (op, dt, n))
 
 
+# x and y at the same offset from a 16-byte boundary: the elements before the
+# first boundary take the scalar kernel, the rest the vector kernels; lengths
+# shorter than, equal to and just past that head, and x and y at different
+# offsets (the scalar kernel throughout). Padding around y must stay untouched.
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("xoff,yoff", [(1, 1), (2, 2), (3, 3), (5, 5), (7, 7), (1, 0), (0, 3), (2, 5)])
+def test_offsets(q, dt, xoff, yoff):
+    V = 4 if dt == "f32" else 8
+    esz = 4 if dt == "f32" else 2
+    if (xoff * esz) % 16 == 0 and xoff:
+        pytest.skip("offset is a whole vector")
+    head = ((16 - (xoff * esz) % 16) % 16) // esz
+    for n in sorted({1, max(1, head - 1), max(1, head), head + 1, head + V + 1, 5000, 1_000_003}):
+        x = synth.normal((n + 8,), 3.0, dt, 110 + n % 31 + xoff)
+        xb = host_bits(x)[xoff:xoff + n].copy()
+        xg = x.to("cuda:0")
+        yfull = torch.full((n + 8,), 5.0, dtype=x.dtype, device="cuda:0")
+        src, dst = xg[xoff:xoff + n], yfull[yoff:yoff + n]
+        for op in ("exp", "gelu", "sigmoid", "silu"):
+            say("offsets", op, dt, n, xoff, yoff)
+            if op == "exp":
+                q.quake_exp(src, dst, mode=2)
+                ref = oracle.exp(xb, dt, 2, threads=THREADS)
+            elif op == "gelu":
+                q.quake_gelu(src, dst, mode=2)
+                ref = oracle.gelu(xb, dt, 2, threads=THREADS)
+            else:
+                q.quake_sigmoid(src, dst, mode=2, silu=(op == "silu"))
+                ref = oracle.sigmoid(xb, dt, 2, silu=(op == "silu"), threads=THREADS)
+            torch.cuda.synchronize()
+            out = host_bits(yfull)
+            assert_parity(out[yoff:yoff + n].copy(), ref, dt, kind_of(op, 2),
+                          "offsets %s %s n %d x+%d y+%d" % (op, dt, n, xoff, yoff))
+            pad = np.concatenate([out[:yoff], out[yoff + n:]])
+            assert np.all(oracle.decode(pad, dt) == 5.0), "write outside y"
+
+
 @pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
 def test_misaligned_and_inplace(q, dt):
     x = synth.normal((100_003,), 3.0, dt, 103)

@@ -47,7 +47,8 @@ def test_every_pattern_bit_exact(q, dt, mode):
 
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
 @pytest.mark.parametrize("n,off", [(1, 0), (7, 0), (8, 0), (1000, 0), (1000, 1), (3 << 20, 0),
-                                   ((1 << 22) + 13, 0), ((1 << 20) + 5, 3)])
+                                   ((1 << 22) + 13, 0), ((1 << 20) + 5, 3), (1, 5), (2, 7),
+                                   (3, 5), (4, 5), (9, 1), (100_001, 6), (1 << 22, 2)])
 def test_lengths_and_alignment(q, dt, n, off):
     x = synth.uniform((n + off,), -12.0, 12.0, dt, 1300 + n % 97)
     xb = host_bits(x)[off:]
