@@ -226,8 +226,10 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
   // around the loads, so the whole row stays in registers without merges.
   // With the causal mask only vectors holding live entries are read. FULL:
   // the row is exactly NV vectors per lane, so there is nothing to pad.
-  const uint32_t L = (uint32_t)live_len<CAUSAL>(ca, row, (int64_t)nvr * V);
-  const uint32_t nvl = CAUSAL ? (L + V - 1) / V : nvr;
+  // live entries: row elements [0, L) (the causal mask), i.e. elements
+  // [s, s + L) of the vector space; nvl vectors hold them
+  const uint32_t L = (uint32_t)live_len<CAUSAL>(ca, row, SHIFT ? (int64_t)cols : (int64_t)nvr * V);
+  const uint32_t nvl = !CAUSAL ? nvr : L == 0 ? 0 : (s + L + V - 1) / V;
   const uint32_t vlast = (nvl > 0 ? nvl : 1) - 1;
   u32x4 raw[NV];
 #pragma unroll
@@ -242,12 +244,13 @@ __global__ __launch_bounds__(kSmBlock) void sm_rows_kernel(const char* __restric
     // per word); only the causal boundary needs a per-element mask
     if (!FULL && !CAUSAL && vi >= nvr) raw[k] = neg_inf_vec<DT>();
     unpack<DT>(raw[k], f[k]);
-    if constexpr (SHIFT) {
+    if constexpr (SHIFT && !CAUSAL) {
       if (vi == 0 || vi + 1 == nvr) mask_outside<V>(f[k], vi, s, cols);
     }
 #pragma unroll
     for (int j = 0; j < V; ++j) {
-      if constexpr (CAUSAL) f[k][j] = (vi * V + j < L) ? f[k][j] : -INFINITY;
+      // with SHIFT, elements before the row start wrap to large values
+      if constexpr (CAUSAL) f[k][j] = (vi * V + j - s < L) ? f[k][j] : -INFINITY;
       lmax = fmaxf(lmax, f[k][j]);
     }
   }
@@ -1163,27 +1166,27 @@ static quake_status launch_split(const SmArgs& a, char* ws) {
 }
 
 // Rows whose start is not 16-byte aligned, at the same offset in x and y:
-// the register-row kernels (up to 16384 elements) and the row-resident kernel
-// (up to its capacity) read the aligned vectors that cover each row. Classes
-// by the most vectors a row of this length can cover, (cols + 2V - 2) / V.
+// the register-row kernels (up to 16384 elements, also with the implicit
+// causal mask) and the row-resident kernel (up to its capacity) read the
+// aligned vectors that cover each row. Classes by the most vectors a row of
+// this length can cover, (cols + 2V - 2) / V.
 template <int DT>
 static bool shifted_fits(const void* x, const void* y, int64_t rows, int64_t cols, int64_t ldx,
                          int64_t ldy) {
-  constexpr int V = kV<DT>;
   constexpr int64_t esz = kEsz<DT>;
   const uintptr_t ux = (uintptr_t)x, uy = (uintptr_t)y;
   return ux % esz == 0 && uy % esz == 0 && ((ux - uy) & 15u) == 0 &&
          (rows <= 1 || (((ldx & 15) * esz) & 15) == (((ldy & 15) * esz) & 15)) &&
-         (cols + 2 * V - 2) / V <= (int64_t)ResShape<DT>::kMax;
+         cols < (int64_t(1) << 31);
 }
 
-template <int DT, int MODE, int NV, int WAVES>
+template <int DT, int MODE, bool CAUSAL, int NV, int WAVES>
 static quake_status launch_rows_shifted(const SmArgs& a) {
   constexpr int RPB = kSmBlock / (64 * WAVES);
   for (int64_t r0 = 0; r0 < a.rows; r0 += kRowChunk) {
     const int64_t nr = std::min(kRowChunk, a.rows - r0);
     const uint32_t grid = (uint32_t)((nr + RPB - 1) / RPB);
-    hipLaunchKernelGGL((sm_rows_kernel<DT, MODE, true, false, NV, WAVES, false, true>),
+    hipLaunchKernelGGL((sm_rows_kernel<DT, MODE, true, CAUSAL, NV, WAVES, false, true>),
                        dim3(grid), dim3(kSmBlock), 0, a.s, a.x + r0 * a.ldx_b,
                        a.y + r0 * a.ldy_b, (uint32_t)nr, (uint32_t)a.cols, a.ldx_b, a.ldy_b,
                        a.kc, causal_at(a, r0));
@@ -1220,20 +1223,31 @@ static quake_status launch_res_shifted(const SmArgs& a) {
   return QUAKE_OK;
 }
 
-template <int DT, int MODE>
+// Whether the shifted-row kernels take rows of this length (the implicit
+// causal mask only in the register-row kernels).
+template <int DT, bool CAUSAL>
+static bool shifted_length(int64_t cols) {
+  constexpr int V = kV<DT>;
+  const int64_t nvm = (cols + 2 * V - 2) / V;
+  if (CAUSAL) return nvm <= (DT == F32 ? 4096 : 2048);
+  return nvm <= (int64_t)ResShape<DT>::kMax;
+}
+
+template <int DT, int MODE, bool CAUSAL>
 static quake_status launch_shifted(const SmArgs& a) {
   constexpr int V = kV<DT>;
   const int64_t nvm = (a.cols + 2 * V - 2) / V;
-  if (nvm <= 64) return launch_rows_shifted<DT, MODE, 1, 1>(a);
-  if (nvm <= 128) return launch_rows_shifted<DT, MODE, 2, 1>(a);
-  if (nvm <= 256) return launch_rows_shifted<DT, MODE, 4, 1>(a);
-  if (nvm <= 512) return launch_rows_shifted<DT, MODE, 8, 1>(a);
-  if (nvm <= 1024) return launch_rows_shifted<DT, MODE, 4, 4>(a);
-  if (nvm <= 2048) return launch_rows_shifted<DT, MODE, 8, 4>(a);
+  if (nvm <= 64) return launch_rows_shifted<DT, MODE, CAUSAL, 1, 1>(a);
+  if (nvm <= 128) return launch_rows_shifted<DT, MODE, CAUSAL, 2, 1>(a);
+  if (nvm <= 256) return launch_rows_shifted<DT, MODE, CAUSAL, 4, 1>(a);
+  if (nvm <= 512) return launch_rows_shifted<DT, MODE, CAUSAL, 8, 1>(a);
+  if (nvm <= 1024) return launch_rows_shifted<DT, MODE, CAUSAL, 4, 4>(a);
+  if (nvm <= 2048) return launch_rows_shifted<DT, MODE, CAUSAL, 8, 4>(a);
   if constexpr (DT == F32) {
-    if (nvm <= 4096) return launch_rows_shifted<DT, MODE, 16, 4>(a);
+    if (nvm <= 4096) return launch_rows_shifted<DT, MODE, CAUSAL, 16, 4>(a);
   }
-  return launch_res_shifted<DT, MODE>(a);
+  if constexpr (CAUSAL) return QUAKE_EINVAL;   // excluded by shifted_length
+  else return launch_res_shifted<DT, MODE>(a);
 }
 
 template <int DT, int MODE, bool FUSE, bool CAUSAL>
@@ -1250,8 +1264,9 @@ static quake_status sm_dispatch(const void* x, void* y, int64_t ldx, int64_t ldy
   a.ldx_b = ldx * esz;
   a.ldy_b = ldy * esz;
   if (!vec) {
-    if constexpr (FUSE && !CAUSAL) {
-      if (shifted_fits<DT>(x, y, a.rows, cols, ldx, ldy)) return launch_shifted<DT, MODE>(a);
+    if constexpr (FUSE) {
+      if (shifted_fits<DT>(x, y, a.rows, cols, ldx, ldy) && shifted_length<DT, CAUSAL>(cols))
+        return launch_shifted<DT, MODE, CAUSAL>(a);
     }
     return launch_generic<DT, MODE, FUSE, CAUSAL>(x, y, ain, ldx, ldy);
   }

@@ -347,8 +347,14 @@ def _run_causal(q, x_cpu, mode, t, period, shift):
     return host_bits(yg), ref, dt
 
 
+# ragged lengths (rows start at every offset from 16 bytes): the shifted
+# register-row kernels up to 4096 (binary32) / 2048 (16-bit) covered vectors,
+# then the scalar kernel (16383 f32, 16378 bf16)
 @pytest.mark.parametrize("cols,dt", [(64, "f32"), (512, "bf16"), (1000, "bf16"), (4096, "f32"),
-                                     (16384, "f32"), (40000, "f32"), (32768, "bf16")])
+                                     (16384, "f32"), (40000, "f32"), (32768, "bf16"),
+                                     (1, "f32"), (3, "bf16"), (63, "f32"), (1001, "bf16"),
+                                     (4095, "f32"), (2047, "f16"), (16381, "f32"), (16383, "f32"),
+                                     (16377, "bf16"), (16378, "bf16")])
 @pytest.mark.parametrize("mode", MODES)
 def test_causal(q, cols, dt, mode):
     rows = min(2 * cols, 96) if cols <= 4096 else 9
@@ -381,7 +387,8 @@ def test_workload_attn_implicit_causal(q, mode):
     assert check_bits(host_bits(implicit), host_bits(explicit)) is None
 
 
-@pytest.mark.parametrize("cols,dt", [(512, "bf16"), (4096, "f32"), (40000, "f32"), (1000, "bf16")])
+@pytest.mark.parametrize("cols,dt", [(512, "bf16"), (4096, "f32"), (40000, "f32"), (1000, "bf16"),
+                                     (1001, "bf16"), (333, "f32"), (20001, "f32")])
 def test_causal_without_masked_writes(q, cols, dt):
     rows = 64 if cols <= 4096 else 6
     x = synth.normal((rows, cols), 2.0, dt, 1100 + cols % 61)
@@ -396,7 +403,13 @@ def test_causal_without_masked_writes(q, cols, dt):
     i = np.arange(rows)[:, None] % cols
     j = np.arange(cols)[None, :]
     live = j <= i
-    written = (j // vec) <= (i // vec) if cols % vec == 0 else live
+    # vector kernels write whole 16-byte vectors that hold a live entry: row r
+    # starts s = r * cols mod vec elements past a 16-byte boundary (the
+    # shifted-row kernels up to 4096 / 2048 vectors); the scalar kernel
+    # writes the live entries only
+    s = (np.arange(rows)[:, None] * cols) % vec
+    vector_path = cols % vec == 0 or (cols + 2 * vec - 2) // vec <= (4096 if dt == "f32" else 2048)
+    written = ((s + j) // vec) <= ((s + i) // vec) if vector_path else live
     # live outputs match the oracle; untouched outputs keep their old value
     assert_parity(g[live], ref[live], dt, "op", "causal no-writes %s %d" % (dt, cols))
     gv = oracle.decode(g.reshape(-1), dt).reshape(rows, cols)
