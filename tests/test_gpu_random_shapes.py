@@ -92,6 +92,58 @@ def test_random_softmax(q, rows, cols, dt, mode, t, ld_pad, ws, seed):
         dt, rows, cols, mode, t, ld_pad, ws, seed))
 
 
+def _offset_cases(n, seed):
+    """(rows, cols, dt, mode, ld_pad, offset, ws, seed): x and y both a few
+    elements past a 16-byte boundary, with ragged lengths and strides, so rows
+    start at every offset (the shifted-row kernels and, past their lengths,
+    the scalar kernel)."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        cols = int(rng.integers(1, 140000)) if rng.random() < 0.7 else int(rng.integers(1, 600))
+        rows = int(rng.integers(1, max(2, min(200, 1_500_000 // cols)) + 1))
+        dt = str(rng.choice(["f32", "bf16", "f16"]))
+        out.append((rows, cols, dt, int(rng.integers(0, 4)), int(rng.choice([0, 1, 3, 8])),
+                    int(rng.integers(1, 8)), bool(cols > 16384 and rng.random() < 0.5),
+                    int(rng.integers(0, 1 << 20))))
+    return out
+
+
+@pytest.mark.parametrize("rows,cols,dt,mode,ld_pad,offset,ws,seed", _offset_cases(24, 1001))
+def test_random_softmax_offsets(q, rows, cols, dt, mode, ld_pad, offset, ws, seed):
+    say("random softmax offsets", dt, rows, cols, mode, ld_pad, offset, "workspace" if ws else "", seed)
+    x = synth.normal((rows, cols), 3.0, dt, seed)
+    g, r, d = ts._run(q, x, mode, 0.9, ld_pad=ld_pad, offset=offset, ws=ws)
+    assert_parity(g, r, d, "op", "random softmax offsets %s %dx%d m%d pad%d off%d ws%d seed%d" % (
+        dt, rows, cols, mode, ld_pad, offset, ws, seed))
+
+
+def _causal_cases(n, seed):
+    """(rows, cols, dt, mode, period, shift, seed): implicit causal masks over
+    ragged and aligned lengths, square and rectangular periods, shifts that
+    leave rows empty or full."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        cols = int(rng.integers(1, 20000)) if rng.random() < 0.6 else int(rng.integers(1, 1100))
+        rows = int(rng.integers(1, max(2, min(400, 1_500_000 // cols)) + 1))
+        dt = str(rng.choice(["f32", "bf16", "f16"]))
+        kind = int(rng.integers(0, 3))
+        period = cols if kind == 0 else int(rng.integers(1, 2 * cols + 2))
+        shift = 0 if kind == 0 else int(rng.integers(-cols, cols + 1))
+        out.append((rows, cols, dt, int(rng.integers(0, 4)), period, shift, int(rng.integers(0, 1 << 20))))
+    return out
+
+
+@pytest.mark.parametrize("rows,cols,dt,mode,period,shift,seed", _causal_cases(24, 2025))
+def test_random_causal(q, rows, cols, dt, mode, period, shift, seed):
+    say("random causal", dt, rows, cols, mode, period, shift, seed)
+    x = synth.normal((rows, cols), 2.0, dt, seed)
+    g, r, d = ts._run_causal(q, x, mode, 0.6, period, shift)
+    assert_parity(g, r, d, "op", "random causal %s %dx%d m%d p%d s%d seed%d" % (
+        dt, rows, cols, mode, period, shift, seed))
+
+
 def _elementwise_cases(n, seed):
     """(op, n, dt, mode, a, b, seed): lengths from one element to past the
     resident-grid limit of 16-bit vectors (2^25 elements), ragged tails, and
