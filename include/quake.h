@@ -137,11 +137,12 @@ quake_status quake_exp(const void* x, void* y, int64_t n, quake_dtype dtype,
  * registers and LDS (each element read once); longer rows, and the layouts
  * that take the scalar kernel, are reduced by one workgroup that reads the
  * row three times (max, sum, normalise; the re-reads are served by the
- * caches). quake_softmax_ws computes the same operator for 16-byte-aligned
- * long rows (the partial sums in another order) over several workgroups per
- * row, every element read from HBM once; rows that are not 16-byte aligned
- * take the one-workgroup kernels there too. The library allocates nothing
- * and keeps no state.
+ * caches). quake_softmax_ws computes the same operator for long rows (the
+ * partial sums in another order) over several workgroups per row, every
+ * element read from HBM once (rows that are not 16-byte aligned: when
+ * ceil(cols / 16384) chunks cover the aligned blocks of every row, else the
+ * one-workgroup kernels). The library allocates nothing and keeps no
+ * state.
  */
 quake_status quake_softmax(const void* x, void* y, int64_t rows, int64_t cols,
                            int64_t ldx, int64_t ldy, quake_dtype dtype,

@@ -482,15 +482,16 @@ __device__ __forceinline__ void widen_masked(u32x4 raw, uint32_t vi, uint32_t nv
 // q*CHV + k*256 + t, k = 0 .. NV-1, as the owner's thread t holds them, so the
 // per-vector partial sums, the per-lane double accumulation, the wave trees
 // and the cross-wave pairing are the owner's, bit for bit.
-template <int DT, bool CAUSAL, int NV>
+template <int DT, bool CAUSAL, int NV, bool SHIFT>
 __device__ float chunk_max_from_x(const u32x4* xr, uint32_t q, uint32_t nvr, uint32_t vlast,
-                                  uint32_t L, float* s4) {
+                                  uint32_t L, float* s4, uint32_t s, uint32_t cols) {
   constexpr int V = kV<DT>;
   float lmax = -INFINITY;
   for (int k = 0; k < NV; ++k) {
     const uint32_t vi = q * (kSmBlock * NV) + k * kSmBlock + threadIdx.x;
     float f[V];
     widen_masked<DT, CAUSAL>(__builtin_nontemporal_load(xr + umin32(vi, vlast)), vi, nvr, L, f);
+    if (SHIFT && (vi == 0 || vi + 1 == nvr)) mask_outside<V>(f, vi, s, cols);
 #pragma unroll
     for (int j = 0; j < V; ++j) lmax = fmaxf(lmax, f[j]);
   }
@@ -501,28 +502,30 @@ __device__ float chunk_max_from_x(const u32x4* xr, uint32_t q, uint32_t nvr, uin
   return fmaxf(fmaxf(s4[0], s4[1]), fmaxf(s4[2], s4[3]));
 }
 
-template <int DT, int MODE, bool FUSE, bool CAUSAL, int NV>
+template <int DT, int MODE, bool FUSE, bool CAUSAL, int NV, bool SHIFT>
 __device__ double chunk_sum_from_x(const u32x4* xr, uint32_t q, uint32_t nvr, uint32_t vlast,
-                                   uint32_t L, const RowExp<MODE, FUSE>& ex, double* s4) {
+                                   uint32_t L, const RowExp<MODE, FUSE>& ex, double* s4,
+                                   uint32_t s, uint32_t cols) {
   constexpr int V = kV<DT>;
   double acc = 0.0;
   for (int k = 0; k < NV; ++k) {
     const uint32_t vi = q * (kSmBlock * NV) + k * kSmBlock + threadIdx.x;
     float f[V];
     widen_masked<DT, CAUSAL>(__builtin_nontemporal_load(xr + umin32(vi, vlast)), vi, nvr, L, f);
+    if (SHIFT && (vi == 0 || vi + 1 == nvr)) mask_outside<V>(f, vi, s, cols);
     float part = 0.0f;
 #pragma unroll
     for (int j = 0; j < V; ++j) part += ex(f[j]);
     acc += (double)part;
   }
-  const double s = wave_sum(acc);
+  const double ws = wave_sum(acc);
   __syncthreads();
-  if ((threadIdx.x & 63) == 0) s4[threadIdx.x >> 6] = s;
+  if ((threadIdx.x & 63) == 0) s4[threadIdx.x >> 6] = ws;
   __syncthreads();
   return (s4[0] + s4[1]) + (s4[2] + s4[3]);
 }
 
-template <int DT, int MODE, bool FUSE, bool CAUSAL, int NV>
+template <int DT, int MODE, bool FUSE, bool CAUSAL, int NV, bool SHIFT = false>
 __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restrict__ x,
                                                            char* __restrict__ y, uint32_t nvr,
                                                            int64_t ldx_b, int64_t ldy_b,
@@ -557,8 +560,22 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
   const uint32_t lim_in = ws.hdr[0];
   const uint64_t limit = lim_in ? (uint64_t)lim_in : kDefaultWaitTicks;
 
-  const u32x4* xr = reinterpret_cast<const u32x4*>(x + (int64_t)rr * ldx_b);
-  u32x4* yr = reinterpret_cast<u32x4*>(y + (int64_t)rr * ldy_b);
+  // SHIFT: nvr carries the row length in elements; the row is read as the
+  // aligned vectors that cover it (x and y rows share their offset s). The
+  // launch's chunk count covers the most vectors any row can span, so a
+  // row's last chunk may hold no element of it (max -inf, sum 0).
+  const char* xrow = x + (int64_t)rr * ldx_b;
+  char* yrow = y + (int64_t)rr * ldy_b;
+  uint32_t s = 0, cols = 0;
+  if constexpr (SHIFT) {
+    s = (uint32_t)(((uintptr_t)xrow & 15u) / kEsz<DT>);
+    cols = nvr;
+    nvr = (s + cols + V - 1) / V;
+    xrow -= s * kEsz<DT>;
+    yrow -= s * kEsz<DT>;
+  }
+  const u32x4* xr = reinterpret_cast<const u32x4*>(xrow);
+  u32x4* yr = reinterpret_cast<u32x4*>(yrow);
   const uint32_t v0 = g * CHV;
 
   const uint32_t L = (uint32_t)live_len<CAUSAL>(ca, rr, (int64_t)nvr * V);
@@ -572,7 +589,11 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
   float lmax = -INFINITY;
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
-    widen_masked<DT, CAUSAL>(raw[k], v0 + k * kSmBlock + threadIdx.x, nvr, L, f[k]);
+    const uint32_t vi = v0 + k * kSmBlock + threadIdx.x;
+    widen_masked<DT, CAUSAL>(raw[k], vi, nvr, L, f[k]);
+    if constexpr (SHIFT) {
+      if (vi == 0 || vi + 1 == nvr) mask_outside<V>(f[k], vi, s, cols);
+    }
 #pragma unroll
     for (int j = 0; j < V; ++j) lmax = fmaxf(lmax, f[k][j]);
   }
@@ -600,7 +621,7 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
   if (missing_max) {   // uniform: every thread reads the same LDS words
     for (uint32_t q = 0; q < G; ++q) {
       if (s_pmax[q] != s_pmax[q])
-        m = fmaxf(m, chunk_max_from_x<DT, CAUSAL, NV>(xr, q, nvr, vlast, L, s_fmax));
+        m = fmaxf(m, chunk_max_from_x<DT, CAUSAL, NV, SHIFT>(xr, q, nvr, vlast, L, s_fmax, s, cols));
     }
   }
 
@@ -649,7 +670,8 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
       const double sq = s_psum[q];
       __syncthreads();   // every thread has read s_psum[q] before thread 0 may rewrite it
       if (sq != sq) {
-        const double v = chunk_sum_from_x<DT, MODE, FUSE, CAUSAL, NV>(xr, q, nvr, vlast, L, ex, s_fsum);
+        const double v = chunk_sum_from_x<DT, MODE, FUSE, CAUSAL, NV, SHIFT>(xr, q, nvr, vlast, L, ex,
+                                                                             s_fsum, s, cols);
         if (threadIdx.x == 0) s_psum[q] = v;
       }
     }
@@ -681,7 +703,10 @@ __global__ __launch_bounds__(kSmBlock) void sm_split_kernel(const char* __restri
     if (vi < nvr && (!CAUSAL || ca.write_masked || vi < nvl)) {
 #pragma unroll
       for (int j = 0; j < V; ++j) f[k][j] *= r;
-      __builtin_nontemporal_store(pack<DT>(f[k]), yr + vi);
+      if (SHIFT && (vi == 0 || vi + 1 == nvr))
+        store_inside<DT>(yrow, vi, s, cols, f[k]);
+      else
+        __builtin_nontemporal_store(pack<DT>(f[k]), yr + vi);
     }
   }
 }
@@ -1144,19 +1169,22 @@ static SplitWs split_ws_view(char* base, int64_t rows, uint32_t G) {
   return w;
 }
 
-template <int DT, int MODE, bool FUSE, bool CAUSAL>
+// SHIFT: rows not 16-byte aligned; the chunk count (and the workspace's
+// layout) is the one of cols, which the caller has checked covers the most
+// vectors such a row can span.
+template <int DT, int MODE, bool FUSE, bool CAUSAL, bool SHIFT = false>
 static quake_status launch_split(const SmArgs& a, char* ws) {
   constexpr int V = kV<DT>;
   constexpr int NV = (DT == F32) ? 16 : 8;
   static_assert(kSmBlock * NV * V == kChunkElems, "chunk geometry");
   uint32_t G = 0;
   if (!split_chunks(a.cols, &G)) return QUAKE_EINVAL;
-  const uint32_t nvr = (uint32_t)(a.cols / V);
+  const uint32_t nvr = SHIFT ? (uint32_t)a.cols : (uint32_t)(a.cols / V);
   const SplitWs w = split_ws_view(ws, a.rows, G);
   for (int64_t r0 = 0; r0 < a.rows; r0 += kSplitRows) {
     const int64_t nr = std::min(kSplitRows, a.rows - r0);
     const uint32_t xcd = (nr % 8 == 0 && G <= 32) ? 1u : 0u;
-    hipLaunchKernelGGL((sm_split_kernel<DT, MODE, FUSE, CAUSAL, NV>), dim3((uint32_t)(nr * G)),
+    hipLaunchKernelGGL((sm_split_kernel<DT, MODE, FUSE, CAUSAL, NV, SHIFT>), dim3((uint32_t)(nr * G)),
                        dim3(kSmBlock), 0, a.s, a.x + r0 * a.ldx_b, a.y + r0 * a.ldy_b, nvr, a.ldx_b,
                        a.ldy_b, a.kc, causal_at(a, r0), G, xcd, w);
     const quake_status st = launch_status();
@@ -1265,8 +1293,18 @@ static quake_status sm_dispatch(const void* x, void* y, int64_t ldx, int64_t ldy
   a.ldy_b = ldy * esz;
   if (!vec) {
     if constexpr (FUSE) {
-      if (shifted_fits<DT>(x, y, a.rows, cols, ldx, ldy) && shifted_length<DT, CAUSAL>(cols))
-        return launch_shifted<DT, MODE, CAUSAL>(a);
+      if (shifted_fits<DT>(x, y, a.rows, cols, ldx, ldy)) {
+        if constexpr (!CAUSAL) {
+          // longer than the register-row kernels, with a workspace: the split
+          // rows, when cols' chunk count covers every row's vectors
+          const int64_t nvm = (cols + 2 * V - 2) / V;
+          uint32_t G = 0, Gs = 0;
+          if (ws != nullptr && nvm > (DT == F32 ? 4096 : 2048) && split_chunks(cols, &G) &&
+              split_chunks(nvm * V, &Gs) && Gs == G)
+            return launch_split<DT, MODE, FUSE, CAUSAL, true>(a, ws);
+        }
+        if (shifted_length<DT, CAUSAL>(cols)) return launch_shifted<DT, MODE, CAUSAL>(a);
+      }
     }
     return launch_generic<DT, MODE, FUSE, CAUSAL>(x, y, ain, ldx, ldy);
   }
