@@ -73,9 +73,11 @@ int main(void) {
   /* rows of 40000 binary32 values with a workspace the caller allocates and
    * zero-fills: the split-row path, whose chunks exchange their maxima and
    * sums through it. Rows sum to 1, agree with the workspace-free kernel
-   * within the softmax tolerance, and the slots are zero again afterwards. */
-  {
-    const int R = 4, C = 40000;
+   * within the softmax tolerance, and the slots are zero again afterwards.
+   * Then rows of 40001 values, which start at every offset from 16 bytes:
+   * the same paths in their shifted forms. */
+  for (int pass = 0; pass < 2; ++pass) {
+    const int R = 4, C = pass ? 40001 : 40000;
     float* lx = (float*)malloc(sizeof(float) * R * C);
     float* la = (float*)malloc(sizeof(float) * R * C);
     float* lb = (float*)malloc(sizeof(float) * R * C);
