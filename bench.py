@@ -86,10 +86,13 @@ def parse():
     ap.add_argument("--mode", default="quake2", choices=sorted(MODE_IDS))
     ap.add_argument("--only", action="store_true",
                     help="time only --workload in --mode (for profiler passes)")
-    ap.add_argument("--section", choices=["attention", "linear_gelu"],
-                    help="time only the fused attention (quake_attention) or "
+    ap.add_argument("--section", choices=["attention", "linear_gelu", "softmax"],
+                    help="time only the fused attention (quake_attention), "
                          "quake_linear_gelu (the BERT-base MLP's up-projection with its GELU, "
-                         "and its down-projection) and print its JSON (for profiler passes)")
+                         "and its down-projection) or the softmax layouts (LM-head rows with, "
+                         "without and on the fixed scratch, a ragged vocabulary, long rows, "
+                         "1001-key attention rows with the mask given and implied) and print "
+                         "its JSON (for profiler passes)")
     ap.add_argument("--attn-config", default=None,
                     help="with --section attention: only this heads x seq, optionally with "
                          ":causal or :noncausal, e.g. 32x2048:noncausal (for counter passes)")
@@ -749,6 +752,68 @@ def implicit_causal(q, timer, synth, a):
                       % (max(a.steps, nbuf), timer.windows)}
 
 
+def softmax_layouts(q, timer, synth, a):
+    """Row softmax beyond the workloads' own layouts, QuAKE2 and EXACT, graph
+    timed: the LM-head rows with a workspace (split rows), without one (a
+    workgroup per row holding the row) and on the library's fixed scratch;
+    a vocabulary that is not a multiple of 16 bytes (rows start at every
+    offset); long rows over many rows; attention rows of 1001 keys with the
+    mask given as input and implied. Bytes: every input read once and every
+    output written once (implied mask: live inputs and every output)."""
+    import torch
+    L = q.lib
+    out = {}
+    cases = [("lmhead_f32_64x128256", "f32", 64, 128256, "spiked", ("ws", "none", "noalloc")),
+             ("lmhead_f32_64x50257", "f32", 64, 50257, "spiked", ("ws", "none")),
+             ("f32_4096x16400", "f32", 4096, 16400, "normal", ("none",)),
+             ("bf16_1024x32768", "bf16", 1024, 32768, "normal", ("none",)),
+             ("attn_bf16_96096x1001", "bf16", 96096, 1001, "causal", ("none", "implied"))]
+    dtid = {"f32": 0, "f16": 1, "bf16": 2}
+    for name, dt, rows, cols, kind, paths in cases:
+        if kind == "spiked":
+            xh = synth.spiked_logits(rows, cols, 3.0, 16, 20.0, dt, 2412)
+        elif kind == "causal":
+            xh = synth.causal_scores(rows // cols, cols, dt, 2412)
+        else:
+            xh = synth.normal((rows, cols), 3.0, dt, 2412)
+        esz = xh.element_size()
+        nb = max(2, min(16, (1 << 30) // (2 * esz * rows * cols) + 1))
+        xs = [xh.to("cuda:0") for _ in range(nb)]
+        ys = [torch.empty_like(xs[0]) for _ in range(nb)]
+        wsb = q.softmax_workspace(rows, cols, xs[0].dtype)
+        wsp = wsb.data_ptr() if wsb is not None else None
+        wsn = wsb.numel() if wsb is not None else 0
+        fns = {}
+        for mode in (0, 2):
+            for pth in paths:
+                def f(i, s, mode=mode, pth=pth):
+                    xp, yp = xs[i % nb].data_ptr(), ys[i % nb].data_ptr()
+                    if pth == "ws":
+                        return L.quake_softmax_ws(xp, yp, rows, cols, cols, cols, dtid[dt], mode, 1.0,
+                                                  wsp, wsn, s)
+                    if pth == "noalloc":
+                        return L.quake_softmax_noalloc(xp, yp, rows, cols, cols, cols, dtid[dt], mode,
+                                                       1.0, s)
+                    if pth == "implied":
+                        return L.quake_softmax_causal(xp, yp, rows, cols, cols, cols, cols, 0, 1,
+                                                      dtid[dt], mode, 1.0, s)
+                    return L.quake_softmax(xp, yp, rows, cols, cols, cols, dtid[dt], mode, 1.0, s)
+                fns["softmax_%s:%s:mode%d" % (name, pth, mode)] = f
+        r = graph_ms(timer, fns, max(a.steps, nb))
+        algo = 2 * esz * rows * cols
+        ent = {}
+        for pth in paths:
+            ms = r["softmax_%s:%s:mode2" % (name, pth)]
+            b = algo if pth != "implied" else esz * (rows * cols + (rows // cols) * cols * (cols + 1) // 2
+                                                     + (rows % cols) * ((rows % cols) + 1) // 2)
+            ent[pth] = {"quake2_ms": ms, "quake2_gbps": round(b / (ms * 1e-3) / 1e9, 2),
+                        "speedup_vs_exact": round(r["softmax_%s:%s:mode0" % (name, pth)] / ms, 4)}
+        out["softmax_%s" % name] = ent
+        del xs, ys, wsb
+        torch.cuda.empty_cache()
+    return out
+
+
 def table4(q, timer, synth, a):
     """The paper's fusion study (Sec. V-A, Table IV) on this GPU: the vanilla
     operator (unfused, exact exp), QuAKE plugged in without folding, and the
@@ -954,6 +1019,10 @@ def main():
                    "attention_bf16_64x1024x64": fused_attention(q, timer, synth, a, 64, 1024),
                    "attention_bf16_32x2048x64": fused_attention(q, timer, synth, a, 32, 2048)}
         print(json.dumps(res), flush=True)
+        write_windows(a, timer)
+        return
+    if a.section == "softmax":
+        print(json.dumps(softmax_layouts(q, timer, synth, a)), flush=True)
         write_windows(a, timer)
         return
     if a.section == "linear_gelu":
