@@ -7,8 +7,10 @@
 // vector per lane for large inputs, and a resident, software-pipelined
 // grid-stride loop for mid-size ones (where launch ramp and tail dominate).
 // Elements past the last whole vector are handled by one workgroup's first
-// lanes with scalar accesses. Buffers that are not 16-byte aligned take a
-// scalar grid-stride kernel with the same per-element arithmetic.
+// lanes with scalar accesses. Buffers that are not both 16-byte aligned take
+// a kernel that writes y in aligned vectors, each assembled from the aligned
+// vectors of x that hold its bytes, with scalar accesses before y's first
+// 16-byte boundary and after its last whole vector.
 //
 // Per-element arithmetic (Sec. III-A, III-B, III-D of arXiv:2412.00408):
 //   exp      y = QuAKEx(x; c0, c1)                     (Eq. 5, Alg. 1)
@@ -20,6 +22,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "quake_device.hpp"
 #include "quake_host.hpp"
@@ -124,6 +127,63 @@ __global__ __launch_bounds__(kEwBlock) void ew_pipe_kernel(const u32x4* __restri
   }
 }
 
+// Buffers that are not both 16-byte aligned: y is written in aligned 16-byte
+// vectors, each built from the two aligned vectors of x that hold its bytes
+// (d bytes into the first, d a multiple of the element size, uniform; d = 0
+// when x and y sit at the same offset, and then one vector), so every access
+// is an aligned vector access: an aligned vector never crosses a page, and a
+// lane's second load is the next lane's first (served by the cache). The
+// elements before y's first 16-byte boundary (head) and after its last whole
+// vector (tail) take scalar accesses in the first and the last workgroup.
+template <int DT>
+__device__ __forceinline__ u32x4 realign(const u32x4& a, const u32x4& b, uint32_t d) {
+  const uint32_t w[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  const uint32_t rb = d & 3u;
+  u32x4 o;
+  auto take = [&](auto wq) {
+    constexpr int Q = decltype(wq)::value;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) o[j] = __builtin_amdgcn_alignbyte(w[j + Q + 1], w[j + Q], rb);
+  };
+  switch (d >> 2) {
+    case 0: take(std::integral_constant<int, 0>{}); break;
+    case 1: take(std::integral_constant<int, 1>{}); break;
+    case 2: take(std::integral_constant<int, 2>{}); break;
+    default: take(std::integral_constant<int, 3>{}); break;
+  }
+  return o;
+}
+
+template <int DT, int OP, int MODE>
+__global__ __launch_bounds__(kEwBlock) void ew_realign_kernel(const void* __restrict__ x,
+                                                             void* __restrict__ y, uint32_t head,
+                                                             uint32_t nvec, uint32_t tail,
+                                                             uint32_t d, EwParams p) {
+  constexpr int V = kV<DT>;
+  constexpr int64_t esz = kEsz<DT>;
+  // x's element at y's first 16-byte boundary sits d bytes past xa's start
+  const u32x4* xa = reinterpret_cast<const u32x4*>(static_cast<const char*>(x) + head * esz - d);
+  u32x4* ya = reinterpret_cast<u32x4*>(static_cast<char*>(y) + head * esz);
+  const uint32_t i = blockIdx.x * kEwBlock + threadIdx.x;
+  if (i < nvec) {
+    const u32x4 a = __builtin_nontemporal_load(xa + i);
+    // d = 0 (x and y at the same offset): the vector is a itself, and the
+    // next aligned vector of x may lie past its end
+    const u32x4 b = d ? __builtin_nontemporal_load(xa + i + 1) : a;
+    float f[V];
+    unpack<DT>(realign<DT>(a, b, d), f);
+#pragma unroll
+    for (int k = 0; k < V; ++k) f[k] = ew_op<OP, MODE>(f[k], p);
+    __builtin_nontemporal_store(pack<DT>(f), ya + i);
+  }
+  if (blockIdx.x == 0 && threadIdx.x < head)
+    store1<DT>(y, threadIdx.x, ew_op<OP, MODE>(load1<DT>(x, threadIdx.x), p));
+  if (blockIdx.x == gridDim.x - 1 && threadIdx.x < tail) {
+    const int64_t e = (int64_t)head + (int64_t)nvec * V + threadIdx.x;
+    store1<DT>(y, e, ew_op<OP, MODE>(load1<DT>(x, e), p));
+  }
+}
+
 template <int DT, int OP, int MODE>
 __global__ __launch_bounds__(kEwBlock) void ew_scalar_kernel(const void* __restrict__ x,
                                                             void* __restrict__ y, uint32_t n,
@@ -153,10 +213,22 @@ template <int DT, int OP, int MODE>
 quake_status ew_launch(const void* x, void* y, int64_t n, const EwParams& p, hipStream_t s) {
   constexpr int V = kV<DT>;
   constexpr int64_t esz = kEsz<DT>;
-  // x and y at the same offset from a 16-byte boundary (an offset view of
-  // aligned buffers): the few elements before the first boundary take the
-  // scalar kernel, the rest the vector kernels.
   const uintptr_t ux = (uintptr_t)x, uy = (uintptr_t)y;
+  // not both 16-byte aligned (element-aligned): y in aligned vectors, each
+  // assembled from aligned vectors of x, scalar head and tail, one launch
+  if (((ux | uy) & 15u) != 0 && ux % esz == 0 && uy % esz == 0 && n >= 2 * V &&
+      n < (int64_t(1) << 31)) {
+    const int64_t head = (int64_t)((16u - (uy & 15u)) & 15u) / esz;
+    const int64_t nvec = (n - head) / V, tail = (n - head) % V;
+    const uint32_t d = (uint32_t)((ux + head * esz) & 15u);
+    const uint32_t grid = (uint32_t)std::max<int64_t>(1, (nvec + kEwBlock - 1) / kEwBlock);
+    hipLaunchKernelGGL((ew_realign_kernel<DT, OP, MODE>), dim3(grid), dim3(kEwBlock), 0, s, x, y,
+                       (uint32_t)head, (uint32_t)nvec, (uint32_t)tail, d, p);
+    return launch_status();
+  }
+  // x and y at the same offset from a 16-byte boundary, beyond that length
+  // range: the few elements before the first boundary take the scalar
+  // kernel, the rest the vector kernels.
   if ((ux & 15u) != 0 && ((ux - uy) & 15u) == 0 && ux % esz == 0) {
     const int64_t head = std::min<int64_t>(n, (int64_t)((16u - (ux & 15u)) & 15u) / esz);
     hipLaunchKernelGGL((ew_scalar_kernel<DT, OP, MODE>), dim3(1), dim3(kEwBlock), 0, s, x, y,

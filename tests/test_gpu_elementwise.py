@@ -106,17 +106,21 @@ def test_ragged_lengths(q, n, dt):
 
 # x and y at the same offset from a 16-byte boundary: the elements before the
 # first boundary take the scalar kernel, the rest the vector kernels; lengths
-# shorter than, equal to and just past that head, and x and y at different
-# offsets (the scalar kernel throughout). Padding around y must stay untouched.
+# shorter than, equal to and just past that head. x and y at different
+# offsets: each aligned vector of y assembled from two aligned vectors of x
+# (every byte shift), scalar head and tail. Padding around y must stay
+# untouched.
 @pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
-@pytest.mark.parametrize("xoff,yoff", [(1, 1), (2, 2), (3, 3), (5, 5), (7, 7), (1, 0), (0, 3), (2, 5)])
+@pytest.mark.parametrize("xoff,yoff", [(1, 1), (2, 2), (3, 3), (5, 5), (7, 7), (1, 0), (0, 3), (2, 5),
+                                       (3, 1), (7, 2), (5, 0), (0, 1), (6, 7), (4, 0)])
 def test_offsets(q, dt, xoff, yoff):
     V = 4 if dt == "f32" else 8
     esz = 4 if dt == "f32" else 2
-    if (xoff * esz) % 16 == 0 and xoff:
+    if (xoff * esz) % 16 == 0 and xoff or (yoff * esz) % 16 == 0 and yoff:
         pytest.skip("offset is a whole vector")
-    head = ((16 - (xoff * esz) % 16) % 16) // esz
-    for n in sorted({1, max(1, head - 1), max(1, head), head + 1, head + V + 1, 5000, 1_000_003}):
+    head = ((16 - (yoff * esz) % 16) % 16) // esz
+    for n in sorted({1, max(1, head - 1), max(1, head), head + 1, head + V + 1, 2 * V - 1, 2 * V,
+                     2 * V + 1, 5000, 1_000_003}):
         x = synth.normal((n + 8,), 3.0, dt, 110 + n % 31 + xoff)
         xb = host_bits(x)[xoff:xoff + n].copy()
         xg = x.to("cuda:0")

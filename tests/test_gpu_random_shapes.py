@@ -176,6 +176,49 @@ def test_random_elementwise(q, op, n, dt, mode, a, b, seed):
         op, dt, n, mode, a, b, seed))
 
 
+def _elementwise_offset_cases(n, seed):
+    """(op, n, dt, xoff, yoff, seed): x and y views at random element offsets
+    (the same or different offsets from 16 bytes), random lengths."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        op = str(rng.choice(["exp", "gelu", "sigmoid", "silu", "gelu_unfused"]))
+        ne = int(rng.integers(1, 2_000_000)) if rng.random() < 0.7 else int(rng.integers(1, 64))
+        out.append((op, ne, str(rng.choice(["f32", "bf16", "f16"])), int(rng.integers(0, 8)),
+                    int(rng.integers(0, 8)), int(rng.integers(0, 1 << 20))))
+    return out
+
+
+@pytest.mark.parametrize("op,n,dt,xoff,yoff,seed", _elementwise_offset_cases(24, 77))
+def test_random_elementwise_offsets(q, op, n, dt, xoff, yoff, seed):
+    import oracle
+    from gpu_util import THREADS, host_bits
+    say("random elementwise offsets", op, n, dt, xoff, yoff, seed)
+    x = synth.uniform_with_outliers(n + 8, -14.0, 14.0, 0.01, 80.0, dt, seed)
+    xb = host_bits(x)[xoff:xoff + n].copy()
+    xg = x.to("cuda:0")
+    yfull = torch.full((n + 8,), 5.0, dtype=x.dtype, device="cuda:0")
+    src, dst = xg[xoff:xoff + n], yfull[yoff:yoff + n]
+    if op == "exp":
+        q.quake_exp(src, dst, mode=2)
+        ref = oracle.exp(xb, dt, 2, threads=THREADS)
+    elif op == "gelu":
+        q.quake_gelu(src, dst, mode=2)
+        ref = oracle.gelu(xb, dt, 2, threads=THREADS)
+    elif op == "gelu_unfused":
+        q.quake_gelu_unfused(src, dst, mode=2)
+        ref = oracle.gelu_unfused(xb, dt, 2, threads=THREADS)
+    else:
+        q.quake_sigmoid(src, dst, mode=2, silu=(op == "silu"))
+        ref = oracle.sigmoid(xb, dt, 2, silu=(op == "silu"), threads=THREADS)
+    torch.cuda.synchronize()
+    out = host_bits(yfull)
+    assert_parity(out[yoff:yoff + n].copy(), ref, dt, kind_of(op, 2),
+                  "random offsets %s %s n%d x+%d y+%d seed%d" % (op, dt, n, xoff, yoff, seed))
+    pad = np.concatenate([out[:yoff], out[yoff + n:]])
+    assert np.all(oracle.decode(pad, dt) == 5.0), "write outside y"
+
+
 def _linear_cases(n, seed):
     """(m, n, k, mode, dt, gelu, pad, seed): output widths around multiples
     of 128 and 192 (grids this small take the 128-wide tile), ragged m and n,
