@@ -14,9 +14,14 @@
  *   current HIP device, e.g. by torch). The library never allocates, frees or
  *   retains them. x and y have the same element type (quake_dtype); all
  *   arithmetic is binary32. In-place (x == y) is allowed; partial overlap is
- *   undefined. Any alignment is accepted; 16-byte-aligned buffers (and, for
- *   softmax, row strides that are a multiple of 16 bytes) take the vectorised
- *   path.
+ *   undefined. Any alignment is accepted. Element-aligned buffers are read
+ *   and written as aligned 16-byte vectors: 16-byte-aligned ones directly;
+ *   the elementwise operators (below 2^31 elements) and the softmax rows at
+ *   the same offset from 16 bytes in x and y through the aligned 16-byte
+ *   blocks that hold their bytes, with the elements outside the operand
+ *   never written (up to 15 bytes around an operand may be read, never
+ *   outside a 16-byte block that holds some of its bytes). Other layouts take
+ *   scalar kernels.
  * - `stream` is a hipStream_t passed as an opaque pointer (NULL = the legacy
  *   default stream). Every call is asynchronous and stream-ordered: the status
  *   covers argument validation and the launch itself (hipGetLastError right
