@@ -810,12 +810,14 @@ __global__ __launch_bounds__(kLongBlock) void sm_long_kernel(const char* __restr
 // twice. Thread t holds vectors k * 512 + t. Whole blocks of 512 vectors past
 // the row's end are skipped (a workgroup-uniform branch); inside the last
 // block, lanes past the end load the last vector again, which leaves the max
-// unchanged, is left out of the sum and is never stored. REGFULL: every
-// register block lies inside the row, so those loads are unconditional and
-// the compiler's vmcnt waits stay per load. The LDS part is loaded first, so
-// the VGPRs it passes through are free again before the register part
-// arrives. Sums as in sm_long: fp32 within a vector, then double across
-// vectors, lanes and waves in a fixed order.
+// unchanged (SHIFT: masked to -inf like the elements outside the row), is
+// left out of the sum and is never stored. REGFULL: every register block
+// lies inside the row, so those loads are unconditional and the compiler's
+// vmcnt waits stay per load. MINB: workgroups per CU the registers are
+// budgeted for. The LDS part is loaded first, so the VGPRs it passes through
+// are free again before the register part arrives. Sums as in sm_long: fp32
+// within a vector, then double across vectors, lanes and waves in a fixed
+// order.
 // ---------------------------------------------------------------------------
 constexpr int kResBlock = 512;
 
