@@ -110,14 +110,16 @@ def test_ragged_lengths(q, n, dt):
 # offsets: each aligned vector of y assembled from two aligned vectors of x
 # (every byte shift), scalar head and tail. Padding around y must stay
 # untouched.
-@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
-@pytest.mark.parametrize("xoff,yoff", [(1, 1), (2, 2), (3, 3), (5, 5), (7, 7), (1, 0), (0, 3), (2, 5),
-                                       (3, 1), (7, 2), (5, 0), (0, 1), (6, 7), (4, 0)])
+OFFSETS = [(1, 1), (2, 2), (3, 3), (5, 5), (7, 7), (1, 0), (0, 3), (2, 5), (3, 1), (7, 2), (5, 0),
+           (0, 1), (6, 7), (4, 0)]
+
+
+# (a nonzero offset of a whole 16-byte vector, 4 binary32 elements, is left out)
+@pytest.mark.parametrize("dt,xoff,yoff", [(dt, a, b) for dt in ("f32", "f16", "bf16") for a, b in OFFSETS
+                                          if dt != "f32" or not any(o and o % 4 == 0 for o in (a, b))])
 def test_offsets(q, dt, xoff, yoff):
     V = 4 if dt == "f32" else 8
     esz = 4 if dt == "f32" else 2
-    if (xoff * esz) % 16 == 0 and xoff or (yoff * esz) % 16 == 0 and yoff:
-        pytest.skip("offset is a whole vector")
     head = ((16 - (yoff * esz) % 16) % 16) // esz
     for n in sorted({1, max(1, head - 1), max(1, head), head + 1, head + V + 1, 2 * V - 1, 2 * V,
                      2 * V + 1, 5000, 1_000_003}):
