@@ -135,25 +135,6 @@ __global__ __launch_bounds__(kEwBlock) void ew_pipe_kernel(const u32x4* __restri
 // lane's second load is the next lane's first (served by the cache). The
 // elements before y's first 16-byte boundary (head) and after its last whole
 // vector (tail) take scalar accesses in the first and the last workgroup.
-template <int DT>
-__device__ __forceinline__ u32x4 realign(const u32x4& a, const u32x4& b, uint32_t d) {
-  const uint32_t w[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
-  const uint32_t rb = d & 3u;
-  u32x4 o;
-  auto take = [&](auto wq) {
-    constexpr int Q = decltype(wq)::value;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) o[j] = __builtin_amdgcn_alignbyte(w[j + Q + 1], w[j + Q], rb);
-  };
-  switch (d >> 2) {
-    case 0: take(std::integral_constant<int, 0>{}); break;
-    case 1: take(std::integral_constant<int, 1>{}); break;
-    case 2: take(std::integral_constant<int, 2>{}); break;
-    default: take(std::integral_constant<int, 3>{}); break;
-  }
-  return o;
-}
-
 template <int DT, int OP, int MODE>
 __global__ __launch_bounds__(kEwBlock) void ew_realign_kernel(const void* __restrict__ x,
                                                              void* __restrict__ y, uint32_t head,
@@ -171,7 +152,7 @@ __global__ __launch_bounds__(kEwBlock) void ew_realign_kernel(const void* __rest
     // next aligned vector of x may lie past its end
     const u32x4 b = d ? __builtin_nontemporal_load(xa + i + 1) : a;
     float f[V];
-    unpack<DT>(realign<DT>(a, b, d), f);
+    unpack<DT>(realign(a, b, d), f);
 #pragma unroll
     for (int k = 0; k < V; ++k) f[k] = ew_op<OP, MODE>(f[k], p);
     __builtin_nontemporal_store(pack<DT>(f), ya + i);

@@ -111,7 +111,46 @@ __global__ __launch_bounds__(kN16Block) void exp16_vec_kernel(const u32x4* __res
   }
 }
 
-// Unaligned buffers: one element per lane, grid-stride.
+// Buffers not both 16-byte aligned (element-aligned): y in aligned vectors,
+// each assembled from the one or two aligned vectors of x that hold its bytes
+// (d bytes into the first; d = 0 when x and y share their offset), the
+// elements before y's first 16-byte boundary and after its last whole vector
+// in the first and the last workgroup, one element per lane.
+template <int DT, int MODE>
+__device__ __forceinline__ uint16_t exp16_one(uint16_t h, const N16Const& k) {
+  const float xv = DT == F16 ? (float)__builtin_bit_cast(_Float16, h) : as_f((uint32_t)h << 16);
+  return (uint16_t)(n16_pair<DT, MODE>(xv, 0.0f, k) & 0xFFFFu);
+}
+
+template <int DT, int MODE>
+__global__ __launch_bounds__(kN16Block) void exp16_realign_kernel(const uint16_t* __restrict__ x,
+                                                                 uint16_t* __restrict__ y,
+                                                                 uint32_t head, uint32_t nvec,
+                                                                 uint32_t tail, uint32_t d,
+                                                                 N16Const k) {
+  const u32x4* xa =
+      reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(x + head) - d);
+  u32x4* ya = reinterpret_cast<u32x4*>(y + head);
+  const uint32_t i = blockIdx.x * kN16Block + threadIdx.x;
+  if (i < nvec) {
+    const u32x4 a = __builtin_nontemporal_load(xa + i);
+    // d = 0: the vector is a itself, and the next aligned vector of x may
+    // lie past its end
+    const u32x4 b = d ? __builtin_nontemporal_load(xa + i + 1) : a;
+    const u32x4 v = realign(a, b, d);
+    u32x4 o;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) o[w] = n16_pair<DT, MODE>(n16_lo<DT>(v[w]), n16_hi<DT>(v[w]), k);
+    __builtin_nontemporal_store(o, ya + i);
+  }
+  if (blockIdx.x == 0 && threadIdx.x < head) y[threadIdx.x] = exp16_one<DT, MODE>(x[threadIdx.x], k);
+  if (blockIdx.x == gridDim.x - 1 && threadIdx.x < tail) {
+    const int64_t e = (int64_t)head + (int64_t)nvec * 8 + threadIdx.x;
+    y[e] = exp16_one<DT, MODE>(x[e], k);
+  }
+}
+
+// Buffers not element-aligned, or short: one element per lane, grid-stride.
 template <int DT, int MODE>
 __global__ __launch_bounds__(kN16Block) void exp16_scalar_kernel(const uint16_t* __restrict__ x,
                                                                 uint16_t* __restrict__ y,
@@ -128,9 +167,20 @@ constexpr int64_t kN16Chunk = int64_t(1) << 30;   // elements per launch, a mult
 template <int DT, int MODE>
 static quake_status exp16_launch(const void* x, void* y, int64_t n, const N16Const& k,
                                  hipStream_t s) {
-  // x and y at the same offset from a 16-byte boundary: the elements before
-  // the first boundary take the scalar kernel, the rest the vector kernel.
   const uintptr_t ux = (uintptr_t)x, uy = (uintptr_t)y;
+  if (((ux | uy) & 15u) != 0 && ux % 2 == 0 && uy % 2 == 0 && n >= 16 && n < (int64_t(1) << 31)) {
+    const int64_t head = (int64_t)((16u - (uy & 15u)) & 15u) / 2;
+    const int64_t nvec = (n - head) / 8, tail = (n - head) % 8;
+    const uint32_t d = (uint32_t)((ux + head * 2) & 15u);
+    const uint32_t grid = (uint32_t)std::max<int64_t>(1, (nvec + kN16Block - 1) / kN16Block);
+    hipLaunchKernelGGL((exp16_realign_kernel<DT, MODE>), dim3(grid), dim3(kN16Block), 0, s,
+                       static_cast<const uint16_t*>(x), static_cast<uint16_t*>(y),
+                       (uint32_t)head, (uint32_t)nvec, (uint32_t)tail, d, k);
+    return launch_status();
+  }
+  // x and y at the same offset from a 16-byte boundary, beyond that length
+  // range: the elements before the first boundary take the scalar kernel, the
+  // rest the vector kernel.
   if ((ux & 15u) != 0 && ((ux - uy) & 15u) == 0 && ux % 2 == 0) {
     const int64_t head = std::min<int64_t>(n, (int64_t)((16u - (ux & 15u)) & 15u) / 2);
     hipLaunchKernelGGL((exp16_scalar_kernel<DT, MODE>), dim3(1), dim3(kN16Block), 0, s,

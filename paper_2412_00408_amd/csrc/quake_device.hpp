@@ -19,6 +19,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace qk {
 
 enum Mode : int { EXACT = 0, Q1 = 1, Q2 = 2, Q2M = 3 };
@@ -191,6 +193,27 @@ __device__ __forceinline__ u32x4 pack(const float* f) {
       v[k] = (DT == BF16) ? pack_bf16(f[2 * k], f[2 * k + 1]) : pack_f16(f[2 * k], f[2 * k + 1]);
   }
   return v;
+}
+
+// The 16 bytes that start d bytes into the aligned vector a and continue into
+// the next aligned vector b (d uniform, 0 <= d < 16): one v_alignbyte per
+// dword, so an unaligned run of memory is read as aligned vectors.
+__device__ __forceinline__ u32x4 realign(const u32x4& a, const u32x4& b, uint32_t d) {
+  const uint32_t w[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  const uint32_t rb = d & 3u;
+  u32x4 o;
+  auto take = [&](auto wq) {
+    constexpr int Q = decltype(wq)::value;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) o[j] = __builtin_amdgcn_alignbyte(w[j + Q + 1], w[j + Q], rb);
+  };
+  switch (d >> 2) {
+    case 0: take(std::integral_constant<int, 0>{}); break;
+    case 1: take(std::integral_constant<int, 1>{}); break;
+    case 2: take(std::integral_constant<int, 2>{}); break;
+    default: take(std::integral_constant<int, 3>{}); break;
+  }
+  return o;
 }
 
 // A 16-byte vector of -inf in each format (masked lanes of a softmax row).

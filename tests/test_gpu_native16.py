@@ -64,6 +64,25 @@ def test_lengths_and_alignment(q, dt, n, off):
         assert np.all(oracle.decode(out[:off], dt) == 3.0)
 
 
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("n,xoff,yoff", [(15, 1, 0), (16, 1, 0), (17, 0, 3), (1000, 3, 6),
+                                         (100_003, 7, 2), ((1 << 20) + 5, 5, 1), (33, 6, 6)])
+def test_offsets_differ(q, dt, n, xoff, yoff):
+    # x and y at different offsets from 16 bytes: each aligned vector of y
+    # assembled from two aligned vectors of x; padding around y untouched
+    x = synth.uniform((n + 8,), -12.0, 12.0, dt, 1350 + n % 83)
+    xb = host_bits(x)[xoff:xoff + n].copy()
+    xg = x.to("cuda:0")
+    y = torch.full((n + 8,), 3.0, dtype=TD[dt], device="cuda:0")
+    say("exp16 offsets", dt, n, xoff, yoff)
+    q.quake_exp16(xg[xoff:xoff + n], y[yoff:yoff + n], mode=2)
+    torch.cuda.synchronize()
+    out = host_bits(y)
+    ref = oracle.exp16(xb, dt, 2, threads=THREADS)
+    assert check_bits(out[yoff:yoff + n].copy(), ref, "exp16 %s n %d x+%d y+%d" % (dt, n, xoff, yoff)) is None
+    assert np.all(oracle.decode(np.concatenate([out[:yoff], out[yoff + n:]]), dt) == 3.0)
+
+
 def test_in_place_and_stream(q):
     x = synth.uniform((1 << 20,), -9.0, 9.0, "f16", 1400).to("cuda:0")
     ref = q.quake_exp16(x, mode=1)
