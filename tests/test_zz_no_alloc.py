@@ -1,8 +1,9 @@
 """quake_softmax_noalloc (the split-row softmax on the library's fixed device
 scratch, for callers that cannot allocate) against quake_softmax_ws (the same
-kernels on a caller workspace), through the C ABI on cuda:0: two calls in a
-row, the second on a smaller input, bit for bit; the first also against the
-oracle; a shape beyond the scratch is refused before any launch."""
+kernels on a caller workspace), through the C ABI on cuda:0: calls in a row,
+the later ones on smaller inputs (the last with rows that are not 16-byte
+aligned), bit for bit; the first also against the oracle; a shape beyond the
+scratch is refused before any launch."""
 import ctypes
 
 import numpy as np
@@ -36,7 +37,9 @@ def _noalloc(q, x, y, mode=2, t=1.0):
 def test_noalloc_matches_the_workspace_entry_point(q):
     w = synth.WORKLOADS["lmhead_softmax_f32_64x128256"]
     cases = [(w.make(), "f32 64x128256"),
-             (synth.normal((24, 40000), 3.0, "bf16", 1400), "bf16 24x40000")]
+             (synth.normal((24, 40000), 3.0, "bf16", 1400), "bf16 24x40000"),
+             # rows starting at every offset from 16 bytes: the shifted split form
+             (synth.normal((16, 50257), 3.0, "f32", 1402), "f32 16x50257")]
     for i, (xc, name) in enumerate(cases):
         x = xc.to("cuda:0")
         rows, cols = x.shape
