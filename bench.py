@@ -86,13 +86,14 @@ def parse():
     ap.add_argument("--mode", default="quake2", choices=sorted(MODE_IDS))
     ap.add_argument("--only", action="store_true",
                     help="time only --workload in --mode (for profiler passes)")
-    ap.add_argument("--section", choices=["attention", "linear_gelu", "softmax"],
+    ap.add_argument("--section", choices=["attention", "linear_gelu", "softmax", "elementwise"],
                     help="time only the fused attention (quake_attention), "
                          "quake_linear_gelu (the BERT-base MLP's up-projection with its GELU, "
                          "and its down-projection) or the softmax layouts (LM-head rows with, "
                          "without and on the fixed scratch, a ragged vocabulary, long rows, "
-                         "1001-key attention rows with the mask given and implied) and print "
-                         "its JSON (for profiler passes)")
+                         "1001-key attention rows with the mask given and implied) or the "
+                         "elementwise operators on offset views, and print its JSON (for "
+                         "profiler passes)")
     ap.add_argument("--attn-config", default=None,
                     help="with --section attention: only this heads x seq, optionally with "
                          ":causal or :noncausal, e.g. 32x2048:noncausal (for counter passes)")
@@ -814,6 +815,40 @@ def softmax_layouts(q, timer, synth, a):
     return out
 
 
+def elementwise_layouts(q, timer, synth, a):
+    """GELU bf16 4096 x 3072 and Logistic fp16 2^26 on offset views, QuAKE2,
+    graph timed: x and y 16-byte aligned, both one element past a 16-byte
+    boundary, and x one element past one with y aligned (the realigning
+    kernel). Operand sets rotate over at least 1 GiB."""
+    import torch
+    L = q.lib
+    out = {}
+    for name, dt, n, seed in (("gelu_bf16_4096x3072", "bf16", 4096 * 3072, 2),
+                              ("sigmoid_f16_2p26", "f16", 1 << 26, 4)):
+        esz = 2
+        nb = max(2, min(16, (1 << 30) // (2 * esz * n) + 1))
+        xh = synth.normal((n + 16,), 2.0, dt, seed)
+        xs = [xh.to("cuda:0") for _ in range(nb)]
+        ys = [torch.empty_like(xs[0]) for _ in range(nb)]
+        dtid = {"f16": 1, "bf16": 2}[dt]
+        fns = {}
+        for lay, xo, yo in (("aligned", 0, 0), ("shared_offset", 1, 1), ("x_offset", 1, 0)):
+            def f(i, s, xo=xo, yo=yo):
+                xp = xs[i % nb].data_ptr() + xo * esz
+                yp = ys[i % nb].data_ptr() + yo * esz
+                if name.startswith("gelu"):
+                    return L.quake_gelu(xp, yp, n, dtid, 2, s)
+                return L.quake_sigmoid(xp, yp, n, dtid, 2, 0, s)
+            fns["ew_%s:%s" % (name, lay)] = f
+        r = graph_ms(timer, fns, max(a.steps, nb))
+        out["ew_" + name] = {lay: {"quake2_ms": r["ew_%s:%s" % (name, lay)],
+                                   "quake2_gbps": round(2 * esz * n / (r["ew_%s:%s" % (name, lay)] * 1e-3) / 1e9, 2)}
+                             for lay in ("aligned", "shared_offset", "x_offset")}
+        del xs, ys
+        torch.cuda.empty_cache()
+    return out
+
+
 def table4(q, timer, synth, a):
     """The paper's fusion study (Sec. V-A, Table IV) on this GPU: the vanilla
     operator (unfused, exact exp), QuAKE plugged in without folding, and the
@@ -1023,6 +1058,10 @@ def main():
         return
     if a.section == "softmax":
         print(json.dumps(softmax_layouts(q, timer, synth, a)), flush=True)
+        write_windows(a, timer)
+        return
+    if a.section == "elementwise":
+        print(json.dumps(elementwise_layouts(q, timer, synth, a)), flush=True)
         write_windows(a, timer)
         return
     if a.section == "linear_gelu":

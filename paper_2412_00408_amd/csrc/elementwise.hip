@@ -146,11 +146,16 @@ __global__ __launch_bounds__(kEwBlock) void ew_realign_kernel(const void* __rest
   const u32x4* xa = reinterpret_cast<const u32x4*>(static_cast<const char*>(x) + head * esz - d);
   u32x4* ya = reinterpret_cast<u32x4*>(static_cast<char*>(y) + head * esz);
   const uint32_t i = blockIdx.x * kEwBlock + threadIdx.x;
+  // d = 0 (x and y at the same offset): the vector is a itself, and the next
+  // aligned vector of x may lie past its end; else a and b from aligned_pair
+  u32x4 a, b;
+  if (d == 0) {
+    if (i < nvec) a = __builtin_nontemporal_load(xa + i);
+    b = a;
+  } else {
+    aligned_pair(xa, i, nvec, a, b);
+  }
   if (i < nvec) {
-    const u32x4 a = __builtin_nontemporal_load(xa + i);
-    // d = 0 (x and y at the same offset): the vector is a itself, and the
-    // next aligned vector of x may lie past its end
-    const u32x4 b = d ? __builtin_nontemporal_load(xa + i + 1) : a;
     float f[V];
     unpack<DT>(realign(a, b, d), f);
 #pragma unroll

@@ -132,11 +132,16 @@ __global__ __launch_bounds__(kN16Block) void exp16_realign_kernel(const uint16_t
       reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(x + head) - d);
   u32x4* ya = reinterpret_cast<u32x4*>(y + head);
   const uint32_t i = blockIdx.x * kN16Block + threadIdx.x;
+  // d = 0: the vector is a itself, and the next aligned vector of x may lie
+  // past its end; else a and b from aligned_pair
+  u32x4 a, b;
+  if (d == 0) {
+    if (i < nvec) a = __builtin_nontemporal_load(xa + i);
+    b = a;
+  } else {
+    aligned_pair(xa, i, nvec, a, b);
+  }
   if (i < nvec) {
-    const u32x4 a = __builtin_nontemporal_load(xa + i);
-    // d = 0: the vector is a itself, and the next aligned vector of x may
-    // lie past its end
-    const u32x4 b = d ? __builtin_nontemporal_load(xa + i + 1) : a;
     const u32x4 v = realign(a, b, d);
     u32x4 o;
 #pragma unroll

@@ -216,6 +216,20 @@ __device__ __forceinline__ u32x4 realign(const u32x4& a, const u32x4& b, uint32_
   return o;
 }
 
+// The aligned vectors a and b that hold the 16 bytes starting d bytes into
+// vector i of xa (d > 0): every lane loads its own a (past the last vector,
+// the one after it, which still holds bytes of the operand) and takes b from
+// the next lane (ds_bpermute), so each aligned vector is fetched once; the
+// wave's last lane loads its b. Every lane of the wave must call this.
+__device__ __forceinline__ void aligned_pair(const u32x4* xa, uint32_t i, uint32_t nvec, u32x4& a,
+                                             u32x4& b) {
+  a = __builtin_nontemporal_load(xa + (i < nvec ? i : nvec));
+  const int src = (int)((((threadIdx.x & 63u) + 1u) & 63u) << 2);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) b[j] = (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)a[j]);
+  if ((threadIdx.x & 63u) == 63u) b = __builtin_nontemporal_load(xa + (i + 1 < nvec ? i + 1 : nvec));
+}
+
 // A 16-byte vector of -inf in each format (masked lanes of a softmax row).
 template <int DT>
 __device__ __forceinline__ u32x4 neg_inf_vec() {
